@@ -20,7 +20,8 @@
  *       by its structural path id (4 bits per level, digit = sibling index - 1),
  *       not by creation order.  Per-token draws: c0 = y>>2, word y&3.  Per-stage
  *       draws: c0 = j, word 0.  Tags: 1 expand, 2 accept, 3 bonus.
- *   R2  u = ((w>>8) + 0.5) * 2^-24, never 0 or 1.
+ *   R2  u = ((w>>9) + 0.5) * 2^-23: 24 significant bits, so the value is exact
+ *       in fp32 as well as fp64; never 0 or 1 (it lies in [2^-24, 1 - 2^-24]).
  *   R3  sibling draws without replacement are realised as Gumbel-top-k over
  *       z/T + G(u): the order of the perturbed keys is a sequence of draws
  *       without replacement (Plackett-Luce), i.e. the residual-proposal draws.
@@ -81,9 +82,9 @@ static uint32_t draw_word(uint64_t seed, int request, int depth, uint64_t path,
   return out[word];
 }
 
-/* Reading R2: a uniform in (0,1) from the top 24 bits of a word. */
+/* Reading R2: a uniform in (0,1) from the top 23 bits of a word. */
 static double word_to_uniform(uint32_t w) {
-  return ((double)(w >> 8) + 0.5) * (1.0 / 16777216.0);
+  return ((double)(w >> 9) + 0.5) * (1.0 / 8388608.0);
 }
 
 double tso_u_token(uint64_t seed, int request, int depth, uint64_t path, int tag, int y) {

@@ -59,13 +59,18 @@ def test_uniform_counter_layout_and_range():
     for y in (0, 1, 2, 3, 4, 77, 4095):
         ctr = [y >> 2, path & 0xFFFFFFFF, path >> 32, (req << 12) | (depth << 4) | o.TAG_EXPAND]
         w = o.philox4x32_10(ctr, [seed & 0xFFFFFFFF, seed >> 32])[y & 3]
-        assert o.u_token(seed, req, depth, path, o.TAG_EXPAND, y) == ((int(w) >> 8) + 0.5) / 2**24
+        assert o.u_token(seed, req, depth, path, o.TAG_EXPAND, y) == ((int(w) >> 9) + 0.5) / 2**23
     for j in (1, 2, 7):
         ctr = [j, path & 0xFFFFFFFF, path >> 32, (req << 12) | (depth << 4) | o.TAG_ACCEPT]
         w = o.philox4x32_10(ctr, [seed & 0xFFFFFFFF, seed >> 32])[0]
-        assert o.u_stage(seed, req, depth, path, o.TAG_ACCEPT, j) == ((int(w) >> 8) + 0.5) / 2**24
+        assert o.u_stage(seed, req, depth, path, o.TAG_ACCEPT, j) == ((int(w) >> 9) + 0.5) / 2**23
     us = np.array([o.u_token(7, 0, 0, 0, 1, y) for y in range(20000)])
     assert us.min() > 0.0 and us.max() < 1.0
+    # every value is exact in fp32 (24 significant bits), including the extremes
+    assert np.all(us.astype(np.float32).astype(np.float64) == us)
+    for w in (0, 0xFFFFFFFF, 0x80000000, 0x7FFFFFFF):
+        u = ((w >> 9) + 0.5) / 2**23
+        assert 0.0 < u < 1.0 and float(np.float32(u)) == u
     # uniformity of the mapped draws
     assert stats.kstest(us, "uniform").pvalue > 1e-3
 
@@ -197,7 +202,7 @@ def _universe_brute_force(model_arrays, V, D, r, anchor, theta, N, K, T, seed, a
     def philox_u(depth, path, tag, y):
         ctr = [y >> 2, path & 0xFFFFFFFF, path >> 32, (0 << 12) | (depth << 4) | tag]
         w = o.philox4x32_10(ctr, [seed & 0xFFFFFFFF, seed >> 32])[y & 3]
-        return ((int(w) >> 8) + 0.5) / 2**24
+        return ((int(w) >> 9) + 0.5) / 2**23
 
     def logphat(lq):
         q = math.exp(lq)
