@@ -1,0 +1,203 @@
+/*
+ * treespark.h -- C ABI of the TreeSpark draft-tree step on MI355X (gfx950).
+ *
+ * The library computes one speculative-decoding round's draft tree and its
+ * verification, as described in "TreeSpark" (arXiv 2609.22098):
+ *   ts_expand      parent-conditioned expansion of a frontier of parents
+ *                  (§1 Eq. 1; §3.2 item 1; §3.3 residual-proposal equation;
+ *                  §3.4 Eq. 3; §5.6 per-node work)
+ *   ts_build_tree  best-first expansion of whole trees under (N, K, theta)
+ *                  (§3.2 Algorithm 1; §3.5)
+ *   ts_verify      greedy exact-match or recursive-rejection verification
+ *                  (§3.2 item 3; §3.3 and Proposition 1)
+ *
+ * Conventions shared by every call
+ *   - Model tensors are DEVICE pointers owned by the caller, row-major:
+ *       U  [R][D][V]  drafter base logits; row d of request q gives the logits
+ *                     of the children of a depth-d parent (the LM-shifted
+ *                     block semantics of §3.1)
+ *       E  [V][r]     W1 of the Markov head: row x = W1[x]
+ *       W2 [V][r]     W2 of the Markov head: row v = W2[v], so the transition
+ *                     bias is B(x, v) = <W1[x], W2[v]> (§3.1); as an r x V
+ *                     matrix W this is W2 transposed
+ *     All three share one dtype (TS_F32 or TS_BF16).  Accumulation is fp32.
+ *   - The library never frees, retains or writes caller tensors other than
+ *     the documented outputs.  It allocates no device memory: scratch comes
+ *     from the caller's workspace (sizes from the *_workspace_size calls).
+ *   - Randomness is Philox4x32-10 keyed by `seed`, counter
+ *     (c0, path lo32, path hi32, request<<12 | depth<<4 | tag), where a node
+ *     is named by its structural path id: 4 bits per level, digit = sibling
+ *     index - 1, level d at bits [4d, 4d+4).  Per-token draws use c0 = y>>2
+ *     and word y&3; per-stage draws use c0 = j and word 0; tags are 1 (expand),
+ *     2 (accept), 3 (bonus).  A uniform is u = ((w>>9) + 0.5) * 2^-23.
+ *   - Every call returns TS_OK (0) or a negative ts_status.  On an error
+ *     detected on the host nothing is launched and no output is written;
+ *     ts_last_error() (per thread) describes it.  No exception crosses the ABI.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ */
+#ifndef TREESPARK_H
+#define TREESPARK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TS_OK = 0,
+  TS_EINVAL = -1,        /* bad argument (null pointer, size out of range, ...) */
+  TS_EUNSUPPORTED = -2,  /* valid but not supported by this build (see limits) */
+  TS_EHIP = -3,          /* a HIP runtime call failed */
+  TS_ENOSPACE = -4,      /* workspace smaller than the *_workspace_size result */
+  TS_EINTERNAL = -5      /* an internal consistency check failed */
+} ts_status;
+
+typedef enum { TS_F32 = 0, TS_BF16 = 1 } ts_dtype;
+
+/* Limits of this build: K <= TS_MAX_K siblings, D <= TS_MAX_D (the path id
+ * holds 4 bits per level), R < 2^20 requests; r must be a multiple of 32 for
+ * bf16 and of 4 for fp32, and at most 256. */
+#define TS_MAX_K 16
+#define TS_MAX_D 16
+#define TS_MAX_R (1 << 20)
+#define TS_MAX_RANK 256
+
+/* Drafter outputs of one round (device pointers, see above). */
+typedef struct {
+  const void* U;
+  const void* E;
+  const void* W2;
+  int32_t R, D, V, r;
+  int32_t dtype; /* ts_dtype of U, E and W2 */
+} ts_drafter;
+
+/* Calibrated edge acceptance p-hat = sigmoid(a * logit(q0) + b), §3.4 Eq. 3.
+ * The paper's deployed values are a = 0.67, b = -0.46. */
+typedef struct {
+  float a, b;
+} ts_calib;
+
+/* One frontier parent (device array element, 24 bytes). */
+typedef struct {
+  int32_t token;    /* parent token x_p, 0 <= token < V */
+  int32_t depth;    /* 0 <= depth < D; its children use U row `depth` */
+  int32_t request;  /* 0 <= request < R */
+  float log_surv;   /* log S(parent): log of the path survival (§3.5) */
+  uint64_t path;    /* structural path id of the parent */
+} ts_parent;
+
+/* Outputs of ts_expand, DEVICE pointers, [P][k] row-major unless noted.
+ * Children are in draw order: at T = 0 the top-k tokens of q0 by (q0 desc,
+ * id asc); at T > 0 the k draws without replacement from q_T (Gumbel-top-k).
+ * Slot j (1-based) of parent p creates child j; its key is the heap priority
+ * of Algorithm 1: at T = 0 the child's own log survival, at T > 0 the
+ * admissible pre-draw bound log S(p) + log p-hat(max q0 over tokens not drawn
+ * before j) of §3.2.  Optional pointers may be NULL. */
+typedef struct {
+  int32_t* child_token;    /* [P][k] required */
+  float* child_log_q0;     /* [P][k] required: log q0(child | parent) */
+  float* child_log_qT;     /* [P][k] optional: log qT(child | parent); NaN at T = 0 */
+  float* child_log_surv;   /* [P][k] required: log S(child) = log S(p) + log p-hat */
+  float* slot_key;         /* [P][k] required */
+  int32_t* rank_token;     /* [P][k] optional: top-k tokens by q0 */
+  float* rank_log_q0;      /* [P][k] optional: their log q0 */
+  float* lse0;             /* [P] optional: log-sum-exp of the logits z */
+  float* lseT;             /* [P] optional: log-sum-exp of z / T; NaN at T = 0 */
+  int32_t* diag;           /* [P] optional: candidate runs whose recomputed maximum differed
+                              from the streaming pass (always 0 unless the device misbehaves) */
+} ts_expand_out;
+
+/* Bytes of device workspace ts_expand needs for P parents (0 if P == 0). */
+size_t ts_expand_workspace_size(const ts_drafter* d, int32_t P, int32_t k, float T);
+
+/*
+ * ts_expand: evaluate P frontier parents.  For each parent p with token x,
+ * depth d and request q, the logits are z[y] = U[q][d][y] + <E[x], W2[y]>
+ * (§1 Eq. 1); q0 = softmax(z), qT = softmax(z / T).  Each of the k children
+ * gets log q0, log qT, log p-hat and log S(child) = log S(p) + log p-hat
+ * (Eq. 3; §3.5).  parents is a DEVICE array of P ts_parent.
+ * Asynchronous on `stream`.  Arguments checked on the host: null pointers,
+ * sizes, k in [1, min(V, TS_MAX_K)], T >= 0 and finite, workspace size.
+ * Parent fields are checked on the device: a parent with a token, depth or
+ * request out of range gets child_token -1 and NaN values, and nothing out
+ * of bounds is read.
+ * Performance note: parents that share (request, depth) should be adjacent.
+ */
+int32_t ts_expand(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_calib calib,
+                  int32_t k, float T, uint64_t seed, const ts_expand_out* out,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* A draft tree per request, HOST memory, capacity `cap` = N + 1 rows per
+ * request ([R][cap] row-major), node 0 = the root (anchor token, depth 0).
+ * Nodes are in creation order, which is the pop order of Algorithm 1. */
+typedef struct {
+  int32_t R, cap;
+  int32_t* n;          /* [R] materialised nodes, root excluded */
+  int32_t* token;      /* [R][cap] */
+  int32_t* parent;     /* [R][cap], -1 for the root */
+  int32_t* depth;      /* [R][cap] */
+  int32_t* rank;       /* [R][cap] sibling draw index (1-based), 0 for the root */
+  uint64_t* path;      /* [R][cap] structural path id */
+  float* log_surv;     /* [R][cap] log S(node) */
+  float* log_q0;       /* [R][cap] log q0(token | parent), 0 for the root */
+  float* log_qT;       /* [R][cap] log qT(token | parent), NaN at T = 0 and for the root */
+  float* key;          /* [R][cap] key of the slot whose pop created the node */
+} ts_tree;
+
+size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, float T);
+
+/*
+ * ts_build_tree: grow one tree per request by best-first expansion
+ * (§3.2 Algorithm 1): pop the slot with the largest key (ties: shallower
+ * child, then smaller child path id), stop when the popped key is below
+ * log(theta[q]) (theta = 0 never stops, the fixed-budget case of §3.2) or
+ * when N nodes exist; a node at depth D gets no slot; a node re-offers a
+ * slot for its next child until it has K children.  The result equals the
+ * sequential heap of Algorithm 1; it is computed in breadth waves, each one
+ * ts_expand call over all requests' pending parents.
+ * anchor [R], theta [R] are HOST arrays.  out->cap must be >= N + 1 and
+ * out->R == d->R.  Synchronises `stream` once per wave.
+ */
+int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* theta, int32_t N,
+                      int32_t K, ts_calib calib, float T, uint64_t seed, ts_tree* out,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+size_t ts_verify_workspace_size(const ts_drafter* d, int32_t cap, float T);
+
+/*
+ * ts_verify: accept a root path of each request's tree and emit one bonus
+ * (correction) token.  target is a DEVICE array [R][cap][V] of dtype
+ * target_dtype: row i of request q holds the target model's next-token
+ * logits after the root path of node i.
+ *   T == 0: exact match (§3.2 item 3): from the root, descend to the child
+ *           whose token is the target argmax (ties: smallest id); the bonus
+ *           is the argmax at the node where no child matches.
+ *   T  > 0: recursive rejection (§3.3): at each visited node the target
+ *           residual starts at p = softmax(row / T); siblings are tried in
+ *           draw order with q_j = qT restricted to tokens not drawn before j
+ *           and renormalised (qT is recomputed from U, E, W2); child j is
+ *           accepted iff u < p_j(x_j) / q_j(x_j), else
+ *           p_{j+1} = norm(max(p_j - q_j, 0)); the bonus is a Gumbel-max draw
+ *           from the final residual.
+ * tree is the HOST tree from ts_build_tree (tree->R == d->R, tree->cap ==
+ * cap of target).  path_nodes [R][TS_MAX_D], path_len [R], bonus [R] are
+ * HOST outputs (node indices into the tree).  Synchronises `stream`.
+ */
+int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target,
+                  int32_t target_dtype, float T, uint64_t seed, int32_t* path_nodes,
+                  int32_t* path_len, int32_t* bonus, void* workspace, size_t workspace_bytes,
+                  void* stream);
+
+/* Description of the last error on the calling thread ("" if none). */
+const char* ts_last_error(void);
+
+/* Library version string. */
+const char* ts_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TREESPARK_H */

@@ -1,0 +1,283 @@
+"""ctypes binding of libtreespark.so (the C ABI in include/treespark.h).
+
+Argument marshalling only: every step of the draft-tree path runs in the HIP
+kernels behind the C ABI.  PyTorch provides device memory and the stream.
+The binding raises if the shared library is missing; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtreespark.so")
+
+TS_OK, TS_EINVAL, TS_EUNSUPPORTED, TS_EHIP, TS_ENOSPACE, TS_EINTERNAL = 0, -1, -2, -3, -4, -5
+TS_F32, TS_BF16 = 0, 1
+TS_MAX_K, TS_MAX_D = 16, 16
+
+# Every symbol include/treespark.h declares.
+EXPORTED = ("ts_expand_workspace_size", "ts_expand", "ts_build_tree_workspace_size", "ts_build_tree",
+            "ts_verify_workspace_size", "ts_verify", "ts_last_error", "ts_version")
+
+
+class TreeSparkError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"treespark error {code}: {msg}")
+        self.code = code
+
+
+class Drafter(ctypes.Structure):
+    _fields_ = [("U", ctypes.c_void_p), ("E", ctypes.c_void_p), ("W2", ctypes.c_void_p),
+                ("R", ctypes.c_int32), ("D", ctypes.c_int32), ("V", ctypes.c_int32),
+                ("r", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class Calib(ctypes.Structure):
+    _fields_ = [("a", ctypes.c_float), ("b", ctypes.c_float)]
+
+
+class ExpandOut(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_void_p) for name in
+                ("child_token", "child_log_q0", "child_log_qT", "child_log_surv", "slot_key",
+                 "rank_token", "rank_log_q0", "lse0", "lseT", "diag")]
+
+
+class Tree(ctypes.Structure):
+    _fields_ = [("R", ctypes.c_int32), ("cap", ctypes.c_int32)] + [
+        (name, ctypes.c_void_p) for name in
+        ("n", "token", "parent", "depth", "rank", "path", "log_surv", "log_q0", "log_qT", "key")]
+
+
+# ts_parent: 24 bytes
+PARENT_DTYPE = np.dtype([("token", "<i4"), ("depth", "<i4"), ("request", "<i4"),
+                         ("log_surv", "<f4"), ("path", "<u8")])
+assert PARENT_DTYPE.itemsize == 24
+
+_lib = None
+
+
+def lib():
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it first (__graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I32, U64, SZ, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t, ctypes.c_float
+        L.ts_expand_workspace_size.argtypes = [P, I32, I32, F]
+        L.ts_expand_workspace_size.restype = SZ
+        L.ts_expand.argtypes = [P, P, I32, Calib, I32, F, U64, P, P, SZ, P]
+        L.ts_expand.restype = I32
+        L.ts_build_tree_workspace_size.argtypes = [P, I32, I32, F]
+        L.ts_build_tree_workspace_size.restype = SZ
+        L.ts_build_tree.argtypes = [P, P, P, I32, I32, Calib, F, U64, P, P, SZ, P]
+        L.ts_build_tree.restype = I32
+        L.ts_verify_workspace_size.argtypes = [P, I32, F]
+        L.ts_verify_workspace_size.restype = SZ
+        L.ts_verify.argtypes = [P, P, P, I32, F, U64, P, P, P, P, SZ, P]
+        L.ts_verify.restype = I32
+        L.ts_last_error.restype = ctypes.c_char_p
+        L.ts_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(rc):
+    if rc != TS_OK:
+        raise TreeSparkError(rc, lib().ts_last_error().decode())
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(stream):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return TS_BF16
+    if t.dtype == torch.float32:
+        return TS_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+@dataclass
+class DeviceDrafter:
+    """Device tensors U [R][D][V], E [V][r], W2 [V][r] (same dtype, contiguous)."""
+    U: object
+    E: object
+    W2: object
+
+    def __post_init__(self):
+        R, D, V = self.U.shape
+        r = self.E.shape[1]
+        assert self.E.shape == (V, r) and self.W2.shape == (V, r)
+        assert self.U.is_contiguous() and self.E.is_contiguous() and self.W2.is_contiguous()
+        assert self.U.dtype == self.E.dtype == self.W2.dtype
+        self.struct = Drafter(self.U.data_ptr(), self.E.data_ptr(), self.W2.data_ptr(), R, D, V, r,
+                              _dtype_code(self.U))
+
+    @property
+    def R(self):
+        return self.struct.R
+
+    @property
+    def D(self):
+        return self.struct.D
+
+    @property
+    def V(self):
+        return self.struct.V
+
+    @property
+    def r(self):
+        return self.struct.r
+
+    def ref(self):
+        return ctypes.byref(self.struct)
+
+
+def drafter_from_host(dr, device="cuda"):
+    """Copy a synth.Drafter to the device."""
+    torch = _torch()
+
+    def dev(a):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        if a.dtype == np.uint16:
+            t = t.view(torch.bfloat16)
+        return t.to(device)
+
+    return DeviceDrafter(dev(dr.U), dev(dr.E), dev(dr.W2))
+
+
+def parents_to_device(token, depth, request, log_surv, path, device="cuda"):
+    """Pack frontier parents into a device byte tensor of ts_parent records."""
+    torch = _torch()
+    a = np.zeros(len(token), dtype=PARENT_DTYPE)
+    a["token"], a["depth"], a["request"] = token, depth, request
+    a["log_surv"], a["path"] = log_surv, path
+    return torch.from_numpy(a.view(np.uint8).copy()).to(device)
+
+
+def expand_workspace_size(d: DeviceDrafter, P, k, T):
+    return lib().ts_expand_workspace_size(d.ref(), P, k, float(T))
+
+
+def expand(d: DeviceDrafter, parents, P, k, T, seed, calib=(0.67, -0.46), workspace=None,
+           stream=None, outputs=None):
+    """ts_expand.  parents: device uint8 tensor of P ts_parent records.  Returns a dict of
+    device tensors (asynchronous on the stream)."""
+    torch = _torch()
+    dev = parents.device
+    if outputs is None:
+        outputs = dict(
+            child_token=torch.empty((P, k), dtype=torch.int32, device=dev),
+            child_log_q0=torch.empty((P, k), dtype=torch.float32, device=dev),
+            child_log_qT=torch.empty((P, k), dtype=torch.float32, device=dev),
+            child_log_surv=torch.empty((P, k), dtype=torch.float32, device=dev),
+            slot_key=torch.empty((P, k), dtype=torch.float32, device=dev),
+            rank_token=torch.empty((P, k), dtype=torch.int32, device=dev),
+            rank_log_q0=torch.empty((P, k), dtype=torch.float32, device=dev),
+            lse0=torch.empty((P,), dtype=torch.float32, device=dev),
+            lseT=torch.empty((P,), dtype=torch.float32, device=dev),
+            diag=torch.empty((P,), dtype=torch.int32, device=dev))
+    if workspace is None:
+        n = expand_workspace_size(d, P, k, T)
+        workspace = torch.empty((max(n, 1),), dtype=torch.uint8, device=dev)
+    out = ExpandOut(*[outputs[name].data_ptr() if outputs.get(name) is not None else None
+                      for name, _ in ExpandOut._fields_])
+    rc = lib().ts_expand(d.ref(), ctypes.c_void_p(parents.data_ptr()), P, Calib(*calib), k, float(T),
+                         ctypes.c_uint64(seed), ctypes.byref(out), ctypes.c_void_p(workspace.data_ptr()),
+                         workspace.numel(), _stream(stream))
+    _check(rc)
+    outputs["_workspace"] = workspace
+    return outputs
+
+
+@dataclass
+class HostTree:
+    n: np.ndarray
+    token: np.ndarray
+    parent: np.ndarray
+    depth: np.ndarray
+    rank: np.ndarray
+    path: np.ndarray
+    log_surv: np.ndarray
+    log_q0: np.ndarray
+    log_qT: np.ndarray
+    key: np.ndarray
+
+    @classmethod
+    def empty(cls, R, cap):
+        z = lambda dt: np.zeros((R, cap), dtype=dt)
+        return cls(np.zeros(R, np.int32), z(np.int32), z(np.int32), z(np.int32), z(np.int32),
+                   z(np.uint64), z(np.float32), z(np.float32), z(np.float32), z(np.float32))
+
+    @property
+    def R(self):
+        return self.token.shape[0]
+
+    @property
+    def cap(self):
+        return self.token.shape[1]
+
+    def struct(self):
+        return Tree(self.R, self.cap, *[getattr(self, f).ctypes.data for f, _ in Tree._fields_[2:]])
+
+
+def build_tree_workspace_size(d: DeviceDrafter, N, K, T):
+    return lib().ts_build_tree_workspace_size(d.ref(), N, K, float(T))
+
+
+def build_tree(d: DeviceDrafter, anchor, theta, N, K, T, seed, calib=(0.67, -0.46), workspace=None,
+               stream=None, tree=None) -> HostTree:
+    torch = _torch()
+    anchor = np.ascontiguousarray(anchor, dtype=np.int32)
+    theta = np.ascontiguousarray(theta, dtype=np.float32)
+    if tree is None:
+        tree = HostTree.empty(d.R, N + 1)
+    if workspace is None:
+        n = build_tree_workspace_size(d, N, K, T)
+        workspace = torch.empty((max(n, 1),), dtype=torch.uint8, device=d.U.device)
+    s = tree.struct()
+    rc = lib().ts_build_tree(d.ref(), anchor.ctypes.data, theta.ctypes.data, N, K, Calib(*calib),
+                             float(T), ctypes.c_uint64(seed), ctypes.byref(s),
+                             ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream(stream))
+    _check(rc)
+    return tree
+
+
+def verify_workspace_size(d: DeviceDrafter, cap, T):
+    return lib().ts_verify_workspace_size(d.ref(), cap, float(T))
+
+
+def verify(d: DeviceDrafter, tree: HostTree, target, T, seed, workspace=None, stream=None):
+    """ts_verify.  target: device tensor [R][cap][V] (float32 or bfloat16).
+    Returns (path_nodes [R][16], path_len [R], bonus [R]) as numpy arrays."""
+    torch = _torch()
+    R, cap = tree.R, tree.cap
+    assert tuple(target.shape) == (R, cap, d.V) and target.is_contiguous()
+    path = np.zeros((R, TS_MAX_D), np.int32)
+    plen = np.zeros(R, np.int32)
+    bonus = np.zeros(R, np.int32)
+    if workspace is None:
+        n = verify_workspace_size(d, cap, T)
+        workspace = torch.empty((max(n, 1),), dtype=torch.uint8, device=target.device)
+    s = tree.struct()
+    rc = lib().ts_verify(d.ref(), ctypes.byref(s), ctypes.c_void_p(target.data_ptr()), _dtype_code(target),
+                         float(T), ctypes.c_uint64(seed), path.ctypes.data, plen.ctypes.data,
+                         bonus.ctypes.data, ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                         _stream(stream))
+    _check(rc)
+    return path, plen, bonus

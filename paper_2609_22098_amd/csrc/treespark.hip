@@ -1,0 +1,635 @@
+// C ABI of the TreeSpark draft-tree step: argument checks, launch plans,
+// the best-first wave builder and the verification drivers.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "expand_kernels.hpp"
+#include "verify_kernels.hpp"
+
+namespace ts {
+namespace {
+
+thread_local std::string g_last_error;
+
+int32_t fail(int32_t code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+#define TS_HIP(call)                                                                     \
+  do {                                                                                   \
+    hipError_t e_ = (call);                                                              \
+    if (e_ != hipSuccess) return fail(TS_EHIP, "%s: %s", #call, hipGetErrorString(e_));  \
+  } while (0)
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ---------------------------------------------------------------- checks
+
+int32_t check_drafter(const ts_drafter* d) {
+  if (!d) return fail(TS_EINVAL, "drafter is NULL");
+  if (!d->U || !d->E || !d->W2) return fail(TS_EINVAL, "drafter tensor pointer is NULL");
+  if (d->R <= 0 || d->D <= 0 || d->V <= 0 || d->r <= 0)
+    return fail(TS_EINVAL, "drafter sizes must be positive (R=%d D=%d V=%d r=%d)", d->R, d->D, d->V, d->r);
+  if (d->dtype != TS_F32 && d->dtype != TS_BF16) return fail(TS_EINVAL, "unknown dtype %d", d->dtype);
+  if (d->D > TS_MAX_D) return fail(TS_EUNSUPPORTED, "D=%d exceeds %d (4-bit path digits)", d->D, TS_MAX_D);
+  if (d->R >= TS_MAX_R) return fail(TS_EUNSUPPORTED, "R=%d exceeds %d", d->R, TS_MAX_R - 1);
+  const bool ok = d->dtype == TS_BF16 ? (d->r == 32 || d->r == 64 || d->r == 128 || d->r == 256)
+                                      : (d->r == 16 || d->r == 32 || d->r == 64);
+  if (!ok) return fail(TS_EUNSUPPORTED, "rank r=%d not supported for dtype %d", d->r, d->dtype);
+  return TS_OK;
+}
+
+int32_t check_k_T(const ts_drafter* d, int32_t k, float T) {
+  if (k < 1 || k > TS_MAX_K) return fail(k < 1 ? TS_EINVAL : TS_EUNSUPPORTED, "k=%d outside [1, %d]", k, TS_MAX_K);
+  if (k > d->V) return fail(TS_EINVAL, "k=%d exceeds V=%d", k, d->V);
+  if (!(T >= 0.0f) || !std::isfinite(T)) return fail(TS_EINVAL, "T must be finite and >= 0");
+  return TS_OK;
+}
+
+PhiloxKeys philox_keys(uint64_t seed) {
+  PhiloxKeys k;
+  uint32_t a = (uint32_t)seed, b = (uint32_t)(seed >> 32);
+  for (int r = 0; r < 10; ++r) {
+    k.k0[r] = a;
+    k.k1[r] = b;
+    a += 0x9E3779B9u;
+    b += 0xBB67AE85u;
+  }
+  return k;
+}
+
+// ---------------------------------------------------------------- expansion plan
+
+struct Plan {
+  int NB, Vc, S, n_pblocks, wpg, n_pgroups, S8;
+  int ks;
+  bool sample;
+  size_t off_m, off_s0, off_sT, off_zb1, off_zb2, off_zr, off_gb1, off_gb2, off_gr, off_err;
+  size_t bytes;
+};
+
+Plan make_plan(const ts_drafter* d, int P, float T) {
+  Plan pl{};
+  pl.sample = T > 0.0f;
+  pl.ks = d->dtype == TS_BF16 ? d->r / 32 : d->r / 4;
+  const int nb_big = (d->dtype == TS_BF16 && d->r == 256) ? 2 : 4;
+  pl.NB = P >= 512 ? nb_big : 1;
+  pl.n_pblocks = (P + 16 * pl.NB - 1) / (16 * pl.NB);
+  pl.wpg = std::min(4, std::max(1, pl.n_pblocks));
+  pl.n_pgroups = (pl.n_pblocks + pl.wpg - 1) / pl.wpg;
+  // Enough waves to fill 256 CUs several times over, chunks of 256..4096
+  // tokens, and at most 2048 chunks (the merge keeps a 32-bit mask per lane).
+  const int target_waves = 4096;
+  const int s_target = std::max(1, (target_waves + pl.n_pblocks - 1) / pl.n_pblocks);
+  int vc = (d->V + s_target - 1) / s_target;
+  vc = std::max(vc, (d->V + 2047) / 2048);
+  vc = ((vc + 63) / 64) * 64;
+  vc = std::min(std::max(vc, 256), 4096);
+  pl.Vc = vc;
+  pl.S = (d->V + vc - 1) / vc;
+  pl.S8 = ((pl.S + 7) / 8) * 8;
+  const size_t a = align256((size_t)std::max(P, 1) * pl.S * 4);
+  size_t o = 0;
+  pl.off_m = o; o += a;
+  pl.off_s0 = o; o += a;
+  pl.off_zb1 = o; o += a;
+  pl.off_zb2 = o; o += a;
+  pl.off_zr = o; o += a;
+  if (pl.sample) {
+    pl.off_sT = o; o += a;
+    pl.off_gb1 = o; o += a;
+    pl.off_gb2 = o; o += a;
+    pl.off_gr = o; o += a;
+  }
+  pl.off_err = o; o += 256;
+  pl.bytes = o;
+  return pl;
+}
+
+size_t expand_ws_max(const ts_drafter* d, int Pmax, float T) {
+  size_t m = 0;
+  for (int P = 1; P <= Pmax; ++P) m = std::max(m, make_plan(d, P, T).bytes);
+  return m;
+}
+
+template <typename TE, int KS, int NB>
+void launch_eval_nb(const ExpandParams& p, bool sample, dim3 grid, dim3 block, hipStream_t s) {
+  if (sample)
+    hipLaunchKernelGGL((expand_eval_kernel<TE, KS, NB, true>), grid, block, 0, s, p);
+  else
+    hipLaunchKernelGGL((expand_eval_kernel<TE, KS, NB, false>), grid, block, 0, s, p);
+}
+
+template <typename TE, int KS>
+void launch_eval_ks(const ExpandParams& p, int NB, bool sample, dim3 grid, dim3 block, hipStream_t s) {
+  if (NB == 1)
+    launch_eval_nb<TE, KS, 1>(p, sample, grid, block, s);
+  else if (NB == 2)
+    launch_eval_nb<TE, KS, 2>(p, sample, grid, block, s);
+  else
+    launch_eval_nb<TE, KS, 4>(p, sample, grid, block, s);
+}
+
+template <typename TE, int KS>
+void launch_merge_ks(const MergeParams& p, bool sample, dim3 grid, dim3 block, hipStream_t s) {
+  if (sample)
+    hipLaunchKernelGGL((expand_merge_kernel<TE, KS, true>), grid, block, 0, s, p);
+  else
+    hipLaunchKernelGGL((expand_merge_kernel<TE, KS, false>), grid, block, 0, s, p);
+}
+
+void launch_eval(const ts_drafter* d, const ExpandParams& p, const Plan& pl, hipStream_t s) {
+  const dim3 grid(pl.S8 * pl.n_pgroups), block(64 * pl.wpg);
+  if (d->dtype == TS_BF16) {
+    switch (pl.ks) {
+      case 1: launch_eval_ks<uint16_t, 1>(p, pl.NB, pl.sample, grid, block, s); break;
+      case 2: launch_eval_ks<uint16_t, 2>(p, pl.NB, pl.sample, grid, block, s); break;
+      case 4: launch_eval_ks<uint16_t, 4>(p, pl.NB, pl.sample, grid, block, s); break;
+      default: launch_eval_ks<uint16_t, 8>(p, pl.NB, pl.sample, grid, block, s); break;
+    }
+  } else {
+    switch (pl.ks) {
+      case 4: launch_eval_ks<float, 4>(p, pl.NB, pl.sample, grid, block, s); break;
+      case 8: launch_eval_ks<float, 8>(p, pl.NB, pl.sample, grid, block, s); break;
+      default: launch_eval_ks<float, 16>(p, pl.NB, pl.sample, grid, block, s); break;
+    }
+  }
+}
+
+void launch_merge(const ts_drafter* d, const MergeParams& p, const Plan& pl, hipStream_t s) {
+  const dim3 grid((p.P + 3) / 4), block(256);
+  if (d->dtype == TS_BF16) {
+    switch (pl.ks) {
+      case 1: launch_merge_ks<uint16_t, 1>(p, pl.sample, grid, block, s); break;
+      case 2: launch_merge_ks<uint16_t, 2>(p, pl.sample, grid, block, s); break;
+      case 4: launch_merge_ks<uint16_t, 4>(p, pl.sample, grid, block, s); break;
+      default: launch_merge_ks<uint16_t, 8>(p, pl.sample, grid, block, s); break;
+    }
+  } else {
+    switch (pl.ks) {
+      case 4: launch_merge_ks<float, 4>(p, pl.sample, grid, block, s); break;
+      case 8: launch_merge_ks<float, 8>(p, pl.sample, grid, block, s); break;
+      default: launch_merge_ks<float, 16>(p, pl.sample, grid, block, s); break;
+    }
+  }
+}
+
+ExpandParams eval_params(const ts_drafter* d, const ts_parent* parents, int P, float T, uint64_t seed,
+                         const Plan& pl, char* ws, float* z_out) {
+  ExpandParams p{};
+  p.U = d->U; p.E = d->E; p.W2 = d->W2;
+  p.R = d->R; p.D = d->D; p.V = d->V; p.r = d->r;
+  p.parents = parents;
+  p.P = P;
+  p.Vc = pl.Vc; p.S = pl.S;
+  p.n_pblocks = pl.n_pblocks; p.wpg = pl.wpg; p.n_pgroups = pl.n_pgroups;
+  p.cT = T > 0.0f ? kLog2e / T : 0.0f;
+  p.need_T = (T > 0.0f && T != 1.0f) ? 1 : 0;
+  p.keys = philox_keys(seed);
+  p.part_m = reinterpret_cast<float*>(ws + pl.off_m);
+  p.part_s0 = reinterpret_cast<float*>(ws + pl.off_s0);
+  p.part_sT = pl.sample ? reinterpret_cast<float*>(ws + pl.off_sT) : nullptr;
+  p.zb1 = reinterpret_cast<float*>(ws + pl.off_zb1);
+  p.zb2 = reinterpret_cast<float*>(ws + pl.off_zb2);
+  p.zrun = reinterpret_cast<int*>(ws + pl.off_zr);
+  if (pl.sample) {
+    p.gb1 = reinterpret_cast<float*>(ws + pl.off_gb1);
+    p.gb2 = reinterpret_cast<float*>(ws + pl.off_gb2);
+    p.grun = reinterpret_cast<int*>(ws + pl.off_gr);
+  }
+  p.z_out = z_out;
+  return p;
+}
+
+// Both passes of one expansion; all arguments already checked.
+int32_t run_expand(const ts_drafter* d, const ts_parent* parents, int P, ts_calib calib, int k,
+                   float T, uint64_t seed, const ts_expand_out* out, char* ws, hipStream_t s) {
+  if (P == 0) return TS_OK;
+  const Plan pl = make_plan(d, P, T);
+  const ExpandParams ep = eval_params(d, parents, P, T, seed, pl, ws, nullptr);
+  launch_eval(d, ep, pl, s);
+  TS_HIP(hipGetLastError());
+  MergeParams mp{};
+  mp.U = d->U; mp.E = d->E; mp.W2 = d->W2;
+  mp.R = d->R; mp.D = d->D; mp.V = d->V; mp.r = d->r;
+  mp.parents = parents;
+  mp.P = P;
+  mp.Vc = pl.Vc; mp.S = pl.S;
+  mp.K = k;
+  mp.T = T; mp.cT = ep.cT; mp.need_T = ep.need_T;
+  mp.calib_a = calib.a; mp.calib_b = calib.b;
+  mp.keys = ep.keys;
+  mp.part_m = ep.part_m; mp.part_s0 = ep.part_s0; mp.part_sT = ep.part_sT;
+  mp.zb1 = ep.zb1; mp.zb2 = ep.zb2; mp.zrun = ep.zrun;
+  mp.gb1 = ep.gb1; mp.gb2 = ep.gb2; mp.grun = ep.grun;
+  mp.out = *out;
+  launch_merge(d, mp, pl, s);
+  TS_HIP(hipGetLastError());
+  return TS_OK;
+}
+
+// ---------------------------------------------------------------- tree building
+
+struct Slot {
+  float key;
+  int depth;       // depth of the child this slot creates
+  uint64_t path;   // path id of that child
+  int token;
+  float log_surv, log_q0, log_qT;
+  bool evaluated;  // the child has been evaluated (its own slots are known)
+};
+
+// (key desc, child depth asc, child path asc): the pop order of Algorithm 1.
+inline bool slot_before(const Slot& a, const Slot& b) {
+  if (a.key != b.key) return a.key > b.key;
+  if (a.depth != b.depth) return a.depth < b.depth;
+  return a.path < b.path;
+}
+
+struct BuildLayout {
+  size_t off_par, off_tok, off_q0, off_qT, off_ls, off_key, off_exp, bytes;
+  int Pmax;
+};
+
+BuildLayout build_layout(const ts_drafter* d, int N, int K, float T) {
+  BuildLayout b{};
+  b.Pmax = d->R * std::max(N, 1);
+  const size_t pk = align256((size_t)b.Pmax * K * 4);
+  size_t o = 0;
+  b.off_par = o; o += align256((size_t)b.Pmax * sizeof(ts_parent));
+  b.off_tok = o; o += pk;
+  b.off_q0 = o; o += pk;
+  b.off_qT = o; o += pk;
+  b.off_ls = o; o += pk;
+  b.off_key = o; o += pk;
+  b.off_exp = o; o += expand_ws_max(d, b.Pmax, T);
+  b.bytes = o;
+  return b;
+}
+
+struct VerifyLayout {
+  size_t off_rows, off_arg, off_gap, off_items, off_res, off_par, off_z, off_exp, bytes;
+};
+
+VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
+  VerifyLayout v{};
+  size_t o = 0;
+  if (T == 0.0f) {
+    const size_t rows = (size_t)d->R * cap;
+    v.off_rows = o; o += align256(rows * 4);
+    v.off_arg = o; o += align256(rows * 4);
+    v.off_gap = o; o += align256(rows * 4);
+  } else {
+    v.off_items = o; o += align256((size_t)d->R * sizeof(VerifyItem));
+    v.off_res = o; o += align256((size_t)d->R * sizeof(VerifyResult));
+    v.off_par = o; o += align256((size_t)d->R * sizeof(ts_parent));
+    v.off_z = o; o += align256((size_t)d->R * d->V * 4);
+    v.off_exp = o; o += expand_ws_max(d, d->R, T);
+  }
+  v.bytes = o;
+  return v;
+}
+
+}  // namespace
+}  // namespace ts
+
+using namespace ts;
+
+extern "C" {
+
+const char* ts_last_error(void) { return g_last_error.c_str(); }
+
+const char* ts_version(void) { return "treespark-mi355x 0.1 (gfx950)"; }
+
+size_t ts_expand_workspace_size(const ts_drafter* d, int32_t P, int32_t k, float T) {
+  (void)k;
+  if (check_drafter(d) != TS_OK || P <= 0) return 0;
+  return make_plan(d, P, T).bytes;
+}
+
+int32_t ts_expand(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_calib calib,
+                  int32_t k, float T, uint64_t seed, const ts_expand_out* out, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  int32_t rc = check_drafter(d);
+  if (rc != TS_OK) return rc;
+  if ((rc = check_k_T(d, k, T)) != TS_OK) return rc;
+  if (P < 0) return fail(TS_EINVAL, "P=%d is negative", P);
+  if (P == 0) return TS_OK;
+  if (!parents) return fail(TS_EINVAL, "parents is NULL");
+  if (!out || !out->child_token || !out->child_log_q0 || !out->child_log_surv || !out->slot_key)
+    return fail(TS_EINVAL, "a required output pointer is NULL");
+  if (!std::isfinite(calib.a) || !std::isfinite(calib.b)) return fail(TS_EINVAL, "calibration must be finite");
+  const size_t need = make_plan(d, P, T).bytes;
+  if (!workspace || workspace_bytes < need)
+    return fail(TS_ENOSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
+  return run_expand(d, parents, P, calib, k, T, seed, out, static_cast<char*>(workspace),
+                    static_cast<hipStream_t>(stream));
+}
+
+size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, float T) {
+  if (check_drafter(d) != TS_OK || N < 0 || K < 1 || K > TS_MAX_K) return 0;
+  return build_layout(d, N, K, T).bytes;
+}
+
+int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* theta, int32_t N,
+                      int32_t K, ts_calib calib, float T, uint64_t seed, ts_tree* out,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  int32_t rc = check_drafter(d);
+  if (rc != TS_OK) return rc;
+  if ((rc = check_k_T(d, K, T)) != TS_OK) return rc;
+  if (N < 0) return fail(TS_EINVAL, "N=%d is negative", N);
+  if (!anchor || !theta || !out) return fail(TS_EINVAL, "anchor, theta or out is NULL");
+  if (!out->n || !out->token || !out->parent || !out->depth || !out->rank || !out->path ||
+      !out->log_surv || !out->log_q0 || !out->log_qT || !out->key)
+    return fail(TS_EINVAL, "a tree array is NULL");
+  if (out->R != d->R || out->cap < N + 1) return fail(TS_EINVAL, "tree has R=%d cap=%d, need R=%d cap>=%d", out->R, out->cap, d->R, N + 1);
+  if (!std::isfinite(calib.a) || !std::isfinite(calib.b)) return fail(TS_EINVAL, "calibration must be finite");
+  const int R = d->R;
+  for (int q = 0; q < R; ++q) {
+    if (anchor[q] < 0 || anchor[q] >= d->V) return fail(TS_EINVAL, "anchor[%d]=%d outside [0, V)", q, anchor[q]);
+    if (!(theta[q] >= 0.0f) || !std::isfinite(theta[q])) return fail(TS_EINVAL, "theta[%d] must be finite and >= 0", q);
+  }
+  const BuildLayout bl = build_layout(d, N, K, T);
+  if (!workspace || workspace_bytes < bl.bytes)
+    return fail(TS_ENOSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, bl.bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  ts_parent* dpar = reinterpret_cast<ts_parent*>(ws + bl.off_par);
+  ts_expand_out eo{};
+  eo.child_token = reinterpret_cast<int32_t*>(ws + bl.off_tok);
+  eo.child_log_q0 = reinterpret_cast<float*>(ws + bl.off_q0);
+  eo.child_log_qT = reinterpret_cast<float*>(ws + bl.off_qT);
+  eo.child_log_surv = reinterpret_cast<float*>(ws + bl.off_ls);
+  eo.slot_key = reinterpret_cast<float*>(ws + bl.off_key);
+
+  std::vector<float> log_theta(R);
+  for (int q = 0; q < R; ++q) log_theta[q] = theta[q] > 0.0f ? logf(theta[q]) : -INFINITY;
+  std::vector<std::vector<Slot>> known(R);
+  std::vector<ts_parent> frontier;
+  if (N > 0)
+    for (int q = 0; q < R; ++q) frontier.push_back(ts_parent{anchor[q], 0, q, 0.0f, 0});
+  std::vector<int32_t> h_tok;
+  std::vector<float> h_q0, h_qT, h_ls, h_key;
+  while (!frontier.empty()) {
+    const int P = (int)frontier.size();
+    TS_HIP(hipMemcpyAsync(dpar, frontier.data(), P * sizeof(ts_parent), hipMemcpyHostToDevice, s));
+    rc = run_expand(d, dpar, P, calib, K, T, seed, &eo, ws + bl.off_exp, s);
+    if (rc != TS_OK) return rc;
+    const size_t nk = (size_t)P * K;
+    h_tok.resize(nk); h_q0.resize(nk); h_qT.resize(nk); h_ls.resize(nk); h_key.resize(nk);
+    TS_HIP(hipMemcpyAsync(h_tok.data(), eo.child_token, nk * 4, hipMemcpyDeviceToHost, s));
+    TS_HIP(hipMemcpyAsync(h_q0.data(), eo.child_log_q0, nk * 4, hipMemcpyDeviceToHost, s));
+    TS_HIP(hipMemcpyAsync(h_qT.data(), eo.child_log_qT, nk * 4, hipMemcpyDeviceToHost, s));
+    TS_HIP(hipMemcpyAsync(h_ls.data(), eo.child_log_surv, nk * 4, hipMemcpyDeviceToHost, s));
+    TS_HIP(hipMemcpyAsync(h_key.data(), eo.slot_key, nk * 4, hipMemcpyDeviceToHost, s));
+    TS_HIP(hipStreamSynchronize(s));
+    for (int i = 0; i < P; ++i) {
+      const ts_parent& par = frontier[i];
+      for (int j = 0; j < K; ++j) {
+        const size_t o = (size_t)i * K + j;
+        Slot sl;
+        sl.key = h_key[o];
+        sl.depth = par.depth + 1;
+        sl.path = par.path | ((uint64_t)j << (4 * par.depth));
+        sl.token = h_tok[o];
+        sl.log_surv = h_ls[o];
+        sl.log_q0 = h_q0[o];
+        sl.log_qT = h_qT[o];
+        sl.evaluated = false;
+        known[par.request].push_back(sl);
+      }
+    }
+    // Next wave: children of slots that rank strictly above the N-th known slot
+    // (or all, if fewer than N are known), with key >= log(theta) and depth < D.
+    // Any slot of the final top-N descends from such a child, because a slot's
+    // key never exceeds the key of the slot whose pop created it.
+    frontier.clear();
+    for (int q = 0; q < R; ++q) {
+      std::vector<Slot>& ks = known[q];
+      const bool have_n = (int)ks.size() >= N;
+      Slot nth{};
+      if (have_n && N > 0) {
+        std::vector<Slot> tmp(ks);
+        std::nth_element(tmp.begin(), tmp.begin() + (N - 1), tmp.end(), slot_before);
+        nth = tmp[N - 1];
+      }
+      const size_t first = frontier.size();
+      for (Slot& sl : ks) {
+        if (sl.evaluated || sl.depth >= d->D || sl.key < log_theta[q]) continue;
+        if (have_n && !slot_before(sl, nth)) continue;
+        sl.evaluated = true;
+        frontier.push_back(ts_parent{sl.token, sl.depth, q, sl.log_surv, sl.path});
+      }
+      std::sort(frontier.begin() + first, frontier.end(),
+                [](const ts_parent& a, const ts_parent& b) { return a.depth < b.depth; });
+    }
+  }
+  // The tree: the first N known slots in pop order, stopping at a key below log(theta).
+  const int cap = out->cap;
+  for (int q = 0; q < R; ++q) {
+    std::vector<Slot>& ks = known[q];
+    std::sort(ks.begin(), ks.end(), slot_before);
+    const size_t b = (size_t)q * cap;
+    out->token[b] = anchor[q];
+    out->parent[b] = -1;
+    out->depth[b] = 0;
+    out->rank[b] = 0;
+    out->path[b] = 0;
+    out->log_surv[b] = 0.0f;
+    out->log_q0[b] = 0.0f;
+    out->log_qT[b] = NAN;
+    out->key[b] = 0.0f;
+    std::unordered_map<uint64_t, int> node_of[TS_MAX_D + 1];
+    node_of[0][0] = 0;
+    int n = 0;
+    for (const Slot& sl : ks) {
+      if (n >= N || sl.key < log_theta[q]) break;
+      const int pd = sl.depth - 1;
+      const uint64_t ppath = sl.path & ((pd == 0) ? 0ull : ((1ull << (4 * pd)) - 1ull));
+      const auto it = node_of[pd].find(ppath);
+      if (it == node_of[pd].end()) return fail(TS_EINTERNAL, "request %d: slot without a materialised parent", q);
+      const int c = ++n;
+      out->token[b + c] = sl.token;
+      out->parent[b + c] = it->second;
+      out->depth[b + c] = sl.depth;
+      out->rank[b + c] = (int)((sl.path >> (4 * pd)) & 15ull) + 1;
+      out->path[b + c] = sl.path;
+      out->log_surv[b + c] = sl.log_surv;
+      out->log_q0[b + c] = sl.log_q0;
+      out->log_qT[b + c] = sl.log_qT;
+      out->key[b + c] = sl.key;
+      node_of[sl.depth][sl.path] = c;
+    }
+    out->n[q] = n;
+  }
+  return TS_OK;
+}
+
+size_t ts_verify_workspace_size(const ts_drafter* d, int32_t cap, float T) {
+  if (check_drafter(d) != TS_OK || cap < 1 || !(T >= 0.0f)) return 0;
+  return verify_layout(d, cap, T).bytes;
+}
+
+int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, int32_t target_dtype,
+                  float T, uint64_t seed, int32_t* path_nodes, int32_t* path_len, int32_t* bonus,
+                  void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  int32_t rc = check_drafter(d);
+  if (rc != TS_OK) return rc;
+  if (!tree || !target || !path_nodes || !path_len || !bonus)
+    return fail(TS_EINVAL, "tree, target or an output is NULL");
+  if (!tree->n || !tree->token || !tree->parent || !tree->depth || !tree->path)
+    return fail(TS_EINVAL, "a tree array is NULL");
+  if (tree->R != d->R || tree->cap < 1) return fail(TS_EINVAL, "tree R=%d cap=%d does not match R=%d", tree->R, tree->cap, d->R);
+  if (target_dtype != TS_F32 && target_dtype != TS_BF16) return fail(TS_EINVAL, "unknown target dtype %d", target_dtype);
+  if (!(T >= 0.0f) || !std::isfinite(T)) return fail(TS_EINVAL, "T must be finite and >= 0");
+  const int R = d->R, cap = tree->cap, V = d->V;
+  for (int q = 0; q < R; ++q) {
+    const int n = tree->n[q];
+    if (n < 0 || n >= cap) return fail(TS_EINVAL, "tree n[%d]=%d outside [0, cap)", q, n);
+    for (int i = 1; i <= n; ++i) {
+      const size_t o = (size_t)q * cap + i;
+      const int pa = tree->parent[o];
+      if (pa < 0 || pa >= i || tree->token[o] < 0 || tree->token[o] >= V ||
+          tree->depth[o] != tree->depth[(size_t)q * cap + pa] + 1 || tree->depth[o] > d->D)
+        return fail(TS_EINVAL, "tree of request %d is malformed at node %d", q, i);
+    }
+    if (tree->token[(size_t)q * cap] < 0 || tree->token[(size_t)q * cap] >= V)
+      return fail(TS_EINVAL, "root token of request %d outside [0, V)", q);
+  }
+  const VerifyLayout vl = verify_layout(d, cap, T);
+  if (!workspace || workspace_bytes < vl.bytes)
+    return fail(TS_ENOSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, vl.bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+
+  // children of every node in creation order (= draw order)
+  std::vector<std::vector<std::vector<int>>> kids(R);
+  for (int q = 0; q < R; ++q) {
+    kids[q].assign(tree->n[q] + 1, {});
+    for (int i = 1; i <= tree->n[q]; ++i) kids[q][tree->parent[(size_t)q * cap + i]].push_back(i);
+  }
+  for (int q = 0; q < R; ++q) path_len[q] = 0;
+
+  if (T == 0.0f) {
+    std::vector<int> rows;
+    for (int q = 0; q < R; ++q)
+      for (int i = 0; i <= tree->n[q]; ++i) rows.push_back(q * cap + i);
+    const int nrows = (int)rows.size();
+    int* drows = reinterpret_cast<int*>(ws + vl.off_rows);
+    int* darg = reinterpret_cast<int*>(ws + vl.off_arg);
+    float* dgap = reinterpret_cast<float*>(ws + vl.off_gap);
+    TS_HIP(hipMemcpyAsync(drows, rows.data(), nrows * 4, hipMemcpyHostToDevice, s));
+    if (target_dtype == TS_BF16)
+      hipLaunchKernelGGL((verify_argmax_kernel<uint16_t>), dim3(nrows), dim3(kVerifyThreads), 0, s,
+                         static_cast<const uint16_t*>(target), V, drows, nrows, darg, dgap);
+    else
+      hipLaunchKernelGGL((verify_argmax_kernel<float>), dim3(nrows), dim3(kVerifyThreads), 0, s,
+                         static_cast<const float*>(target), V, drows, nrows, darg, dgap);
+    TS_HIP(hipGetLastError());
+    std::vector<int> arg(nrows);
+    TS_HIP(hipMemcpyAsync(arg.data(), darg, nrows * 4, hipMemcpyDeviceToHost, s));
+    TS_HIP(hipStreamSynchronize(s));
+    int base = 0;
+    for (int q = 0; q < R; ++q) {
+      int cur = 0, len = 0;
+      for (;;) {
+        const int gtok = arg[base + cur];
+        int next = -1;
+        for (int c : kids[q][cur])
+          if (tree->token[(size_t)q * cap + c] == gtok) { next = c; break; }
+        if (next < 0 || len >= TS_MAX_D) { bonus[q] = gtok; break; }
+        path_nodes[(size_t)q * TS_MAX_D + len++] = next;
+        cur = next;
+      }
+      path_len[q] = len;
+      base += tree->n[q] + 1;
+    }
+    return TS_OK;
+  }
+
+  // T > 0: one level of the walk per iteration, batched over the requests still walking.
+  VerifyItem* ditems = reinterpret_cast<VerifyItem*>(ws + vl.off_items);
+  VerifyResult* dres = reinterpret_cast<VerifyResult*>(ws + vl.off_res);
+  ts_parent* dpar = reinterpret_cast<ts_parent*>(ws + vl.off_par);
+  float* zbuf = reinterpret_cast<float*>(ws + vl.off_z);
+  const PhiloxKeys keys = philox_keys(seed);
+  std::vector<int> cur(R, 0), active(R);
+  for (int q = 0; q < R; ++q) active[q] = q;
+  std::vector<VerifyItem> items;
+  std::vector<ts_parent> zpar;
+  std::vector<VerifyResult> res;
+  while (!active.empty()) {
+    items.clear();
+    zpar.clear();
+    for (int q : active) {
+      const size_t o = (size_t)q * cap + cur[q];
+      VerifyItem it{};
+      it.request = q;
+      it.node = cur[q];
+      it.depth = tree->depth[o];
+      it.path = tree->path[o];
+      const std::vector<int>& ch = kids[q][cur[q]];
+      it.m = (int)std::min<size_t>(ch.size(), TS_MAX_K);
+      for (int j = 0; j < it.m; ++j) it.child_tok[j] = tree->token[(size_t)q * cap + ch[j]];
+      it.zrow = -1;
+      if (it.m > 0) {
+        it.zrow = (int)zpar.size();
+        zpar.push_back(ts_parent{tree->token[o], tree->depth[o], q, 0.0f, tree->path[o]});
+      }
+      items.push_back(it);
+    }
+    const int ni = (int)items.size();
+    if (!zpar.empty()) {
+      const int P = (int)zpar.size();
+      TS_HIP(hipMemcpyAsync(dpar, zpar.data(), P * sizeof(ts_parent), hipMemcpyHostToDevice, s));
+      const Plan pl = make_plan(d, P, T);
+      const ExpandParams ep = eval_params(d, dpar, P, T, seed, pl, ws + vl.off_exp, zbuf);
+      launch_eval(d, ep, pl, s);
+      TS_HIP(hipGetLastError());
+    }
+    TS_HIP(hipMemcpyAsync(ditems, items.data(), ni * sizeof(VerifyItem), hipMemcpyHostToDevice, s));
+    if (target_dtype == TS_BF16)
+      hipLaunchKernelGGL((verify_stage_kernel<uint16_t>), dim3(ni), dim3(kVerifyThreads), 0, s,
+                         static_cast<const uint16_t*>(target), cap, V, ditems, ni, zbuf, T, keys, dres);
+    else
+      hipLaunchKernelGGL((verify_stage_kernel<float>), dim3(ni), dim3(kVerifyThreads), 0, s,
+                         static_cast<const float*>(target), cap, V, ditems, ni, zbuf, T, keys, dres);
+    TS_HIP(hipGetLastError());
+    res.resize(ni);
+    TS_HIP(hipMemcpyAsync(res.data(), dres, ni * sizeof(VerifyResult), hipMemcpyDeviceToHost, s));
+    TS_HIP(hipStreamSynchronize(s));
+    std::vector<int> next;
+    for (int i = 0; i < ni; ++i) {
+      const int q = items[i].request;
+      if (res[i].accepted > 0 && path_len[q] < TS_MAX_D) {
+        const int c = kids[q][cur[q]][res[i].accepted - 1];
+        path_nodes[(size_t)q * TS_MAX_D + path_len[q]++] = c;
+        cur[q] = c;
+        next.push_back(q);
+      } else {
+        bonus[q] = res[i].bonus;
+      }
+    }
+    active.swap(next);
+  }
+  return TS_OK;
+}
+
+}  // extern "C"

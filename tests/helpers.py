@@ -1,0 +1,151 @@
+"""Comparison helpers: GPU results against the oracle, with near-tie accounting.
+
+Parity rules (from the benchmark spec of the method's contract):
+  - token ids, tree topology and accepted paths are bit-exact wherever the
+    oracle's competing scores differ by more than TIE * max(1, |score|);
+    positions after the first near-tie are not compared, and near-ties are
+    counted;
+  - log-probabilities and survival values agree within 1e-5 relative
+    (fp32 inputs) or 2e-3 (bf16 inputs), relative to max(1, |x|).
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from oracle import oracle as o
+
+TIE = 1e-5
+
+
+def value_tol(dtype: str) -> float:
+    return 1e-5 if dtype == "f32" else 2e-3
+
+
+def close(a, b, tol) -> bool:
+    a, b = float(a), float(b)
+    if math.isnan(b):
+        return math.isnan(a)
+    if math.isinf(b):
+        return a == b
+    return abs(a - b) <= tol * max(1.0, abs(b))
+
+
+@dataclass
+class Tally:
+    compared: int = 0
+    near_ties: int = 0
+    max_err: float = 0.0
+    failures: list = field(default_factory=list)
+
+    def err(self, a, b):
+        a, b = float(a), float(b)
+        if math.isfinite(b):
+            self.max_err = max(self.max_err, abs(a - b) / max(1.0, abs(b)))
+
+    def check(self, ok, msg):
+        if not ok:
+            self.failures.append(msg)
+
+
+def first_tie(vals, upto):
+    """Index of the first i < upto with vals[i] - vals[i+1] <= TIE*max(1,|vals[i]|), else upto."""
+    for i in range(upto):
+        if not np.isfinite(vals[i + 1]):
+            continue
+        if vals[i] - vals[i + 1] <= TIE * max(1.0, abs(vals[i])):
+            return i
+    return upto
+
+
+def compare_parent(gpu: dict, i: int, ev: o.Eval, log_surv_p: float, T: float, K: int, dtype: str,
+                   tally: Tally, a=0.67, b=-0.46, tag=""):
+    """Compare ts_expand outputs of parent row i with the oracle evaluation ev."""
+    tol = value_tol(dtype)
+    tally.compared += 1
+    tally.err(gpu["lse0"][i], ev.lse0)
+    tally.check(close(gpu["lse0"][i], ev.lse0, tol), f"{tag} lse0 {gpu['lse0'][i]} vs {ev.lse0}")
+    # greedy order pi
+    t_pi = first_tie(ev.pi_z, K)
+    if t_pi < K:
+        tally.near_ties += 1
+    tally.check(list(gpu["rank_token"][i][:t_pi]) == list(ev.pi[:t_pi]),
+                f"{tag} rank tokens {list(gpu['rank_token'][i])} vs {list(ev.pi)} (first tie {t_pi})")
+    for j in range(t_pi):
+        lq = ev.pi_z[j] - ev.lse0
+        tally.err(gpu["rank_log_q0"][i][j], lq)
+        tally.check(close(gpu["rank_log_q0"][i][j], lq, tol), f"{tag} rank log q0[{j}]")
+    if T == 0:
+        upto = t_pi
+        for j in range(upto):
+            lq = ev.pi_z[j] - ev.lse0
+            ls = log_surv_p + o.log_phat(lq, a, b)
+            tally.check(gpu["child_token"][i][j] == ev.pi[j], f"{tag} child token {j}")
+            for name, want in (("child_log_q0", lq), ("child_log_surv", ls), ("slot_key", ls)):
+                tally.err(gpu[name][i][j], want)
+                tally.check(close(gpu[name][i][j], want, tol), f"{tag} {name}[{j}] {gpu[name][i][j]} vs {want}")
+        return
+    tally.err(gpu["lseT"][i], ev.lseT)
+    tally.check(close(gpu["lseT"][i], ev.lseT, tol), f"{tag} lseT {gpu['lseT'][i]} vs {ev.lseT}")
+    t_sig = first_tie(ev.sigma_g, K)
+    if t_sig < K:
+        tally.near_ties += 1
+    tally.check(list(gpu["child_token"][i][:t_sig]) == list(ev.sigma[:t_sig]),
+                f"{tag} drawn tokens {list(gpu['child_token'][i])} vs {list(ev.sigma)} (first tie {t_sig})")
+    for j in range(t_sig):
+        lq = ev.sigma_z[j] - ev.lse0
+        lqT = ev.sigma_z[j] / T - ev.lseT
+        ls = log_surv_p + o.log_phat(lq, a, b)
+        bound = next(k for k in range(K) if ev.pi[k] not in list(ev.sigma[:j]))
+        key = log_surv_p + o.log_phat(ev.pi_z[bound] - ev.lse0, a, b)
+        for name, want in (("child_log_q0", lq), ("child_log_qT", lqT), ("child_log_surv", ls),
+                           ("slot_key", key)):
+            tally.err(gpu[name][i][j], want)
+            tally.check(close(gpu[name][i][j], want, tol), f"{tag} {name}[{j}] {gpu[name][i][j]} vs {want}")
+
+
+def tree_compare_limit(ref: o.Tree, theta: float):
+    """Number of leading nodes of the oracle tree that no near-tie can change, and the tie count."""
+    lt = math.log(theta) if theta > 0 else -math.inf
+    limit = ref.n + 1
+    ties = 0
+    for c in range(1, ref.n + 1):
+        tied = False
+        if ref.margin[c] <= TIE * max(1.0, abs(ref.key[c])):
+            tied = True
+        p = ref.parent[c]
+        if np.isfinite(ref.eval_gap[p]) and ref.eval_gap[p] <= TIE:
+            tied = True
+        if math.isfinite(lt) and abs(ref.key[c] - lt) <= TIE * max(1.0, abs(lt)):
+            tied = True
+        if tied:
+            ties += 1
+            limit = min(limit, c)
+    if math.isfinite(lt) and np.isfinite(ref.stop_key) and abs(ref.stop_key - lt) <= TIE * max(1.0, abs(lt)):
+        ties += 1
+    return limit, ties
+
+
+def compare_tree(gpu_tree, q: int, ref: o.Tree, theta: float, dtype: str, tally: Tally, tag=""):
+    tol = value_tol(dtype)
+    limit, ties = tree_compare_limit(ref, theta)
+    tally.near_ties += ties
+    tally.compared += 1
+    n = int(gpu_tree.n[q])
+    if ties == 0:
+        tally.check(n == ref.n, f"{tag} tree size {n} vs {ref.n}")
+    upto = min(limit, n + 1, ref.n + 1)
+    for name in ("token", "parent", "depth", "rank"):
+        g = list(getattr(gpu_tree, name)[q][:upto])
+        r = list(getattr(ref, name)[:upto])
+        tally.check(g == r, f"{tag} {name} {g} vs {r}")
+    tally.check([int(x) for x in gpu_tree.path[q][:upto]] == [int(x) for x in ref.path[:upto]], f"{tag} path")
+    for name in ("log_surv", "log_q0", "key"):
+        for c in range(1, upto):
+            want = getattr(ref, name)[c]
+            got = getattr(gpu_tree, name)[q][c]
+            tally.err(got, want)
+            tally.check(close(got, want, tol), f"{tag} {name}[{c}] {got} vs {want}")
+    return upto

@@ -1,0 +1,123 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects bad
+arguments on the host before touching a GPU (no compute calls here)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2609_22098_amd import binding as b
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x1000  # a non-null address that is never dereferenced
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "treespark.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:const char\*|size_t|int32_t)\s+(ts_\w+)\s*\(", txt, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    declared = _declared()
+    assert len(declared) == 8
+    assert sorted(b.EXPORTED) == declared
+    L = b.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+    assert b"gfx950" in L.ts_version()
+
+
+def _drafter(R=1, D=4, V=1000, r=16, dtype=b.TS_F32, null=False):
+    return b.Drafter(None if null else FAKE, FAKE, FAKE, R, D, V, r, dtype)
+
+
+def _expand(d, P=4, k=2, T=0.0, ws_bytes=1 << 30, out=True, parents=FAKE):
+    o = b.ExpandOut(FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, None, None) if out else None
+    return b.lib().ts_expand(ctypes.byref(d), parents, P, b.Calib(0.67, -0.46), k, T, 0,
+                             ctypes.byref(o) if o else None, FAKE, ws_bytes, None)
+
+
+def test_expand_rejects_bad_arguments():
+    L = b.lib()
+    assert _expand(_drafter(null=True)) == b.TS_EINVAL
+    assert b"NULL" in L.ts_last_error()
+    assert _expand(_drafter(V=0)) == b.TS_EINVAL
+    assert _expand(_drafter(D=17)) == b.TS_EUNSUPPORTED
+    assert _expand(_drafter(r=24)) == b.TS_EUNSUPPORTED
+    assert _expand(_drafter(r=16, dtype=b.TS_BF16)) == b.TS_EUNSUPPORTED
+    assert _expand(_drafter(dtype=7)) == b.TS_EINVAL
+    assert _expand(_drafter(), k=0) == b.TS_EINVAL
+    assert _expand(_drafter(), k=17) == b.TS_EUNSUPPORTED
+    assert _expand(_drafter(V=3), k=4) == b.TS_EINVAL
+    assert _expand(_drafter(), T=-1.0) == b.TS_EINVAL
+    assert _expand(_drafter(), T=float("inf")) == b.TS_EINVAL
+    assert _expand(_drafter(), T=float("nan")) == b.TS_EINVAL
+    assert _expand(_drafter(), P=-1) == b.TS_EINVAL
+    assert _expand(_drafter(), parents=None) == b.TS_EINVAL
+    assert _expand(_drafter(), out=False) == b.TS_EINVAL
+    assert _expand(_drafter(), ws_bytes=16) == b.TS_ENOSPACE
+    # an empty frontier is valid and launches nothing
+    assert _expand(_drafter(), P=0) == b.TS_OK
+
+
+def test_workspace_sizes_are_monotone_and_positive():
+    d = _drafter(V=151936, r=64, dtype=b.TS_BF16, D=16, R=64)
+    L = b.lib()
+    s0 = L.ts_expand_workspace_size(ctypes.byref(d), 2048, 8, 0.0)
+    s1 = L.ts_expand_workspace_size(ctypes.byref(d), 2048, 8, 0.7)
+    assert 0 < s0 < s1 < 64 << 20
+    assert L.ts_expand_workspace_size(ctypes.byref(d), 0, 8, 0.0) == 0
+    assert L.ts_build_tree_workspace_size(ctypes.byref(d), 64, 8, 0.7) > s1
+    assert L.ts_verify_workspace_size(ctypes.byref(d), 65, 0.7) >= 64 * 151936 * 4
+
+
+def test_build_tree_rejects_bad_arguments():
+    L = b.lib()
+    d = _drafter(R=2)
+    tree = b.HostTree.empty(2, 9)
+    s = tree.struct()
+    anchor = np.array([1, 2], np.int32)
+    theta = np.array([0.0, 0.1], np.float32)
+
+    def call(anchor=anchor, theta=theta, N=8, K=2, T=0.0, ws=1 << 30, st=s):
+        return L.ts_build_tree(ctypes.byref(d), anchor.ctypes.data, theta.ctypes.data, N, K,
+                               b.Calib(0.67, -0.46), T, 0, ctypes.byref(st), FAKE, ws, None)
+
+    assert call(anchor=np.array([1, 5000], np.int32)) == b.TS_EINVAL
+    assert call(theta=np.array([0.0, -0.1], np.float32)) == b.TS_EINVAL
+    assert call(N=9) == b.TS_EINVAL       # cap 9 < N + 1
+    assert call(N=-1) == b.TS_EINVAL
+    assert call(K=0) == b.TS_EINVAL
+    assert call(ws=8) == b.TS_ENOSPACE
+    bad = b.HostTree.empty(3, 9).struct()
+    assert call(st=bad) == b.TS_EINVAL
+
+
+def test_verify_rejects_malformed_trees():
+    L = b.lib()
+    d = _drafter(R=1, D=4, V=100)
+    tree = b.HostTree.empty(1, 5)
+    tree.n[0] = 2
+    tree.token[0, :3] = [1, 2, 3]
+    tree.parent[0, :3] = [-1, 0, 0]
+    tree.depth[0, :3] = [0, 1, 1]
+    path = np.zeros((1, 16), np.int32); plen = np.zeros(1, np.int32); bonus = np.zeros(1, np.int32)
+
+    def call(T=0.0, ws=1 << 30, tdt=b.TS_F32):
+        s = tree.struct()
+        return L.ts_verify(ctypes.byref(d), ctypes.byref(s), FAKE, tdt, T, 0, path.ctypes.data,
+                           plen.ctypes.data, bonus.ctypes.data, FAKE, ws, None)
+
+    tree.parent[0, 2] = 2  # a node cannot be its own parent
+    assert call() == b.TS_EINVAL
+    tree.parent[0, 2] = 0
+    tree.depth[0, 2] = 2   # depth must be the parent's + 1
+    assert call() == b.TS_EINVAL
+    tree.depth[0, 2] = 1
+    tree.token[0, 1] = 100  # token outside [0, V)
+    assert call() == b.TS_EINVAL
+    tree.token[0, 1] = 2
+    assert call(tdt=9) == b.TS_EINVAL
+    assert call(T=-0.5) == b.TS_EINVAL
+    assert call(ws=4) == b.TS_ENOSPACE

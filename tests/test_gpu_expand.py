@@ -1,0 +1,129 @@
+"""GPU parity of ts_expand against the oracle, element by element."""
+import numpy as np
+import pytest
+
+from oracle import oracle as o
+from paper_2609_22098_amd import synth
+from helpers import Tally, compare_parent
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2609_22098_amd import binding
+    binding.lib()
+    return t
+
+
+def _expand_and_compare(torch, dr, fr, K, T, seed, sample=None, calib=(0.67, -0.46), tag=""):
+    from paper_2609_22098_amd import binding
+    dd = binding.drafter_from_host(dr)
+    P = len(fr["token"])
+    parents = binding.parents_to_device(fr["token"], fr["depth"], fr["request"], fr["log_surv"], fr["path"])
+    out = binding.expand(dd, parents, P, K, T, seed, calib=calib)
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in out.items() if not k.startswith("_")}
+    assert np.all(g["diag"] == 0), "recomputed candidate runs differ from the streaming pass"
+    om = o.Model(dr.U32, dr.E32, dr.W2_32)
+    idx = range(P) if sample is None else sample
+    tally = Tally()
+    for i in idx:
+        ev = o.eval_node(om, int(fr["request"][i]), int(fr["token"][i]), int(fr["depth"][i]),
+                         int(fr["path"][i]), T, seed, K, want_z=False)
+        compare_parent(g, i, ev, float(fr["log_surv"][i]), T, K, dr.dtype, tally, a=calib[0], b=calib[1],
+                       tag=f"{tag} parent {i}")
+    print(f"{tag}: compared {tally.compared} parents, near-ties {tally.near_ties}, "
+          f"max rel err {tally.max_err:.2e}")
+    assert not tally.failures, tally.failures[:5]
+    return g
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0, 0.6])
+def test_tiny_workload_all_parents(torch, T):
+    """V=4096, D=8, r=16, fp32 (the tiny oracle workload): every parent of a 3-per-depth frontier."""
+    dr = synth.make_workload_drafter(0, seed=0)
+    fr = synth.make_frontier(dr, per_depth=3, seed=1)
+    _expand_and_compare(torch, dr, fr, 4, T, seed=0, tag=f"tiny T={T}")
+
+
+@pytest.mark.parametrize("dtype,r,V", [("f32", 16, 1000), ("f32", 32, 4097), ("bf16", 32, 4097),
+                                       ("bf16", 64, 100), ("f32", 64, 77), ("bf16", 128, 3000)])
+@pytest.mark.parametrize("T", [0.0, 0.8])
+def test_ragged_shapes(torch, dtype, r, V, T):
+    """Vocabularies that are not multiples of the 16/64-token tiles, tiny vocabularies and a
+    ragged parent count (37)."""
+    dr = synth.make_drafter(V, 5, r, R=3, dtype=dtype, u_sigma=2.0, planted=None, zipf=(6.0, 1.1),
+                            ew_sigma=0.2, seed=7)
+    fr = synth.make_frontier(dr, per_depth=3, seed=2)
+    keep = np.arange(37)
+    fr = {k: v[keep] for k, v in fr.items()}
+    _expand_and_compare(torch, dr, fr, min(5, V), T, seed=3, tag=f"ragged {dtype} r={r} V={V} T={T}")
+
+
+@pytest.mark.parametrize("T", [0.0, 0.7])
+def test_wide_frontier_blocks(torch, T):
+    """A frontier of 700 parents (the 4-block-per-wave layout) with shared rows, bf16 r=64."""
+    dr = synth.make_drafter(20000, 16, 64, R=22, dtype="bf16", seed=11)
+    fr = synth.make_frontier(dr, per_depth=2, seed=3)
+    sample = list(range(0, 704, 11))
+    _expand_and_compare(torch, dr, fr, 8, T, seed=5, sample=sample, tag=f"wide T={T}")
+
+
+def test_single_request_v128256_frontier(torch):
+    """V=128256, D=16, r=64, bf16, T=0: the whole 64-parent frontier (4 per depth)."""
+    dr = synth.make_workload_drafter(1, seed=0)
+    fr = synth.make_frontier(dr, per_depth=4, seed=0)
+    _expand_and_compare(torch, dr, fr, 8, 0.0, seed=0, tag="v128256")
+
+
+def test_single_request_v151936_r256_sampling(torch):
+    """V=151936, D=16, r=256, bf16, T=1: 128 parents, 24 sampled for the oracle."""
+    dr = synth.make_workload_drafter(2, seed=0)
+    fr = synth.make_frontier(dr, per_depth=8, seed=0)
+    rng = np.random.default_rng(0)
+    sample = sorted(rng.choice(128, 24, replace=False))
+    _expand_and_compare(torch, dr, fr, 8, 1.0, seed=0, sample=sample, tag="v151936 r256 T=1")
+
+
+def test_serving_2048_parent_frontier(torch):
+    """64 requests, V=151936, r=64, bf16, T=0.7: the 2048-parent frontier timed by the bench,
+    in the same launch configuration; 40 sampled parents against the oracle."""
+    dr = synth.make_workload_drafter(3, seed=0)
+    fr = synth.make_frontier(dr, per_depth=2, seed=0)
+    assert len(fr["token"]) == 2048
+    rng = np.random.default_rng(1)
+    sample = sorted(rng.choice(2048, 40, replace=False))
+    _expand_and_compare(torch, dr, fr, 8, 0.7, seed=0, sample=sample, tag="serving T=0.7")
+    _expand_and_compare(torch, dr, fr, 8, 0.0, seed=0, sample=sample[:16], tag="serving T=0")
+
+
+def test_deterministic_and_invalid_parents(torch):
+    """Two calls give bitwise-identical outputs; a parent with an out-of-range field gets
+    token -1 and NaN values without disturbing the others."""
+    from paper_2609_22098_amd import binding
+    dr = synth.make_drafter(5000, 6, 32, R=2, dtype="bf16", seed=4)
+    fr = synth.make_frontier(dr, per_depth=3, seed=4)
+    fr["token"][5] = 5000      # out of range
+    fr["depth"][9] = 6         # out of range
+    fr["request"][11] = -1     # out of range
+    dd = binding.drafter_from_host(dr)
+    P = len(fr["token"])
+    parents = binding.parents_to_device(fr["token"], fr["depth"], fr["request"], fr["log_surv"], fr["path"])
+    outs = []
+    for _ in range(2):
+        out = binding.expand(dd, parents, P, 6, 0.9, 17)
+        torch.cuda.synchronize()
+        outs.append({k: v.cpu().numpy() for k, v in out.items() if not k.startswith("_")})
+    for k in outs[0]:
+        assert np.array_equal(outs[0][k].view(np.uint8), outs[1][k].view(np.uint8)), k
+    for bad in (5, 9, 11):
+        assert np.all(outs[0]["child_token"][bad] == -1)
+        assert np.all(np.isnan(outs[0]["child_log_q0"][bad]))
+    good = [i for i in range(P) if i not in (5, 9, 11)]
+    assert np.all(outs[0]["child_token"][good] >= 0)
+    # the valid parents still match the oracle
+    fr_ok = {k: v[good] for k, v in fr.items()}
+    _expand_and_compare(torch, dr, fr_ok, 6, 0.9, 17, sample=list(range(0, len(good), 4)), tag="valid rows")

@@ -1,0 +1,201 @@
+"""GPU parity of ts_build_tree and ts_verify against the oracle."""
+import math
+
+import numpy as np
+import pytest
+from scipy import special, stats
+
+from oracle import oracle as o
+from paper_2609_22098_amd import synth
+from helpers import TIE, Tally, compare_tree
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2609_22098_amd import binding
+    binding.lib()
+    return t
+
+
+def _trees(dr, anchors, thetas, N, K, T, seed):
+    from paper_2609_22098_amd import binding
+    dd = binding.drafter_from_host(dr)
+    tree = binding.build_tree(dd, anchors, thetas, N, K, T, seed)
+    return dd, tree
+
+
+def _compare_all(dr, tree, anchors, thetas, N, K, T, seed, requests=None, tag=""):
+    om = o.Model(dr.U32, dr.E32, dr.W2_32)
+    tally = Tally()
+    refs = {}
+    for q in (range(dr.R) if requests is None else requests):
+        ref = o.expand_tree(om, q, int(anchors[q]), float(thetas[q]), N, K, T, seed)
+        refs[q] = ref
+        compare_tree(tree, q, ref, float(thetas[q]), dr.dtype, tally, tag=f"{tag} request {q}")
+    sizes = [int(tree.n[q]) for q in refs]
+    print(f"{tag}: {tally.compared} trees, sizes {min(sizes)}..{max(sizes)}, near-ties {tally.near_ties}, "
+          f"max rel err {tally.max_err:.2e}")
+    assert not tally.failures, tally.failures[:5]
+    return refs
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0])
+def test_tiny_workload_tree(torch, T):
+    """V=4096, D=8, r=16, fp32, K=4, theta=0.05, N<=32 (the tiny oracle workload)."""
+    dr = synth.make_workload_drafter(0, seed=0)
+    anchors, _, _ = synth.make_controls(1, dr.V, 0.05, seed=0)
+    thetas = np.array([0.05], np.float32)
+    _, tree = _trees(dr, anchors, thetas, 32, 4, T, 0)
+    _compare_all(dr, tree, anchors, thetas, 32, 4, T, 0, tag=f"tiny T={T}")
+
+
+@pytest.mark.parametrize("T,theta", [(0.0, 0.0), (0.0, 0.02), (1.0, 0.0), (0.5, 0.01)])
+def test_sharp_multi_request_trees(torch, T, theta):
+    """Deeper trees (logits x3) for 6 requests with per-request theta: several waves, all depths."""
+    dr = synth.make_drafter(3000, 8, 32, R=6, dtype="bf16", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
+                            ew_sigma=0.3, seed=3, u_scale=3.0)
+    anchors, _, _ = synth.make_controls(6, dr.V, theta, seed=3)
+    thetas = np.array([theta, theta * 2, theta / 2, 0.0, theta, theta * 4], np.float32)
+    _, tree = _trees(dr, anchors, thetas, 40, 3, T, 9)
+    refs = _compare_all(dr, tree, anchors, thetas, 40, 3, T, 9, tag=f"sharp T={T} theta={theta}")
+    assert max(int(r.depth.max()) for r in refs.values()) >= 3
+
+
+def test_chain_special_case(torch):
+    """K=1, theta=0, N=D at T=0 is the chain decoder: x_k = argmax(U_k + B(x_{k-1}))."""
+    dr = synth.make_drafter(5000, 8, 64, R=4, dtype="bf16", seed=12)
+    anchors = np.array([1, 2, 3, 4], np.int32)
+    thetas = np.zeros(4, np.float32)
+    _, tree = _trees(dr, anchors, thetas, 8, 1, 0.0, 0)
+    for q in range(4):
+        x = int(anchors[q])
+        for d in range(8):
+            z = dr.U32[q, d].astype(np.float64) + dr.W2_32.astype(np.float64) @ dr.E32[x].astype(np.float64)
+            x = int(np.argmax(z))
+            assert tree.token[q, d + 1] == x
+            assert tree.parent[q, d + 1] == d
+
+
+def test_single_request_v128256_tree(torch):
+    """V=128256, D=16, r=64, bf16, K=8, fixed budget N=64 (theta = 0), T=0."""
+    dr = synth.make_workload_drafter(1, seed=0)
+    anchors, _, _ = synth.make_controls(1, dr.V, 0.0, seed=0)
+    thetas = np.zeros(1, np.float32)
+    _, tree = _trees(dr, anchors, thetas, 64, 8, 0.0, 0)
+    _compare_all(dr, tree, anchors, thetas, 64, 8, 0.0, 0, tag="v128256 N=64")
+    assert tree.n[0] == 64
+
+
+def test_single_request_v151936_r256_tree(torch):
+    """V=151936, D=16, r=256, bf16, K=8, N=128 (theta = 0), T=1 with Gumbel-top-k draws."""
+    dr = synth.make_workload_drafter(2, seed=0)
+    anchors, _, _ = synth.make_controls(1, dr.V, 0.0, seed=0)
+    thetas = np.zeros(1, np.float32)
+    _, tree = _trees(dr, anchors, thetas, 128, 8, 1.0, 0)
+    _compare_all(dr, tree, anchors, thetas, 128, 8, 1.0, 0, tag="v151936 r256 N=128 T=1")
+
+
+def test_serving_natural_trees(torch):
+    """64 requests, V=151936, r=64, bf16, per-request theta in {0.02, 0.05, 0.1, 0.2}, T=0.7."""
+    w = synth.WORKLOADS[3]
+    dr = synth.make_workload_drafter(3, seed=0)
+    anchors, thetas, _ = synth.make_controls(dr.R, dr.V, w["theta"], seed=0)
+    _, tree = _trees(dr, anchors, thetas, w["N"], w["K"], 0.7, 0)
+    _compare_all(dr, tree, anchors, thetas, w["N"], w["K"], 0.7, 0, tag="serving natural")
+
+
+# ---------------------------------------------------------------- verification
+
+def _prefixes(tree, q):
+    pre = [()]
+    for i in range(1, int(tree.n[q]) + 1):
+        pre.append(pre[tree.parent[q, i]] + (int(tree.token[q, i]),))
+    return pre
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0, 0.7])
+def test_verify_parity_multi_request(torch, T):
+    """ts_verify against the oracle walk on 8 requests (greedy and recursive rejection)."""
+    from paper_2609_22098_amd import binding
+    dr = synth.make_drafter(3000, 6, 32, R=8, dtype="bf16", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
+                            ew_sigma=0.3, seed=5, u_scale=2.0)
+    anchors, _, _ = synth.make_controls(8, dr.V, 0.0, seed=5)
+    thetas = np.full(8, 0.01, np.float32)
+    N, K = 24, 4
+    dd, tree = _trees(dr, anchors, thetas, N, K, T, 21)
+    cap = N + 1
+    tgt = np.zeros((8, cap, dr.V), np.uint16)
+    tgt32 = np.zeros((8, cap, dr.V), np.float32)
+    for q in range(8):
+        n1 = int(tree.n[q]) + 1
+        s, v = synth.make_target_rows(dr, q, tree.depth[q, :n1], 1.0, seed=2)
+        tgt[q, :n1], tgt32[q, :n1] = s, v
+    target = torch.from_numpy(tgt).view(torch.bfloat16).cuda()
+    path, plen, bonus = binding.verify(dd, tree, target, T, 33)
+    om = o.Model(dr.U32, dr.E32, dr.W2_32)
+    ties = 0
+    for q in range(8):
+        n1 = int(tree.n[q]) + 1
+        ot = o.Tree(int(tree.n[q]), 0, tree.token[q, :n1].copy(), tree.parent[q, :n1].copy(),
+                    tree.depth[q, :n1].copy(), tree.rank[q, :n1].copy(), tree.path[q, :n1].copy(),
+                    tree.log_surv[q, :n1].astype(np.float64), tree.log_q0[q, :n1].astype(np.float64),
+                    tree.log_qT[q, :n1].astype(np.float64), tree.key[q, :n1].astype(np.float64),
+                    np.zeros(n1), np.zeros(n1), float("nan"))
+        if T == 0:
+            rp, rb, gap = o.verify_greedy(ot, tgt32[q, :n1])
+        else:
+            rp, rb, gap = o.verify_sample(om, q, ot, tgt32[q, :n1], T, 33)
+        if gap <= 1e-4:
+            ties += 1
+            continue
+        assert list(path[q, :plen[q]]) == list(rp), (q, path[q, :plen[q]], rp)
+        assert bonus[q] == rb, (q, bonus[q], rb)
+    print(f"verify T={T}: {8 - ties} requests compared, near-ties {ties}, "
+          f"accepted lengths {list(plen)}")
+
+
+def test_verify_losslessness_chi_square(torch):
+    """Proposition 1 on the GPU: 60000 replicate requests (independent Philox streams through the
+    request field) build sampled trees and verify them against prefix-keyed target rows; the first
+    emitted token follows softmax(target_root / T) and the token after an accepted child x follows
+    softmax(target_x / T)."""
+    from paper_2609_22098_amd import binding
+    import itertools
+    V, D, K, N, T, R = 6, 3, 3, 7, 1.0, 60000
+    base = synth.make_drafter(V, D, 16, R=1, dtype="f32", u_sigma=0.8, planted=None, zipf=None,
+                              ew_sigma=0.6, seed=41)
+    U = np.repeat(base.U32, R, axis=0)
+    dr = synth.Drafter(R, D, V, 16, "f32", U, base.E, base.W2, U, base.E32, base.W2_32)
+    rng = np.random.default_rng(7)
+    rows = {}
+    for depth in range(D + 1):
+        for pre in itertools.product(range(V), repeat=depth):
+            rows[pre] = rng.normal(size=V).astype(np.float32)
+    dd = binding.drafter_from_host(dr)
+    anchors = np.ones(R, np.int32)
+    tree = binding.build_tree(dd, anchors, np.zeros(R, np.float32), N, K, T, 99)
+    cap = N + 1
+    tgt = np.zeros((R, cap, V), np.float32)
+    for q in range(R):
+        for i, p in enumerate(_prefixes(tree, q)):
+            tgt[q, i] = rows[p]
+    target = torch.from_numpy(tgt).cuda()
+    path, plen, bonus = binding.verify(dd, tree, target, T, 1234)
+    first = np.zeros(V)
+    second = {}
+    for q in range(R):
+        em = [int(tree.token[q, c]) for c in path[q, :plen[q]]] + [int(bonus[q])]
+        first[em[0]] += 1
+        if plen[q] >= 1:
+            second.setdefault(em[0], np.zeros(V))[em[1]] += 1
+    p_root = special.softmax(rows[()].astype(np.float64) / T)
+    p1 = stats.chisquare(first, p_root * R).pvalue
+    x1 = max(second, key=lambda k: second[k].sum())
+    cnt = second[x1]
+    p2 = stats.chisquare(cnt, special.softmax(rows[(x1,)].astype(np.float64) / T) * cnt.sum()).pvalue
+    print(f"chi-square p-values: first token {p1:.3g}, after x1={x1} ({int(cnt.sum())} samples) {p2:.3g}")
+    assert p1 > 1e-3 and p2 > 1e-3
