@@ -57,12 +57,13 @@ typedef enum {
 typedef enum { TS_F32 = 0, TS_BF16 = 1 } ts_dtype;
 
 /* Limits of this build: K <= TS_MAX_K siblings, D <= TS_MAX_D (the path id
- * holds 4 bits per level), R < 2^20 requests; r must be a multiple of 32 for
- * bf16 and of 4 for fp32, and at most 256. */
+ * holds 4 bits per level), R < 2^20 requests, V <= TS_MAX_V; the rank r is
+ * one of 32, 64, 128, 256 for bf16 and one of 16, 32, 64 for fp32. */
 #define TS_MAX_K 16
 #define TS_MAX_D 16
 #define TS_MAX_R (1 << 20)
 #define TS_MAX_RANK 256
+#define TS_MAX_V (512 * 4096)
 
 /* Drafter outputs of one round (device pointers, see above). */
 typedef struct {
@@ -107,6 +108,8 @@ typedef struct {
   float* lseT;             /* [P] optional: log-sum-exp of z / T; NaN at T = 0 */
   int32_t* diag;           /* [P] optional: candidate runs whose recomputed maximum differed
                               from the streaming pass (always 0 unless the device misbehaves) */
+  void** events;           /* optional: 3 caller-created hipEvent_t, recorded on `stream`
+                              before pass 1, between the passes and after pass 2 (timing) */
 } ts_expand_out;
 
 /* Bytes of device workspace ts_expand needs for P parents (0 if P == 0). */
@@ -144,6 +147,7 @@ typedef struct {
   float* log_q0;       /* [R][cap] log q0(token | parent), 0 for the root */
   float* log_qT;       /* [R][cap] log qT(token | parent), NaN at T = 0 and for the root */
   float* key;          /* [R][cap] key of the slot whose pop created the node */
+  int32_t* evals;      /* [R] optional (may be NULL): parents evaluated for the request */
 } ts_tree;
 
 size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, float T);

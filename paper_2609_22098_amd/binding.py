@@ -43,13 +43,13 @@ class Calib(ctypes.Structure):
 class ExpandOut(ctypes.Structure):
     _fields_ = [(name, ctypes.c_void_p) for name in
                 ("child_token", "child_log_q0", "child_log_qT", "child_log_surv", "slot_key",
-                 "rank_token", "rank_log_q0", "lse0", "lseT", "diag")]
+                 "rank_token", "rank_log_q0", "lse0", "lseT", "diag", "events")]
 
 
 class Tree(ctypes.Structure):
     _fields_ = [("R", ctypes.c_int32), ("cap", ctypes.c_int32)] + [
         (name, ctypes.c_void_p) for name in
-        ("n", "token", "parent", "depth", "rank", "path", "log_surv", "log_q0", "log_qT", "key")]
+        ("n", "token", "parent", "depth", "rank", "path", "log_surv", "log_q0", "log_qT", "key", "evals")]
 
 
 # ts_parent: 24 bytes
@@ -64,6 +64,12 @@ def lib():
     """Load the HIP library; raises if it has not been built."""
     global _lib
     if _lib is None:
+        try:
+            # Bind to the HIP runtime torch already loaded (same soname), so that
+            # torch's streams and events are this library's streams and events.
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it first (__graft_entry__.build())")
         L = ctypes.CDLL(LIB_PATH)
@@ -175,9 +181,10 @@ def expand_workspace_size(d: DeviceDrafter, P, k, T):
 
 
 def expand(d: DeviceDrafter, parents, P, k, T, seed, calib=(0.67, -0.46), workspace=None,
-           stream=None, outputs=None):
+           stream=None, outputs=None, events=None):
     """ts_expand.  parents: device uint8 tensor of P ts_parent records.  Returns a dict of
-    device tensors (asynchronous on the stream)."""
+    device tensors (asynchronous on the stream).  events: optional ctypes array of three
+    hipEvent_t handles recorded around the two kernels, given by address."""
     torch = _torch()
     dev = parents.device
     if outputs is None:
@@ -196,7 +203,8 @@ def expand(d: DeviceDrafter, parents, P, k, T, seed, calib=(0.67, -0.46), worksp
         n = expand_workspace_size(d, P, k, T)
         workspace = torch.empty((max(n, 1),), dtype=torch.uint8, device=dev)
     out = ExpandOut(*[outputs[name].data_ptr() if outputs.get(name) is not None else None
-                      for name, _ in ExpandOut._fields_])
+                      for name, _ in ExpandOut._fields_[:-1]],
+                    events)
     rc = lib().ts_expand(d.ref(), ctypes.c_void_p(parents.data_ptr()), P, Calib(*calib), k, float(T),
                          ctypes.c_uint64(seed), ctypes.byref(out), ctypes.c_void_p(workspace.data_ptr()),
                          workspace.numel(), _stream(stream))
@@ -217,12 +225,14 @@ class HostTree:
     log_q0: np.ndarray
     log_qT: np.ndarray
     key: np.ndarray
+    evals: np.ndarray
 
     @classmethod
     def empty(cls, R, cap):
         z = lambda dt: np.zeros((R, cap), dtype=dt)
         return cls(np.zeros(R, np.int32), z(np.int32), z(np.int32), z(np.int32), z(np.int32),
-                   z(np.uint64), z(np.float32), z(np.float32), z(np.float32), z(np.float32))
+                   z(np.uint64), z(np.float32), z(np.float32), z(np.float32), z(np.float32),
+                   np.zeros(R, np.int32))
 
     @property
     def R(self):

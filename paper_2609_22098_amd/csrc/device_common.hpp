@@ -14,6 +14,7 @@ constexpr float kNegInf = -__builtin_huge_valf();
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Philox4x32-10 round keys, precomputed on the host from the 64-bit seed
 // (k0 = seed lo32, k1 = seed hi32; each round adds the Weyl constants).

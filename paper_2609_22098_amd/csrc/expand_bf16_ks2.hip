@@ -1,0 +1,7 @@
+// Expansion kernels for bf16 drafter tensors with KS = 2.
+#include "expand_inst.hpp"
+
+namespace ts {
+template void launch_eval_t<uint16_t, 2>(const ExpandParams&, int, bool, bool, bool, dim3, dim3, hipStream_t);
+template void launch_merge_t<uint16_t, 2>(const MergeParams&, bool, dim3, dim3, hipStream_t);
+}  // namespace ts

@@ -1,0 +1,7 @@
+// Expansion kernels for f32 drafter tensors with KS = 16.
+#include "expand_inst.hpp"
+
+namespace ts {
+template void launch_eval_t<float, 16>(const ExpandParams&, int, bool, bool, bool, dim3, dim3, hipStream_t);
+template void launch_merge_t<float, 16>(const MergeParams&, bool, dim3, dim3, hipStream_t);
+}  // namespace ts

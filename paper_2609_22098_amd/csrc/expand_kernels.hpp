@@ -29,6 +29,15 @@
 
 namespace ts {
 
+// Per-(parent, chunk) arrays [P][S] of a RunTop2 summary.
+struct RunSummaryPtr {
+  float* m1;
+  float* m2;
+  float* rest;
+  int* r1;
+  int* r2;
+};
+
 struct ExpandParams {
   const void* U;
   const void* E;
@@ -47,12 +56,8 @@ struct ExpandParams {
   float* part_m;   // [P][S] running max of z
   float* part_s0;  // [P][S] sum exp(z - m)
   float* part_sT;  // [P][S] sum exp((z - m) / T)
-  float* zb1;      // [P][S] best run maximum of z
-  float* zb2;      // [P][S] best maximum of the other runs
-  int* zrun;       // [P][S] run index of zb1 (step * 4 + lane group)
-  float* gb1;      // same three for the Gumbel keys (T > 0)
-  float* gb2;
-  int* grun;
+  RunSummaryPtr zs;  // per (parent, chunk): the two best runs of z and the rest
+  RunSummaryPtr gs;  // the same for the Gumbel keys (T > 0)
   float* z_out;    // optional [P][V]: the logits themselves (verification recompute)
 };
 
@@ -72,12 +77,8 @@ struct MergeParams {
   const float* part_m;
   const float* part_s0;
   const float* part_sT;
-  const float* zb1;
-  const float* zb2;
-  const int* zrun;
-  const float* gb1;
-  const float* gb2;
-  const int* grun;
+  RunSummaryPtr zs;
+  RunSummaryPtr gs;
   ts_expand_out out;
 };
 
@@ -120,50 +121,120 @@ struct Frag<float> {
   __device__ static __forceinline__ float to_f32(float v) { return v; }
 };
 
-// 16 consecutive logits U[row][t .. t+16) as fp32; tokens >= V read as -inf.
+// The 16 logits U[row][t .. t+16) one lane needs for one parent in a step,
+// kept in their storage format until the accumulator is seeded.  Tokens >= V
+// read as -inf.  U is streamed once, so its loads are non-temporal.
 template <typename TE>
-__device__ __forceinline__ void load_u16(const TE* row, int t, int V, bool vec_ok, float (&u)[16]) {
-  if (vec_ok && t + 16 <= V) {
-    if constexpr (sizeof(TE) == 2) {
-      const uint4* p = reinterpret_cast<const uint4*>(row + t);
-      const uint4 a = p[0], b = p[1];
-      const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+struct URun;
+
+template <>
+struct URun<uint16_t> {
+  uint32_t w[8];
+  __device__ __forceinline__ void load(const uint16_t* row, int t) {
+    const u32x4* p = reinterpret_cast<const u32x4*>(row + t);
+    const u32x4 a = __builtin_nontemporal_load(p);
+    const u32x4 b = __builtin_nontemporal_load(p + 1);
+    w[0] = a[0]; w[1] = a[1]; w[2] = a[2]; w[3] = a[3];
+    w[4] = b[0]; w[5] = b[1]; w[6] = b[2]; w[7] = b[3];
+  }
+  __device__ __forceinline__ void load_masked(const uint16_t* row, int t, int V) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        u[2 * i] = __uint_as_float(w[i] << 16);
-        u[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
-      }
-    } else {
-      const float4* p = reinterpret_cast<const float4*>(row + t);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float4 v = p[i];
-        u[4 * i] = v.x; u[4 * i + 1] = v.y; u[4 * i + 2] = v.z; u[4 * i + 3] = v.w;
-      }
+    for (int i = 0; i < 8; ++i) {
+      const int y0 = t + 2 * i, y1 = y0 + 1;
+      const uint32_t lo = y0 < V ? row[min(y0, V - 1)] : 0xFF80u;  // bf16 -inf
+      const uint32_t hi = y1 < V ? row[min(y1, V - 1)] : 0xFF80u;
+      w[i] = lo | (hi << 16);
     }
-  } else {
+  }
+  __device__ __forceinline__ float get(int i) const {
+    return (i & 1) ? __uint_as_float(w[i >> 1] & 0xFFFF0000u) : __uint_as_float(w[i >> 1] << 16);
+  }
+};
+
+template <>
+struct URun<float> {
+  float f[16];
+  __device__ __forceinline__ void load(const float* row, int t) {
+    const f32x4* p = reinterpret_cast<const f32x4*>(row + t);
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      u[i] = (t + i < V) ? Frag<TE>::to_f32(row[t + i]) : kNegInf;
+    for (int i = 0; i < 4; ++i) {
+      const f32x4 v = __builtin_nontemporal_load(p + i);
+      f[4 * i] = v[0]; f[4 * i + 1] = v[1]; f[4 * i + 2] = v[2]; f[4 * i + 3] = v[3];
+    }
+  }
+  __device__ __forceinline__ void load_masked(const float* row, int t, int V) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float v = row[min(t + i, V - 1)];
+      f[i] = (t + i < V) ? v : kNegInf;
+    }
+  }
+  __device__ __forceinline__ float get(int i) const { return f[i]; }
+};
+
+// Summary of a set of runs for one key: the two best run maxima with their
+// run indices, and the largest maximum of every other run.  Order: larger
+// value first, ties to the smaller run index.
+struct RunTop2 {
+  float m1, m2, rest;
+  int r1, r2;
+};
+
+__device__ __forceinline__ bool run_before(float v, int r, float w, int s) {
+  return v > w || (v == w && r < s);
+}
+
+__device__ __forceinline__ void top2_init(RunTop2& t) {
+  t.m1 = kNegInf; t.m2 = kNegInf; t.rest = kNegInf; t.r1 = 0x7FFFFFFF; t.r2 = 0x7FFFFFFF;
+}
+
+// Add one run (runs arrive in increasing index order within a lane).
+__device__ __forceinline__ void top2_add(RunTop2& t, float v, int run) {
+  if (v > t.m1) {
+    t.rest = fmaxf(t.rest, t.m2);
+    t.m2 = t.m1; t.r2 = t.r1;
+    t.m1 = v; t.r1 = run;
+  } else if (v > t.m2) {
+    t.rest = fmaxf(t.rest, t.m2);
+    t.m2 = v; t.r2 = run;
+  } else {
+    t.rest = fmaxf(t.rest, v);
   }
 }
 
-// Order of (max, second, run) bucket summaries: larger max wins, ties go to
-// the smaller run index; the loser's max joins the second-best.
-__device__ __forceinline__ void bucket_combine(float& b1, float& b2, int& run, float o1, float o2,
-                                               int orun) {
-  if (o1 > b1 || (o1 == b1 && orun < run)) {
-    b2 = fmaxf(o2, b1);
-    b1 = o1;
-    run = orun;
+// Merge two summaries of disjoint run sets (symmetric in its arguments).
+__device__ __forceinline__ void top2_combine(RunTop2& a, const RunTop2& b) {
+  RunTop2 o;
+  o.rest = fmaxf(a.rest, b.rest);
+  if (run_before(a.m1, a.r1, b.m1, b.r1)) {
+    o.m1 = a.m1; o.r1 = a.r1;
+    if (run_before(a.m2, a.r2, b.m1, b.r1)) { o.m2 = a.m2; o.r2 = a.r2; o.rest = fmaxf(o.rest, b.m1); }
+    else { o.m2 = b.m1; o.r2 = b.r1; o.rest = fmaxf(o.rest, a.m2); }
+    o.rest = fmaxf(o.rest, b.m2);
   } else {
-    b2 = fmaxf(b2, o1);
+    o.m1 = b.m1; o.r1 = b.r1;
+    if (run_before(b.m2, b.r2, a.m1, a.r1)) { o.m2 = b.m2; o.r2 = b.r2; o.rest = fmaxf(o.rest, a.m1); }
+    else { o.m2 = a.m1; o.r2 = a.r1; o.rest = fmaxf(o.rest, b.m2); }
+    o.rest = fmaxf(o.rest, a.m2);
   }
+  a = o;
+}
+
+__device__ __forceinline__ RunTop2 top2_shfl_xor(const RunTop2& t, int o) {
+  RunTop2 u;
+  u.m1 = __shfl_xor(t.m1, o, 64); u.m2 = __shfl_xor(t.m2, o, 64);
+  u.rest = __shfl_xor(t.rest, o, 64);
+  u.r1 = __shfl_xor(t.r1, o, 64); u.r2 = __shfl_xor(t.r2, o, 64);
+  return u;
+}
+
+__device__ __forceinline__ void top2_store(const RunSummaryPtr& d, size_t o, const RunTop2& t) {
+  d.m1[o] = t.m1; d.m2[o] = t.m2; d.rest[o] = t.rest; d.r1[o] = t.r1; d.r2[o] = t.r2;
 }
 
 // ---------------------------------------------------------------- pass 1
 
-template <typename TE, int KS, int NB, bool SAMPLE>
+template <typename TE, int KS, int NB, bool SAMPLE, bool STORE_Z>
 __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) {
   typedef Frag<TE> F;
   typedef typename F::type FT;
@@ -215,22 +286,20 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
     pc3[nb] = counter_word3(req, dep, 1u);
   }
 
-  float m0[NB], s0[NB], sT[NB], zb1[NB], zb2[NB], gb1[NB], gb2[NB];
-  int zr[NB], gr[NB];
+  float m0[NB], s0[NB], sT[NB];
+  RunTop2 zt[NB], gt[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     m0[nb] = kNegInf; s0[nb] = 0.0f; sT[nb] = 0.0f;
-    zb1[nb] = kNegInf; zb2[nb] = kNegInf; zr[nb] = -1;
-    gb1[nb] = kNegInf; gb2[nb] = kNegInf; gr[nb] = -1;
+    top2_init(zt[nb]);
+    top2_init(gt[nb]);
   }
 
-  const int tbeg = chunk * p.Vc;
-  const int tend = min(tbeg + p.Vc, V);
-  int step = 0;
-  for (int t0 = tbeg; t0 < tend; t0 += 64, ++step) {
-    // A: row n of M-block bb is token t0 + (n/4)*16 + bb*4 + n%4, so that the
-    // C layout gives lane group g the 16 contiguous tokens t0 + g*16 + [0,16).
-    FT afrag[4][KS];
+  // One 64-token step: 16 tokens per lane group, each lane owns one parent
+  // per block.  u holds this step's U values (prefetched one step ahead).
+  // A: row n of M-block bb is token t0 + (n/4)*16 + bb*4 + n%4, so that the
+  // C layout gives lane group g the 16 contiguous tokens t0 + g*16 + [0,16).
+  auto load_a = [&](FT (&afrag)[4][KS], int t0) {
 #pragma unroll
     for (int bb = 0; bb < 4; ++bb) {
       const int tA = min(t0 + (n >> 2) * 16 + bb * 4 + (n & 3), V - 1);
@@ -238,21 +307,23 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) afrag[bb][kk] = F::load(wrow, kk * F::kPerStep, g);
     }
+  };
+
+  auto do_step = [&](const URun<TE> (&u)[NB], const FT (&afrag)[4][KS], int t0, int step) {
     f32x4 acc[4][NB];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      float u[16];
-      load_u16<TE>(urow[nb], t0 + g * 16, V, vec_ok, u);
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int bb = 0; bb < 4; ++bb)
-        acc[bb][nb] = f32x4{u[bb * 4], u[bb * 4 + 1], u[bb * 4 + 2], u[bb * 4 + 3]};
-    }
+        acc[bb][nb] = f32x4{u[nb].get(bb * 4), u[nb].get(bb * 4 + 1), u[nb].get(bb * 4 + 2),
+                            u[nb].get(bb * 4 + 3)};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
       for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[bb][nb] = F::mma(afrag[bb][kk], bfrag[nb][kk], acc[bb][nb]);
+        for (int nb = 0; nb < NB; ++nb)
+          acc[bb][nb] = F::mma(afrag[bb][kk], bfrag[nb][kk], acc[bb][nb]);
 
     const int run = step * 4 + g;
     const int tl = t0 + g * 16;
@@ -263,11 +334,13 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
       for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[bb * 4 + e] = acc[bb][nb][e];
-      if (p.z_out != nullptr && pidx[nb] < p.P) {
-        float* zo = p.z_out + (size_t)pidx[nb] * V;
+      if constexpr (STORE_Z) {
+        if (pidx[nb] < p.P) {
+          float* zo = p.z_out + (size_t)pidx[nb] * V;
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (tl + j < V) zo[tl + j] = v[j];
+          for (int j = 0; j < 16; ++j)
+            if (tl + j < V) zo[tl + j] = v[j];
+        }
       }
       float bm = v[0];
 #pragma unroll
@@ -287,13 +360,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
         sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)), aT);
       }
       m0[nb] = mn;
-      if (bm > zb1[nb]) {
-        zb2[nb] = zb1[nb];
-        zb1[nb] = bm;
-        zr[nb] = run;
-      } else {
-        zb2[nb] = fmaxf(zb2[nb], bm);
-      }
+      top2_add(zt[nb], bm, run);
       if constexpr (SAMPLE) {
         float gm = kNegInf;
         const uint32_t cbase = (uint32_t)tl >> 2;
@@ -309,15 +376,41 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
             gm = fmaxf(gm, key);
           }
         }
-        if (gm > gb1[nb]) {
-          gb2[nb] = gb1[nb];
-          gb1[nb] = gm;
-          gr[nb] = run;
-        } else {
-          gb2[nb] = fmaxf(gb2[nb], gm);
-        }
+        top2_add(gt[nb], gm, run);
       }
     }
+  };
+
+  auto load_u = [&](URun<TE> (&u)[NB], int t0) {
+    if (vec_ok && t0 + 64 <= V) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) u[nb].load(urow[nb], t0 + g * 16);
+    } else {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) u[nb].load_masked(urow[nb], t0 + g * 16, V);
+    }
+  };
+
+  // Steps alternate between two buffers of U values and W2 fragments: the
+  // next step's loads are in flight while the current step computes.
+  const int tbeg = chunk * p.Vc;
+  const int tend = min(tbeg + p.Vc, V);
+  URun<TE> ua[NB], ub[NB];
+  FT aa[4][KS], ab[4][KS];
+  int t0 = tbeg, step = 0;
+  load_u(ua, t0);
+  load_a(aa, t0);
+  for (;;) {
+    const bool more1 = t0 + 64 < tend;
+    if (more1) { load_u(ub, t0 + 64); load_a(ab, t0 + 64); }
+    do_step(ua, aa, t0, step);
+    if (!more1) break;
+    t0 += 64; ++step;
+    const bool more2 = t0 + 64 < tend;
+    if (more2) { load_u(ua, t0 + 64); load_a(aa, t0 + 64); }
+    do_step(ub, ab, t0, step);
+    if (!more2) break;
+    t0 += 64; ++step;
   }
 
   // Combine the four lane groups of each parent (lanes n, n+16, n+32, n+48).
@@ -336,67 +429,253 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
       st += __shfl_xor(st, 16, 64);
       st += __shfl_xor(st, 32, 64);
     }
-    float b1 = zb1[nb], b2 = zb2[nb];
-    int rr = zr[nb];
+    RunTop2 zc = zt[nb], gc = gt[nb];
 #pragma unroll
     for (int o = 16; o <= 32; o <<= 1) {
-      const float o1 = __shfl_xor(b1, o, 64), o2 = __shfl_xor(b2, o, 64);
-      const int orr = __shfl_xor(rr, o, 64);
-      bucket_combine(b1, b2, rr, o1, o2, orr);
-    }
-    float h1 = gb1[nb], h2 = gb2[nb];
-    int hr = gr[nb];
-    if constexpr (SAMPLE) {
-#pragma unroll
-      for (int o = 16; o <= 32; o <<= 1) {
-        const float o1 = __shfl_xor(h1, o, 64), o2 = __shfl_xor(h2, o, 64);
-        const int orr = __shfl_xor(hr, o, 64);
-        bucket_combine(h1, h2, hr, o1, o2, orr);
-      }
+      top2_combine(zc, top2_shfl_xor(zc, o));
+      if constexpr (SAMPLE) top2_combine(gc, top2_shfl_xor(gc, o));
     }
     if (g == 0 && pidx[nb] < p.P) {
       const size_t o = (size_t)pidx[nb] * p.S + chunk;
       p.part_m[o] = M;
       p.part_s0[o] = s;
       if (p.part_sT) p.part_sT[o] = st;
-      p.zb1[o] = b1;
-      p.zb2[o] = b2;
-      p.zrun[o] = rr;
-      if constexpr (SAMPLE) {
-        p.gb1[o] = h1;
-        p.gb2[o] = h2;
-        p.grun[o] = hr;
+      top2_store(p.zs, o, zc);
+      if constexpr (SAMPLE) top2_store(p.gs, o, gc);
+    }
+  }
+}
+
+// Streaming pass, bf16, staged through LDS.  The four waves of a workgroup
+// work on one chunk with different parent blocks.  Each 64-token step needs a
+// W2 tile (64 rows of r bf16, shared by the four waves) and one U tile per
+// wave; both are brought in with direct global->LDS loads one step ahead, in
+// two buffers used alternately, so no registers hold prefetched data.  The W2
+// tile is laid out in 16-byte pieces in the exact order the A fragments are
+// read (piece (bb*KS + kk)*64 + lane), so every fragment read is one
+// conflict-free ds_read_b128.  Requires V % 8 == 0.
+__device__ __forceinline__ void lds_dma16(const void* src, u32x4* dst_wave_base) {
+  typedef __attribute__((address_space(3))) void* lds_ptr;
+  __builtin_amdgcn_global_load_lds(src, (lds_ptr)dst_wave_base, 16, 0, 0);
+}
+
+template <int KS, int NB, bool SAMPLE>
+__global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams p) {
+  typedef Frag<uint16_t> F;
+  typedef typename F::type FT;
+  constexpr int kW = 4 * KS * 64;  // 16-byte pieces of one W2 tile
+  constexpr int kU = NB * 2 * 64;  // 16-byte pieces of one wave's U tile
+  __shared__ __attribute__((aligned(16))) u32x4 w0[kW];
+  __shared__ __attribute__((aligned(16))) u32x4 w1[kW];
+  __shared__ __attribute__((aligned(16))) u32x4 u0[4 * kU];
+  __shared__ __attribute__((aligned(16))) u32x4 u1[4 * kU];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int n = lane & 15;
+  const int g = lane >> 4;
+
+  const int b = blockIdx.x;
+  const int kx = b >> 3;
+  const int chunk = (b & 7) + 8 * (kx / p.n_pgroups);
+  const int pgroup = kx % p.n_pgroups;
+  if (chunk >= p.S) return;  // uniform over the workgroup
+  const int pb = pgroup * 4 + wv;
+  const bool active = pb < p.n_pblocks;  // idle waves still load W2 and join the barriers
+
+  const uint16_t* U = static_cast<const uint16_t*>(p.U);
+  const uint16_t* E = static_cast<const uint16_t*>(p.E);
+  const uint16_t* W2 = static_cast<const uint16_t*>(p.W2);
+  const int V = p.V, r = p.r;
+
+  const uint16_t* urow[NB];
+  FT bfrag[NB][KS];
+  uint32_t pc1[NB], pc2[NB], pc3[NB];
+  int pidx[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    pidx[nb] = (pb * NB + nb) * 16 + n;
+    int tok = 0, dep = 0, req = 0;
+    uint64_t path = 0;
+    if (active && pidx[nb] < p.P) {
+      const ts_parent par = p.parents[pidx[nb]];
+      if (par.token >= 0 && par.token < V && par.depth >= 0 && par.depth < p.D &&
+          par.request >= 0 && par.request < p.R) {
+        tok = par.token; dep = par.depth; req = par.request; path = par.path;
       }
+    }
+    urow[nb] = U + ((size_t)req * p.D + dep) * (size_t)V;
+    const uint16_t* erow = E + (size_t)tok * r;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) bfrag[nb][kk] = F::load(erow, kk * F::kPerStep, g);
+    pc1[nb] = (uint32_t)path;
+    pc2[nb] = (uint32_t)(path >> 32);
+    pc3[nb] = counter_word3(req, dep, 1u);
+  }
+
+  float m0[NB], s0[NB], sT[NB];
+  RunTop2 zt[NB], gt[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    m0[nb] = kNegInf; s0[nb] = 0.0f; sT[nb] = 0.0f;
+    top2_init(zt[nb]);
+    top2_init(gt[nb]);
+  }
+
+  auto issue = [&](u32x4* wb, u32x4* ub, int t0) {
+    // W2: this wave loads pieces (wv*KS + j)*64 + lane of the tile
+#pragma unroll
+    for (int j = 0; j < KS; ++j) {
+      const int i = wv * KS + j;
+      const int bb = i / KS, kk = i % KS;
+      const int tok = min(t0 + (n >> 2) * 16 + bb * 4 + (n & 3), V - 1);
+      lds_dma16(W2 + (size_t)tok * r + kk * 32 + g * 8, wb + i * 64);
+    }
+    // U: tokens t0 + g*16 + 8h + [0, 8) of this lane's parent in block nb
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int tt = min(t0 + g * 16 + 8 * h, V - 8);
+        lds_dma16(urow[nb] + tt, ub + wv * kU + (nb * 2 + h) * 64);
+      }
+  };
+
+  auto compute = [&](const u32x4* wb, const u32x4* ub, int t0, int step) {
+    const int tl = t0 + g * 16;
+    f32x4 acc[4][NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      URun<uint16_t> u;
+      const u32x4 a = ub[wv * kU + (nb * 2) * 64 + lane];
+      const u32x4 c = ub[wv * kU + (nb * 2 + 1) * 64 + lane];
+      u.w[0] = a[0]; u.w[1] = a[1]; u.w[2] = a[2]; u.w[3] = a[3];
+      u.w[4] = c[0]; u.w[5] = c[1]; u.w[6] = c[2]; u.w[7] = c[3];
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb)
+        acc[bb][nb] = f32x4{u.get(bb * 4), u.get(bb * 4 + 1), u.get(bb * 4 + 2), u.get(bb * 4 + 3)};
+      if (tl + 16 > V) {
+#pragma unroll
+        for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (tl + bb * 4 + e >= V) acc[bb][nb][e] = kNegInf;
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) {
+        const FT a = __builtin_bit_cast(FT, wb[(bb * KS + kk) * 64 + lane]);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[bb][nb] = F::mma(a, bfrag[nb][kk], acc[bb][nb]);
+      }
+
+    const int run = step * 4 + g;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      float v[16];
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[bb * 4 + e] = acc[bb][nb][e];
+      float bm = v[0];
+#pragma unroll
+      for (int j = 1; j < 16; ++j) bm = fmaxf(bm, v[j]);
+      const float mn = fmaxf(m0[nb], bm);
+      const float mref = fmaxf(mn, -1e30f);
+      const float ml = mref * kLog2e;
+      float a0 = 0.0f;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) a0 += exp2_fast(__builtin_fmaf(v[j], kLog2e, -ml));
+      s0[nb] = __builtin_fmaf(s0[nb], exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -ml)), a0);
+      if (SAMPLE && p.need_T) {
+        const float mlT = mref * p.cT;
+        float aT = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) aT += exp2_fast(__builtin_fmaf(v[j], p.cT, -mlT));
+        sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)), aT);
+      }
+      m0[nb] = mn;
+      top2_add(zt[nb], bm, run);
+      if constexpr (SAMPLE) {
+        float gm = kNegInf;
+        const uint32_t cbase = (uint32_t)tl >> 2;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          uint32_t c0 = cbase + i, c1 = pc1[nb], c2 = pc2[nb], c3 = pc3[nb];
+          philox10(c0, c1, c2, c3, p.keys);
+          const uint32_t w[4] = {c0, c1, c2, c3};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int j = i * 4 + q;
+            const float key = (tl + j < V) ? gumbel_key2(v[j], p.cT, w[q]) : kNegInf;
+            gm = fmaxf(gm, key);
+          }
+        }
+        top2_add(gt[nb], gm, run);
+      }
+    }
+  };
+
+  const int tbeg = chunk * p.Vc;
+  const int tend = min(tbeg + p.Vc, V);
+  int t0 = tbeg, step = 0;
+  issue(w0, u0, t0);
+  for (;;) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    const bool more1 = t0 + 64 < tend;
+    if (more1) issue(w1, u1, t0 + 64);
+    if (active) compute(w0, u0, t0, step);
+    if (!more1) break;
+    t0 += 64; ++step;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    const bool more2 = t0 + 64 < tend;
+    if (more2) issue(w0, u0, t0 + 64);
+    if (active) compute(w1, u1, t0, step);
+    if (!more2) break;
+    t0 += 64; ++step;
+  }
+  if (!active) return;
+
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    float M = m0[nb];
+    M = fmaxf(M, __shfl_xor(M, 16, 64));
+    M = fmaxf(M, __shfl_xor(M, 32, 64));
+    const float Mref = fmaxf(M, -1e30f);
+    float s = s0[nb] * exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -Mref * kLog2e));
+    s += __shfl_xor(s, 16, 64);
+    s += __shfl_xor(s, 32, 64);
+    float st = 0.0f;
+    if (SAMPLE && p.need_T) {
+      st = sT[nb] * exp2_fast(__builtin_fmaf(m0[nb], p.cT, -Mref * p.cT));
+      st += __shfl_xor(st, 16, 64);
+      st += __shfl_xor(st, 32, 64);
+    }
+    RunTop2 zc = zt[nb], gc = gt[nb];
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      top2_combine(zc, top2_shfl_xor(zc, o));
+      if constexpr (SAMPLE) top2_combine(gc, top2_shfl_xor(gc, o));
+    }
+    if (g == 0 && pidx[nb] < p.P) {
+      const size_t o = (size_t)pidx[nb] * p.S + chunk;
+      p.part_m[o] = M;
+      p.part_s0[o] = s;
+      if (p.part_sT) p.part_sT[o] = st;
+      top2_store(p.zs, o, zc);
+      if constexpr (SAMPLE) top2_store(p.gs, o, gc);
     }
   }
 }
 
 // ---------------------------------------------------------------- pass 2
 
-// Recompute the logits of 16 consecutive tokens [t, t+16) for one parent with
-// the MFMA sequence of pass 1 (same operands in the same K positions, same
-// accumulator start).  The parent sits in column 0; lanes 0, 16, 32, 48 get
-// tokens t + g*4 + [0, 4).
-template <typename TE, int KS>
-__device__ __forceinline__ f32x4 recompute_run(const TE* W2, const TE* urow, int V, int r, int t,
-                                               const typename Frag<TE>::type (&bcol)[KS]) {
-  typedef Frag<TE> F;
-  const int lane = threadIdx.x & 63;
-  const int n = lane & 15, g = lane >> 4;
-  const int tA = min(t + n, V - 1);
-  const TE* wrow = W2 + (size_t)tA * r;
-  f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-  if (n == 0) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int tok = t + g * 4 + e;
-      acc[e] = tok < V ? F::to_f32(urow[tok]) : kNegInf;
-    }
-  }
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) acc = F::mma(F::load(wrow, kk * F::kPerStep, g), bcol[kk], acc);
-  return acc;
-}
+constexpr int kMaxChunks = 512;          // chunks per parent (8 per lane)
+constexpr int kChunkSlots = kMaxChunks / 64;
+constexpr int kBatch = 8;                // runs recomputed together
 
 // Insert (v, id) into a list sorted by (value desc, id asc) holding at most K entries.
 __device__ __forceinline__ void topk_insert(float* val, int* ids, float* aux, int& cnt, int K,
@@ -422,100 +701,256 @@ struct MergeLds {
   float gval[TS_MAX_K];
   int gid[TS_MAX_K];
   float gz[TS_MAX_K];  // z of the drawn tokens
-  float buf_z[16];
-  float buf_g[16];
-  int zcnt, gcnt;
+  float bz[kBatch][16];  // logits of a batch of recomputed runs
+  float bk[kBatch][16];  // their keys (z, or the Gumbel keys)
+  int item[2 * kMaxChunks];  // candidate items: chunk * 4 + kind (0: run 1, 1: run 2, 2: whole chunk)
 };
 
-// Select the chunks that can hold a top-K element of one key (z or Gumbel) and
-// rescan their candidate runs; fills the sorted list in LDS (lane 0 inserts).
-template <typename TE, int KS, bool GUMBEL>
-__device__ int select_and_rescan(const MergeParams& p, const float* b1, const float* b2,
-                                  const int* brun, size_t pbase, const TE* urow,
-                                  const typename Frag<TE>::type (&bcol)[KS], uint32_t pc1,
-                                  uint32_t pc2, uint32_t pc3, MergeLds& L, float* val, int* ids,
-                                  float* aux, int& cnt_lds) {
-  const int lane = threadIdx.x & 63;
-  const int g = lane >> 4;
-  const int S = p.S, K = p.K, V = p.V;
-  // threshold: the K-th largest chunk maximum (ties by chunk index)
-  uint32_t taken = 0u;  // bit i: chunk lane + 64 i already picked
-  float thr = kNegInf;
-  int picked = 0;
-  for (; picked < K; ++picked) {
-    float bv = kNegInf;
-    int bc = 0x7FFFFFFF;
-    for (int c = lane, i = 0; c < S; c += 64, ++i) {
-      if (taken & (1u << i)) continue;
-      const float v = b1[pbase + c];
-      if (v > bv || (v == bv && c < bc)) { bv = v; bc = c; }
-    }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oc = __shfl_xor(bc, o, 64);
-      if (ov > bv || (ov == bv && oc < bc)) { bv = ov; bc = oc; }
-    }
-    if (bc == 0x7FFFFFFF) break;
-    if ((bc & 63) == lane) taken |= 1u << (bc >> 6);
-    thr = bv;
-  }
-  if (picked < K) thr = kNegInf;  // fewer than K chunks: every token is a candidate
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
-  if (lane == 0) cnt_lds = 0;
-  int cnt = 0;  // lane 0's view of the list length
-  int mismatches = 0;
-  for (int c = 0; c < S; ++c) {
-    const float cm = b1[pbase + c];
-    if (!(cm >= thr)) continue;
-    const bool whole = b2[pbase + c] >= thr;
-    const int best = brun[pbase + c];
-    const int cbeg = c * p.Vc;
-    const int nruns = ((min(cbeg + p.Vc, V) - cbeg + 63) / 64) * 4;
-    for (int ri = 0; ri < nruns; ++ri) {
-      const int run = whole ? ri : best;
-      if (!whole && ri > 0) break;
-      const int t = cbeg + (run >> 2) * 64 + (run & 3) * 16;
-      if (t >= V) continue;
-      const f32x4 z4 = recompute_run<TE, KS>(static_cast<const TE*>(p.W2), urow, V, p.r, t, bcol);
+// Recompute up to kBatch runs of 16 tokens [t, t+16) for one parent with the
+// MFMA sequence of pass 1 (same operands in the same K positions, same
+// accumulator start), so the values are bit-identical to the streaming pass.
+// The parent sits in column 0; lanes 0, 16, 32, 48 get tokens t + g*4 + [0,4).
+// Every lane then checks kBatch*16/64 of the keys against thr and lane 0
+// inserts the (few) candidates into the sorted list.  A run whose expected
+// maximum is given (not NaN) counts a mismatch if its recomputed maximum differs.
+template <typename TE, int KS, bool GUMBEL>
+__device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* urow,
+                                             const typename Frag<TE>::type (&bcol)[KS],
+                                             uint32_t pc1, uint32_t pc2, uint32_t pc3,
+                                             const int (&t)[kBatch], const float (&expect)[kBatch],
+                                             int nrun, float thr, MergeLds& L, float* val,
+                                             int* ids, float* aux, int& cnt, int& mism) {
+  typedef Frag<TE> F;
+  const int lane = threadIdx.x & 63;
+  const int n = lane & 15, g = lane >> 4;
+  const int V = p.V;
+  const TE* W2 = static_cast<const TE*>(p.W2);
+  f32x4 acc[kBatch];
+#pragma unroll
+  for (int b = 0; b < kBatch; ++b) {
+    const int tb = b < nrun ? t[b] : 0;
+    acc[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    if (n == 0) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int tok = tb + g * 4 + e;
+        acc[b][e] = tok < V ? F::to_f32(urow[min(tok, V - 1)]) : kNegInf;
+      }
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < kBatch; ++b) {
+    const int tb = b < nrun ? t[b] : 0;
+    const TE* wrow = W2 + (size_t)min(tb + n, V - 1) * p.r;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) acc[b] = F::mma(F::load(wrow, kk * F::kPerStep, g), bcol[kk], acc[b]);
+  }
+  if (n == 0) {
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int tb = b < nrun ? t[b] : 0;
       float k4[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) k4[e] = z4[e];
+      for (int e = 0; e < 4; ++e) k4[e] = acc[b][e];
       if constexpr (GUMBEL) {
-        // lanes 0/16/32/48 hold tokens t + g*4 + [0,4): one Philox call each
-        uint32_t c0 = (uint32_t)(t + g * 4) >> 2, c1 = pc1, c2 = pc2, c3 = pc3;
+        // tokens tb + g*4 + [0,4) are exactly one Philox call
+        uint32_t c0 = (uint32_t)(tb + g * 4) >> 2, c1 = pc1, c2 = pc2, c3 = pc3;
         philox10(c0, c1, c2, c3, p.keys);
         const uint32_t w[4] = {c0, c1, c2, c3};
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          k4[e] = (t + g * 4 + e < V) ? gumbel_key2(z4[e], p.cT, w[e]) : kNegInf;
+          k4[e] = (tb + g * 4 + e < V) ? gumbel_key2(acc[b][e], p.cT, w[e]) : kNegInf;
       }
-      if ((lane & 15) == 0) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          L.buf_z[g * 4 + e] = z4[e];
-          L.buf_g[g * 4 + e] = k4[e];
-        }
+      for (int e = 0; e < 4; ++e) {
+        L.bz[b][g * 4 + e] = acc[b][e];
+        L.bk[b][g * 4 + e] = k4[e];
       }
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      if (lane == 0) {
-        float rm = kNegInf;
-        for (int j = 0; j < 16; ++j) {
-          const float kv = L.buf_g[j];
-          rm = fmaxf(rm, kv);
-          if (kv >= thr && t + j < V) topk_insert(val, ids, aux, cnt, K, kv, t + j, L.buf_z[j]);
-        }
-        if (run == best && rm != cm) ++mismatches;
-      }
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
   }
-  if (lane == 0) cnt_lds = cnt;
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-  return mismatches;
+  wave_sync_lds();
+#ifdef TS_DEBUG_RUNS
+  mism += nrun * 1000;
+#endif
+  // lane l checks key j = l + 64 h of the batch (run j / 16, token j % 16)
+#pragma unroll
+  for (int h = 0; h < kBatch / 4; ++h) {
+    const int j = lane + 64 * h;
+    const int b = j >> 4, e = j & 15;
+    const float kv = L.bk[b][e];
+    int tb = 0;
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q)
+      if (q == b) tb = t[q];
+    float ex = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q)
+      if (q == b) ex = expect[q];
+    const bool live = b < nrun && tb + e < V;
+    // run maximum over the 16 lanes of this run
+    float rm = live ? kv : kNegInf;
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
+    const bool bad = live && e == 0 && !__builtin_isnan(ex) && rm != ex;
+    mism += __popcll(__ballot(bad));
+    uint64_t mask = __ballot(live && kv >= thr);
+    if (lane == 0) {
+      while (mask) {
+        const int src = __ffsll((unsigned long long)mask) - 1;
+        mask &= mask - 1;
+        const int jj = src + 64 * h;
+        const int bb = jj >> 4, ee = jj & 15;
+        int tt = 0;
+        for (int q = 0; q < kBatch; ++q)
+          if (q == bb) tt = t[q];
+        topk_insert(val, ids, aux, cnt, p.K, L.bk[bb][ee], tt + ee, L.bz[bb][ee]);
+      }
+    }
+  }
+  wave_sync_lds();
+}
+
+// Exact top-K of one key (z, or the Gumbel keys) for one parent from the
+// per-chunk run summaries; fills the sorted list (lane 0 writes it).
+// Threshold: the K-th largest of all recorded run maxima (two per chunk).
+// Those are maxima of K distinct runs, hence K distinct tokens, so the K-th
+// largest key over the whole vocabulary is at least the threshold.  A token
+// with a key >= threshold lies in a run whose maximum is >= threshold: one of
+// its chunk's two recorded runs, or, if the chunk's rest maximum also reaches
+// the threshold, somewhere in the chunk (then every run of it is recomputed).
+template <typename TE, int KS, bool GUMBEL>
+__device__ __forceinline__ void select_and_rescan(const MergeParams& p, const RunSummaryPtr& sm,
+                                                  size_t pbase, const TE* urow,
+                                                  const typename Frag<TE>::type (&bcol)[KS],
+                                                  uint32_t pc1, uint32_t pc2, uint32_t pc3,
+                                                  MergeLds& L, float* val, int* ids, float* aux,
+                                                  int& mism) {
+  const int lane = threadIdx.x & 63;
+  const int S = p.S, K = p.K, V = p.V;
+  float c1[kChunkSlots], c2[kChunkSlots], cx[kChunkSlots];
+  int r1[kChunkSlots], r2[kChunkSlots];
+#pragma unroll
+  for (int i = 0; i < kChunkSlots; ++i) {
+    const int c = lane + 64 * i;
+    const bool in = c < S;
+    c1[i] = in ? sm.m1[pbase + c] : kNegInf;
+    c2[i] = in ? sm.m2[pbase + c] : kNegInf;
+    cx[i] = in ? sm.rest[pbase + c] : kNegInf;
+    r1[i] = in ? sm.r1[pbase + c] : 0;
+    r2[i] = in ? sm.r2[pbase + c] : 0;
+  }
+  // threshold: K rounds of a wave argmax over the recorded maxima (ties by slot id)
+  uint32_t taken = 0u;  // bit 2i: c1[i] taken, bit 2i+1: c2[i] taken
+  float thr = kNegInf;
+  int picked = 0;
+  for (; picked < K; ++picked) {
+    float bv = kNegInf;
+    int bid = 0x7FFFFFFF;
+#pragma unroll
+    for (int i = 0; i < kChunkSlots; ++i) {
+      const int c = lane + 64 * i;
+      if (c >= S) continue;
+      if (!(taken & (1u << (2 * i))) && run_before(c1[i], 2 * c, bv, bid)) { bv = c1[i]; bid = 2 * c; }
+      if (!(taken & (2u << (2 * i))) && run_before(c2[i], 2 * c + 1, bv, bid)) { bv = c2[i]; bid = 2 * c + 1; }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int oi = __shfl_xor(bid, o, 64);
+      if (run_before(ov, oi, bv, bid)) { bv = ov; bid = oi; }
+    }
+    if (bid == 0x7FFFFFFF || bv == kNegInf) break;
+    const int cb = bid >> 1;
+    if ((cb & 63) == lane) taken |= (1u + (uint32_t)(bid & 1)) << (2 * (cb >> 6));
+    thr = bv;
+  }
+  if (picked < K) thr = kNegInf;  // fewer than K runs recorded: every token is a candidate
+
+  // Candidate items (listed in LDS first so the recompute below is one loop).
+  int nitems = 0;
+#pragma unroll
+  for (int i = 0; i < kChunkSlots; ++i) {
+    const int c = lane + 64 * i;
+    const bool sel = c < S && c1[i] >= thr;
+    const bool whole = sel && cx[i] >= thr;
+    const int mine = sel ? (whole ? 1 : (c2[i] >= thr ? 2 : 1)) : 0;
+    // exclusive prefix over lanes of the number of items each lane adds
+    int incl = mine;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += v;
+    }
+    const int base = nitems + incl - mine;
+    if (sel) {
+      if (whole) {
+        L.item[base] = c * 4 + 2;
+      } else {
+        L.item[base] = c * 4 + 0;
+        if (mine == 2) L.item[base + 1] = c * 4 + 1;
+      }
+    }
+    nitems += __shfl(incl, 63, 64);
+  }
+  wave_sync_lds();
+
+  int cnt = 0;
+  const float nan = __builtin_nanf("");
+  int it = 0, sub = 0;
+#pragma unroll 1
+  while (it < nitems) {
+    int qt[kBatch];
+    float qe[kBatch];
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) { qt[q] = 0; qe[q] = nan; }
+    int nr = 0;
+#pragma unroll 1
+    while (nr < kBatch && it < nitems) {
+      const int code = L.item[it];
+      const int cc = code >> 2, kind = code & 3;
+      const int slot = cc >> 6, src = cc & 63;
+      // the summary of chunk cc lives in lane src, slot `slot`
+      float m1 = 0.0f, m2 = 0.0f;
+      int q1 = 0, q2 = 0;
+#pragma unroll
+      for (int i = 0; i < kChunkSlots; ++i) {
+        if (i == slot) {
+          m1 = __shfl(c1[i], src, 64); m2 = __shfl(c2[i], src, 64);
+          q1 = __shfl(r1[i], src, 64); q2 = __shfl(r2[i], src, 64);
+        }
+      }
+      int t;
+      float e;
+      if (kind == 2) {
+        const int cbeg = cc * p.Vc;
+        const int nruns = ((min(cbeg + p.Vc, V) - cbeg + 63) / 64) * 4;
+        t = cbeg + (sub >> 2) * 64 + (sub & 3) * 16;
+        e = sub == q1 ? m1 : (sub == q2 ? m2 : nan);
+        if (++sub == nruns) { sub = 0; ++it; }
+        if (t >= V) continue;
+      } else {
+        const int run = kind == 0 ? q1 : q2;
+        t = cc * p.Vc + (run >> 2) * 64 + (run & 3) * 16;
+        e = kind == 0 ? m1 : m2;
+        ++it;
+      }
+      // shift the queue so that entries [0, nr] are the ones pushed
+#pragma unroll
+      for (int q = kBatch - 1; q > 0; --q) { qt[q] = qt[q - 1]; qe[q] = qe[q - 1]; }
+      qt[0] = t;
+      qe[0] = e;
+      ++nr;
+    }
+    if (nr > 0)
+      rescan_batch<TE, KS, GUMBEL>(p, urow, bcol, pc1, pc2, pc3, qt, qe, nr, thr, L, val, ids, aux,
+                                   cnt, mism);
+  }
 }
 
 template <typename TE, int KS, bool SAMPLE>
@@ -528,6 +963,9 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   const int n = lane & 15, g = lane >> 4;
   const int pidx = blockIdx.x * 4 + wv;
   if (pidx >= p.P) return;
+#ifdef TS_DEBUG_RUNS
+  const long long t_start = clock64();
+#endif
   MergeLds& L = lds[wv];
   const int K = p.K, V = p.V, S = p.S;
   const ts_parent par = p.parents[pidx];
@@ -580,11 +1018,12 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   const uint32_t pc1 = (uint32_t)par.path, pc2 = (uint32_t)(par.path >> 32);
   const uint32_t pc3 = counter_word3(par.request, par.depth, 1u);
 
-  int mism = select_and_rescan<TE, KS, false>(p, p.zb1, p.zb2, p.zrun, pbase, urow, bcol, pc1,
-                                              pc2, pc3, L, L.zval, L.zid, L.zaux, L.zcnt);
+  int mism = 0;
+  select_and_rescan<TE, KS, false>(p, p.zs, pbase, urow, bcol, pc1, pc2, pc3, L, L.zval, L.zid,
+                                   L.zaux, mism);
   if constexpr (SAMPLE)
-    mism += select_and_rescan<TE, KS, true>(p, p.gb1, p.gb2, p.grun, pbase, urow, bcol, pc1, pc2,
-                                            pc3, L, L.gval, L.gid, L.gz, L.gcnt);
+    select_and_rescan<TE, KS, true>(p, p.gs, pbase, urow, bcol, pc1, pc2, pc3, L, L.gval, L.gid,
+                                    L.gz, mism);
 
   // Child scoring: lane j handles slot j + 1 (Algorithm 1; §3.2 pre-draw bound; Eq. 3).
   if (lane < K) {
@@ -624,6 +1063,9 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   if (lane == 0) {
     if (p.out.lse0) p.out.lse0[pidx] = lse0;
     if (p.out.lseT) p.out.lseT[pidx] = lseT;
+#ifdef TS_DEBUG_RUNS
+    if (p.out.rank_log_q0) p.out.rank_log_q0[ob + K - 1] = (float)(clock64() - t_start);
+#endif
     if (p.out.diag) p.out.diag[pidx] = mism;
   }
 }

@@ -1,0 +1,27 @@
+// Kernel launchers shared by the host API.  Each (dtype, rank) pair is
+// instantiated in its own translation unit so the kernels compile in parallel.
+#pragma once
+
+#include "expand_kernels.hpp"
+#include "verify_kernels.hpp"
+
+namespace ts {
+
+// Streaming pass of the expansion.  KS = r / 32 (bf16) or r / 4 (f32); nb =
+// parent blocks of 16 per wave (1, 2 or 4); store_z runs with nb == 1.
+// lds selects the LDS-staged bf16 kernel (V % 8 == 0, four waves per block).
+template <typename TE, int KS>
+void launch_eval_t(const ExpandParams& p, int nb, bool sample, bool store_z, bool lds, dim3 grid,
+                   dim3 block, hipStream_t s);
+// Per-parent merge, exact top-k and child scoring.
+template <typename TE, int KS>
+void launch_merge_t(const MergeParams& p, bool sample, dim3 grid, dim3 block, hipStream_t s);
+
+// Verification.
+void launch_verify_argmax(const void* target, bool bf16, int V, const int* rows, int nrows,
+                          int* argmax_out, float* gap_out, hipStream_t s);
+void launch_verify_stage(const void* target, bool bf16, int cap, int V, const VerifyItem* items,
+                         int nitems, const float* zbuf, float T, PhiloxKeys keys,
+                         VerifyResult* results, hipStream_t s);
+
+}  // namespace ts

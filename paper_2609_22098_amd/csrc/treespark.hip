@@ -11,8 +11,7 @@
 #include <unordered_map>
 #include <vector>
 
-#include "expand_kernels.hpp"
-#include "verify_kernels.hpp"
+#include "launch.hpp"
 
 namespace ts {
 namespace {
@@ -47,6 +46,7 @@ int32_t check_drafter(const ts_drafter* d) {
   if (d->dtype != TS_F32 && d->dtype != TS_BF16) return fail(TS_EINVAL, "unknown dtype %d", d->dtype);
   if (d->D > TS_MAX_D) return fail(TS_EUNSUPPORTED, "D=%d exceeds %d (4-bit path digits)", d->D, TS_MAX_D);
   if (d->R >= TS_MAX_R) return fail(TS_EUNSUPPORTED, "R=%d exceeds %d", d->R, TS_MAX_R - 1);
+  if (d->V > TS_MAX_V) return fail(TS_EUNSUPPORTED, "V=%d exceeds %d", d->V, TS_MAX_V);
   const bool ok = d->dtype == TS_BF16 ? (d->r == 32 || d->r == 64 || d->r == 128 || d->r == 256)
                                       : (d->r == 16 || d->r == 32 || d->r == 64);
   if (!ok) return fail(TS_EUNSUPPORTED, "rank r=%d not supported for dtype %d", d->r, d->dtype);
@@ -78,25 +78,33 @@ struct Plan {
   int NB, Vc, S, n_pblocks, wpg, n_pgroups, S8;
   int ks;
   bool sample;
-  size_t off_m, off_s0, off_sT, off_zb1, off_zb2, off_zr, off_gb1, off_gb2, off_gr, off_err;
+  bool lds;  // LDS-staged bf16 streaming kernel
+  size_t off_m, off_s0, off_sT, off_z[5], off_g[5];
   size_t bytes;
 };
 
-Plan make_plan(const ts_drafter* d, int P, float T) {
+// store_z: the verification recompute, which writes the logits and runs one
+// parent block per wave.
+Plan make_plan(const ts_drafter* d, int P, float T, bool store_z = false) {
   Plan pl{};
   pl.sample = T > 0.0f;
   pl.ks = d->dtype == TS_BF16 ? d->r / 32 : d->r / 4;
   const int nb_big = (d->dtype == TS_BF16 && d->r == 256) ? 2 : 4;
   pl.NB = P >= 512 ? nb_big : 1;
+#ifdef TS_FORCE_NB
+  pl.NB = TS_FORCE_NB;
+#endif
+  if (store_z) pl.NB = 1;
+  pl.lds = d->dtype == TS_BF16 && d->V % 8 == 0 && !store_z;
   pl.n_pblocks = (P + 16 * pl.NB - 1) / (16 * pl.NB);
-  pl.wpg = std::min(4, std::max(1, pl.n_pblocks));
+  pl.wpg = pl.lds ? 4 : std::min(4, std::max(1, pl.n_pblocks));
   pl.n_pgroups = (pl.n_pblocks + pl.wpg - 1) / pl.wpg;
   // Enough waves to fill 256 CUs several times over, chunks of 256..4096
-  // tokens, and at most 2048 chunks (the merge keeps a 32-bit mask per lane).
+  // tokens, and at most kMaxChunks chunks (the merge keeps them in registers).
   const int target_waves = 4096;
   const int s_target = std::max(1, (target_waves + pl.n_pblocks - 1) / pl.n_pblocks);
   int vc = (d->V + s_target - 1) / s_target;
-  vc = std::max(vc, (d->V + 2047) / 2048);
+  vc = std::max(vc, (d->V + kMaxChunks - 1) / kMaxChunks);
   vc = ((vc + 63) / 64) * 64;
   vc = std::min(std::max(vc, 256), 4096);
   pl.Vc = vc;
@@ -106,66 +114,46 @@ Plan make_plan(const ts_drafter* d, int P, float T) {
   size_t o = 0;
   pl.off_m = o; o += a;
   pl.off_s0 = o; o += a;
-  pl.off_zb1 = o; o += a;
-  pl.off_zb2 = o; o += a;
-  pl.off_zr = o; o += a;
+  for (int i = 0; i < 5; ++i) { pl.off_z[i] = o; o += a; }
   if (pl.sample) {
     pl.off_sT = o; o += a;
-    pl.off_gb1 = o; o += a;
-    pl.off_gb2 = o; o += a;
-    pl.off_gr = o; o += a;
+    for (int i = 0; i < 5; ++i) { pl.off_g[i] = o; o += a; }
   }
-  pl.off_err = o; o += 256;
   pl.bytes = o;
   return pl;
 }
 
-size_t expand_ws_max(const ts_drafter* d, int Pmax, float T) {
+RunSummaryPtr summary_ptr(char* ws, const size_t (&off)[5]) {
+  RunSummaryPtr r;
+  r.m1 = reinterpret_cast<float*>(ws + off[0]);
+  r.m2 = reinterpret_cast<float*>(ws + off[1]);
+  r.rest = reinterpret_cast<float*>(ws + off[2]);
+  r.r1 = reinterpret_cast<int*>(ws + off[3]);
+  r.r2 = reinterpret_cast<int*>(ws + off[4]);
+  return r;
+}
+
+size_t expand_ws_max(const ts_drafter* d, int Pmax, float T, bool store_z = false) {
   size_t m = 0;
-  for (int P = 1; P <= Pmax; ++P) m = std::max(m, make_plan(d, P, T).bytes);
+  for (int P = 1; P <= Pmax; ++P) m = std::max(m, make_plan(d, P, T, store_z).bytes);
   return m;
-}
-
-template <typename TE, int KS, int NB>
-void launch_eval_nb(const ExpandParams& p, bool sample, dim3 grid, dim3 block, hipStream_t s) {
-  if (sample)
-    hipLaunchKernelGGL((expand_eval_kernel<TE, KS, NB, true>), grid, block, 0, s, p);
-  else
-    hipLaunchKernelGGL((expand_eval_kernel<TE, KS, NB, false>), grid, block, 0, s, p);
-}
-
-template <typename TE, int KS>
-void launch_eval_ks(const ExpandParams& p, int NB, bool sample, dim3 grid, dim3 block, hipStream_t s) {
-  if (NB == 1)
-    launch_eval_nb<TE, KS, 1>(p, sample, grid, block, s);
-  else if (NB == 2)
-    launch_eval_nb<TE, KS, 2>(p, sample, grid, block, s);
-  else
-    launch_eval_nb<TE, KS, 4>(p, sample, grid, block, s);
-}
-
-template <typename TE, int KS>
-void launch_merge_ks(const MergeParams& p, bool sample, dim3 grid, dim3 block, hipStream_t s) {
-  if (sample)
-    hipLaunchKernelGGL((expand_merge_kernel<TE, KS, true>), grid, block, 0, s, p);
-  else
-    hipLaunchKernelGGL((expand_merge_kernel<TE, KS, false>), grid, block, 0, s, p);
 }
 
 void launch_eval(const ts_drafter* d, const ExpandParams& p, const Plan& pl, hipStream_t s) {
   const dim3 grid(pl.S8 * pl.n_pgroups), block(64 * pl.wpg);
+  const bool z = p.z_out != nullptr;
   if (d->dtype == TS_BF16) {
     switch (pl.ks) {
-      case 1: launch_eval_ks<uint16_t, 1>(p, pl.NB, pl.sample, grid, block, s); break;
-      case 2: launch_eval_ks<uint16_t, 2>(p, pl.NB, pl.sample, grid, block, s); break;
-      case 4: launch_eval_ks<uint16_t, 4>(p, pl.NB, pl.sample, grid, block, s); break;
-      default: launch_eval_ks<uint16_t, 8>(p, pl.NB, pl.sample, grid, block, s); break;
+      case 1: launch_eval_t<uint16_t, 1>(p, pl.NB, pl.sample, z, pl.lds, grid, block, s); break;
+      case 2: launch_eval_t<uint16_t, 2>(p, pl.NB, pl.sample, z, pl.lds, grid, block, s); break;
+      case 4: launch_eval_t<uint16_t, 4>(p, pl.NB, pl.sample, z, pl.lds, grid, block, s); break;
+      default: launch_eval_t<uint16_t, 8>(p, pl.NB, pl.sample, z, pl.lds, grid, block, s); break;
     }
   } else {
     switch (pl.ks) {
-      case 4: launch_eval_ks<float, 4>(p, pl.NB, pl.sample, grid, block, s); break;
-      case 8: launch_eval_ks<float, 8>(p, pl.NB, pl.sample, grid, block, s); break;
-      default: launch_eval_ks<float, 16>(p, pl.NB, pl.sample, grid, block, s); break;
+      case 4: launch_eval_t<float, 4>(p, pl.NB, pl.sample, z, false, grid, block, s); break;
+      case 8: launch_eval_t<float, 8>(p, pl.NB, pl.sample, z, false, grid, block, s); break;
+      default: launch_eval_t<float, 16>(p, pl.NB, pl.sample, z, false, grid, block, s); break;
     }
   }
 }
@@ -174,16 +162,16 @@ void launch_merge(const ts_drafter* d, const MergeParams& p, const Plan& pl, hip
   const dim3 grid((p.P + 3) / 4), block(256);
   if (d->dtype == TS_BF16) {
     switch (pl.ks) {
-      case 1: launch_merge_ks<uint16_t, 1>(p, pl.sample, grid, block, s); break;
-      case 2: launch_merge_ks<uint16_t, 2>(p, pl.sample, grid, block, s); break;
-      case 4: launch_merge_ks<uint16_t, 4>(p, pl.sample, grid, block, s); break;
-      default: launch_merge_ks<uint16_t, 8>(p, pl.sample, grid, block, s); break;
+      case 1: launch_merge_t<uint16_t, 1>(p, pl.sample, grid, block, s); break;
+      case 2: launch_merge_t<uint16_t, 2>(p, pl.sample, grid, block, s); break;
+      case 4: launch_merge_t<uint16_t, 4>(p, pl.sample, grid, block, s); break;
+      default: launch_merge_t<uint16_t, 8>(p, pl.sample, grid, block, s); break;
     }
   } else {
     switch (pl.ks) {
-      case 4: launch_merge_ks<float, 4>(p, pl.sample, grid, block, s); break;
-      case 8: launch_merge_ks<float, 8>(p, pl.sample, grid, block, s); break;
-      default: launch_merge_ks<float, 16>(p, pl.sample, grid, block, s); break;
+      case 4: launch_merge_t<float, 4>(p, pl.sample, grid, block, s); break;
+      case 8: launch_merge_t<float, 8>(p, pl.sample, grid, block, s); break;
+      default: launch_merge_t<float, 16>(p, pl.sample, grid, block, s); break;
     }
   }
 }
@@ -203,14 +191,8 @@ ExpandParams eval_params(const ts_drafter* d, const ts_parent* parents, int P, f
   p.part_m = reinterpret_cast<float*>(ws + pl.off_m);
   p.part_s0 = reinterpret_cast<float*>(ws + pl.off_s0);
   p.part_sT = pl.sample ? reinterpret_cast<float*>(ws + pl.off_sT) : nullptr;
-  p.zb1 = reinterpret_cast<float*>(ws + pl.off_zb1);
-  p.zb2 = reinterpret_cast<float*>(ws + pl.off_zb2);
-  p.zrun = reinterpret_cast<int*>(ws + pl.off_zr);
-  if (pl.sample) {
-    p.gb1 = reinterpret_cast<float*>(ws + pl.off_gb1);
-    p.gb2 = reinterpret_cast<float*>(ws + pl.off_gb2);
-    p.grun = reinterpret_cast<int*>(ws + pl.off_gr);
-  }
+  p.zs = summary_ptr(ws, pl.off_z);
+  if (pl.sample) p.gs = summary_ptr(ws, pl.off_g);
   p.z_out = z_out;
   return p;
 }
@@ -221,8 +203,11 @@ int32_t run_expand(const ts_drafter* d, const ts_parent* parents, int P, ts_cali
   if (P == 0) return TS_OK;
   const Plan pl = make_plan(d, P, T);
   const ExpandParams ep = eval_params(d, parents, P, T, seed, pl, ws, nullptr);
+  hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(out->events);
+  if (ev) TS_HIP(hipEventRecord(ev[0], s));
   launch_eval(d, ep, pl, s);
   TS_HIP(hipGetLastError());
+  if (ev) TS_HIP(hipEventRecord(ev[1], s));
   MergeParams mp{};
   mp.U = d->U; mp.E = d->E; mp.W2 = d->W2;
   mp.R = d->R; mp.D = d->D; mp.V = d->V; mp.r = d->r;
@@ -234,11 +219,12 @@ int32_t run_expand(const ts_drafter* d, const ts_parent* parents, int P, ts_cali
   mp.calib_a = calib.a; mp.calib_b = calib.b;
   mp.keys = ep.keys;
   mp.part_m = ep.part_m; mp.part_s0 = ep.part_s0; mp.part_sT = ep.part_sT;
-  mp.zb1 = ep.zb1; mp.zb2 = ep.zb2; mp.zrun = ep.zrun;
-  mp.gb1 = ep.gb1; mp.gb2 = ep.gb2; mp.grun = ep.grun;
+  mp.zs = ep.zs;
+  mp.gs = ep.gs;
   mp.out = *out;
   launch_merge(d, mp, pl, s);
   TS_HIP(hipGetLastError());
+  if (ev) TS_HIP(hipEventRecord(ev[2], s));
   return TS_OK;
 }
 
@@ -298,7 +284,7 @@ VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
     v.off_res = o; o += align256((size_t)d->R * sizeof(VerifyResult));
     v.off_par = o; o += align256((size_t)d->R * sizeof(ts_parent));
     v.off_z = o; o += align256((size_t)d->R * d->V * 4);
-    v.off_exp = o; o += expand_ws_max(d, d->R, T);
+    v.off_exp = o; o += expand_ws_max(d, d->R, T, true);
   }
   v.bytes = o;
   return v;
@@ -382,6 +368,7 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
   for (int q = 0; q < R; ++q) log_theta[q] = theta[q] > 0.0f ? logf(theta[q]) : -INFINITY;
   std::vector<std::vector<Slot>> known(R);
   std::vector<ts_parent> frontier;
+  std::vector<int32_t> evals(R, 0);
   if (N > 0)
     for (int q = 0; q < R; ++q) frontier.push_back(ts_parent{anchor[q], 0, q, 0.0f, 0});
   std::vector<int32_t> h_tok;
@@ -401,6 +388,7 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
     TS_HIP(hipStreamSynchronize(s));
     for (int i = 0; i < P; ++i) {
       const ts_parent& par = frontier[i];
+      ++evals[par.request];
       for (int j = 0; j < K; ++j) {
         const size_t o = (size_t)i * K + j;
         Slot sl;
@@ -477,6 +465,7 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
       node_of[sl.depth][sl.path] = c;
     }
     out->n[q] = n;
+    if (out->evals) out->evals[q] = evals[q];
   }
   return TS_OK;
 }
@@ -536,12 +525,7 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     int* darg = reinterpret_cast<int*>(ws + vl.off_arg);
     float* dgap = reinterpret_cast<float*>(ws + vl.off_gap);
     TS_HIP(hipMemcpyAsync(drows, rows.data(), nrows * 4, hipMemcpyHostToDevice, s));
-    if (target_dtype == TS_BF16)
-      hipLaunchKernelGGL((verify_argmax_kernel<uint16_t>), dim3(nrows), dim3(kVerifyThreads), 0, s,
-                         static_cast<const uint16_t*>(target), V, drows, nrows, darg, dgap);
-    else
-      hipLaunchKernelGGL((verify_argmax_kernel<float>), dim3(nrows), dim3(kVerifyThreads), 0, s,
-                         static_cast<const float*>(target), V, drows, nrows, darg, dgap);
+    launch_verify_argmax(target, target_dtype == TS_BF16, V, drows, nrows, darg, dgap, s);
     TS_HIP(hipGetLastError());
     std::vector<int> arg(nrows);
     TS_HIP(hipMemcpyAsync(arg.data(), darg, nrows * 4, hipMemcpyDeviceToHost, s));
@@ -599,18 +583,13 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     if (!zpar.empty()) {
       const int P = (int)zpar.size();
       TS_HIP(hipMemcpyAsync(dpar, zpar.data(), P * sizeof(ts_parent), hipMemcpyHostToDevice, s));
-      const Plan pl = make_plan(d, P, T);
+      const Plan pl = make_plan(d, P, T, true);
       const ExpandParams ep = eval_params(d, dpar, P, T, seed, pl, ws + vl.off_exp, zbuf);
       launch_eval(d, ep, pl, s);
       TS_HIP(hipGetLastError());
     }
     TS_HIP(hipMemcpyAsync(ditems, items.data(), ni * sizeof(VerifyItem), hipMemcpyHostToDevice, s));
-    if (target_dtype == TS_BF16)
-      hipLaunchKernelGGL((verify_stage_kernel<uint16_t>), dim3(ni), dim3(kVerifyThreads), 0, s,
-                         static_cast<const uint16_t*>(target), cap, V, ditems, ni, zbuf, T, keys, dres);
-    else
-      hipLaunchKernelGGL((verify_stage_kernel<float>), dim3(ni), dim3(kVerifyThreads), 0, s,
-                         static_cast<const float*>(target), cap, V, ditems, ni, zbuf, T, keys, dres);
+    launch_verify_stage(target, target_dtype == TS_BF16, cap, V, ditems, ni, zbuf, T, keys, dres, s);
     TS_HIP(hipGetLastError());
     res.resize(ni);
     TS_HIP(hipMemcpyAsync(res.data(), dres, ni * sizeof(VerifyResult), hipMemcpyDeviceToHost, s));

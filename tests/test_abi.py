@@ -33,7 +33,7 @@ def _drafter(R=1, D=4, V=1000, r=16, dtype=b.TS_F32, null=False):
 
 
 def _expand(d, P=4, k=2, T=0.0, ws_bytes=1 << 30, out=True, parents=FAKE):
-    o = b.ExpandOut(FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, None, None) if out else None
+    o = b.ExpandOut(FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, None, None, None) if out else None
     return b.lib().ts_expand(ctypes.byref(d), parents, P, b.Calib(0.67, -0.46), k, T, 0,
                              ctypes.byref(o) if o else None, FAKE, ws_bytes, None)
 
