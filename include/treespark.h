@@ -63,7 +63,7 @@ typedef enum { TS_F32 = 0, TS_BF16 = 1 } ts_dtype;
 #define TS_MAX_D 16
 #define TS_MAX_R (1 << 20)
 #define TS_MAX_RANK 256
-#define TS_MAX_V (512 * 4096)
+#define TS_MAX_V (256 * 4096) /* 256 chunks of at most 4096 tokens per parent */
 
 /* Drafter outputs of one round (device pointers, see above). */
 typedef struct {

@@ -4,4 +4,5 @@
 namespace ts {
 template void launch_eval_t<uint16_t, 4>(const ExpandParams&, int, bool, bool, bool, dim3, dim3, hipStream_t);
 template void launch_merge_t<uint16_t, 4>(const MergeParams&, bool, dim3, dim3, hipStream_t);
+template int eval_blocks_per_cu_t<uint16_t, 4>(int, bool, bool, bool, int);
 }  // namespace ts

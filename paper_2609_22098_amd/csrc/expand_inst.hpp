@@ -55,6 +55,31 @@ void launch_eval_t(const ExpandParams& p, int nb, bool sample, bool store_z, boo
 }
 
 template <typename TE, int KS>
+int eval_blocks_per_cu_t(int nb, bool sample, bool store_z, bool lds, int block) {
+  int n = 0;
+  hipError_t e = hipSuccess;
+#define TS_OCC(kern) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, block, 0)
+  if constexpr (sizeof(TE) == 2) {
+    if (lds && !store_z) {
+      if (nb == 1) { if (sample) TS_OCC((expand_eval_lds_kernel<KS, 1, true>)); else TS_OCC((expand_eval_lds_kernel<KS, 1, false>)); }
+      else if (nb == 2) { if (sample) TS_OCC((expand_eval_lds_kernel<KS, 2, true>)); else TS_OCC((expand_eval_lds_kernel<KS, 2, false>)); }
+      else { if (sample) TS_OCC((expand_eval_lds_kernel<KS, 4, true>)); else TS_OCC((expand_eval_lds_kernel<KS, 4, false>)); }
+      return e == hipSuccess ? n : 0;
+    }
+  }
+  if (nb == 1 || store_z) {
+    if (store_z) { if (sample) TS_OCC((expand_eval_kernel<TE, KS, 1, true, true>)); else TS_OCC((expand_eval_kernel<TE, KS, 1, false, true>)); }
+    else { if (sample) TS_OCC((expand_eval_kernel<TE, KS, 1, true, false>)); else TS_OCC((expand_eval_kernel<TE, KS, 1, false, false>)); }
+  } else if (nb == 2) {
+    if (sample) TS_OCC((expand_eval_kernel<TE, KS, 2, true, false>)); else TS_OCC((expand_eval_kernel<TE, KS, 2, false, false>));
+  } else {
+    if (sample) TS_OCC((expand_eval_kernel<TE, KS, 4, true, false>)); else TS_OCC((expand_eval_kernel<TE, KS, 4, false, false>));
+  }
+#undef TS_OCC
+  return e == hipSuccess ? n : 0;
+}
+
+template <typename TE, int KS>
 void launch_merge_t(const MergeParams& p, bool sample, dim3 grid, dim3 block, hipStream_t s) {
   if (sample)
     hipLaunchKernelGGL((expand_merge_kernel<TE, KS, true>), grid, block, 0, s, p);

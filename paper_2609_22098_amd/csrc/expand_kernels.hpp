@@ -29,13 +29,13 @@
 
 namespace ts {
 
-// Per-(parent, chunk) arrays [P][S] of a RunTop2 summary.
+constexpr int kTopRuns = 4;  // best runs recorded per (parent, chunk)
+
+// Per-(parent, chunk) run summaries: m and r are [P][S][kTopRuns], rest is [P][S].
 struct RunSummaryPtr {
-  float* m1;
-  float* m2;
+  float* m;
+  int* r;
   float* rest;
-  int* r1;
-  int* r2;
 };
 
 struct ExpandParams {
@@ -172,64 +172,92 @@ struct URun<float> {
   __device__ __forceinline__ float get(int i) const { return f[i]; }
 };
 
-// Summary of a set of runs for one key: the two best run maxima with their
-// run indices, and the largest maximum of every other run.  Order: larger
-// value first, ties to the smaller run index.
-struct RunTop2 {
-  float m1, m2, rest;
-  int r1, r2;
+// Summary of a set of runs for one key: the kTopRuns best run maxima with
+// their run indices (sorted: larger value first, ties to the smaller run
+// index; empty entries are -inf), and the largest maximum of every other run.
+struct RunTop {
+  float m[kTopRuns];
+  int r[kTopRuns];
+  float rest;
 };
 
 __device__ __forceinline__ bool run_before(float v, int r, float w, int s) {
   return v > w || (v == w && r < s);
 }
 
-__device__ __forceinline__ void top2_init(RunTop2& t) {
-  t.m1 = kNegInf; t.m2 = kNegInf; t.rest = kNegInf; t.r1 = 0x7FFFFFFF; t.r2 = 0x7FFFFFFF;
+__device__ __forceinline__ void top_init(RunTop& t) {
+#pragma unroll
+  for (int i = 0; i < kTopRuns; ++i) { t.m[i] = kNegInf; t.r[i] = 0x7FFFFFFF; }
+  t.rest = kNegInf;
 }
 
-// Add one run (runs arrive in increasing index order within a lane).
-__device__ __forceinline__ void top2_add(RunTop2& t, float v, int run) {
-  if (v > t.m1) {
-    t.rest = fmaxf(t.rest, t.m2);
-    t.m2 = t.m1; t.r2 = t.r1;
-    t.m1 = v; t.r1 = run;
-  } else if (v > t.m2) {
-    t.rest = fmaxf(t.rest, t.m2);
-    t.m2 = v; t.r2 = run;
-  } else {
-    t.rest = fmaxf(t.rest, v);
+// Add one run.  Runs arrive in increasing index order within a lane, so a
+// strict comparison keeps the earlier run ahead on ties.
+__device__ __forceinline__ void top_add(RunTop& t, float v, int run) {
+  float cv = v;
+  int cr = run;
+#pragma unroll
+  for (int i = 0; i < kTopRuns; ++i) {
+    const bool sw = cv > t.m[i];
+    const float om = t.m[i];
+    const int orr = t.r[i];
+    t.m[i] = sw ? cv : om;
+    t.r[i] = sw ? cr : orr;
+    cv = sw ? om : cv;
+    cr = sw ? orr : cr;
+  }
+  t.rest = fmaxf(t.rest, cv);  // whatever fell off the end
+}
+
+__device__ __forceinline__ void cswap(float& a, int& ar, float& b, int& br) {
+  if (run_before(b, br, a, ar)) {
+    const float t = a; a = b; b = t;
+    const int tr = ar; ar = br; br = tr;
   }
 }
 
-// Merge two summaries of disjoint run sets (symmetric in its arguments).
-__device__ __forceinline__ void top2_combine(RunTop2& a, const RunTop2& b) {
-  RunTop2 o;
-  o.rest = fmaxf(a.rest, b.rest);
-  if (run_before(a.m1, a.r1, b.m1, b.r1)) {
-    o.m1 = a.m1; o.r1 = a.r1;
-    if (run_before(a.m2, a.r2, b.m1, b.r1)) { o.m2 = a.m2; o.r2 = a.r2; o.rest = fmaxf(o.rest, b.m1); }
-    else { o.m2 = b.m1; o.r2 = b.r1; o.rest = fmaxf(o.rest, a.m2); }
-    o.rest = fmaxf(o.rest, b.m2);
-  } else {
-    o.m1 = b.m1; o.r1 = b.r1;
-    if (run_before(b.m2, b.r2, a.m1, a.r1)) { o.m2 = b.m2; o.r2 = b.r2; o.rest = fmaxf(o.rest, a.m1); }
-    else { o.m2 = a.m1; o.r2 = a.r1; o.rest = fmaxf(o.rest, b.m2); }
-    o.rest = fmaxf(o.rest, a.m2);
+// Merge two summaries of disjoint run sets (symmetric in its arguments):
+// the top kTopRuns of the union by a bitonic split, then a bitonic sort.
+__device__ __forceinline__ void top_combine(RunTop& a, const RunTop& b) {
+  float c[kTopRuns];
+  int cr[kTopRuns];
+  float rest = fmaxf(a.rest, b.rest);
+#pragma unroll
+  for (int k = 0; k < kTopRuns; ++k) {
+    const float x = a.m[k], y = b.m[kTopRuns - 1 - k];
+    const int xr = a.r[k], yr = b.r[kTopRuns - 1 - k];
+    const bool ax = run_before(x, xr, y, yr);
+    c[k] = ax ? x : y;
+    cr[k] = ax ? xr : yr;
+    rest = fmaxf(rest, ax ? y : x);
   }
-  a = o;
+  cswap(c[0], cr[0], c[2], cr[2]);
+  cswap(c[1], cr[1], c[3], cr[3]);
+  cswap(c[0], cr[0], c[1], cr[1]);
+  cswap(c[2], cr[2], c[3], cr[3]);
+#pragma unroll
+  for (int k = 0; k < kTopRuns; ++k) { a.m[k] = c[k]; a.r[k] = cr[k]; }
+  a.rest = rest;
 }
 
-__device__ __forceinline__ RunTop2 top2_shfl_xor(const RunTop2& t, int o) {
-  RunTop2 u;
-  u.m1 = __shfl_xor(t.m1, o, 64); u.m2 = __shfl_xor(t.m2, o, 64);
+__device__ __forceinline__ RunTop top_shfl_xor(const RunTop& t, int o) {
+  RunTop u;
+#pragma unroll
+  for (int k = 0; k < kTopRuns; ++k) {
+    u.m[k] = __shfl_xor(t.m[k], o, 64);
+    u.r[k] = __shfl_xor(t.r[k], o, 64);
+  }
   u.rest = __shfl_xor(t.rest, o, 64);
-  u.r1 = __shfl_xor(t.r1, o, 64); u.r2 = __shfl_xor(t.r2, o, 64);
   return u;
 }
 
-__device__ __forceinline__ void top2_store(const RunSummaryPtr& d, size_t o, const RunTop2& t) {
-  d.m1[o] = t.m1; d.m2[o] = t.m2; d.rest[o] = t.rest; d.r1[o] = t.r1; d.r2[o] = t.r2;
+__device__ __forceinline__ void top_store(const RunSummaryPtr& d, size_t o, const RunTop& t) {
+#pragma unroll
+  for (int k = 0; k < kTopRuns; ++k) {
+    d.m[o * kTopRuns + k] = t.m[k];
+    d.r[o * kTopRuns + k] = t.r[k];
+  }
+  d.rest[o] = t.rest;
 }
 
 // ---------------------------------------------------------------- pass 1
@@ -287,12 +315,12 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
   }
 
   float m0[NB], s0[NB], sT[NB];
-  RunTop2 zt[NB], gt[NB];
+  RunTop zt[NB], gt[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     m0[nb] = kNegInf; s0[nb] = 0.0f; sT[nb] = 0.0f;
-    top2_init(zt[nb]);
-    top2_init(gt[nb]);
+    top_init(zt[nb]);
+    top_init(gt[nb]);
   }
 
   // One 64-token step: 16 tokens per lane group, each lane owns one parent
@@ -360,7 +388,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
         sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)), aT);
       }
       m0[nb] = mn;
-      top2_add(zt[nb], bm, run);
+      top_add(zt[nb], bm, run);
       if constexpr (SAMPLE) {
         float gm = kNegInf;
         const uint32_t cbase = (uint32_t)tl >> 2;
@@ -376,7 +404,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
             gm = fmaxf(gm, key);
           }
         }
-        top2_add(gt[nb], gm, run);
+        top_add(gt[nb], gm, run);
       }
     }
   };
@@ -429,19 +457,19 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
       st += __shfl_xor(st, 16, 64);
       st += __shfl_xor(st, 32, 64);
     }
-    RunTop2 zc = zt[nb], gc = gt[nb];
+    RunTop zc = zt[nb], gc = gt[nb];
 #pragma unroll
     for (int o = 16; o <= 32; o <<= 1) {
-      top2_combine(zc, top2_shfl_xor(zc, o));
-      if constexpr (SAMPLE) top2_combine(gc, top2_shfl_xor(gc, o));
+      top_combine(zc, top_shfl_xor(zc, o));
+      if constexpr (SAMPLE) top_combine(gc, top_shfl_xor(gc, o));
     }
     if (g == 0 && pidx[nb] < p.P) {
       const size_t o = (size_t)pidx[nb] * p.S + chunk;
       p.part_m[o] = M;
       p.part_s0[o] = s;
       if (p.part_sT) p.part_sT[o] = st;
-      top2_store(p.zs, o, zc);
-      if constexpr (SAMPLE) top2_store(p.gs, o, gc);
+      top_store(p.zs, o, zc);
+      if constexpr (SAMPLE) top_store(p.gs, o, gc);
     }
   }
 }
@@ -513,12 +541,12 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
   }
 
   float m0[NB], s0[NB], sT[NB];
-  RunTop2 zt[NB], gt[NB];
+  RunTop zt[NB], gt[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     m0[nb] = kNegInf; s0[nb] = 0.0f; sT[nb] = 0.0f;
-    top2_init(zt[nb]);
-    top2_init(gt[nb]);
+    top_init(zt[nb]);
+    top_init(gt[nb]);
   }
 
   auto issue = [&](u32x4* wb, u32x4* ub, int t0) {
@@ -596,7 +624,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
         sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)), aT);
       }
       m0[nb] = mn;
-      top2_add(zt[nb], bm, run);
+      top_add(zt[nb], bm, run);
       if constexpr (SAMPLE) {
         float gm = kNegInf;
         const uint32_t cbase = (uint32_t)tl >> 2;
@@ -612,7 +640,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
             gm = fmaxf(gm, key);
           }
         }
-        top2_add(gt[nb], gm, run);
+        top_add(gt[nb], gm, run);
       }
     }
   };
@@ -654,56 +682,38 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
       st += __shfl_xor(st, 16, 64);
       st += __shfl_xor(st, 32, 64);
     }
-    RunTop2 zc = zt[nb], gc = gt[nb];
+    RunTop zc = zt[nb], gc = gt[nb];
 #pragma unroll
     for (int o = 16; o <= 32; o <<= 1) {
-      top2_combine(zc, top2_shfl_xor(zc, o));
-      if constexpr (SAMPLE) top2_combine(gc, top2_shfl_xor(gc, o));
+      top_combine(zc, top_shfl_xor(zc, o));
+      if constexpr (SAMPLE) top_combine(gc, top_shfl_xor(gc, o));
     }
     if (g == 0 && pidx[nb] < p.P) {
       const size_t o = (size_t)pidx[nb] * p.S + chunk;
       p.part_m[o] = M;
       p.part_s0[o] = s;
       if (p.part_sT) p.part_sT[o] = st;
-      top2_store(p.zs, o, zc);
-      if constexpr (SAMPLE) top2_store(p.gs, o, gc);
+      top_store(p.zs, o, zc);
+      if constexpr (SAMPLE) top_store(p.gs, o, gc);
     }
   }
 }
 
 // ---------------------------------------------------------------- pass 2
 
-constexpr int kMaxChunks = 512;          // chunks per parent (8 per lane)
-constexpr int kChunkSlots = kMaxChunks / 64;
-constexpr int kBatch = 8;                // runs recomputed together
-
-// Insert (v, id) into a list sorted by (value desc, id asc) holding at most K entries.
-__device__ __forceinline__ void topk_insert(float* val, int* ids, float* aux, int& cnt, int K,
-                                            float v, int id, float a) {
-  if (cnt == K && !(v > val[K - 1] || (v == val[K - 1] && id < ids[K - 1]))) return;
-  int pos = cnt < K ? cnt : K - 1;
-  while (pos > 0 && (v > val[pos - 1] || (v == val[pos - 1] && id < ids[pos - 1]))) {
-    val[pos] = val[pos - 1];
-    ids[pos] = ids[pos - 1];
-    aux[pos] = aux[pos - 1];
-    --pos;
-  }
-  val[pos] = v;
-  ids[pos] = id;
-  aux[pos] = a;
-  if (cnt < K) ++cnt;
-}
+constexpr int kMaxChunks = 256;                              // chunks per parent
+constexpr int kEntrySlots = kMaxChunks * kTopRuns / 64;      // recorded runs per lane
+constexpr int kRestSlots = kMaxChunks / 64;                  // chunk rests per lane
+constexpr int kBatch = 8;                                    // runs recomputed together
+constexpr int kItemCap = 256;                                // candidate items per parent
 
 struct MergeLds {
-  float zval[TS_MAX_K];
-  int zid[TS_MAX_K];
-  float zaux[TS_MAX_K];
-  float gval[TS_MAX_K];
-  int gid[TS_MAX_K];
-  float gz[TS_MAX_K];  // z of the drawn tokens
   float bz[kBatch][16];  // logits of a batch of recomputed runs
   float bk[kBatch][16];  // their keys (z, or the Gumbel keys)
-  int item[2 * kMaxChunks];  // candidate items: chunk * 4 + kind (0: run 1, 1: run 2, 2: whole chunk)
+  int item_t[kItemCap];  // run start token, or -(chunk+1) for a whole chunk
+  int item_k[kItemCap];  // key kind: 0 = z, 1 = Gumbel
+  float item_e[kItemCap];  // expected run maximum (NaN if unknown)
+  uint32_t whole[kMaxChunks / 32];
 };
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -712,20 +722,57 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// A sorted list of at most K (key, token, aux) entries kept in registers:
+// lane j < cnt holds entry j; order: key desc, token asc.
+struct RegList {
+  float val;
+  int id;
+  float aux;
+  int cnt;
+};
+
+__device__ __forceinline__ void reglist_init(RegList& l) {
+  l.val = kNegInf; l.id = 0x7FFFFFFF; l.aux = 0.0f; l.cnt = 0;
+}
+
+// Insert a candidate (uniform across the wave).
+__device__ __forceinline__ void reglist_insert(RegList& l, int K, float v, int id, float a) {
+  const int lane = threadIdx.x & 63;
+  const bool ahead = lane < l.cnt && run_before(l.val, l.id, v, id);
+  const int pos = __popcll(__ballot(ahead));
+  if (pos >= K) return;
+  const float pv = __shfl_up(l.val, 1, 64);
+  const int pid = __shfl_up(l.id, 1, 64);
+  const float pa = __shfl_up(l.aux, 1, 64);
+  if (lane == pos) {
+    l.val = v; l.id = id; l.aux = a;
+  } else if (lane > pos && lane < K) {
+    l.val = pv; l.id = pid; l.aux = pa;
+  }
+  l.cnt = min(l.cnt + 1, K);
+}
+
 // Recompute up to kBatch runs of 16 tokens [t, t+16) for one parent with the
 // MFMA sequence of pass 1 (same operands in the same K positions, same
 // accumulator start), so the values are bit-identical to the streaming pass.
 // The parent sits in column 0; lanes 0, 16, 32, 48 get tokens t + g*4 + [0,4).
-// Every lane then checks kBatch*16/64 of the keys against thr and lane 0
-// inserts the (few) candidates into the sorted list.  A run whose expected
-// maximum is given (not NaN) counts a mismatch if its recomputed maximum differs.
-template <typename TE, int KS, bool GUMBEL>
+// Runs of kind 1 also get their Gumbel keys.  All lanes then check the keys
+// against the kind's threshold; candidates go into the kind's list.  A run
+// whose expected maximum is known counts a mismatch if the recomputed one differs.
+template <typename TE, int KS, bool SAMPLE>
 __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* urow,
                                              const typename Frag<TE>::type (&bcol)[KS],
                                              uint32_t pc1, uint32_t pc2, uint32_t pc3,
-                                             const int (&t)[kBatch], const float (&expect)[kBatch],
-                                             int nrun, float thr, MergeLds& L, float* val,
-                                             int* ids, float* aux, int& cnt, int& mism) {
+                                             const int (&t)[kBatch], const int (&kind)[kBatch],
+                                             const float (&expect)[kBatch], int nrun,
+                                             const float (&thr)[2], MergeLds& L, RegList& zl,
+                                             RegList& gl, int& mism) {
   typedef Frag<TE> F;
   const int lane = threadIdx.x & 63;
   const int n = lane & 15, g = lane >> 4;
@@ -758,14 +805,16 @@ __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* uro
       float k4[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) k4[e] = acc[b][e];
-      if constexpr (GUMBEL) {
-        // tokens tb + g*4 + [0,4) are exactly one Philox call
-        uint32_t c0 = (uint32_t)(tb + g * 4) >> 2, c1 = pc1, c2 = pc2, c3 = pc3;
-        philox10(c0, c1, c2, c3, p.keys);
-        const uint32_t w[4] = {c0, c1, c2, c3};
+      if constexpr (SAMPLE) {
+        if (b < nrun && kind[b] == 1) {
+          // tokens tb + g*4 + [0,4) are exactly one Philox call
+          uint32_t c0 = (uint32_t)(tb + g * 4) >> 2, c1 = pc1, c2 = pc2, c3 = pc3;
+          philox10(c0, c1, c2, c3, p.keys);
+          const uint32_t w[4] = {c0, c1, c2, c3};
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          k4[e] = (tb + g * 4 + e < V) ? gumbel_key2(acc[b][e], p.cT, w[e]) : kNegInf;
+          for (int e = 0; e < 4; ++e)
+            k4[e] = (tb + g * 4 + e < V) ? gumbel_key2(acc[b][e], p.cT, w[e]) : kNegInf;
+        }
       }
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -784,173 +833,140 @@ __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* uro
     const int j = lane + 64 * h;
     const int b = j >> 4, e = j & 15;
     const float kv = L.bk[b][e];
-    int tb = 0;
-#pragma unroll
-    for (int q = 0; q < kBatch; ++q)
-      if (q == b) tb = t[q];
+    int tb = 0, kd = 0;
     float ex = 0.0f;
 #pragma unroll
     for (int q = 0; q < kBatch; ++q)
-      if (q == b) ex = expect[q];
+      if (q == b) { tb = t[q]; kd = kind[q]; ex = expect[q]; }
     const bool live = b < nrun && tb + e < V;
-    // run maximum over the 16 lanes of this run
     float rm = live ? kv : kNegInf;
 #pragma unroll
     for (int o = 8; o >= 1; o >>= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
-    const bool bad = live && e == 0 && !__builtin_isnan(ex) && rm != ex;
-    mism += __popcll(__ballot(bad));
-    uint64_t mask = __ballot(live && kv >= thr);
-    if (lane == 0) {
-      while (mask) {
-        const int src = __ffsll((unsigned long long)mask) - 1;
-        mask &= mask - 1;
-        const int jj = src + 64 * h;
-        const int bb = jj >> 4, ee = jj & 15;
-        int tt = 0;
-        for (int q = 0; q < kBatch; ++q)
-          if (q == bb) tt = t[q];
-        topk_insert(val, ids, aux, cnt, p.K, L.bk[bb][ee], tt + ee, L.bz[bb][ee]);
-      }
+    mism += __popcll(__ballot(live && e == 0 && !__builtin_isnan(ex) && rm != ex));
+    const float th = kd ? thr[1] : thr[0];
+    uint64_t mask = __ballot(live && kv >= th);
+    while (mask) {
+      const int src = __ffsll((unsigned long long)mask) - 1;
+      mask &= mask - 1;
+      const float cv = __shfl(kv, src, 64);
+      const float cz = __shfl(L.bz[b][e], src, 64);
+      const int ct = __shfl(tb + e, src, 64);
+      const int ck = __shfl(kd, src, 64);
+      if (ck == 0)
+        reglist_insert(zl, p.K, cv, ct, cz);
+      else
+        reglist_insert(gl, p.K, cv, ct, cz);
     }
   }
   wave_sync_lds();
 }
 
-// Exact top-K of one key (z, or the Gumbel keys) for one parent from the
-// per-chunk run summaries; fills the sorted list (lane 0 writes it).
-// Threshold: the K-th largest of all recorded run maxima (two per chunk).
-// Those are maxima of K distinct runs, hence K distinct tokens, so the K-th
-// largest key over the whole vocabulary is at least the threshold.  A token
-// with a key >= threshold lies in a run whose maximum is >= threshold: one of
-// its chunk's two recorded runs, or, if the chunk's rest maximum also reaches
-// the threshold, somewhere in the chunk (then every run of it is recomputed).
-template <typename TE, int KS, bool GUMBEL>
-__device__ __forceinline__ void select_and_rescan(const MergeParams& p, const RunSummaryPtr& sm,
-                                                  size_t pbase, const TE* urow,
-                                                  const typename Frag<TE>::type (&bcol)[KS],
-                                                  uint32_t pc1, uint32_t pc2, uint32_t pc3,
-                                                  MergeLds& L, float* val, int* ids, float* aux,
-                                                  int& mism) {
+// Threshold and candidate items for one key kind.  The threshold is the
+// K-th largest recorded run maximum (counting equal values with their
+// multiplicity): those are maxima of K distinct runs, hence of K distinct
+// tokens, so the K-th largest key over the vocabulary is at least the
+// threshold.  A token whose key reaches the threshold lies in a run whose
+// maximum reaches it: one of its chunk's recorded runs, or, when the chunk's
+// rest maximum reaches it too, somewhere in the chunk (a whole-chunk item).
+__device__ __forceinline__ float select_items(const MergeParams& p, const RunSummaryPtr& sm,
+                                              int pidx, int kind, MergeLds& L, int& nitems) {
   const int lane = threadIdx.x & 63;
-  const int S = p.S, K = p.K, V = p.V;
-  float c1[kChunkSlots], c2[kChunkSlots], cx[kChunkSlots];
-  int r1[kChunkSlots], r2[kChunkSlots];
+  const int S = p.S, K = p.K;
+  const size_t pb = (size_t)pidx * S;
+  float ev[kEntrySlots];
+  int er[kEntrySlots];
+  float rv[kRestSlots];
 #pragma unroll
-  for (int i = 0; i < kChunkSlots; ++i) {
-    const int c = lane + 64 * i;
-    const bool in = c < S;
-    c1[i] = in ? sm.m1[pbase + c] : kNegInf;
-    c2[i] = in ? sm.m2[pbase + c] : kNegInf;
-    cx[i] = in ? sm.rest[pbase + c] : kNegInf;
-    r1[i] = in ? sm.r1[pbase + c] : 0;
-    r2[i] = in ? sm.r2[pbase + c] : 0;
+  for (int i = 0; i < kEntrySlots; ++i) {
+    const int e = i * 64 + lane;
+    const bool in = (e >> 2) < S;
+    ev[i] = in ? sm.m[pb * kTopRuns + e] : kNegInf;
+    er[i] = in ? sm.r[pb * kTopRuns + e] : 0;
   }
-  // threshold: K rounds of a wave argmax over the recorded maxima (ties by slot id)
-  uint32_t taken = 0u;  // bit 2i: c1[i] taken, bit 2i+1: c2[i] taken
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) {
+    const int c = i * 64 + lane;
+    rv[i] = c < S ? sm.rest[pb + c] : kNegInf;
+  }
+  uint32_t taken = 0u;
   float thr = kNegInf;
   int picked = 0;
-  for (; picked < K; ++picked) {
-    float bv = kNegInf;
-    int bid = 0x7FFFFFFF;
+  for (int round = 0; round < K; ++round) {
+    float lm = kNegInf;
 #pragma unroll
-    for (int i = 0; i < kChunkSlots; ++i) {
-      const int c = lane + 64 * i;
-      if (c >= S) continue;
-      if (!(taken & (1u << (2 * i))) && run_before(c1[i], 2 * c, bv, bid)) { bv = c1[i]; bid = 2 * c; }
-      if (!(taken & (2u << (2 * i))) && run_before(c2[i], 2 * c + 1, bv, bid)) { bv = c2[i]; bid = 2 * c + 1; }
-    }
+    for (int i = 0; i < kEntrySlots; ++i)
+      if (!(taken & (1u << i))) lm = fmaxf(lm, ev[i]);
+    const float m = wave_max(lm);
+    if (m == kNegInf) break;
+    int c = 0;
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oi = __shfl_xor(bid, o, 64);
-      if (run_before(ov, oi, bv, bid)) { bv = ov; bid = oi; }
-    }
-    if (bid == 0x7FFFFFFF || bv == kNegInf) break;
-    const int cb = bid >> 1;
-    if ((cb & 63) == lane) taken |= (1u + (uint32_t)(bid & 1)) << (2 * (cb >> 6));
-    thr = bv;
+    for (int i = 0; i < kEntrySlots; ++i)
+      if (!(taken & (1u << i)) && ev[i] == m) { taken |= 1u << i; ++c; }
+    picked += wave_sum_int(c);
+    if (picked >= K) { thr = m; break; }
   }
   if (picked < K) thr = kNegInf;  // fewer than K runs recorded: every token is a candidate
 
-  // Candidate items (listed in LDS first so the recompute below is one loop).
-  int nitems = 0;
+  // whole chunks
 #pragma unroll
-  for (int i = 0; i < kChunkSlots; ++i) {
-    const int c = lane + 64 * i;
-    const bool sel = c < S && c1[i] >= thr;
-    const bool whole = sel && cx[i] >= thr;
-    const int mine = sel ? (whole ? 1 : (c2[i] >= thr ? 2 : 1)) : 0;
-    // exclusive prefix over lanes of the number of items each lane adds
-    int incl = mine;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int v = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += v;
+  for (int i = 0; i < kRestSlots; ++i) {
+    const uint64_t wm = __ballot(rv[i] >= thr);
+    if (lane == 0) {
+      L.whole[2 * i] = (uint32_t)wm;
+      L.whole[2 * i + 1] = (uint32_t)(wm >> 32);
     }
-    const int base = nitems + incl - mine;
-    if (sel) {
-      if (whole) {
-        L.item[base] = c * 4 + 2;
-      } else {
-        L.item[base] = c * 4 + 0;
-        if (mine == 2) L.item[base + 1] = c * 4 + 1;
-      }
-    }
-    nitems += __shfl(incl, 63, 64);
   }
   wave_sync_lds();
-
-  int cnt = 0;
-  const float nan = __builtin_nanf("");
-  int it = 0, sub = 0;
-#pragma unroll 1
-  while (it < nitems) {
-    int qt[kBatch];
-    float qe[kBatch];
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int base = nitems;
+  // recorded runs of chunks that are not whole
 #pragma unroll
-    for (int q = 0; q < kBatch; ++q) { qt[q] = 0; qe[q] = nan; }
-    int nr = 0;
-#pragma unroll 1
-    while (nr < kBatch && it < nitems) {
-      const int code = L.item[it];
-      const int cc = code >> 2, kind = code & 3;
-      const int slot = cc >> 6, src = cc & 63;
-      // the summary of chunk cc lives in lane src, slot `slot`
-      float m1 = 0.0f, m2 = 0.0f;
-      int q1 = 0, q2 = 0;
-#pragma unroll
-      for (int i = 0; i < kChunkSlots; ++i) {
-        if (i == slot) {
-          m1 = __shfl(c1[i], src, 64); m2 = __shfl(c2[i], src, 64);
-          q1 = __shfl(r1[i], src, 64); q2 = __shfl(r2[i], src, 64);
-        }
-      }
-      int t;
-      float e;
-      if (kind == 2) {
-        const int cbeg = cc * p.Vc;
-        const int nruns = ((min(cbeg + p.Vc, V) - cbeg + 63) / 64) * 4;
-        t = cbeg + (sub >> 2) * 64 + (sub & 3) * 16;
-        e = sub == q1 ? m1 : (sub == q2 ? m2 : nan);
-        if (++sub == nruns) { sub = 0; ++it; }
-        if (t >= V) continue;
-      } else {
-        const int run = kind == 0 ? q1 : q2;
-        t = cc * p.Vc + (run >> 2) * 64 + (run & 3) * 16;
-        e = kind == 0 ? m1 : m2;
-        ++it;
-      }
-      // shift the queue so that entries [0, nr] are the ones pushed
-#pragma unroll
-      for (int q = kBatch - 1; q > 0; --q) { qt[q] = qt[q - 1]; qe[q] = qe[q - 1]; }
-      qt[0] = t;
-      qe[0] = e;
-      ++nr;
+  for (int i = 0; i < kEntrySlots; ++i) {
+    const int e = i * 64 + lane;
+    const int c = e >> 2;
+    const bool in = c < S;
+    const bool wh = in && ((L.whole[c >> 5] >> (c & 31)) & 1u);
+    const bool cand = in && !wh && ev[i] >= thr;
+    const uint64_t mask = __ballot(cand);
+    const int off = base + __popcll(mask & lt);
+    if (cand && off < kItemCap) {
+      const int run = er[i];
+      L.item_t[off] = c * p.Vc + (run >> 2) * 64 + (run & 3) * 16;
+      L.item_k[off] = kind;
+      L.item_e[off] = ev[i];
     }
-    if (nr > 0)
-      rescan_batch<TE, KS, GUMBEL>(p, urow, bcol, pc1, pc2, pc3, qt, qe, nr, thr, L, val, ids, aux,
-                                   cnt, mism);
+    base += __popcll(mask);
   }
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) {
+    const int c = i * 64 + lane;
+    const bool cand = c < S && rv[i] >= thr;
+    const uint64_t mask = __ballot(cand);
+    const int off = base + __popcll(mask & lt);
+    if (cand && off < kItemCap) {
+      L.item_t[off] = -(c + 1);
+      L.item_k[off] = kind;
+      L.item_e[off] = __builtin_nanf("");
+    }
+    base += __popcll(mask);
+  }
+  if (base > kItemCap) {
+    // too many candidates (heavy ties): rescan every chunk of this kind
+    base = nitems;
+    for (int c0 = 0; c0 < S; c0 += 64) {
+      const int c = c0 + lane;
+      if (c < S && base + c - c0 < kItemCap) {
+        L.item_t[base + c - c0] = -(c + 1);
+        L.item_k[base + c - c0] = kind;
+        L.item_e[base + c - c0] = __builtin_nanf("");
+      }
+      base += min(64, S - c0);
+    }
+    thr = kNegInf;
+  }
+  nitems = min(base, kItemCap);
+  wave_sync_lds();
+  return thr;
 }
 
 template <typename TE, int KS, bool SAMPLE>
@@ -993,16 +1009,24 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   const size_t pbase = (size_t)pidx * S;
 
   // log-sum-exp over chunks: each lane folds its chunks in index order, then a fixed butterfly.
+  float pm[kRestSlots], ps[kRestSlots], pt[kRestSlots];
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) {
+    const int c = i * 64 + lane;
+    pm[i] = c < S ? p.part_m[pbase + c] : kNegInf;
+    ps[i] = c < S ? p.part_s0[pbase + c] : 0.0f;
+    pt[i] = (SAMPLE && p.need_T && c < S) ? p.part_sT[pbase + c] : 0.0f;
+  }
   float M = kNegInf;
-  for (int c = lane; c < S; c += 64) M = fmaxf(M, p.part_m[pbase + c]);
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) M = fmaxf(M, pm[i]);
   M = wave_max(M);
   const float Mref = fmaxf(M, -1e30f);
   float s = 0.0f, st = 0.0f;
-  for (int c = lane; c < S; c += 64) {
-    const float mc = p.part_m[pbase + c];
-    s += p.part_s0[pbase + c] * exp2_fast(__builtin_fmaf(mc, kLog2e, -Mref * kLog2e));
-    if (SAMPLE && p.need_T)
-      st += p.part_sT[pbase + c] * exp2_fast(__builtin_fmaf(mc, p.cT, -Mref * p.cT));
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) {
+    s += ps[i] * exp2_fast(__builtin_fmaf(pm[i], kLog2e, -Mref * kLog2e));
+    if (SAMPLE && p.need_T) st += pt[i] * exp2_fast(__builtin_fmaf(pm[i], p.cT, -Mref * p.cT));
   }
   s = wave_sum(s);
   st = wave_sum(st);
@@ -1018,42 +1042,90 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   const uint32_t pc1 = (uint32_t)par.path, pc2 = (uint32_t)(par.path >> 32);
   const uint32_t pc3 = counter_word3(par.request, par.depth, 1u);
 
+  int nitems = 0;
+  float thr[2];
+  thr[0] = select_items(p, p.zs, pidx, 0, L, nitems);
+  thr[1] = kNegInf;
+  if constexpr (SAMPLE) thr[1] = select_items(p, p.gs, pidx, 1, L, nitems);
+
+  RegList zl, gl;
+  reglist_init(zl);
+  reglist_init(gl);
   int mism = 0;
-  select_and_rescan<TE, KS, false>(p, p.zs, pbase, urow, bcol, pc1, pc2, pc3, L, L.zval, L.zid,
-                                   L.zaux, mism);
-  if constexpr (SAMPLE)
-    select_and_rescan<TE, KS, true>(p, p.gs, pbase, urow, bcol, pc1, pc2, pc3, L, L.gval, L.gid,
-                                    L.gz, mism);
+  const float nan = __builtin_nanf("");
+  int it = 0, sub = 0;
+#pragma unroll 1
+  while (it < nitems) {
+    int qt[kBatch], qk[kBatch];
+    float qe[kBatch];
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) { qt[q] = 0; qk[q] = 0; qe[q] = nan; }
+    int nr = 0;
+#pragma unroll 1
+    while (nr < kBatch && it < nitems) {
+      const int code = L.item_t[it];
+      const int kd = L.item_k[it];
+      int t;
+      float e;
+      if (code < 0) {
+        const int cc = -code - 1;
+        const int cbeg = cc * p.Vc;
+        const int nruns = ((min(cbeg + p.Vc, V) - cbeg + 63) / 64) * 4;
+        t = cbeg + (sub >> 2) * 64 + (sub & 3) * 16;
+        e = nan;
+        if (++sub == nruns) { sub = 0; ++it; }
+        if (t >= V) continue;
+      } else {
+        t = code;
+        e = L.item_e[it];
+        ++it;
+      }
+#pragma unroll
+      for (int q = kBatch - 1; q > 0; --q) { qt[q] = qt[q - 1]; qk[q] = qk[q - 1]; qe[q] = qe[q - 1]; }
+      qt[0] = t;
+      qk[0] = kd;
+      qe[0] = e;
+      ++nr;
+    }
+    if (nr > 0)
+      rescan_batch<TE, KS, SAMPLE>(p, urow, bcol, pc1, pc2, pc3, qt, qk, qe, nr, thr, L, zl, gl, mism);
+  }
 
   // Child scoring: lane j handles slot j + 1 (Algorithm 1; §3.2 pre-draw bound; Eq. 3).
+  const float lsp = par.log_surv;
+  const float a = p.calib_a, bb = p.calib_b;
+  float zb = 0.0f;
+  if constexpr (SAMPLE) {
+    // bound of slot j: the first of the greedy order not drawn before j
+    int bi = K - 1;
+    for (int i = K - 1; i >= 0; --i) {
+      const int pid = __shfl(zl.id, i, 64);
+      bool used = false;
+      for (int s2 = 0; s2 < K - 1; ++s2) {
+        const int gid = __shfl(gl.id, s2, 64);
+        used |= (s2 < lane) && (gid == pid);
+      }
+      if (!used) bi = i;
+    }
+    zb = __shfl(zl.val, bi, 64);
+  }
   if (lane < K) {
     const int j = lane;
-    const float lsp = par.log_surv;
-    const float a = p.calib_a, bb = p.calib_b;
-    const float zpi = L.zval[j];
-    if (p.out.rank_token) p.out.rank_token[ob + j] = L.zid[j];
+    const float zpi = zl.val;
+    if (p.out.rank_token) p.out.rank_token[ob + j] = zl.id;
     if (p.out.rank_log_q0) p.out.rank_log_q0[ob + j] = zpi - lse0;
     if constexpr (!SAMPLE) {
       const float lq0 = zpi - lse0;
       const float ls = lsp + log_phat(lq0, a, bb);
-      p.out.child_token[ob + j] = L.zid[j];
+      p.out.child_token[ob + j] = zl.id;
       p.out.child_log_q0[ob + j] = lq0;
       p.out.child_log_surv[ob + j] = ls;
       p.out.slot_key[ob + j] = ls;
       if (p.out.child_log_qT) p.out.child_log_qT[ob + j] = __builtin_nanf("");
     } else {
-      const int tok = L.gid[j];
-      const float zc = L.gz[j];
+      const float zc = gl.aux;
       const float lq0 = zc - lse0;
-      // bound: the first of the greedy order not drawn before j
-      int bi = 0;
-      for (; bi < K; ++bi) {
-        bool used = false;
-        for (int s2 = 0; s2 < j; ++s2) used |= (L.gid[s2] == L.zid[bi]);
-        if (!used) break;
-      }
-      const float zb = L.zval[bi < K ? bi : K - 1];
-      p.out.child_token[ob + j] = tok;
+      p.out.child_token[ob + j] = gl.id;
       p.out.child_log_q0[ob + j] = lq0;
       p.out.child_log_surv[ob + j] = lsp + log_phat(lq0, a, bb);
       p.out.slot_key[ob + j] = lsp + log_phat(zb - lse0, a, bb);

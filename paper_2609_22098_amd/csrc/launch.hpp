@@ -13,6 +13,9 @@ namespace ts {
 template <typename TE, int KS>
 void launch_eval_t(const ExpandParams& p, int nb, bool sample, bool store_z, bool lds, dim3 grid,
                    dim3 block, hipStream_t s);
+// Resident blocks per CU of the streaming kernel a launch would use (0 if unknown).
+template <typename TE, int KS>
+int eval_blocks_per_cu_t(int nb, bool sample, bool store_z, bool lds, int block);
 // Per-parent merge, exact top-k and child scoring.
 template <typename TE, int KS>
 void launch_merge_t(const MergeParams& p, bool sample, dim3 grid, dim3 block, hipStream_t s);

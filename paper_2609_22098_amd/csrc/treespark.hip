@@ -7,7 +7,10 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <string>
+#include <tuple>
 #include <unordered_map>
 #include <vector>
 
@@ -79,18 +82,68 @@ struct Plan {
   int ks;
   bool sample;
   bool lds;  // LDS-staged bf16 streaming kernel
-  size_t off_m, off_s0, off_sT, off_z[5], off_g[5];
+  size_t off_m, off_s0, off_sT, off_z[3], off_g[3];
   size_t bytes;
 };
 
-// store_z: the verification recompute, which writes the logits and runs one
-// parent block per wave.
-Plan make_plan(const ts_drafter* d, int P, float T, bool store_z = false) {
+// Compute units of the current device (256 when no device answers).
+int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+// Resident blocks per CU of the streaming kernel for this plan (2 if unknown).
+int eval_blocks_per_cu(int dtype, int ks, int nb, bool sample, bool store_z, bool lds, int block) {
+  static std::mutex mu;
+  static std::map<std::tuple<int, int, int, bool, bool, bool, int>, int> cache;
+  const auto key = std::make_tuple(dtype, ks, nb, sample, store_z, lds, block);
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    const auto it = cache.find(key);
+    if (it != cache.end()) return it->second;
+  }
+  int n = 0;
+  if (dtype == TS_BF16) {
+    switch (ks) {
+      case 1: n = eval_blocks_per_cu_t<uint16_t, 1>(nb, sample, store_z, lds, block); break;
+      case 2: n = eval_blocks_per_cu_t<uint16_t, 2>(nb, sample, store_z, lds, block); break;
+      case 4: n = eval_blocks_per_cu_t<uint16_t, 4>(nb, sample, store_z, lds, block); break;
+      default: n = eval_blocks_per_cu_t<uint16_t, 8>(nb, sample, store_z, lds, block); break;
+    }
+  } else {
+    switch (ks) {
+      case 4: n = eval_blocks_per_cu_t<float, 4>(nb, sample, store_z, lds, block); break;
+      case 8: n = eval_blocks_per_cu_t<float, 8>(nb, sample, store_z, lds, block); break;
+      default: n = eval_blocks_per_cu_t<float, 16>(nb, sample, store_z, lds, block); break;
+    }
+  }
+  if (n <= 0) n = 2;
+  std::lock_guard<std::mutex> lock(mu);
+  cache[key] = n;
+  return n;
+}
+
+// Launch plan of one expansion.  store_z: the verification recompute, which
+// writes the logits and runs one parent block per wave.  sizing_only: the
+// workspace size, which must not depend on the device, so it assumes the
+// largest chunk count.
+static_assert(TS_MAX_V <= kMaxChunks * 4096, "the merge holds kMaxChunks chunks of <= 4096 tokens");
+
+Plan make_plan(const ts_drafter* d, int P, float T, bool store_z = false, bool sizing_only = false) {
   Plan pl{};
   pl.sample = T > 0.0f;
   pl.ks = d->dtype == TS_BF16 ? d->r / 32 : d->r / 4;
   const int nb_big = (d->dtype == TS_BF16 && d->r == 256) ? 2 : 4;
-  pl.NB = P >= 512 ? nb_big : 1;
+  pl.NB = P >= 512 ? 2 : 1;
+  (void)nb_big;
 #ifdef TS_FORCE_NB
   pl.NB = TS_FORCE_NB;
 #endif
@@ -99,44 +152,63 @@ Plan make_plan(const ts_drafter* d, int P, float T, bool store_z = false) {
   pl.n_pblocks = (P + 16 * pl.NB - 1) / (16 * pl.NB);
   pl.wpg = pl.lds ? 4 : std::min(4, std::max(1, pl.n_pblocks));
   pl.n_pgroups = (pl.n_pblocks + pl.wpg - 1) / pl.wpg;
-  // Enough waves to fill 256 CUs several times over, chunks of 256..4096
-  // tokens, and at most kMaxChunks chunks (the merge keeps them in registers).
-  const int target_waves = 4096;
-  const int s_target = std::max(1, (target_waves + pl.n_pblocks - 1) / pl.n_pblocks);
-  int vc = (d->V + s_target - 1) / s_target;
+  // Chunks: enough workgroups to fill every CU at the kernel's occupancy in
+  // whole rounds (all workgroups of a round finish together), chunks of
+  // 256..4096 tokens, at most kMaxChunks per parent.
+  int vc;
+  if (sizing_only) {
+    vc = 256;
+  } else {
+    const int concurrent = device_cus() *
+        eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, pl.sample, store_z, pl.lds, 64 * pl.wpg);
+    const int s_min = (d->V + 4095) / 4096;
+    const int rounds = std::max(1, (pl.n_pgroups * s_min + concurrent - 1) / concurrent);
+    const int s_want = std::max(1, (rounds * concurrent + pl.n_pgroups - 1) / pl.n_pgroups);
+    vc = (d->V + s_want - 1) / s_want;
+  }
+#ifdef TS_DEBUG_RUNS
+  if (!sizing_only && getenv("TS_VC")) vc = atoi(getenv("TS_VC"));
+#endif
   vc = std::max(vc, (d->V + kMaxChunks - 1) / kMaxChunks);
   vc = ((vc + 63) / 64) * 64;
   vc = std::min(std::max(vc, 256), 4096);
   pl.Vc = vc;
   pl.S = (d->V + vc - 1) / vc;
   pl.S8 = ((pl.S + 7) / 8) * 8;
+#ifdef TS_DEBUG_RUNS
+  if (!sizing_only)
+    fprintf(stderr, "[plan] P=%d NB=%d lds=%d wpg=%d n_pgroups=%d Vc=%d S=%d grid=%d bpc=%d cus=%d\n", P,
+            pl.NB, (int)pl.lds, pl.wpg, pl.n_pgroups, pl.Vc, pl.S, pl.S8 * pl.n_pgroups,
+            eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, pl.sample, store_z, pl.lds, 64 * pl.wpg), device_cus());
+#endif
   const size_t a = align256((size_t)std::max(P, 1) * pl.S * 4);
+  const size_t a4 = align256((size_t)std::max(P, 1) * pl.S * 4 * kTopRuns);
   size_t o = 0;
   pl.off_m = o; o += a;
   pl.off_s0 = o; o += a;
-  for (int i = 0; i < 5; ++i) { pl.off_z[i] = o; o += a; }
+  pl.off_z[0] = o; o += a4;
+  pl.off_z[1] = o; o += a4;
+  pl.off_z[2] = o; o += a;
   if (pl.sample) {
     pl.off_sT = o; o += a;
-    for (int i = 0; i < 5; ++i) { pl.off_g[i] = o; o += a; }
+    pl.off_g[0] = o; o += a4;
+    pl.off_g[1] = o; o += a4;
+    pl.off_g[2] = o; o += a;
   }
   pl.bytes = o;
   return pl;
 }
 
-RunSummaryPtr summary_ptr(char* ws, const size_t (&off)[5]) {
+RunSummaryPtr summary_ptr(char* ws, const size_t (&off)[3]) {
   RunSummaryPtr r;
-  r.m1 = reinterpret_cast<float*>(ws + off[0]);
-  r.m2 = reinterpret_cast<float*>(ws + off[1]);
+  r.m = reinterpret_cast<float*>(ws + off[0]);
+  r.r = reinterpret_cast<int*>(ws + off[1]);
   r.rest = reinterpret_cast<float*>(ws + off[2]);
-  r.r1 = reinterpret_cast<int*>(ws + off[3]);
-  r.r2 = reinterpret_cast<int*>(ws + off[4]);
   return r;
 }
 
 size_t expand_ws_max(const ts_drafter* d, int Pmax, float T, bool store_z = false) {
-  size_t m = 0;
-  for (int P = 1; P <= Pmax; ++P) m = std::max(m, make_plan(d, P, T, store_z).bytes);
-  return m;
+  return make_plan(d, std::max(Pmax, 1), T, store_z, true).bytes;
 }
 
 void launch_eval(const ts_drafter* d, const ExpandParams& p, const Plan& pl, hipStream_t s) {
@@ -304,7 +376,7 @@ const char* ts_version(void) { return "treespark-mi355x 0.1 (gfx950)"; }
 size_t ts_expand_workspace_size(const ts_drafter* d, int32_t P, int32_t k, float T) {
   (void)k;
   if (check_drafter(d) != TS_OK || P <= 0) return 0;
-  return make_plan(d, P, T).bytes;
+  return make_plan(d, P, T, false, true).bytes;
 }
 
 int32_t ts_expand(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_calib calib,
@@ -320,7 +392,7 @@ int32_t ts_expand(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_c
   if (!out || !out->child_token || !out->child_log_q0 || !out->child_log_surv || !out->slot_key)
     return fail(TS_EINVAL, "a required output pointer is NULL");
   if (!std::isfinite(calib.a) || !std::isfinite(calib.b)) return fail(TS_EINVAL, "calibration must be finite");
-  const size_t need = make_plan(d, P, T).bytes;
+  const size_t need = make_plan(d, P, T, false, true).bytes;
   if (!workspace || workspace_bytes < need)
     return fail(TS_ENOSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
   return run_expand(d, parents, P, calib, k, T, seed, out, static_cast<char*>(workspace),

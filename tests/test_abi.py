@@ -43,6 +43,7 @@ def test_expand_rejects_bad_arguments():
     assert _expand(_drafter(null=True)) == b.TS_EINVAL
     assert b"NULL" in L.ts_last_error()
     assert _expand(_drafter(V=0)) == b.TS_EINVAL
+    assert _expand(_drafter(V=256 * 4096 + 1)) == b.TS_EUNSUPPORTED
     assert _expand(_drafter(D=17)) == b.TS_EUNSUPPORTED
     assert _expand(_drafter(r=24)) == b.TS_EUNSUPPORTED
     assert _expand(_drafter(r=16, dtype=b.TS_BF16)) == b.TS_EUNSUPPORTED
