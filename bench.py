@@ -76,7 +76,7 @@ class HipEvents:
         return t.value
 
 
-def copy_calibration(gib):
+def copy_calibration(gib, args_out=""):
     """A plain device copy of known size, for scaling the FETCH_SIZE / WRITE_SIZE counters."""
     import torch
     n = int(gib * (1 << 30))
@@ -85,7 +85,62 @@ def copy_calibration(gib):
     for _ in range(3):
         b.copy_(a)
     torch.cuda.synchronize()
-    print(json.dumps({"copy_bytes": n, "launches": 3}))
+    rec = {"copy_bytes": n, "launches": 3}
+    if args_out:
+        os.makedirs(args_out, exist_ok=True)
+        with open(os.path.join(args_out, "copy.json"), "w") as f:
+            json.dump(rec, f)
+    print(json.dumps(rec))
+
+
+EVAL_KERNEL = "expand_eval_lds_kernel"
+
+
+def _counter_per_dispatch(run_dir, counter, name_part):
+    """Per-dispatch totals of one counter (summed over its hardware instances) for the
+    kernels whose name contains name_part, from a rocprofv3 --pmc csv directory, as
+    (grid size, value) pairs."""
+    import csv
+    import glob
+    tot, grid = {}, {}
+    for f in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            for row in csv.DictReader(fh):
+                if row["Counter_Name"] != counter or name_part not in row["Kernel_Name"]:
+                    continue
+                key = (f, row["Dispatch_Id"])
+                tot[key] = tot.get(key, 0.0) + float(row["Counter_Value"])
+                grid[key] = int(row["Grid_Size"])
+    return [(grid[k], v) for k, v in tot.items()]
+
+
+def _largest_grid(pairs):
+    g = max(p[0] for p in pairs)
+    return [v for gk, v in pairs if gk == g]
+
+
+def write_traffic(root, T):
+    """HBM bytes per launch of the streaming pass from FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch), each scaled by what the same counter reads for a plain copy of known size."""
+    with open(os.path.join(root, "copy_fetch", "copy.json")) as f:
+        copy_bytes = json.load(f)["copy_bytes"]
+    scale = {}
+    for counter, sub in (("FETCH_SIZE", "copy_fetch"), ("WRITE_SIZE", "copy_write")):
+        vals = _counter_per_dispatch(os.path.join(root, sub), counter, "")
+        kib = max(v for _, v in vals)  # the copy is by far the largest dispatch of its run
+        scale[counter] = copy_bytes / (kib * 1024.0)
+    # the serving frontier's launch is the largest-grid launch of the streaming pass in a step
+    fetch = _largest_grid(_counter_per_dispatch(os.path.join(root, "fetch"), "FETCH_SIZE", EVAL_KERNEL))
+    write = _largest_grid(_counter_per_dispatch(os.path.join(root, "write"), "WRITE_SIZE", EVAL_KERNEL))
+    fb = float(np.mean(fetch)) * 1024.0 * scale["FETCH_SIZE"]
+    wb = float(np.mean(write)) * 1024.0 * scale["WRITE_SIZE"]
+    rec = {"kernel": EVAL_KERNEL, "T": T, "kernel_source_hash": kernel_source_hash(),
+           "fetch_kib_per_dispatch": float(np.mean(fetch)), "write_kib_per_dispatch": float(np.mean(write)),
+           "dispatches": [len(fetch), len(write)], "copy_bytes": copy_bytes,
+           "copy_scale": scale, "fetch_bytes": fb, "write_bytes": wb, "bytes_per_launch": fb + wb}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
 
 
 def cpu_baseline(dr, fr, K, T, seed, seconds):
@@ -107,14 +162,21 @@ def cpu_baseline(dr, fr, K, T, seed, seconds):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--expand-only", action="store_true", help="time only ts_expand (profiling runs)")
     ap.add_argument("--T", type=float, default=0.7, help="temperature (the workload uses 0.7)")
     ap.add_argument("--copy-gib", type=float, default=0.0, help="run only the copy calibration")
+    ap.add_argument("--copy-out", default="", help="directory for the copy calibration record")
+    ap.add_argument("--traffic-from", default="",
+                    help="directory holding the four FETCH_SIZE / WRITE_SIZE counter runs "
+                         "(fetch, write, copy_fetch, copy_write); writes the traffic file and exits")
     args = ap.parse_args()
+    if args.traffic_from:
+        write_traffic(args.traffic_from, args.T)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the draft-tree step has no "
               f"multi-GPU path in this build.", file=sys.stderr)
@@ -125,7 +187,7 @@ def main():
     binding.lib()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_gib > 0:
-        copy_calibration(args.copy_gib)
+        copy_calibration(args.copy_gib, args.copy_out)
         return
 
     w = synth.WORKLOADS[3]
@@ -224,7 +286,7 @@ def main():
                                             ": 2048-parent ts_expand + best-first trees + T=0.7 verification"),
                    "V": dr.V, "D": dr.D, "r": dr.r, "requests": dr.R, "frontier_parents": P, "K": K,
                    "T": T, "N": N, "tree_evals_per_step": 0 if args.expand_only else tree_evals},
-        "roofline": {"bound": "hbm", "kernel": "expand_eval (streaming pass of ts_expand)",
+        "roofline": {"bound": "hbm", "kernel": EVAL_KERNEL + " (streaming pass of ts_expand)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": float(eval_ms.mean())},

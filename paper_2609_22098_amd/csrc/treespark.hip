@@ -340,8 +340,21 @@ BuildLayout build_layout(const ts_drafter* d, int N, int K, float T) {
 }
 
 struct VerifyLayout {
-  size_t off_rows, off_arg, off_gap, off_items, off_res, off_par, off_z, off_exp, bytes;
+  size_t off_rows, off_arg, off_gap, off_items, off_res, off_par, off_z, off_exp;
+  size_t off_pa, off_zp, off_bp, bytes;
+  int max_chunks;
 };
+
+// Vocabulary chunks per item for the T > 0 passes: about 2048 workgroups in
+// all, chunks a multiple of kVChunkQuantum tokens.
+void verify_chunks(int V, int nitems, int* nchunks, int* chunk) {
+  const int max_chunks = (V + kVChunkQuantum - 1) / kVChunkQuantum;
+  int nc = std::min(max_chunks, std::max(1, (2048 + nitems - 1) / std::max(nitems, 1)));
+  int len = (V + nc - 1) / nc;
+  len = ((len + kVChunkQuantum - 1) / kVChunkQuantum) * kVChunkQuantum;
+  *chunk = len;
+  *nchunks = (V + len - 1) / len;
+}
 
 VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
   VerifyLayout v{};
@@ -357,6 +370,11 @@ VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
     v.off_par = o; o += align256((size_t)d->R * sizeof(ts_parent));
     v.off_z = o; o += align256((size_t)d->R * d->V * 4);
     v.off_exp = o; o += expand_ws_max(d, d->R, T, true);
+    v.max_chunks = (d->V + kVChunkQuantum - 1) / kVChunkQuantum;
+    const size_t ic = (size_t)d->R * v.max_chunks;
+    v.off_pa = o; o += align256(ic * sizeof(VPartA));
+    v.off_zp = o; o += align256(ic * TS_MAX_K * sizeof(double));
+    v.off_bp = o; o += align256(ic * sizeof(VBonusPart));
   }
   v.bytes = o;
   return v;
@@ -661,7 +679,23 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
       TS_HIP(hipGetLastError());
     }
     TS_HIP(hipMemcpyAsync(ditems, items.data(), ni * sizeof(VerifyItem), hipMemcpyHostToDevice, s));
-    launch_verify_stage(target, target_dtype == TS_BF16, cap, V, ditems, ni, zbuf, T, keys, dres, s);
+    VerifyPass vp{};
+    vp.target = target;
+    vp.cap = cap;
+    vp.V = V;
+    vp.items = ditems;
+    vp.nitems = ni;
+    vp.zbuf = zbuf;
+    vp.c = kLog2e / T;
+    vp.keys = keys;
+    verify_chunks(V, ni, &vp.nchunks, &vp.chunk);
+    vp.pa = reinterpret_cast<VPartA*>(ws + vl.off_pa);
+    vp.zp = reinterpret_cast<double*>(ws + vl.off_zp);
+    vp.bp = reinterpret_cast<VBonusPart*>(ws + vl.off_bp);
+    vp.results = dres;
+    int mmax = 0;
+    for (const VerifyItem& it : items) mmax = std::max(mmax, it.m);
+    launch_verify_level(vp, target_dtype == TS_BF16, mmax, s);
     TS_HIP(hipGetLastError());
     res.resize(ni);
     TS_HIP(hipMemcpyAsync(res.data(), dres, ni * sizeof(VerifyResult), hipMemcpyDeviceToHost, s));

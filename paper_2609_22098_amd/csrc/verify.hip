@@ -13,17 +13,20 @@ void launch_verify_argmax(const void* target, bool bf16, int V, const int* rows,
                        static_cast<const float*>(target), V, rows, nrows, argmax_out, gap_out);
 }
 
-void launch_verify_stage(const void* target, bool bf16, int cap, int V, const VerifyItem* items,
-                         int nitems, const float* zbuf, float T, PhiloxKeys keys,
-                         VerifyResult* results, hipStream_t s) {
+template <typename TT>
+static void verify_level_t(const VerifyPass& vp, int mmax, hipStream_t s) {
+  const dim3 grid(vp.nitems * vp.nchunks), block(kVerifyThreads);
+  hipLaunchKernelGGL((verify_pass_a_kernel<TT>), grid, block, 0, s, vp);
+  for (int j = 1; j <= mmax; ++j) hipLaunchKernelGGL((verify_stage_kernel<TT>), grid, block, 0, s, vp, j);
+  hipLaunchKernelGGL((verify_bonus_kernel<TT>), grid, block, 0, s, vp);
+  hipLaunchKernelGGL((verify_resolve_kernel<TT>), dim3(vp.nitems), dim3(64), 0, s, vp);
+}
+
+void launch_verify_level(const VerifyPass& vp, bool bf16, int mmax, hipStream_t s) {
   if (bf16)
-    hipLaunchKernelGGL((verify_stage_kernel<uint16_t>), dim3(nitems), dim3(kVerifyThreads), 0, s,
-                       static_cast<const uint16_t*>(target), cap, V, items, nitems, zbuf, T, keys,
-                       results);
+    verify_level_t<uint16_t>(vp, mmax, s);
   else
-    hipLaunchKernelGGL((verify_stage_kernel<float>), dim3(nitems), dim3(kVerifyThreads), 0, s,
-                       static_cast<const float*>(target), cap, V, items, nitems, zbuf, T, keys,
-                       results);
+    verify_level_t<float>(vp, mmax, s);
 }
 
 }  // namespace ts
