@@ -23,7 +23,7 @@ void launch_merge_t(const MergeParams& p, bool sample, dim3 grid, dim3 block, hi
 // Verification.
 void launch_verify_argmax(const void* target, bool bf16, int V, const int* rows, int nrows,
                           int* argmax_out, float* gap_out, hipStream_t s);
-// One level of the T > 0 walk: pass A, stages 1..mmax, bonus, resolve.
+// One level of the T > 0 walk: pass A, stages 1..max(mmax, 1), bonus, resolve.
 void launch_verify_level(const VerifyPass& vp, bool bf16, int mmax, hipStream_t s);
 
 }  // namespace ts

@@ -39,6 +39,29 @@ int32_t fail(int32_t code, const char* fmt, ...) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Page-locked host staging for the small transfers of the host loops, so that
+// they are true asynchronous DMA copies.  One buffer per host thread, grown on
+// demand and kept until the process ends; every user synchronises its stream
+// before it rewrites or grows the buffer.
+struct HostStage {
+  char* p = nullptr;
+  size_t n = 0;
+};
+int32_t host_stage(size_t bytes, char** out) {
+  thread_local HostStage st;
+  if (st.n < bytes) {
+    if (st.p) TS_HIP(hipHostFree(st.p));
+    st.p = nullptr;
+    st.n = 0;
+    void* q = nullptr;
+    TS_HIP(hipHostMalloc(&q, bytes, hipHostMallocDefault));
+    st.p = static_cast<char*>(q);
+    st.n = bytes;
+  }
+  *out = st.p;
+  return TS_OK;
+}
+
 // ---------------------------------------------------------------- checks
 
 int32_t check_drafter(const ts_drafter* d) {
@@ -141,9 +164,7 @@ Plan make_plan(const ts_drafter* d, int P, float T, bool store_z = false, bool s
   Plan pl{};
   pl.sample = T > 0.0f;
   pl.ks = d->dtype == TS_BF16 ? d->r / 32 : d->r / 4;
-  const int nb_big = (d->dtype == TS_BF16 && d->r == 256) ? 2 : 4;
   pl.NB = P >= 512 ? 2 : 1;
-  (void)nb_big;
 #ifdef TS_FORCE_NB
   pl.NB = TS_FORCE_NB;
 #endif
@@ -319,7 +340,7 @@ inline bool slot_before(const Slot& a, const Slot& b) {
 }
 
 struct BuildLayout {
-  size_t off_par, off_tok, off_q0, off_qT, off_ls, off_key, off_exp, bytes;
+  size_t off_par, off_out, off_exp, bytes;
   int Pmax;
 };
 
@@ -329,11 +350,7 @@ BuildLayout build_layout(const ts_drafter* d, int N, int K, float T) {
   const size_t pk = align256((size_t)b.Pmax * K * 4);
   size_t o = 0;
   b.off_par = o; o += align256((size_t)b.Pmax * sizeof(ts_parent));
-  b.off_tok = o; o += pk;
-  b.off_q0 = o; o += pk;
-  b.off_qT = o; o += pk;
-  b.off_ls = o; o += pk;
-  b.off_key = o; o += pk;
+  b.off_out = o; o += 5 * pk;  // child token, log q0, log qT, log S, key: [P][K] each, packed
   b.off_exp = o; o += expand_ws_max(d, b.Pmax, T);
   b.bytes = o;
   return b;
@@ -341,7 +358,7 @@ BuildLayout build_layout(const ts_drafter* d, int N, int K, float T) {
 
 struct VerifyLayout {
   size_t off_rows, off_arg, off_gap, off_items, off_res, off_par, off_z, off_exp;
-  size_t off_pa, off_zp, off_bp, bytes;
+  size_t off_pa, off_zp, off_bp, off_cst, off_rec, bytes;
   int max_chunks;
 };
 
@@ -375,6 +392,8 @@ VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
     v.off_pa = o; o += align256(ic * sizeof(VPartA));
     v.off_zp = o; o += align256(ic * TS_MAX_K * sizeof(double));
     v.off_bp = o; o += align256(ic * sizeof(VBonusPart));
+    v.off_cst = o; o += align256((size_t)d->R * sizeof(VConst));
+    v.off_rec = o; o += align256((size_t)d->R * TS_MAX_K * sizeof(VRec));
   }
   v.bytes = o;
   return v;
@@ -448,11 +467,9 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
   char* ws = static_cast<char*>(workspace);
   ts_parent* dpar = reinterpret_cast<ts_parent*>(ws + bl.off_par);
   ts_expand_out eo{};
-  eo.child_token = reinterpret_cast<int32_t*>(ws + bl.off_tok);
-  eo.child_log_q0 = reinterpret_cast<float*>(ws + bl.off_q0);
-  eo.child_log_qT = reinterpret_cast<float*>(ws + bl.off_qT);
-  eo.child_log_surv = reinterpret_cast<float*>(ws + bl.off_ls);
-  eo.slot_key = reinterpret_cast<float*>(ws + bl.off_key);
+  char* hs = nullptr;
+  const size_t hs_par = align256((size_t)bl.Pmax * sizeof(ts_parent));
+  if ((rc = host_stage(hs_par + (size_t)5 * bl.Pmax * K * 4, &hs)) != TS_OK) return rc;
 
   std::vector<float> log_theta(R);
   for (int q = 0; q < R; ++q) log_theta[q] = theta[q] > 0.0f ? logf(theta[q]) : -INFINITY;
@@ -461,20 +478,27 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
   std::vector<int32_t> evals(R, 0);
   if (N > 0)
     for (int q = 0; q < R; ++q) frontier.push_back(ts_parent{anchor[q], 0, q, 0.0f, 0});
-  std::vector<int32_t> h_tok;
-  std::vector<float> h_q0, h_qT, h_ls, h_key;
   while (!frontier.empty()) {
     const int P = (int)frontier.size();
-    TS_HIP(hipMemcpyAsync(dpar, frontier.data(), P * sizeof(ts_parent), hipMemcpyHostToDevice, s));
+    const size_t nk = (size_t)P * K;
+    // this wave's five outputs, packed, so that one copy brings them back
+    char* dout = ws + bl.off_out;
+    eo.child_token = reinterpret_cast<int32_t*>(dout);
+    eo.child_log_q0 = reinterpret_cast<float*>(dout + nk * 4);
+    eo.child_log_qT = reinterpret_cast<float*>(dout + nk * 8);
+    eo.child_log_surv = reinterpret_cast<float*>(dout + nk * 12);
+    eo.slot_key = reinterpret_cast<float*>(dout + nk * 16);
+    std::memcpy(hs, frontier.data(), P * sizeof(ts_parent));
+    TS_HIP(hipMemcpyAsync(dpar, hs, P * sizeof(ts_parent), hipMemcpyHostToDevice, s));
     rc = run_expand(d, dpar, P, calib, K, T, seed, &eo, ws + bl.off_exp, s);
     if (rc != TS_OK) return rc;
-    const size_t nk = (size_t)P * K;
-    h_tok.resize(nk); h_q0.resize(nk); h_qT.resize(nk); h_ls.resize(nk); h_key.resize(nk);
-    TS_HIP(hipMemcpyAsync(h_tok.data(), eo.child_token, nk * 4, hipMemcpyDeviceToHost, s));
-    TS_HIP(hipMemcpyAsync(h_q0.data(), eo.child_log_q0, nk * 4, hipMemcpyDeviceToHost, s));
-    TS_HIP(hipMemcpyAsync(h_qT.data(), eo.child_log_qT, nk * 4, hipMemcpyDeviceToHost, s));
-    TS_HIP(hipMemcpyAsync(h_ls.data(), eo.child_log_surv, nk * 4, hipMemcpyDeviceToHost, s));
-    TS_HIP(hipMemcpyAsync(h_key.data(), eo.slot_key, nk * 4, hipMemcpyDeviceToHost, s));
+    char* hout = hs + hs_par;
+    TS_HIP(hipMemcpyAsync(hout, dout, nk * 20, hipMemcpyDeviceToHost, s));
+    const int32_t* h_tok = reinterpret_cast<const int32_t*>(hout);
+    const float* h_q0 = reinterpret_cast<const float*>(hout + nk * 4);
+    const float* h_qT = reinterpret_cast<const float*>(hout + nk * 8);
+    const float* h_ls = reinterpret_cast<const float*>(hout + nk * 12);
+    const float* h_key = reinterpret_cast<const float*>(hout + nk * 16);
     TS_HIP(hipStreamSynchronize(s));
     for (int i = 0; i < P; ++i) {
       const ts_parent& par = frontier[i];
@@ -614,11 +638,14 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     int* drows = reinterpret_cast<int*>(ws + vl.off_rows);
     int* darg = reinterpret_cast<int*>(ws + vl.off_arg);
     float* dgap = reinterpret_cast<float*>(ws + vl.off_gap);
-    TS_HIP(hipMemcpyAsync(drows, rows.data(), nrows * 4, hipMemcpyHostToDevice, s));
+    char* hs = nullptr;
+    if ((rc = host_stage((size_t)nrows * 8, &hs)) != TS_OK) return rc;
+    std::memcpy(hs, rows.data(), (size_t)nrows * 4);
+    TS_HIP(hipMemcpyAsync(drows, hs, nrows * 4, hipMemcpyHostToDevice, s));
     launch_verify_argmax(target, target_dtype == TS_BF16, V, drows, nrows, darg, dgap, s);
     TS_HIP(hipGetLastError());
-    std::vector<int> arg(nrows);
-    TS_HIP(hipMemcpyAsync(arg.data(), darg, nrows * 4, hipMemcpyDeviceToHost, s));
+    const int* arg = reinterpret_cast<const int*>(hs + (size_t)nrows * 4);
+    TS_HIP(hipMemcpyAsync(hs + (size_t)nrows * 4, darg, nrows * 4, hipMemcpyDeviceToHost, s));
     TS_HIP(hipStreamSynchronize(s));
     int base = 0;
     for (int q = 0; q < R; ++q) {
@@ -648,7 +675,11 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
   for (int q = 0; q < R; ++q) active[q] = q;
   std::vector<VerifyItem> items;
   std::vector<ts_parent> zpar;
-  std::vector<VerifyResult> res;
+  char* hs = nullptr;
+  const size_t hs_items = align256((size_t)R * sizeof(VerifyItem));
+  const size_t hs_par = align256((size_t)R * sizeof(ts_parent));
+  if ((rc = host_stage(hs_items + hs_par + (size_t)R * sizeof(VerifyResult), &hs)) != TS_OK) return rc;
+  const VerifyResult* res = reinterpret_cast<const VerifyResult*>(hs + hs_items + hs_par);
   while (!active.empty()) {
     items.clear();
     zpar.clear();
@@ -672,13 +703,15 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     const int ni = (int)items.size();
     if (!zpar.empty()) {
       const int P = (int)zpar.size();
-      TS_HIP(hipMemcpyAsync(dpar, zpar.data(), P * sizeof(ts_parent), hipMemcpyHostToDevice, s));
+      std::memcpy(hs + hs_items, zpar.data(), P * sizeof(ts_parent));
+      TS_HIP(hipMemcpyAsync(dpar, hs + hs_items, P * sizeof(ts_parent), hipMemcpyHostToDevice, s));
       const Plan pl = make_plan(d, P, T, true);
       const ExpandParams ep = eval_params(d, dpar, P, T, seed, pl, ws + vl.off_exp, zbuf);
       launch_eval(d, ep, pl, s);
       TS_HIP(hipGetLastError());
     }
-    TS_HIP(hipMemcpyAsync(ditems, items.data(), ni * sizeof(VerifyItem), hipMemcpyHostToDevice, s));
+    std::memcpy(hs, items.data(), ni * sizeof(VerifyItem));
+    TS_HIP(hipMemcpyAsync(ditems, hs, ni * sizeof(VerifyItem), hipMemcpyHostToDevice, s));
     VerifyPass vp{};
     vp.target = target;
     vp.cap = cap;
@@ -692,13 +725,14 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     vp.pa = reinterpret_cast<VPartA*>(ws + vl.off_pa);
     vp.zp = reinterpret_cast<double*>(ws + vl.off_zp);
     vp.bp = reinterpret_cast<VBonusPart*>(ws + vl.off_bp);
+    vp.consts = reinterpret_cast<VConst*>(ws + vl.off_cst);
+    vp.recs = reinterpret_cast<VRec*>(ws + vl.off_rec);
     vp.results = dres;
     int mmax = 0;
     for (const VerifyItem& it : items) mmax = std::max(mmax, it.m);
     launch_verify_level(vp, target_dtype == TS_BF16, mmax, s);
     TS_HIP(hipGetLastError());
-    res.resize(ni);
-    TS_HIP(hipMemcpyAsync(res.data(), dres, ni * sizeof(VerifyResult), hipMemcpyDeviceToHost, s));
+    TS_HIP(hipMemcpyAsync(hs + hs_items + hs_par, dres, ni * sizeof(VerifyResult), hipMemcpyDeviceToHost, s));
     TS_HIP(hipStreamSynchronize(s));
     std::vector<int> next;
     for (int i = 0; i < ni; ++i) {

@@ -16,10 +16,11 @@ void launch_verify_argmax(const void* target, bool bf16, int V, const int* rows,
 template <typename TT>
 static void verify_level_t(const VerifyPass& vp, int mmax, hipStream_t s) {
   const dim3 grid(vp.nitems * vp.nchunks), block(kVerifyThreads);
+  const int J = mmax > 1 ? mmax : 1;
   hipLaunchKernelGGL((verify_pass_a_kernel<TT>), grid, block, 0, s, vp);
-  for (int j = 1; j <= mmax; ++j) hipLaunchKernelGGL((verify_stage_kernel<TT>), grid, block, 0, s, vp, j);
-  hipLaunchKernelGGL((verify_bonus_kernel<TT>), grid, block, 0, s, vp);
-  hipLaunchKernelGGL((verify_resolve_kernel<TT>), dim3(vp.nitems), dim3(64), 0, s, vp);
+  for (int j = 1; j <= J; ++j) hipLaunchKernelGGL((verify_stage_kernel<TT>), grid, block, 0, s, vp, j);
+  hipLaunchKernelGGL((verify_bonus_kernel<TT>), grid, block, 0, s, vp, J);
+  hipLaunchKernelGGL((verify_resolve_kernel<TT>), dim3(vp.nitems), dim3(64), 0, s, vp, J);
 }
 
 void launch_verify_level(const VerifyPass& vp, bool bf16, int mmax, hipStream_t s) {

@@ -121,12 +121,14 @@ struct VerifyResult {
 // ---- T > 0: passes over (item, vocabulary chunk) workgroups ----------------
 //
 // One level of the walk is a fixed sequence of launches over the items (the
-// requests still walking, each at its current node): pass A, stages 1..m_max,
-// the bonus pass and the resolve kernel.  No launch needs the host in between:
-// every workgroup first rebuilds its item's state (normalisers, alpha, beta,
-// the stages already decided) from the chunk partials of the earlier
-// launches, in one fixed order, so all workgroups of an item agree bit for bit.
-// All logits are handled in base-2 units (x = logit * log2(e) / T).
+// requests still walking, each at its current node): pass A, stages
+// 1..max(m_max, 1), the bonus pass and the resolve kernel.  No launch needs the
+// host in between.  The stage-1 launch turns the pass-A partials into the
+// item's constants; each stage launch then advances the item's record (alpha,
+// beta, the decision so far) by one stage from the previous launch's record
+// and Z partials.  Every workgroup of an item computes that step in the same
+// fixed order, so they agree bit for bit, and chunk 0 stores it.  All logits
+// are handled in base-2 units (x = logit * log2(e) / T).
 
 constexpr int kVChunkQuantum = 4 * kVerifyThreads;  // tokens per sweep of a workgroup
 
@@ -142,6 +144,9 @@ struct VBonusPart {  // per (item, chunk): best and second-best bonus key
   int32_t idx, pad;
 };
 
+struct VConst;
+struct VRec;
+
 struct VerifyPass {
   const void* target;  // [R][cap][V]
   int cap, V;
@@ -154,6 +159,8 @@ struct VerifyPass {
   VPartA* pa;          // [nitems][nchunks]
   double* zp;          // [TS_MAX_K][nitems][nchunks]: chunk shares of Z_j
   VBonusPart* bp;      // [nitems][nchunks]
+  VConst* consts;      // [nitems]: written by the stage-1 launch
+  VRec* recs;          // [TS_MAX_K][nitems]: record after the launch of stage j, at j - 1
   VerifyResult* results;
 };
 
@@ -163,19 +170,49 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return v;
 }
 
-// State of one item after the stages before `upto` (computed by one whole
-// wave; every lane ends with the same values).
-struct VState {
-  float Lt, Lz;       // base-2 log normalisers of p = softmax(t/T) and qT = softmax(z/T)
-  float alpha, beta;  // residual p_s = max(alpha p - beta qT, 0) at the stage reached
-  float betap;        // beta + 1 / R_s at the stage reached
-  int accepted;       // stage (1-based) whose child was accepted, 0 if none so far
-  int reached;        // stage reached (its test rejected or not run), m + 1 after all
-  float margin;       // smallest |log u - log ratio| over the tests run (natural log)
+// Per-item constants of one level, written by the stage-1 launch: the base-2
+// log normalisers and, for each child s in draw order, log2 p(x_s), log2 qT(x_s),
+// log2 R_s, 1/R_s and log2 u_s of its acceptance test.
+struct VConst {
+  float Lt, Lz;
+  float lp[TS_MAX_K], lq[TS_MAX_K], lR[TS_MAX_K], invR[TS_MAX_K], lu[TS_MAX_K];
 };
 
+// Walk state after the launch of stage j.
+enum : int32_t { kRejected = 0, kAccepted = 1, kExhausted = 2 };
+struct VRec {
+  float alpha, beta;  // residual p_s = max(alpha p - beta qT, 0) at the stage reached
+  float betap;        // beta + 1 / R_s when status == kRejected (the Z_s pass uses it)
+  float margin;       // smallest |log u - log ratio| of the tests run (natural log)
+  int32_t status;     // kRejected at `stage` (Z_stage pending), kAccepted at `stage`, kExhausted
+  int32_t stage;
+};
+
+// Acceptance test of child s with the residual (alpha, beta) (wave-uniform).
+__device__ __forceinline__ VRec stage_test(float lp, float lq, float lR, float invR, float lu, int s,
+                                           float alpha, float beta, float margin) {
+  VRec r;
+  float lpj;
+  if (s == 1) {
+    lpj = lp;
+  } else {
+    const float pj = alpha * exp2_fast(lp) - beta * exp2_fast(lq);
+    lpj = pj > 0.0f ? __builtin_amdgcn_logf(pj) : kNegInf;
+  }
+  const float lr = lpj - (lq - lR);
+  r.alpha = alpha;
+  r.beta = beta;
+  r.betap = beta + invR;
+  r.margin = fminf(margin, fabsf(lu - lr) * kLn2);
+  r.status = lu < lr ? kAccepted : kRejected;
+  r.stage = s;
+  return r;
+}
+
+// Constants of item `it` from the pass-A partials (one whole wave; every lane
+// ends with the same values).
 template <typename TT>
-__device__ VState verify_state(const VerifyPass& vp, const VerifyItem& item, int it, int upto) {
+__device__ VConst verify_consts(const VerifyPass& vp, const VerifyItem& item, int it) {
   const int lane = threadIdx.x & 63;
   const int nc = vp.nchunks;
   const VPartA* pa = vp.pa + (size_t)it * nc;
@@ -193,77 +230,80 @@ __device__ VState verify_state(const VerifyPass& vp, const VerifyItem& item, int
   }
   st = wave_sum_f64(st);
   snc = wave_sum_f64(snc);
-  VState v;
-  v.Lt = mt + (float)log2(st);
-  v.alpha = 1.0f;
-  v.beta = 0.0f;
-  v.betap = 1.0f;
-  v.accepted = 0;
-  v.reached = 1;
-  v.margin = __builtin_huge_valf();
-  v.Lz = 0.0f;
+  VConst C;
+  C.Lt = mt + (float)log2(st);
+  C.Lz = 0.0f;
   const int m = item.m;
-  if (m == 0) return v;
+#pragma unroll
+  for (int k = 0; k < TS_MAX_K; ++k) {
+    C.lp[k] = 0.0f; C.lq[k] = 0.0f; C.lR[k] = 0.0f; C.invR[k] = 0.0f; C.lu[k] = 0.0f;
+  }
+  if (m == 0) return C;
   const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
   const float* zrow = vp.zbuf + (size_t)item.zrow * vp.V;
-  // suffix sums of the proposal mass: suf[s] = non-children + children s..m
+  // suffix sums of the proposal mass: suf[s] = non-children + children s..m-1
+  float wz[TS_MAX_K];
   double suf[TS_MAX_K + 1];
   {
     double acc = snc;
     suf[TS_MAX_K] = acc;
 #pragma unroll
     for (int s = TS_MAX_K - 1; s >= 0; --s) {
-      if (s < m) acc += (double)exp2_fast(zrow[item.child_tok[s]] * vp.c - mz);
+      wz[s] = 0.0f;
+      if (s < m) {
+        wz[s] = zrow[item.child_tok[s]] * vp.c;
+        acc += (double)exp2_fast(wz[s] - mz);
+      }
       suf[s] = acc;
     }
   }
-  v.Lz = mz + (float)log2(suf[0]);
+  C.Lz = mz + (float)log2(suf[0]);
   const uint32_t pc1 = (uint32_t)item.path, pc2 = (uint32_t)(item.path >> 32);
   const uint32_t c3 = counter_word3(item.request, item.depth, 2u);
-  const int last = upto < m ? upto : m;
-#pragma unroll 1
-  for (int s = 1; s <= last; ++s) {
-    const int x = item.child_tok[s - 1];
-    const float lp = target_at(trow, x) * vp.c - v.Lt;
-    const float lq = zrow[x] * vp.c - v.Lz;
-    float lpj;
-    if (s == 1) {
-      lpj = lp;
-    } else {
-      const float pj = v.alpha * exp2_fast(lp) - v.beta * exp2_fast(lq);
-      lpj = pj > 0.0f ? __builtin_amdgcn_logf(pj) : kNegInf;
-    }
-    double Rs = 0.0;
 #pragma unroll
-    for (int k = 0; k < TS_MAX_K; ++k)
-      if (k == s - 1) Rs = suf[k] / suf[0];
-    const float lr = lpj - (lq - (float)log2(Rs));
-    uint32_t w0 = (uint32_t)s, w1 = pc1, w2 = pc2, w3 = c3;
-    philox10(w0, w1, w2, w3, vp.keys);
-    const float lu = __builtin_amdgcn_logf(word_to_uniform(w0));
-    v.margin = fminf(v.margin, fabsf(lu - lr) * kLn2);
-    v.betap = v.beta + (float)(1.0 / Rs);
-    v.reached = s;
-    if (lu < lr) {
-      v.accepted = s;
-      return v;
+  for (int s = 0; s < TS_MAX_K; ++s) {
+    if (s < m) {
+      const double Rs = suf[s] / suf[0];
+      C.lp[s] = target_at(trow, item.child_tok[s]) * vp.c - C.Lt;
+      C.lq[s] = wz[s] - C.Lz;
+      C.lR[s] = (float)log2(Rs);
+      C.invR[s] = (float)(1.0 / Rs);
+      uint32_t w0 = (uint32_t)(s + 1), w1 = pc1, w2 = pc2, w3 = c3;
+      philox10(w0, w1, w2, w3, vp.keys);
+      C.lu[s] = __builtin_amdgcn_logf(word_to_uniform(w0));
     }
-    if (s == upto) return v;  // the caller reduces Z_s
-    const double* zs = vp.zp + ((size_t)(s - 1) * vp.nitems + it) * nc;
-    double Z = 0.0;
-    for (int k = lane; k < nc; k += 64) Z += zs[k];
-    Z = wave_sum_f64(Z);
-    if (Z > 0.0) {
-      v.alpha = (float)(v.alpha / Z);
-      v.beta = (float)(v.betap / Z);
-    }
-    v.reached = s + 1;
   }
-  return v;
+  return C;
 }
 
-// Shares the state of wave 0 with the workgroup.
-__device__ __forceinline__ VState share_state(const VState& v, VState* sh) {
+// Record after the launch of stage j >= 2 from the record of stage j - 1.
+__device__ VRec verify_advance(const VerifyPass& vp, const VConst& C, const VRec& prev, int m, int it, int j) {
+  if (prev.status != kRejected) return prev;
+  const int lane = threadIdx.x & 63;
+  const double* zs = vp.zp + ((size_t)(prev.stage - 1) * vp.nitems + it) * vp.nchunks;
+  double Z = 0.0;
+  for (int k = lane; k < vp.nchunks; k += 64) Z += zs[k];
+  Z = wave_sum_f64(Z);
+  float alpha = prev.alpha, beta = prev.beta;
+  if (Z > 0.0) {
+    alpha = (float)(alpha / Z);
+    beta = (float)(prev.betap / Z);
+  }
+  if (j <= m) {
+    const int k = j - 1;
+    return stage_test(C.lp[k], C.lq[k], C.lR[k], C.invR[k], C.lu[k], j, alpha, beta, prev.margin);
+  }
+  VRec r = prev;
+  r.alpha = alpha;
+  r.beta = beta;
+  r.status = kExhausted;
+  r.stage = j;
+  return r;
+}
+
+// Shares a value computed by wave 0 with the workgroup.
+template <typename S>
+__device__ __forceinline__ S share(const S& v, S* sh) {
   if (threadIdx.x == 0) *sh = v;
   __syncthreads();
   return *sh;
@@ -350,36 +390,63 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
   }
 }
 
-// Stage j: if the item's walk reaches stage j and child j is rejected, this
-// workgroup adds its chunk's share of Z_j = sum max(alpha_j p - beta'_j qT, 0)
-// over tokens not drawn up to j.
+// Stage j: advances the item's record by one stage (the stage-1 launch also
+// builds the constants); if child j is rejected, this workgroup adds its
+// chunk's share of Z_j = sum max(alpha_j p - beta'_j qT, 0) over tokens not
+// drawn up to j.  Chunk 0 stores the record for the next launch.
 template <typename TT>
 __global__ __launch_bounds__(kVerifyThreads) void verify_stage_kernel(VerifyPass vp, int j) {
-  __shared__ VState sh;
+  __shared__ VRec shr;
+  __shared__ VConst shc;
   __shared__ double redd[4];
   __shared__ int loc[TS_MAX_K];
   __shared__ int cnt;
   const int it = blockIdx.x / vp.nchunks, ck = blockIdx.x % vp.nchunks;
   if (it >= vp.nitems) return;
   const VerifyItem& item = vp.items[it];
-  if (item.m < j) return;
-  VState v;
-  if (threadIdx.x < 64) v = verify_state<TT>(vp, item, it, j);
-  v = share_state(v, &sh);
-  if (v.accepted != 0 || v.reached != j) return;
+  VRec rec;
+  if (j == 1) {
+    VConst C;
+    if (threadIdx.x < 64) {
+      C = verify_consts<TT>(vp, item, it);
+      if (item.m == 0) {
+        rec.alpha = 1.0f; rec.beta = 0.0f; rec.betap = 1.0f;
+        rec.margin = __builtin_huge_valf();
+        rec.status = kExhausted;
+        rec.stage = 1;
+      } else {
+        rec = stage_test(C.lp[0], C.lq[0], C.lR[0], C.invR[0], C.lu[0], 1, 1.0f, 0.0f,
+                         __builtin_huge_valf());
+      }
+      if (ck == 0 && threadIdx.x == 0) vp.consts[it] = C;
+    }
+    C = share(C, &shc);
+    rec = share(rec, &shr);
+  } else {
+    if (threadIdx.x < 64) {
+      const VRec prev = vp.recs[(size_t)(j - 2) * vp.nitems + it];
+      rec = prev;
+      if (prev.status == kRejected) rec = verify_advance(vp, vp.consts[it], prev, item.m, it, j);
+    }
+    rec = share(rec, &shr);
+  }
+  if (ck == 0 && threadIdx.x == 0) vp.recs[(size_t)(j - 1) * vp.nitems + it] = rec;
+  if (rec.status != kRejected || rec.stage != j) return;
+  const VConst& C = vp.consts[it];
   const int y0 = ck * vp.chunk, y1 = min(vp.V, y0 + vp.chunk);
   const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
   const float* zrow = vp.zbuf + (size_t)item.zrow * vp.V;
   const int nloc = chunk_children(item, j, y0, y1, loc, &cnt);
+  const float Lt = j == 1 ? shc.Lt : C.Lt, Lz = j == 1 ? shc.Lz : C.Lz;
   float acc = 0.0f;
   for (int b = y0 + 4 * threadIdx.x; b < y1; b += kVChunkQuantum) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int y = b + e;
       if (y < y1 && !(nloc && is_listed(y, loc, nloc))) {
-        const float p = exp2_fast(target_at(trow, y) * vp.c - v.Lt);
-        const float q = exp2_fast(zrow[y] * vp.c - v.Lz);
-        acc += fmaxf(v.alpha * p - v.betap * q, 0.0f);
+        const float p = exp2_fast(target_at(trow, y) * vp.c - Lt);
+        const float q = exp2_fast(zrow[y] * vp.c - Lz);
+        acc += fmaxf(rec.alpha * p - rec.betap * q, 0.0f);
       }
     }
   }
@@ -387,11 +454,19 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stage_kernel(VerifyPass
   if (threadIdx.x == 0) vp.zp[((size_t)(j - 1) * vp.nitems + it) * vp.nchunks + ck] = z;
 }
 
+// Final record of an item after the last stage launch (stage J): a pending
+// rejection at J is folded into the residual.
+__device__ __forceinline__ VRec verify_final(const VerifyPass& vp, const VerifyItem& item, int it, int J) {
+  const VRec prev = vp.recs[(size_t)(J - 1) * vp.nitems + it];
+  if (prev.status != kRejected) return prev;
+  return verify_advance(vp, vp.consts[it], prev, item.m, it, J + 1);
+}
+
 // Bonus: when every child was rejected (or there is none), the chunk's best
 // Gumbel-max key log2 r(y) - log2(-log2 u_y) over the final residual r.
 template <typename TT>
-__global__ __launch_bounds__(kVerifyThreads) void verify_bonus_kernel(VerifyPass vp) {
-  __shared__ VState sh;
+__global__ __launch_bounds__(kVerifyThreads) void verify_bonus_kernel(VerifyPass vp, int J) {
+  __shared__ VRec sh;
   __shared__ float redv[4];
   __shared__ int redi[4];
   __shared__ int loc[TS_MAX_K];
@@ -399,10 +474,11 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_bonus_kernel(VerifyPass
   const int it = blockIdx.x / vp.nchunks, ck = blockIdx.x % vp.nchunks;
   if (it >= vp.nitems) return;
   const VerifyItem& item = vp.items[it];
-  VState v;
-  if (threadIdx.x < 64) v = verify_state<TT>(vp, item, it, TS_MAX_K + 1);
-  v = share_state(v, &sh);
-  if (v.accepted != 0) return;
+  VRec v;
+  if (threadIdx.x < 64) v = verify_final(vp, item, it, J);
+  v = share(v, &sh);
+  if (v.status == kAccepted) return;
+  const float Lt = vp.consts[it].Lt, Lz = vp.consts[it].Lz;
   const int y0 = ck * vp.chunk, y1 = min(vp.V, y0 + vp.chunk);
   const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
   const float* zrow = item.m > 0 ? vp.zbuf + (size_t)item.zrow * vp.V : nullptr;
@@ -420,11 +496,11 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_bonus_kernel(VerifyPass
       if (y >= y1) break;
       float l2r;
       if (!zrow) {
-        l2r = target_at(trow, y) * vp.c - v.Lt;
+        l2r = target_at(trow, y) * vp.c - Lt;
       } else {
         if (nloc && is_listed(y, loc, nloc)) continue;
-        const float p = exp2_fast(target_at(trow, y) * vp.c - v.Lt);
-        const float q = exp2_fast(zrow[y] * vp.c - v.Lz);
+        const float p = exp2_fast(target_at(trow, y) * vp.c - Lt);
+        const float q = exp2_fast(zrow[y] * vp.c - Lz);
         const float r = v.alpha * p - v.beta * q;
         if (!(r > 0.0f)) continue;
         l2r = __builtin_amdgcn_logf(r);
@@ -452,18 +528,18 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_bonus_kernel(VerifyPass
 
 // Resolve: one wave per item writes the accepted stage, or the bonus token.
 template <typename TT>
-__global__ __launch_bounds__(64) void verify_resolve_kernel(VerifyPass vp) {
+__global__ __launch_bounds__(64) void verify_resolve_kernel(VerifyPass vp, int J) {
   const int it = blockIdx.x;
   if (it >= vp.nitems) return;
   const VerifyItem& item = vp.items[it];
-  const VState v = verify_state<TT>(vp, item, it, TS_MAX_K + 1);
+  const VRec v = verify_final(vp, item, it, J);
   const int lane = threadIdx.x;
   VerifyResult r;
-  r.accepted = v.accepted;
+  r.accepted = v.status == kAccepted ? v.stage : 0;
   r.bonus = -1;
   r.margin = v.margin;
   r.pad = 0;
-  if (v.accepted == 0) {
+  if (v.status != kAccepted) {
     const VBonusPart* bp = vp.bp + (size_t)it * vp.nchunks;
     float best = kNegInf, second = kNegInf;
     int idx = 0x7FFFFFFF;
