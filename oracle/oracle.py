@@ -69,11 +69,13 @@ def _declare(L):
     L.tso_u_stage.restype = _D
     L.tso_log_phat.argtypes = [_D, _D, _D]
     L.tso_log_phat.restype = _D
-    L.tso_eval.argtypes = [ctypes.POINTER(_Model), _I, _I, _I, _U64, _D, _U64, _I,
+    L.tso_eval.argtypes = [ctypes.POINTER(_Model), _I, _I, _I, _U64, _D, _U64, _I, _I,
                            _P, _P, _P, _P, _P, _P, _P, _P]
     L.tso_eval.restype = _I
     L.tso_expand_tree.argtypes = [ctypes.POINTER(_Model), _I, _I, _D, _I, _I, _D, _D, _D, _U64, _I,
-                                  ctypes.POINTER(_Tree)]
+                                  _I, ctypes.POINTER(_Tree)]
+    L.tso_draw_sequential.argtypes = [_P, _I, _D, _U64, _I, _I, _U64, _I, _P, _P]
+    L.tso_draw_sequential.restype = None
     L.tso_expand_tree.restype = _I
     L.tso_verify_greedy.argtypes = [ctypes.POINTER(_Tree), _P, _I, _P, _P, _P, _P]
     L.tso_verify_greedy.restype = _I
@@ -138,12 +140,17 @@ class Eval:
     sigma_z: np.ndarray   # [K]
 
 
-def eval_node(model: Model, request, token, depth, path, T, seed, K, want_z=True) -> Eval:
+SAMPLERS = {"gumbel": 0, "sequential": 1}
+
+
+def eval_node(model: Model, request, token, depth, path, T, seed, K, want_z=True,
+              sampler="gumbel") -> Eval:
     z = np.zeros(model.V, dtype=np.float64) if want_z else None
     lse0 = np.zeros(1); lseT = np.zeros(1)
     pi = np.zeros(K, dtype=np.int32); pi_z = np.zeros(K + 1)
     sigma = np.zeros(K, dtype=np.int32); sigma_g = np.zeros(K + 1); sigma_z = np.zeros(K)
-    rc = lib().tso_eval(model.struct, request, token, depth, path, float(T), seed, K, _ptr(z),
+    rc = lib().tso_eval(model.struct, request, token, depth, path, float(T), seed, SAMPLERS[sampler], K,
+                        _ptr(z),
                         _ptr(lse0), _ptr(lseT), _ptr(pi), _ptr(pi_z), _ptr(sigma), _ptr(sigma_g),
                         _ptr(sigma_z))
     if rc != 0:
@@ -177,7 +184,7 @@ class Tree:
 
 
 def expand_tree(model: Model, request, anchor, theta, N, K, T, seed, a=0.67, b=-0.46,
-                control_topk=False) -> Tree:
+                control_topk=False, sampler="gumbel") -> Tree:
     cap = N + 1
     arr = dict(token=np.zeros(cap, np.int32), parent=np.zeros(cap, np.int32),
                depth=np.zeros(cap, np.int32), rank=np.zeros(cap, np.int32),
@@ -187,7 +194,7 @@ def expand_tree(model: Model, request, anchor, theta, N, K, T, seed, a=0.67, b=-
     t = Tree(0, 0, stop_key=float("nan"), **arr)
     s = t.struct()
     rc = lib().tso_expand_tree(model.struct, request, anchor, float(theta), N, K, float(a), float(b),
-                               float(T), seed, int(control_topk), ctypes.byref(s))
+                               float(T), seed, SAMPLERS[sampler], int(control_topk), ctypes.byref(s))
     if rc != 0:
         raise ValueError("tso_expand_tree: invalid arguments")
     t.n, t.evals, t.stop_key = s.n, s.evals, s.stop_key
@@ -195,6 +202,17 @@ def expand_tree(model: Model, request, anchor, theta, N, K, T, seed, a=0.67, b=-
     for name in arr:
         setattr(t, name, getattr(t, name)[:n1].copy())
     return t
+
+
+def draw_sequential(z, T, seed, request, depth, path, K):
+    """K sequential draws without replacement from softmax(z / T) (sampler 1).
+    Returns (tokens in draw order, smallest relative gap of the picks)."""
+    z = np.ascontiguousarray(z, dtype=np.float64)
+    sigma = np.zeros(K, np.int32)
+    gap = np.zeros(1)
+    lib().tso_draw_sequential(_ptr(z), len(z), float(T), seed, request, depth, path, K, _ptr(sigma),
+                              _ptr(gap))
+    return sigma, float(gap[0])
 
 
 def _tree_struct(t: Tree):

@@ -22,9 +22,16 @@
  *       draws: c0 = j, word 0.  Tags: 1 expand, 2 accept, 3 bonus.
  *   R2  u = ((w>>9) + 0.5) * 2^-23: 24 significant bits, so the value is exact
  *       in fp32 as well as fp64; never 0 or 1 (it lies in [2^-24, 1 - 2^-24]).
- *   R3  sibling draws without replacement are realised as Gumbel-top-k over
- *       z/T + G(u): the order of the perturbed keys is a sequence of draws
- *       without replacement (Plackett-Luce), i.e. the residual-proposal draws.
+ *   R3  the K sibling draws from the residual proposal q_T^(j) have two
+ *       realisations (the distribution is the same):
+ *       sampler 0, Gumbel-top-k over z/T + G(u_y): the order of the perturbed
+ *         keys is a sequence of draws without replacement (Plackett-Luce);
+ *       sampler 1, sequential draws as the paper states them: draw j picks a
+ *         4096-token segment, then a 64-token block in it, then a token in
+ *         it, each with probability proportional to its remaining q_T mass,
+ *         from the three words of one Philox call (c0 = j, tag 4); at each
+ *         level the pick is the first index whose cumulative mass exceeds
+ *         u * (level total).
  *   R4  ties: top-k by (value desc, id asc); heap by (key desc, child depth asc,
  *       child path asc); argmax by smallest id.
  *   R5  expansion stops iff the popped key < log(theta) (strict); theta = 0 never stops.
@@ -41,6 +48,10 @@
 #define TSO_TAG_EXPAND 1u
 #define TSO_TAG_ACCEPT 2u
 #define TSO_TAG_BONUS 3u
+#define TSO_TAG_DRAW 4u
+
+#define TSO_SEGMENT 4096 /* tokens per segment of the sequential sampler */
+#define TSO_BLOCK 64     /* tokens per block */
 
 /* ------------------------------------------------------------------------- */
 /* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as   */
@@ -173,8 +184,88 @@ static double logsumexp(const double* v, int n, double scale) {
  * Outputs with K+1 entries carry the first excluded value, for tie reporting.
  * z may be NULL.  Returns 0, or -1 on invalid arguments.
  */
+/* One categorical pick: the first i in [0, n) whose cumulative mass exceeds
+ * u * total.  gap: distance of the target to the nearest cumulative boundary,
+ * relative to the total (for near-tie reporting). */
+static int pick(const double* mass, int n, double u, double* gap) {
+  double total = 0.0;
+  for (int i = 0; i < n; ++i) total += mass[i];
+  const double t = u * total;
+  double c = 0.0;
+  int chosen = -1;
+  double lo = 0.0, hi = total;
+  for (int i = 0; i < n; ++i) {
+    if (!(mass[i] > 0.0)) continue;
+    const double c1 = c + mass[i];
+    if (c1 > t) { chosen = i; lo = c; hi = c1; break; }
+    c = c1;
+  }
+  if (chosen < 0) /* rounding at the top end: the last index with mass */
+    for (int i = n - 1; i >= 0 && chosen < 0; --i)
+      if (mass[i] > 0.0) { chosen = i; lo = c - mass[i]; hi = c; }
+  const double d = fmin(t - lo, hi - t) / total;
+  if (d < *gap) *gap = d;
+  return chosen;
+}
+
+/*
+ * K draws without replacement from q_T (R3, sampler 1): §3.3's residual
+ * proposal q_T^(j) = q_T restricted to the tokens not drawn before j, drawn
+ * one after another.  Each draw picks a segment, a block in it and a token in
+ * it, each in proportion to its remaining mass, which makes
+ * P(token) = mass(token) / remaining mass.  gap: smallest relative gap of the
+ * picks (INFINITY if K == 0).
+ */
+void tso_draw_sequential(const double* z, int V, double T, uint64_t seed, int request, int depth,
+                         uint64_t path, int K, int32_t* sigma, double* gap) {
+  const int nseg = (V + TSO_SEGMENT - 1) / TSO_SEGMENT;
+  double* mass = (double*)malloc(sizeof(double) * (size_t)V);
+  unsigned char* drawn = (unsigned char*)calloc((size_t)V, 1);
+  double* seg = (double*)malloc(sizeof(double) * (size_t)nseg);
+  double blk[TSO_SEGMENT / TSO_BLOCK];
+  *gap = INFINITY;
+  for (int j = 1; j <= K; ++j) {
+    /* q_T^(j) up to its normaliser, relative to the largest remaining logit */
+    double mx = -INFINITY;
+    for (int y = 0; y < V; ++y)
+      if (!drawn[y] && z[y] / T > mx) mx = z[y] / T;
+    for (int y = 0; y < V; ++y) mass[y] = drawn[y] ? 0.0 : exp(z[y] / T - mx);
+    uint32_t ctr[4] = {(uint32_t)j, (uint32_t)path, (uint32_t)(path >> 32),
+                       ((uint32_t)request << 12) | ((uint32_t)depth << 4) | TSO_TAG_DRAW};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t w[4];
+    tso_philox4x32_10(ctr, key, w);
+    for (int sg = 0; sg < nseg; ++sg) {
+      seg[sg] = 0.0;
+      for (int y = sg * TSO_SEGMENT; y < V && y < (sg + 1) * TSO_SEGMENT; ++y) seg[sg] += mass[y];
+    }
+    const int sg = pick(seg, nseg, word_to_uniform(w[0]), gap);
+    const int y0 = sg * TSO_SEGMENT;
+    const int nb = ((V - y0 < TSO_SEGMENT ? V - y0 : TSO_SEGMENT) + TSO_BLOCK - 1) / TSO_BLOCK;
+    for (int b = 0; b < nb; ++b) {
+      blk[b] = 0.0;
+      for (int y = y0 + b * TSO_BLOCK; y < V && y < y0 + (b + 1) * TSO_BLOCK; ++y) blk[b] += mass[y];
+    }
+    const int b = pick(blk, nb, word_to_uniform(w[1]), gap);
+    const int t0 = y0 + b * TSO_BLOCK;
+    const int nt = V - t0 < TSO_BLOCK ? V - t0 : TSO_BLOCK;
+    const int t = pick(mass + t0, nt, word_to_uniform(w[2]), gap);
+    sigma[j - 1] = t0 + t;
+    drawn[t0 + t] = 1;
+  }
+  free(seg);
+  free(drawn);
+  free(mass);
+}
+
+/*
+ * One node evaluation (§3.2 item 1; Algorithm 1): the conditional logits z,
+ * lse0, lseT, the top K+1 by z (pi) and at T > 0 the K draws (sigma).
+ * sigma_g: sampler 0, the K+1 largest Gumbel keys; sampler 1, sigma_g[0] is
+ * the smallest relative gap of the sequential picks and the rest is unused.
+ */
 int tso_eval(const tso_model* m, int request, int token, int depth, uint64_t path,
-             double T, uint64_t seed, int K,
+             double T, uint64_t seed, int sampler, int K,
              double* z_out, double* lse0, double* lseT,
              int* pi, double* pi_z, int* sigma, double* sigma_g, double* sigma_z) {
   if (!m || request < 0 || request >= m->R || token < 0 || token >= m->V || depth < 0 ||
@@ -201,7 +292,21 @@ int tso_eval(const tso_model* m, int request, int token, int depth, uint64_t pat
     for (int i = 0; i < m1; ++i) pi_z[i] = vals[i];
     if (m1 == K) pi_z[K] = -INFINITY;
   }
-  if (T > 0.0) {
+  if (T > 0.0 && sampler == 1) {
+    *lseT = logsumexp(z, V, 1.0 / T);
+    int32_t* sg = (int32_t*)malloc(sizeof(int32_t) * (size_t)K);
+    double gap;
+    tso_draw_sequential(z, V, T, seed, request, depth, path, K, sg, &gap);
+    for (int i = 0; i < K; ++i) {
+      if (sigma) sigma[i] = sg[i];
+      if (sigma_z) sigma_z[i] = z[sg[i]];
+    }
+    if (sigma_g) {
+      sigma_g[0] = gap;
+      for (int i = 1; i <= K; ++i) sigma_g[i] = NAN;
+    }
+    free(sg);
+  } else if (T > 0.0) {
     *lseT = logsumexp(z, V, 1.0 / T);
     double* g = (double*)malloc(sizeof(double) * (size_t)V);
     for (int y = 0; y < V; ++y)
@@ -310,7 +415,8 @@ static int slot_before(const slot* x, const slot* y) {
  * at T > 0 the children are the deterministic top-k of q0 instead of draws.
  */
 int tso_expand_tree(const tso_model* m, int request, int anchor, double theta, int N, int K,
-                    double a, double b, double T, uint64_t seed, int control_topk, tso_tree* out) {
+                    double a, double b, double T, uint64_t seed, int sampler, int control_topk,
+                    tso_tree* out) {
   if (!m || !out || N < 0 || K < 1 || K > 16 || K > m->V || m->D > 16 || T < 0.0 ||
       theta < 0.0 || anchor < 0 || anchor >= m->V || request < 0 || request >= m->R)
     return -1;
@@ -337,11 +443,12 @@ int tso_expand_tree(const tso_model* m, int request, int anchor, double theta, i
     e_->sigma = (int*)malloc(sizeof(int) * (size_t)K);                                       \
     e_->sigma_g = (double*)malloc(sizeof(double) * (size_t)(K + 1));                         \
     e_->sigma_z = (double*)malloc(sizeof(double) * (size_t)K);                               \
-    tso_eval(m, request, out->token[node], out->depth[node], out->path[node], T, seed, K,    \
-             NULL, &e_->lse0, &e_->lseT, e_->pi, e_->pi_z, e_->sigma, e_->sigma_g,           \
-             e_->sigma_z);                                                                   \
+    tso_eval(m, request, out->token[node], out->depth[node], out->path[node], T, seed,       \
+             sampler, K, NULL, &e_->lse0, &e_->lseT, e_->pi, e_->pi_z, e_->sigma,            \
+             e_->sigma_g, e_->sigma_z);                                                      \
     double g_ = min_rel_gap(e_->pi_z, K + 1);                                                \
-    if (T > 0.0) g_ = fmin(g_, min_rel_gap(e_->sigma_g, K + 1));                             \
+    if (T > 0.0)                                                                             \
+      g_ = fmin(g_, sampler == 1 ? e_->sigma_g[0] : min_rel_gap(e_->sigma_g, K + 1));        \
     out->eval_gap[node] = g_;                                                                \
     out->evals++;                                                                            \
   } while (0)
@@ -515,7 +622,7 @@ int tso_verify_sample(const tso_model* m, int request, const tso_tree* t, const 
     if (nk > 0) {
       double lse0, lseT;
       int* pi = (int*)malloc(sizeof(int) * 16);
-      tso_eval(m, request, t->token[cur], t->depth[cur], t->path[cur], T, seed, 1, z, &lse0,
+      tso_eval(m, request, t->token[cur], t->depth[cur], t->path[cur], T, seed, 0, 1, z, &lse0,
                &lseT, pi, NULL, NULL, NULL, NULL);
       free(pi);
       for (int y = 0; y < V; ++y) qT[y] = exp(z[y] / T - lseT);

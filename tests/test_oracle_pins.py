@@ -192,9 +192,96 @@ def test_plackett_luce_first_two_draws():
     assert np.all(np.diag(counts) == 0)  # siblings are distinct
 
 
+def test_sequential_draws_reduce_to_inverse_cdf():
+    """Sampler 1 on a one-block vocabulary is textbook inverse-CDF sampling without
+    replacement (numpy cumsum + searchsorted with the same Philox words)."""
+    rng = np.random.default_rng(5)
+    for trial in range(40):
+        V = int(rng.integers(2, 65))
+        z = rng.normal(size=V) * 2.0
+        T = float(rng.choice([0.3, 0.7, 1.0, 2.0]))
+        K = int(rng.integers(1, min(V, 16) + 1))
+        path, depth, req, seed = int(rng.integers(0, 2**40)), int(rng.integers(0, 16)), int(rng.integers(0, 64)), trial
+        got, gap = o.draw_sequential(z, T, seed, req, depth, path, K)
+        want = _inverse_cdf_draws(special.softmax(z / T), K, seed, req, depth, path)
+        if gap > 1e-9:
+            assert list(got) == want, (trial, got, want)
+
+
+def test_sequential_draws_are_distinct_and_cover_the_vocabulary():
+    """Without replacement: K = V draws are a permutation, across segment and block edges."""
+    for V, T in [(64, 1.0), (130, 0.5), (4097, 2.0), (8200, 4.0)]:
+        z = np.random.default_rng(V).normal(size=V)
+        K = min(V, 16)
+        got, _ = o.draw_sequential(z, T, 3, 0, 1, 0x21, K)
+        assert len(set(got.tolist())) == K and got.min() >= 0 and got.max() < V
+    z = np.random.default_rng(1).normal(size=9)
+    got, _ = o.draw_sequential(z, 1.0, 7, 0, 0, 0, 9)
+    assert sorted(got.tolist()) == list(range(9))
+
+
+def test_sequential_draws_low_temperature_limit():
+    """As T -> 0 the residual proposal puts all mass on the best unused token: sigma = pi."""
+    rng = np.random.default_rng(8)
+    z = rng.normal(size=9000) * 3.0
+    got, _ = o.draw_sequential(z, 1e-3, 11, 2, 3, 0x5, 8)
+    assert list(got) == list(np.lexsort((np.arange(len(z)), -z))[:8])
+
+
+def test_sequential_draws_follow_plackett_luce_across_segments():
+    """Pr(s1 = x, s2 = y) = q(x) q(y) / (1 - q(x)) for draws whose tokens sit in different
+    segments and blocks (V = 9000: three segments); chi-square over 40000 seeds."""
+    V, T = 9000, 1.0
+    heavy = [5, 70, 4100, 4160, 8999]
+    z = np.full(V, -6.0)
+    z[heavy] = [1.0, 0.6, 0.9, 0.2, 0.5]
+    q = special.softmax(z / T)
+    cats = heavy + [-1]  # -1: any other token
+    qc = np.array([q[h] for h in heavy] + [1.0 - q[heavy].sum()])
+    expected = np.zeros((6, 6))
+    for i in range(6):
+        for k in range(6):
+            if i == k and i < 5:
+                continue
+            # the "other" bucket holds many tokens, so it can follow itself
+            expected[i, k] = qc[i] * qc[k] / (1.0 - (qc[i] if i < 5 else 0.0))
+    # second draw after "other": its mass loses one light token, negligible at these sizes
+    n = 40_000
+    counts = np.zeros((6, 6))
+    idx = {h: i for i, h in enumerate(heavy)}
+    for s in range(n):
+        got, _ = o.draw_sequential(z, T, s, 0, 2, 0x7, 2)
+        counts[idx.get(int(got[0]), 5), idx.get(int(got[1]), 5)] += 1
+    mask = expected > 0
+    expected = expected / expected[mask].sum()
+    chi = stats.chisquare(counts[mask], expected[mask] * n)
+    assert chi.pvalue > 1e-3, chi
+
+
 # ---------------------------------------------------------------- expansion
 
-def _universe_brute_force(model_arrays, V, D, r, anchor, theta, N, K, T, seed, a=A, b=B):
+def _draw_words(seed, request, depth, path, j):
+    """The three words of one sequential draw (tag 4, c0 = j), from the Philox pin."""
+    ctr = [j, path & 0xFFFFFFFF, path >> 32, (request << 12) | (depth << 4) | 4]
+    w = o.philox4x32_10(ctr, [seed & 0xFFFFFFFF, seed >> 32])
+    return [((int(x) >> 9) + 0.5) / 2**23 for x in w[:3]]
+
+
+def _inverse_cdf_draws(q, K, seed, request, depth, path):
+    """Textbook inverse-CDF draws without replacement for a vocabulary of one 64-token
+    block (segment and block picks are forced): token = searchsorted(cumsum, u * total)."""
+    q = np.array(q, dtype=np.float64)
+    out = []
+    for j in range(1, K + 1):
+        u3 = _draw_words(seed, request, depth, path, j)[2]
+        c = np.cumsum(q)
+        out.append(int(np.searchsorted(c, u3 * c[-1], side="right")))
+        q[out[-1]] = 0.0
+    return out
+
+
+def _universe_brute_force(model_arrays, V, D, r, anchor, theta, N, K, T, seed, a=A, b=B,
+                          sampler="gumbel"):
     """Enumerate the full K-ary universe of slots with numpy and return the top-N keys >= log theta."""
     U, E, W2 = model_arrays
     slots = []
@@ -215,10 +302,11 @@ def _universe_brute_force(model_arrays, V, D, r, anchor, theta, N, K, T, seed, a
         z = U[0, depth].astype(np.float64) + W2.astype(np.float64) @ E[token].astype(np.float64)
         lse0 = special.logsumexp(z)
         pi = list(np.lexsort((np.arange(V), -z))[:K])
-        if T > 0:
+        if T > 0 and sampler == "sequential":
+            sigma = _inverse_cdf_draws(special.softmax(z / T), K, seed, 0, depth, path)
+        elif T > 0:
             g = z / T - np.log(-np.log([philox_u(depth, path, 1, y) for y in range(V)]))
             sigma = list(np.lexsort((np.arange(V), -g))[:K])
-            lseT = special.logsumexp(z / T)
         for j in range(1, K + 1):
             if T == 0:
                 tok = pi[j - 1]
@@ -245,16 +333,21 @@ def _universe_brute_force(model_arrays, V, D, r, anchor, theta, N, K, T, seed, a
     return out
 
 
-@pytest.mark.parametrize("T,theta,N,K,D", [(0.0, 0.0, 9, 3, 3), (0.0, 0.08, 20, 2, 4),
-                                            (1.0, 0.0, 11, 3, 3), (0.7, 0.05, 20, 2, 4)])
-def test_expansion_equals_universe_top_n(T, theta, N, K, D):
+@pytest.mark.parametrize("T,theta,N,K,D,sampler", [(0.0, 0.0, 9, 3, 3, "gumbel"),
+                                                    (0.0, 0.08, 20, 2, 4, "gumbel"),
+                                                    (1.0, 0.0, 11, 3, 3, "gumbel"),
+                                                    (0.7, 0.05, 20, 2, 4, "gumbel"),
+                                                    (1.0, 0.0, 11, 3, 3, "sequential"),
+                                                    (0.7, 0.05, 20, 2, 4, "sequential")])
+def test_expansion_equals_universe_top_n(T, theta, N, K, D, sampler):
     """Best-first expansion (Algorithm 1) returns the top-N slots >= theta of the full K-ary
     universe, in (key desc, depth asc, path asc) order: brute force on a tiny vocabulary."""
     V, r = 7, 3
     dr, m = _tiny_model(V=V, D=D, r=r, seed=31, u_sigma=2.0, ew_sigma=0.8)
     seed = 99
-    tree = o.expand_tree(m, 0, 4, theta, N, K, T, seed)
-    want = _universe_brute_force((dr.U32, dr.E32, dr.W2_32), V, D, r, 4, theta, N, K, T, seed)
+    tree = o.expand_tree(m, 0, 4, theta, N, K, T, seed, sampler=sampler)
+    want = _universe_brute_force((dr.U32, dr.E32, dr.W2_32), V, D, r, 4, theta, N, K, T, seed,
+                                 sampler=sampler)
     assert tree.n == len(want)
     for i, s in enumerate(want, start=1):
         assert tree.key[i] == pytest.approx(s[0], rel=1e-12, abs=1e-12)
@@ -432,10 +525,11 @@ def _emitted(tree, path, bonus):
 
 
 @pytest.mark.slow
-def test_losslessness_chi_square():
+@pytest.mark.parametrize("sampler", ["gumbel", "sequential"])
+def test_losslessness_chi_square(sampler):
     """Proposition 1: with sampled trees and recursive rejection the first emitted token follows
     softmax(target_root / T), and the token after an accepted depth-1 child x follows
-    softmax(target_x / T); chi-square over 1e5 seeds."""
+    softmax(target_x / T); chi-square over 1e5 seeds, for both realisations of the draws."""
     V, D, K, N, T = 6, 3, 3, 7, 1.0
     dr, m = _tiny_model(V=V, D=D, r=3, seed=41, u_sigma=0.8, ew_sigma=0.6)
     rows = _prefix_rows(V, D, 7, 1.0)
@@ -443,7 +537,7 @@ def test_losslessness_chi_square():
     first = np.zeros(V)
     second = {}
     for s in range(n):
-        tree = o.expand_tree(m, 0, 1, 0.0, N, K, T, s)
+        tree = o.expand_tree(m, 0, 1, 0.0, N, K, T, s, sampler=sampler)
         target = np.stack([rows[p] for p in _tree_prefixes(tree)])
         path, bonus, _ = o.verify_sample(m, 0, tree, target, T, s)
         em = _emitted(tree, path, bonus)
