@@ -168,6 +168,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--expand-only", action="store_true", help="time only ts_expand (profiling runs)")
     ap.add_argument("--T", type=float, default=0.7, help="temperature (the workload uses 0.7)")
+    ap.add_argument("--sampler", default="sequential", choices=("sequential", "gumbel"),
+                    help="realisation of the sibling draws at T > 0")
     ap.add_argument("--copy-gib", type=float, default=0.0, help="run only the copy calibration")
     ap.add_argument("--copy-out", default="", help="directory for the copy calibration record")
     ap.add_argument("--traffic-from", default="",
@@ -203,11 +205,12 @@ def main():
     dd2 = binding.DeviceDrafter(dd.U.clone(), dd.E, dd.W2)
     drafters = (dd, dd2)
     parents = binding.parents_to_device(fr["token"], fr["depth"], fr["request"], fr["log_surv"], fr["path"])
-    outs = binding.expand(dd, parents, P, K, T, seed)
+    sampler = args.sampler
+    outs = binding.expand(dd, parents, P, K, T, seed, sampler=sampler)
     ws_e = outs.pop("_workspace")
     ws_b = torch.empty(binding.build_tree_workspace_size(dd, N, K, T), dtype=torch.uint8, device="cuda")
     ws_v = torch.empty(max(1, binding.verify_workspace_size(dd, N + 1, T)), dtype=torch.uint8, device="cuda")
-    tree = binding.build_tree(dd, anchors, thetas, N, K, T, seed, workspace=ws_b)
+    tree = binding.build_tree(dd, anchors, thetas, N, K, T, seed, workspace=ws_b, sampler=sampler)
     # target logits for the trees: row i = U[q][min(depth_i, D-1)] + N(0, 1) noise
     tgt = torch.zeros((dr.R, N + 1, dr.V), dtype=torch.bfloat16, device="cuda")
     for q in range(dr.R):
@@ -223,10 +226,11 @@ def main():
 
     def step(i):
         d = drafters[i % 2]
-        binding.expand(d, parents, P, K, T, seed, outputs=outs, workspace=ws_e, events=ev.address(3 * i))
+        binding.expand(d, parents, P, K, T, seed, outputs=outs, workspace=ws_e, events=ev.address(3 * i),
+                       sampler=sampler)
         if args.expand_only:
             return
-        binding.build_tree(d, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree)
+        binding.build_tree(d, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler)
         binding.verify(d, tree, tgt, T, seed, workspace=ws_v)
 
     for i in range(args.warmup):
@@ -248,9 +252,9 @@ def main():
         tb = tv = te = 0.0
         for i in range(3):
             torch.cuda.synchronize(); a = time.perf_counter()
-            binding.expand(dd, parents, P, K, T, seed, outputs=outs, workspace=ws_e)
+            binding.expand(dd, parents, P, K, T, seed, outputs=outs, workspace=ws_e, sampler=sampler)
             torch.cuda.synchronize(); b = time.perf_counter()
-            binding.build_tree(dd, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree)
+            binding.build_tree(dd, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler)
             c = time.perf_counter()
             binding.verify(dd, tree, tgt, T, seed, workspace=ws_v)
             torch.cuda.synchronize(); e = time.perf_counter()

@@ -28,8 +28,10 @@
  *     (c0, path lo32, path hi32, request<<12 | depth<<4 | tag), where a node
  *     is named by its structural path id: 4 bits per level, digit = sibling
  *     index - 1, level d at bits [4d, 4d+4).  Per-token draws use c0 = y>>2
- *     and word y&3; per-stage draws use c0 = j and word 0; tags are 1 (expand),
- *     2 (accept), 3 (bonus).  A uniform is u = ((w>>9) + 0.5) * 2^-23.
+ *     and word y&3; per-stage draws use c0 = j and word 0; sequential
+ *     sibling draws use c0 = j and words 0..2; tags are 1 (expand, Gumbel),
+ *     2 (accept), 3 (bonus), 4 (expand, sequential).  A uniform is
+ *     u = ((w>>9) + 0.5) * 2^-23.
  *   - Every call returns TS_OK (0) or a negative ts_status.  On an error
  *     detected on the host nothing is launched and no output is written;
  *     ts_last_error() (per thread) describes it.  No exception crosses the ABI.
@@ -55,6 +57,20 @@ typedef enum {
 } ts_status;
 
 typedef enum { TS_F32 = 0, TS_BF16 = 1 } ts_dtype;
+
+/* How the k sibling draws of a parent at T > 0 are realised.  Both give k
+ * draws without replacement from q_T in draw order, i.e. the residual
+ * proposals q_T^(j) of §3.3; they differ in which random words decide them.
+ *   TS_SAMPLER_GUMBEL      the k largest of z / T - log(-log u_y), one word
+ *                          per (parent, token y) (tag 1, c0 = y >> 2).
+ *   TS_SAMPLER_SEQUENTIAL  the draws one after another, as §3.3 states them:
+ *                          draw j picks a 4096-token segment, a 64-token
+ *                          block in it and a token in it, each in proportion
+ *                          to its remaining q_T mass (the first index whose
+ *                          cumulative mass exceeds u * total), from words
+ *                          0, 1, 2 of one Philox call (tag 4, c0 = j).
+ * The sampler does not matter at T = 0. */
+typedef enum { TS_SAMPLER_GUMBEL = 0, TS_SAMPLER_SEQUENTIAL = 1 } ts_sampler;
 
 /* Limits of this build: K <= TS_MAX_K siblings, D <= TS_MAX_D (the path id
  * holds 4 bits per level), R < 2^20 requests, V <= TS_MAX_V; the rank r is
@@ -91,7 +107,7 @@ typedef struct {
 
 /* Outputs of ts_expand, DEVICE pointers, [P][k] row-major unless noted.
  * Children are in draw order: at T = 0 the top-k tokens of q0 by (q0 desc,
- * id asc); at T > 0 the k draws without replacement from q_T (Gumbel-top-k).
+ * id asc); at T > 0 the k draws without replacement from q_T (ts_sampler).
  * Slot j (1-based) of parent p creates child j; its key is the heap priority
  * of Algorithm 1: at T = 0 the child's own log survival, at T > 0 the
  * admissible pre-draw bound log S(p) + log p-hat(max q0 over tokens not drawn
@@ -112,7 +128,8 @@ typedef struct {
                               before pass 1, between the passes and after pass 2 (timing) */
 } ts_expand_out;
 
-/* Bytes of device workspace ts_expand needs for P parents (0 if P == 0). */
+/* Bytes of device workspace ts_expand needs for P parents (0 if P == 0),
+ * for either sampler. */
 size_t ts_expand_workspace_size(const ts_drafter* d, int32_t P, int32_t k, float T);
 
 /*
@@ -121,15 +138,17 @@ size_t ts_expand_workspace_size(const ts_drafter* d, int32_t P, int32_t k, float
  * (§1 Eq. 1); q0 = softmax(z), qT = softmax(z / T).  Each of the k children
  * gets log q0, log qT, log p-hat and log S(child) = log S(p) + log p-hat
  * (Eq. 3; §3.5).  parents is a DEVICE array of P ts_parent.
+ * sampler is a ts_sampler (used at T > 0).
  * Asynchronous on `stream`.  Arguments checked on the host: null pointers,
- * sizes, k in [1, min(V, TS_MAX_K)], T >= 0 and finite, workspace size.
+ * sizes, k in [1, min(V, TS_MAX_K)], T >= 0 and finite, sampler, workspace
+ * size.
  * Parent fields are checked on the device: a parent with a token, depth or
  * request out of range gets child_token -1 and NaN values, and nothing out
  * of bounds is read.
  * Performance note: parents that share (request, depth) should be adjacent.
  */
 int32_t ts_expand(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_calib calib,
-                  int32_t k, float T, uint64_t seed, const ts_expand_out* out,
+                  int32_t k, float T, uint64_t seed, int32_t sampler, const ts_expand_out* out,
                   void* workspace, size_t workspace_bytes, void* stream);
 
 /* A draft tree per request, HOST memory, capacity `cap` = N + 1 rows per
@@ -162,11 +181,12 @@ size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, f
  * sequential heap of Algorithm 1; it is computed in breadth waves, each one
  * ts_expand call over all requests' pending parents.
  * anchor [R], theta [R] are HOST arrays.  out->cap must be >= N + 1 and
- * out->R == d->R.  Synchronises `stream` once per wave.
+ * out->R == d->R.  sampler is a ts_sampler (used at T > 0).  Synchronises
+ * `stream` once per wave.
  */
 int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* theta, int32_t N,
-                      int32_t K, ts_calib calib, float T, uint64_t seed, ts_tree* out,
-                      void* workspace, size_t workspace_bytes, void* stream);
+                      int32_t K, ts_calib calib, float T, uint64_t seed, int32_t sampler,
+                      ts_tree* out, void* workspace, size_t workspace_bytes, void* stream);
 
 size_t ts_verify_workspace_size(const ts_drafter* d, int32_t cap, float T);
 

@@ -206,13 +206,13 @@ def expand_tree(model: Model, request, anchor, theta, N, K, T, seed, a=0.67, b=-
 
 def draw_sequential(z, T, seed, request, depth, path, K):
     """K sequential draws without replacement from softmax(z / T) (sampler 1).
-    Returns (tokens in draw order, smallest relative gap of the picks)."""
+    Returns (tokens in draw order, smallest relative gap of all the picks)."""
     z = np.ascontiguousarray(z, dtype=np.float64)
     sigma = np.zeros(K, np.int32)
-    gap = np.zeros(1)
+    gap = np.zeros(K)
     lib().tso_draw_sequential(_ptr(z), len(z), float(T), seed, request, depth, path, K, _ptr(sigma),
                               _ptr(gap))
-    return sigma, float(gap[0])
+    return sigma, float(gap.min()) if K else float("inf")
 
 
 def _tree_struct(t: Tree):

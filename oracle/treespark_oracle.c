@@ -213,8 +213,8 @@ static int pick(const double* mass, int n, double u, double* gap) {
  * proposal q_T^(j) = q_T restricted to the tokens not drawn before j, drawn
  * one after another.  Each draw picks a segment, a block in it and a token in
  * it, each in proportion to its remaining mass, which makes
- * P(token) = mass(token) / remaining mass.  gap: smallest relative gap of the
- * picks (INFINITY if K == 0).
+ * P(token) = mass(token) / remaining mass.  gap[j - 1]: smallest relative gap
+ * of the three picks of draw j.
  */
 void tso_draw_sequential(const double* z, int V, double T, uint64_t seed, int request, int depth,
                          uint64_t path, int K, int32_t* sigma, double* gap) {
@@ -223,8 +223,9 @@ void tso_draw_sequential(const double* z, int V, double T, uint64_t seed, int re
   unsigned char* drawn = (unsigned char*)calloc((size_t)V, 1);
   double* seg = (double*)malloc(sizeof(double) * (size_t)nseg);
   double blk[TSO_SEGMENT / TSO_BLOCK];
-  *gap = INFINITY;
   for (int j = 1; j <= K; ++j) {
+    double* g = &gap[j - 1];
+    *g = INFINITY;
     /* q_T^(j) up to its normaliser, relative to the largest remaining logit */
     double mx = -INFINITY;
     for (int y = 0; y < V; ++y)
@@ -239,17 +240,17 @@ void tso_draw_sequential(const double* z, int V, double T, uint64_t seed, int re
       seg[sg] = 0.0;
       for (int y = sg * TSO_SEGMENT; y < V && y < (sg + 1) * TSO_SEGMENT; ++y) seg[sg] += mass[y];
     }
-    const int sg = pick(seg, nseg, word_to_uniform(w[0]), gap);
+    const int sg = pick(seg, nseg, word_to_uniform(w[0]), g);
     const int y0 = sg * TSO_SEGMENT;
     const int nb = ((V - y0 < TSO_SEGMENT ? V - y0 : TSO_SEGMENT) + TSO_BLOCK - 1) / TSO_BLOCK;
     for (int b = 0; b < nb; ++b) {
       blk[b] = 0.0;
       for (int y = y0 + b * TSO_BLOCK; y < V && y < y0 + (b + 1) * TSO_BLOCK; ++y) blk[b] += mass[y];
     }
-    const int b = pick(blk, nb, word_to_uniform(w[1]), gap);
+    const int b = pick(blk, nb, word_to_uniform(w[1]), g);
     const int t0 = y0 + b * TSO_BLOCK;
     const int nt = V - t0 < TSO_BLOCK ? V - t0 : TSO_BLOCK;
-    const int t = pick(mass + t0, nt, word_to_uniform(w[2]), gap);
+    const int t = pick(mass + t0, nt, word_to_uniform(w[2]), g);
     sigma[j - 1] = t0 + t;
     drawn[t0 + t] = 1;
   }
@@ -261,8 +262,8 @@ void tso_draw_sequential(const double* z, int V, double T, uint64_t seed, int re
 /*
  * One node evaluation (§3.2 item 1; Algorithm 1): the conditional logits z,
  * lse0, lseT, the top K+1 by z (pi) and at T > 0 the K draws (sigma).
- * sigma_g: sampler 0, the K+1 largest Gumbel keys; sampler 1, sigma_g[0] is
- * the smallest relative gap of the sequential picks and the rest is unused.
+ * sigma_g: sampler 0, the K+1 largest Gumbel keys; sampler 1, sigma_g[j] is
+ * the smallest relative gap of the picks of draw j + 1 (sigma_g[K] unused).
  */
 int tso_eval(const tso_model* m, int request, int token, int depth, uint64_t path,
              double T, uint64_t seed, int sampler, int K,
@@ -295,16 +296,15 @@ int tso_eval(const tso_model* m, int request, int token, int depth, uint64_t pat
   if (T > 0.0 && sampler == 1) {
     *lseT = logsumexp(z, V, 1.0 / T);
     int32_t* sg = (int32_t*)malloc(sizeof(int32_t) * (size_t)K);
-    double gap;
-    tso_draw_sequential(z, V, T, seed, request, depth, path, K, sg, &gap);
+    double* gap = (double*)malloc(sizeof(double) * (size_t)K);
+    tso_draw_sequential(z, V, T, seed, request, depth, path, K, sg, gap);
     for (int i = 0; i < K; ++i) {
       if (sigma) sigma[i] = sg[i];
       if (sigma_z) sigma_z[i] = z[sg[i]];
+      if (sigma_g) sigma_g[i] = gap[i];
     }
-    if (sigma_g) {
-      sigma_g[0] = gap;
-      for (int i = 1; i <= K; ++i) sigma_g[i] = NAN;
-    }
+    if (sigma_g) sigma_g[K] = NAN;
+    free(gap);
     free(sg);
   } else if (T > 0.0) {
     *lseT = logsumexp(z, V, 1.0 / T);
@@ -379,6 +379,13 @@ static double min_rel_gap(const double* vals, int n) {
   return g;
 }
 
+static double min_of(const double* v, int n) {
+  double m = INFINITY;
+  for (int i = 0; i < n; ++i)
+    if (v[i] < m) m = v[i];
+  return m;
+}
+
 /* Token proposed by slot j of node v, its z, and the slot key (Algorithm 1; §3.3 pre-draw bound). */
 static void slot_values(const node_eval* ev, double log_surv_v, int j, double T, int control_topk,
                         double a, double b, int* tok, double* zc, double* key) {
@@ -448,7 +455,7 @@ int tso_expand_tree(const tso_model* m, int request, int anchor, double theta, i
              e_->sigma_g, e_->sigma_z);                                                      \
     double g_ = min_rel_gap(e_->pi_z, K + 1);                                                \
     if (T > 0.0)                                                                             \
-      g_ = fmin(g_, sampler == 1 ? e_->sigma_g[0] : min_rel_gap(e_->sigma_g, K + 1));        \
+      g_ = fmin(g_, sampler == 1 ? min_of(e_->sigma_g, K) : min_rel_gap(e_->sigma_g, K + 1)); \
     out->eval_gap[node] = g_;                                                                \
     out->evals++;                                                                            \
   } while (0)

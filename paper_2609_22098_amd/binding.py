@@ -20,6 +20,7 @@ TS_F32, TS_BF16 = 0, 1
 TS_MAX_K, TS_MAX_D = 16, 16
 
 # Every symbol include/treespark.h declares.
+SAMPLERS = {"gumbel": 0, "sequential": 1}  # ts_sampler
 EXPORTED = ("ts_expand_workspace_size", "ts_expand", "ts_build_tree_workspace_size", "ts_build_tree",
             "ts_verify_workspace_size", "ts_verify", "ts_last_error", "ts_version")
 
@@ -76,11 +77,11 @@ def lib():
         P, I32, U64, SZ, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t, ctypes.c_float
         L.ts_expand_workspace_size.argtypes = [P, I32, I32, F]
         L.ts_expand_workspace_size.restype = SZ
-        L.ts_expand.argtypes = [P, P, I32, Calib, I32, F, U64, P, P, SZ, P]
+        L.ts_expand.argtypes = [P, P, I32, Calib, I32, F, U64, I32, P, P, SZ, P]
         L.ts_expand.restype = I32
         L.ts_build_tree_workspace_size.argtypes = [P, I32, I32, F]
         L.ts_build_tree_workspace_size.restype = SZ
-        L.ts_build_tree.argtypes = [P, P, P, I32, I32, Calib, F, U64, P, P, SZ, P]
+        L.ts_build_tree.argtypes = [P, P, P, I32, I32, Calib, F, U64, I32, P, P, SZ, P]
         L.ts_build_tree.restype = I32
         L.ts_verify_workspace_size.argtypes = [P, I32, F]
         L.ts_verify_workspace_size.restype = SZ
@@ -181,10 +182,11 @@ def expand_workspace_size(d: DeviceDrafter, P, k, T):
 
 
 def expand(d: DeviceDrafter, parents, P, k, T, seed, calib=(0.67, -0.46), workspace=None,
-           stream=None, outputs=None, events=None):
+           stream=None, outputs=None, events=None, sampler="gumbel"):
     """ts_expand.  parents: device uint8 tensor of P ts_parent records.  Returns a dict of
     device tensors (asynchronous on the stream).  events: optional ctypes array of three
-    hipEvent_t handles recorded around the two kernels, given by address."""
+    hipEvent_t handles recorded around the two kernels, given by address.  sampler:
+    "gumbel" or "sequential" (the realisation of the draws at T > 0)."""
     torch = _torch()
     dev = parents.device
     if outputs is None:
@@ -206,7 +208,7 @@ def expand(d: DeviceDrafter, parents, P, k, T, seed, calib=(0.67, -0.46), worksp
                       for name, _ in ExpandOut._fields_[:-1]],
                     events)
     rc = lib().ts_expand(d.ref(), ctypes.c_void_p(parents.data_ptr()), P, Calib(*calib), k, float(T),
-                         ctypes.c_uint64(seed), ctypes.byref(out), ctypes.c_void_p(workspace.data_ptr()),
+                         ctypes.c_uint64(seed), SAMPLERS[sampler], ctypes.byref(out), ctypes.c_void_p(workspace.data_ptr()),
                          workspace.numel(), _stream(stream))
     _check(rc)
     outputs["_workspace"] = workspace
@@ -251,7 +253,7 @@ def build_tree_workspace_size(d: DeviceDrafter, N, K, T):
 
 
 def build_tree(d: DeviceDrafter, anchor, theta, N, K, T, seed, calib=(0.67, -0.46), workspace=None,
-               stream=None, tree=None) -> HostTree:
+               stream=None, tree=None, sampler="gumbel") -> HostTree:
     torch = _torch()
     anchor = np.ascontiguousarray(anchor, dtype=np.int32)
     theta = np.ascontiguousarray(theta, dtype=np.float32)
@@ -262,7 +264,7 @@ def build_tree(d: DeviceDrafter, anchor, theta, N, K, T, seed, calib=(0.67, -0.4
         workspace = torch.empty((max(n, 1),), dtype=torch.uint8, device=d.U.device)
     s = tree.struct()
     rc = lib().ts_build_tree(d.ref(), anchor.ctypes.data, theta.ctypes.data, N, K, Calib(*calib),
-                             float(T), ctypes.c_uint64(seed), ctypes.byref(s),
+                             float(T), ctypes.c_uint64(seed), SAMPLERS[sampler], ctypes.byref(s),
                              ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream(stream))
     _check(rc)
     return tree

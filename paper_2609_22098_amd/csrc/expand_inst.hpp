@@ -6,85 +6,63 @@
 
 namespace ts {
 
-template <typename TE, int KS, int NB>
-void launch_eval_nb(const ExpandParams& p, bool sample, bool store_z, dim3 grid, dim3 block,
-                    hipStream_t s) {
-  if constexpr (NB == 1) {
-    if (store_z) {
-      if (sample)
-        hipLaunchKernelGGL((expand_eval_kernel<TE, KS, 1, true, true>), grid, block, 0, s, p);
-      else
-        hipLaunchKernelGGL((expand_eval_kernel<TE, KS, 1, false, true>), grid, block, 0, s, p);
-      return;
+// The kernel of a launch for one (dtype, rank, parent blocks per wave):
+// the verification recompute stores z and needs no draws (mode 0).
+template <typename TE, int KS, int NB, bool LDS>
+struct EvalKernels {
+  template <int MODE>
+  static auto pick() {
+    if constexpr (LDS)
+      return expand_eval_lds_kernel<KS, NB, MODE>;
+    else
+      return expand_eval_kernel<TE, KS, NB, MODE, false>;
+  }
+  static auto get(int mode) {
+    decltype(pick<0>()) k = pick<0>();
+    if (mode == kModeGumbel) k = pick<kModeGumbel>();
+    if (mode == kModeSeq) k = pick<kModeSeq>();
+    return k;
+  }
+};
+
+template <typename TE, int KS>
+static void (*eval_kernel_for(int nb, int mode, bool store_z, bool lds))(ExpandParams) {
+  if (store_z) return expand_eval_kernel<TE, KS, 1, kModeGreedy, true>;
+  if constexpr (sizeof(TE) == 2) {
+    if (lds) {
+      if (nb == 1) return EvalKernels<TE, KS, 1, true>::get(mode);
+      if (nb == 2) return EvalKernels<TE, KS, 2, true>::get(mode);
+      return EvalKernels<TE, KS, 4, true>::get(mode);
     }
   }
-  if (sample)
-    hipLaunchKernelGGL((expand_eval_kernel<TE, KS, NB, true, false>), grid, block, 0, s, p);
-  else
-    hipLaunchKernelGGL((expand_eval_kernel<TE, KS, NB, false, false>), grid, block, 0, s, p);
-}
-
-template <int KS, int NB>
-void launch_eval_lds_nb(const ExpandParams& p, bool sample, dim3 grid, dim3 block, hipStream_t s) {
-  if (sample)
-    hipLaunchKernelGGL((expand_eval_lds_kernel<KS, NB, true>), grid, block, 0, s, p);
-  else
-    hipLaunchKernelGGL((expand_eval_lds_kernel<KS, NB, false>), grid, block, 0, s, p);
+  if (nb == 1) return EvalKernels<TE, KS, 1, false>::get(mode);
+  if (nb == 2) return EvalKernels<TE, KS, 2, false>::get(mode);
+  return EvalKernels<TE, KS, 4, false>::get(mode);
 }
 
 template <typename TE, int KS>
-void launch_eval_t(const ExpandParams& p, int nb, bool sample, bool store_z, bool lds, dim3 grid,
+void launch_eval_t(const ExpandParams& p, int nb, int mode, bool store_z, bool lds, dim3 grid,
                    dim3 block, hipStream_t s) {
-  if constexpr (sizeof(TE) == 2) {
-    if (lds && !store_z) {
-      if (nb == 1)
-        launch_eval_lds_nb<KS, 1>(p, sample, grid, block, s);
-      else if (nb == 2)
-        launch_eval_lds_nb<KS, 2>(p, sample, grid, block, s);
-      else
-        launch_eval_lds_nb<KS, 4>(p, sample, grid, block, s);
-      return;
-    }
-  }
-  if (nb == 1 || store_z)
-    launch_eval_nb<TE, KS, 1>(p, sample, store_z, grid, block, s);
-  else if (nb == 2)
-    launch_eval_nb<TE, KS, 2>(p, sample, false, grid, block, s);
-  else
-    launch_eval_nb<TE, KS, 4>(p, sample, false, grid, block, s);
+  void (*kernel)(ExpandParams) = eval_kernel_for<TE, KS>(nb, mode, store_z, lds);
+  hipLaunchKernelGGL(kernel, grid, block, 0, s, p);
 }
 
 template <typename TE, int KS>
-int eval_blocks_per_cu_t(int nb, bool sample, bool store_z, bool lds, int block) {
+int eval_blocks_per_cu_t(int nb, int mode, bool store_z, bool lds, int block) {
   int n = 0;
-  hipError_t e = hipSuccess;
-#define TS_OCC(kern) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, block, 0)
-  if constexpr (sizeof(TE) == 2) {
-    if (lds && !store_z) {
-      if (nb == 1) { if (sample) TS_OCC((expand_eval_lds_kernel<KS, 1, true>)); else TS_OCC((expand_eval_lds_kernel<KS, 1, false>)); }
-      else if (nb == 2) { if (sample) TS_OCC((expand_eval_lds_kernel<KS, 2, true>)); else TS_OCC((expand_eval_lds_kernel<KS, 2, false>)); }
-      else { if (sample) TS_OCC((expand_eval_lds_kernel<KS, 4, true>)); else TS_OCC((expand_eval_lds_kernel<KS, 4, false>)); }
-      return e == hipSuccess ? n : 0;
-    }
-  }
-  if (nb == 1 || store_z) {
-    if (store_z) { if (sample) TS_OCC((expand_eval_kernel<TE, KS, 1, true, true>)); else TS_OCC((expand_eval_kernel<TE, KS, 1, false, true>)); }
-    else { if (sample) TS_OCC((expand_eval_kernel<TE, KS, 1, true, false>)); else TS_OCC((expand_eval_kernel<TE, KS, 1, false, false>)); }
-  } else if (nb == 2) {
-    if (sample) TS_OCC((expand_eval_kernel<TE, KS, 2, true, false>)); else TS_OCC((expand_eval_kernel<TE, KS, 2, false, false>));
-  } else {
-    if (sample) TS_OCC((expand_eval_kernel<TE, KS, 4, true, false>)); else TS_OCC((expand_eval_kernel<TE, KS, 4, false, false>));
-  }
-#undef TS_OCC
+  void (*kernel)(ExpandParams) = eval_kernel_for<TE, KS>(nb, mode, store_z, lds);
+  const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, block, 0);
   return e == hipSuccess ? n : 0;
 }
 
 template <typename TE, int KS>
-void launch_merge_t(const MergeParams& p, bool sample, dim3 grid, dim3 block, hipStream_t s) {
-  if (sample)
-    hipLaunchKernelGGL((expand_merge_kernel<TE, KS, true>), grid, block, 0, s, p);
+void launch_merge_t(const MergeParams& p, int mode, dim3 grid, dim3 block, hipStream_t s) {
+  if (mode == kModeGumbel)
+    hipLaunchKernelGGL((expand_merge_kernel<TE, KS, kModeGumbel>), grid, block, 0, s, p);
+  else if (mode == kModeSeq)
+    hipLaunchKernelGGL((expand_merge_kernel<TE, KS, kModeSeq>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((expand_merge_kernel<TE, KS, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((expand_merge_kernel<TE, KS, kModeGreedy>), grid, block, 0, s, p);
 }
 
 }  // namespace ts

@@ -23,6 +23,12 @@
 // those runs are recomputed, with the same MFMA sequence as pass 1 (so the
 // recomputed z are bit-identical, which the kernel checks), and the exact
 // top-k is taken by (value desc, id asc).
+//
+// Sequential draws (the residual-proposal draws of §3.3 taken one after
+// another) replace the Gumbel keys by one number per (parent, 64-token block):
+// the base-2 log of the block's q_T mass.  The merge then makes each draw by
+// picking a 4096-token segment, a block in it and a token in it in proportion
+// to the remaining mass, recomputing only the chosen block.
 #pragma once
 
 #include "device_common.hpp"
@@ -57,9 +63,16 @@ struct ExpandParams {
   float* part_s0;  // [P][S] sum exp(z - m)
   float* part_sT;  // [P][S] sum exp((z - m) / T)
   RunSummaryPtr zs;  // per (parent, chunk): the two best runs of z and the rest
-  RunSummaryPtr gs;  // the same for the Gumbel keys (T > 0)
+  RunSummaryPtr gs;  // the same for the Gumbel keys (Gumbel draws)
+  float* blk;      // [P][nblk]: base-2 log of the q_T mass of each 64-token block (sequential draws)
+  int nblk;        // ceil(V / 64)
   float* z_out;    // optional [P][V]: the logits themselves (verification recompute)
 };
+
+// Sampling modes of a launch: greedy (T = 0), Gumbel-top-k draws, sequential draws.
+enum : int { kModeGreedy = 0, kModeGumbel = 1, kModeSeq = 2 };
+constexpr int kSegTokens = 4096;  // tokens per segment of the sequential draws
+constexpr int kBlkTokens = 64;    // tokens per block
 
 struct MergeParams {
   const void* U;
@@ -79,6 +92,8 @@ struct MergeParams {
   const float* part_sT;
   RunSummaryPtr zs;
   RunSummaryPtr gs;
+  const float* blk;
+  int nblk;
   ts_expand_out out;
 };
 
@@ -262,11 +277,27 @@ __device__ __forceinline__ void top_store(const RunSummaryPtr& d, size_t o, cons
 
 // ---------------------------------------------------------------- pass 1
 
-template <typename TE, int KS, int NB, bool SAMPLE, bool STORE_Z>
+// Base-2 log of the q_T mass of this step's 64-token block for the lane's
+// parent: a is the lane's run sum relative to 2^ml; the four lane groups of a
+// parent (lanes n, n+16, n+32, n+48) hold the block's four runs.
+__device__ __forceinline__ float block_log_mass(float a, float ml) {
+  const float l = a > 0.0f ? ml + __builtin_amdgcn_logf(a) : kNegInf;
+  float m = fmaxf(l, __shfl_xor(l, 16, 64));
+  m = fmaxf(m, __shfl_xor(m, 32, 64));
+  float s = m == kNegInf ? 0.0f : exp2_fast(l - m);
+  s += __shfl_xor(s, 16, 64);
+  s += __shfl_xor(s, 32, 64);
+  return m == kNegInf ? kNegInf : m + __builtin_amdgcn_logf(s);
+}
+
+template <typename TE, int KS, int NB, int MODE, bool STORE_Z>
 __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) {
   typedef Frag<TE> F;
   typedef typename F::type FT;
   const int lane = threadIdx.x & 63;
+  constexpr bool SAMPLE = MODE != kModeGreedy;  // T > 0: lse of z/T and K draws
+  constexpr bool GUMBEL = MODE == kModeGumbel;
+  constexpr bool SEQ = MODE == kModeSeq;
   const int wv = threadIdx.x >> 6;
   const int n = lane & 15;  // parent column / token row inside a 16x16 tile
   const int g = lane >> 4;  // lane group: K sub-block for A/B, row block for C
@@ -373,23 +404,32 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
       float bm = v[0];
 #pragma unroll
       for (int j = 1; j < 16; ++j) bm = fmaxf(bm, v[j]);
+      // run sums are taken relative to the run's own maximum (a run far below
+      // the running maximum keeps its mass), then folded into the running sums
       const float mn = fmaxf(m0[nb], bm);
       const float mref = fmaxf(mn, -1e30f);
-      const float ml = mref * kLog2e;
+      const float bref = fmaxf(bm, -1e30f);
+      const float ml = mref * kLog2e, bl = bref * kLog2e;
       float a0 = 0.0f;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) a0 += exp2_fast(__builtin_fmaf(v[j], kLog2e, -ml));
-      s0[nb] = __builtin_fmaf(s0[nb], exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -ml)), a0);
+      for (int j = 0; j < 16; ++j) a0 += exp2_fast(__builtin_fmaf(v[j], kLog2e, -bl));
+      s0[nb] = __builtin_fmaf(s0[nb], exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -ml)),
+                              a0 * exp2_fast(bl - ml));
+      const float mlT = mref * p.cT, blT = bref * p.cT;
+      float aT = 0.0f;
       if (SAMPLE && p.need_T) {
-        const float mlT = mref * p.cT;
-        float aT = 0.0f;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) aT += exp2_fast(__builtin_fmaf(v[j], p.cT, -mlT));
-        sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)), aT);
+        for (int j = 0; j < 16; ++j) aT += exp2_fast(__builtin_fmaf(v[j], p.cT, -blT));
+        sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)),
+                                aT * exp2_fast(blT - mlT));
       }
       m0[nb] = mn;
       top_add(zt[nb], bm, run);
-      if constexpr (SAMPLE) {
+      if constexpr (SEQ) {
+        const float lb = p.need_T ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
+        if (g == 0 && pidx[nb] < p.P) p.blk[(size_t)pidx[nb] * p.nblk + (t0 >> 6)] = lb;
+      }
+      if constexpr (GUMBEL) {
         float gm = kNegInf;
         const uint32_t cbase = (uint32_t)tl >> 2;
 #pragma unroll
@@ -461,7 +501,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
 #pragma unroll
     for (int o = 16; o <= 32; o <<= 1) {
       top_combine(zc, top_shfl_xor(zc, o));
-      if constexpr (SAMPLE) top_combine(gc, top_shfl_xor(gc, o));
+      if constexpr (GUMBEL) top_combine(gc, top_shfl_xor(gc, o));
     }
     if (g == 0 && pidx[nb] < p.P) {
       const size_t o = (size_t)pidx[nb] * p.S + chunk;
@@ -469,7 +509,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
       p.part_s0[o] = s;
       if (p.part_sT) p.part_sT[o] = st;
       top_store(p.zs, o, zc);
-      if constexpr (SAMPLE) top_store(p.gs, o, gc);
+      if constexpr (GUMBEL) top_store(p.gs, o, gc);
     }
   }
 }
@@ -487,7 +527,7 @@ __device__ __forceinline__ void lds_dma16(const void* src, u32x4* dst_wave_base)
   __builtin_amdgcn_global_load_lds(src, (lds_ptr)dst_wave_base, 16, 0, 0);
 }
 
-template <int KS, int NB, bool SAMPLE>
+template <int KS, int NB, int MODE>
 __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams p) {
   typedef Frag<uint16_t> F;
   typedef typename F::type FT;
@@ -498,6 +538,9 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
   __shared__ __attribute__((aligned(16))) u32x4 u0[4 * kU];
   __shared__ __attribute__((aligned(16))) u32x4 u1[4 * kU];
   const int lane = threadIdx.x & 63;
+  constexpr bool SAMPLE = MODE != kModeGreedy;  // T > 0: lse of z/T and K draws
+  constexpr bool GUMBEL = MODE == kModeGumbel;
+  constexpr bool SEQ = MODE == kModeSeq;
   const int wv = threadIdx.x >> 6;
   const int n = lane & 15;
   const int g = lane >> 4;
@@ -609,23 +652,32 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
       float bm = v[0];
 #pragma unroll
       for (int j = 1; j < 16; ++j) bm = fmaxf(bm, v[j]);
+      // run sums are taken relative to the run's own maximum (a run far below
+      // the running maximum keeps its mass), then folded into the running sums
       const float mn = fmaxf(m0[nb], bm);
       const float mref = fmaxf(mn, -1e30f);
-      const float ml = mref * kLog2e;
+      const float bref = fmaxf(bm, -1e30f);
+      const float ml = mref * kLog2e, bl = bref * kLog2e;
       float a0 = 0.0f;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) a0 += exp2_fast(__builtin_fmaf(v[j], kLog2e, -ml));
-      s0[nb] = __builtin_fmaf(s0[nb], exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -ml)), a0);
+      for (int j = 0; j < 16; ++j) a0 += exp2_fast(__builtin_fmaf(v[j], kLog2e, -bl));
+      s0[nb] = __builtin_fmaf(s0[nb], exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -ml)),
+                              a0 * exp2_fast(bl - ml));
+      const float mlT = mref * p.cT, blT = bref * p.cT;
+      float aT = 0.0f;
       if (SAMPLE && p.need_T) {
-        const float mlT = mref * p.cT;
-        float aT = 0.0f;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) aT += exp2_fast(__builtin_fmaf(v[j], p.cT, -mlT));
-        sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)), aT);
+        for (int j = 0; j < 16; ++j) aT += exp2_fast(__builtin_fmaf(v[j], p.cT, -blT));
+        sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)),
+                                aT * exp2_fast(blT - mlT));
       }
       m0[nb] = mn;
       top_add(zt[nb], bm, run);
-      if constexpr (SAMPLE) {
+      if constexpr (SEQ) {
+        const float lb = p.need_T ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
+        if (g == 0 && pidx[nb] < p.P) p.blk[(size_t)pidx[nb] * p.nblk + (t0 >> 6)] = lb;
+      }
+      if constexpr (GUMBEL) {
         float gm = kNegInf;
         const uint32_t cbase = (uint32_t)tl >> 2;
 #pragma unroll
@@ -686,7 +738,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
 #pragma unroll
     for (int o = 16; o <= 32; o <<= 1) {
       top_combine(zc, top_shfl_xor(zc, o));
-      if constexpr (SAMPLE) top_combine(gc, top_shfl_xor(gc, o));
+      if constexpr (GUMBEL) top_combine(gc, top_shfl_xor(gc, o));
     }
     if (g == 0 && pidx[nb] < p.P) {
       const size_t o = (size_t)pidx[nb] * p.S + chunk;
@@ -694,7 +746,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
       p.part_s0[o] = s;
       if (p.part_sT) p.part_sT[o] = st;
       top_store(p.zs, o, zc);
-      if constexpr (SAMPLE) top_store(p.gs, o, gc);
+      if constexpr (GUMBEL) top_store(p.gs, o, gc);
     }
   }
 }
@@ -969,10 +1021,190 @@ __device__ __forceinline__ float select_items(const MergeParams& p, const RunSum
   return thr;
 }
 
-template <typename TE, int KS, bool SAMPLE>
+// ---------------------------------------------------------------- sequential draws
+
+constexpr int kSegSlots = (TS_MAX_V + 64 * kSegTokens - 1) / (64 * kSegTokens);  // segments per lane
+
+// Inclusive prefix sum over the 64 lanes (fixed order).
+__device__ __forceinline__ float wave_incl_scan(float x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const float y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// One categorical pick over items laid out as item = 64 * slot + lane with
+// masses m >= 0: the first item whose inclusive cumulative mass exceeds
+// u * total (never a zero-mass item); rounding at the top end falls back to
+// the last item with mass.  Returns -1 only if every mass is zero.
+template <int NS>
+__device__ __forceinline__ int wave_pick(const float (&m)[NS], float u) {
+  float c[NS];
+  float base = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    const float x = wave_incl_scan(m[i]);
+    c[i] = base + x;
+    base += __shfl(x, 63, 64);
+  }
+  const float t = u * base;
+  int cnt = 0, last = -1;
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    cnt += __popcll(__ballot(c[i] <= t));
+    const uint64_t pos = __ballot(m[i] > 0.0f);
+    if (pos) last = 64 * i + 63 - __clzll((long long)pos);
+  }
+  return cnt > last ? last : cnt;
+}
+
+// K draws without replacement from q_T, one after another (§3.3 residual
+// proposal): draw j picks a segment, a block in it and a token in it, each in
+// proportion to its remaining mass, from the words of one Philox call
+// (c0 = j, tag 4).  Masses are handled as base-2 logs relative to each
+// level's largest one, so removing drawn tokens never underflows the rest.
+// Draw j lands in lane j - 1 of gl (token, z).
+template <typename TE, int KS>
+__device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const TE* urow,
+                                          const typename Frag<TE>::type (&bcol)[KS], uint32_t pc1,
+                                          uint32_t pc2, uint32_t pc3, MergeLds& L, RegList& gl) {
+  typedef Frag<TE> F;
+  const int lane = threadIdx.x & 63;
+  const int n = lane & 15, g = lane >> 4;
+  const int V = p.V, nblk = p.nblk;
+  const TE* W2 = static_cast<const TE*>(p.W2);
+  const float* blk = p.blk + (size_t)pidx * nblk;
+  constexpr int kBps = kSegTokens / kBlkTokens;  // blocks per segment (64)
+
+  // segment log-masses: lane l holds segment l + 64 i; the wave reduces one
+  // segment (its 64 blocks, one per lane) at a time, eight loads in flight
+  float segL[kSegSlots];
+#pragma unroll
+  for (int i = 0; i < kSegSlots; ++i) segL[i] = kNegInf;
+  const int nseg = (nblk + kBps - 1) / kBps;
+#pragma unroll 1
+  for (int s0 = 0; s0 < nseg; s0 += 8) {
+    float x[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int b = (s0 + k) * kBps + lane;
+      x[k] = (s0 + k < nseg && b < nblk) ? blk[b] : kNegInf;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int sg = s0 + k;
+      const float m = wave_max(x[k]);
+      const float sum = wave_sum(m == kNegInf ? 0.0f : exp2_fast(x[k] - m));
+      const float l = m == kNegInf ? kNegInf : m + __builtin_amdgcn_logf(sum);
+#pragma unroll
+      for (int i = 0; i < kSegSlots; ++i)
+        if (sg < nseg && sg == 64 * i + lane) segL[i] = l;
+    }
+  }
+  // blocks whose mass changed (a token of theirs was drawn): lane k holds entry k
+  int ov_b = -1;
+  float ov_l = kNegInf;
+  int nov = 0;
+  gl.cnt = 0;
+#pragma unroll 1
+  for (int j = 1; j <= p.K; ++j) {
+    uint32_t w0 = (uint32_t)j, w1 = pc1, w2 = pc2, w3 = pc3;
+    philox10(w0, w1, w2, w3, p.keys);
+    // level 1: segment
+    float ms[kSegSlots];
+    float mx = kNegInf;
+#pragma unroll
+    for (int i = 0; i < kSegSlots; ++i) mx = fmaxf(mx, segL[i]);
+    mx = wave_max(mx);
+#pragma unroll
+    for (int i = 0; i < kSegSlots; ++i) ms[i] = segL[i] == kNegInf ? 0.0f : exp2_fast(segL[i] - mx);
+    const int sg = wave_pick(ms, word_to_uniform(w0));
+    // level 2: block within the segment (lane = block offset)
+    const int b = sg * kBps + lane;
+    float lb = (sg >= 0 && b < nblk) ? blk[b] : kNegInf;
+    for (int k = 0; k < nov; ++k) {
+      const int ob = __shfl(ov_b, k, 64);
+      const float ol = __shfl(ov_l, k, 64);
+      if (ob == b) lb = ol;
+    }
+    const float mb = wave_max(lb);
+    float m2[1];
+    m2[0] = lb == kNegInf ? 0.0f : exp2_fast(lb - mb);
+    const int bo = wave_pick(m2, word_to_uniform(w1));
+    const int bsel = sg * kBps + bo;
+    // level 3: token within the block; recompute its 64 logits (four runs of 16)
+    const int t0 = bsel * kBlkTokens;
+    f32x4 acc[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      acc[q] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      if (n == 0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int tok = t0 + 16 * q + g * 4 + e;
+          acc[q][e] = tok < V ? F::to_f32(urow[min(tok, V - 1)]) : kNegInf;
+        }
+      }
+      const TE* wrow = W2 + (size_t)min(t0 + 16 * q + n, V - 1) * p.r;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) acc[q] = F::mma(F::load(wrow, kk * F::kPerStep, g), bcol[kk], acc[q]);
+    }
+    if (n == 0) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) L.bz[q][g * 4 + e] = acc[q][e];
+    }
+    wave_sync_lds();
+    const int y = t0 + lane;
+    const float zy = L.bz[lane >> 4][lane & 15];
+    wave_sync_lds();
+    bool live = y < V && bo >= 0;
+    for (int k = 0; k < j - 1; ++k) live &= __shfl(gl.id, k, 64) != y;
+    const float xy = live ? zy * p.cT : kNegInf;
+    const float mt = wave_max(xy);
+    float m3[1];
+    m3[0] = live ? exp2_fast(xy - mt) : 0.0f;
+    const int to = wave_pick(m3, word_to_uniform(w2));
+    const int tsel = t0 + to;
+    const float zsel = __shfl(zy, to < 0 ? 0 : to, 64);
+    if (lane == j - 1) {
+      gl.id = to < 0 ? -1 : tsel;
+      gl.aux = zsel;
+      gl.val = 0.0f;
+    }
+    // the block and the segment lose the drawn token's mass; both sums are
+    // taken relative to the largest value left, so nothing underflows
+    const bool left = live && lane != to;
+    const float mt2 = wave_max(left ? xy : kNegInf);
+    const float rest3 = wave_sum(left ? exp2_fast(xy - mt2) : 0.0f);
+    const float lnew = mt2 == kNegInf ? kNegInf : mt2 + __builtin_amdgcn_logf(rest3);
+    int slot = -1;
+    for (int k = 0; k < nov; ++k)
+      if (__shfl(ov_b, k, 64) == bsel) slot = k;
+    if (slot < 0) slot = nov++;
+    if (lane == slot) { ov_b = bsel; ov_l = lnew; }
+    const float lb2 = lane == bo ? lnew : lb;
+    const float mb2 = wave_max(lb2);
+    const float rest2 = wave_sum(lb2 == kNegInf ? 0.0f : exp2_fast(lb2 - mb2));
+    const float snew = mb2 == kNegInf ? kNegInf : mb2 + __builtin_amdgcn_logf(rest2);
+#pragma unroll
+    for (int i = 0; i < kSegSlots; ++i)
+      if (sg == 64 * i + lane) segL[i] = snew;
+  }
+  gl.cnt = p.K;
+}
+
+template <typename TE, int KS, int MODE>
 __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) {
   typedef Frag<TE> F;
   typedef typename F::type FT;
+  constexpr bool SAMPLE = MODE != kModeGreedy;
+  constexpr bool GUMBEL = MODE == kModeGumbel;
+  constexpr bool SEQ = MODE == kModeSeq;
   __shared__ MergeLds lds[4];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
@@ -1046,7 +1278,7 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   float thr[2];
   thr[0] = select_items(p, p.zs, pidx, 0, L, nitems);
   thr[1] = kNegInf;
-  if constexpr (SAMPLE) thr[1] = select_items(p, p.gs, pidx, 1, L, nitems);
+  if constexpr (GUMBEL) thr[1] = select_items(p, p.gs, pidx, 1, L, nitems);
 
   RegList zl, gl;
   reglist_init(zl);
@@ -1088,8 +1320,10 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
       ++nr;
     }
     if (nr > 0)
-      rescan_batch<TE, KS, SAMPLE>(p, urow, bcol, pc1, pc2, pc3, qt, qk, qe, nr, thr, L, zl, gl, mism);
+      rescan_batch<TE, KS, GUMBEL>(p, urow, bcol, pc1, pc2, pc3, qt, qk, qe, nr, thr, L, zl, gl, mism);
   }
+  if constexpr (SEQ)
+    seq_draws<TE, KS>(p, pidx, urow, bcol, pc1, pc2, counter_word3(par.request, par.depth, 4u), L, gl);
 
   // Child scoring: lane j handles slot j + 1 (Algorithm 1; §3.2 pre-draw bound; Eq. 3).
   const float lsp = par.log_surv;

@@ -8,17 +8,18 @@
 namespace ts {
 
 // Streaming pass of the expansion.  KS = r / 32 (bf16) or r / 4 (f32); nb =
-// parent blocks of 16 per wave (1, 2 or 4); store_z runs with nb == 1.
-// lds selects the LDS-staged bf16 kernel (V % 8 == 0, four waves per block).
+// parent blocks of 16 per wave (1, 2 or 4); mode is kModeGreedy, kModeGumbel
+// or kModeSeq; store_z (the verification recompute) runs with nb == 1 and no
+// draws.  lds selects the LDS-staged bf16 kernel (V % 8 == 0, four waves).
 template <typename TE, int KS>
-void launch_eval_t(const ExpandParams& p, int nb, bool sample, bool store_z, bool lds, dim3 grid,
+void launch_eval_t(const ExpandParams& p, int nb, int mode, bool store_z, bool lds, dim3 grid,
                    dim3 block, hipStream_t s);
 // Resident blocks per CU of the streaming kernel a launch would use (0 if unknown).
 template <typename TE, int KS>
-int eval_blocks_per_cu_t(int nb, bool sample, bool store_z, bool lds, int block);
-// Per-parent merge, exact top-k and child scoring.
+int eval_blocks_per_cu_t(int nb, int mode, bool store_z, bool lds, int block);
+// Per-parent merge: exact top-k, the draws, child scoring.
 template <typename TE, int KS>
-void launch_merge_t(const MergeParams& p, bool sample, dim3 grid, dim3 block, hipStream_t s);
+void launch_merge_t(const MergeParams& p, int mode, dim3 grid, dim3 block, hipStream_t s);
 
 // Verification.
 void launch_verify_argmax(const void* target, bool bf16, int V, const int* rows, int nrows,

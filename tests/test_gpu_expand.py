@@ -18,12 +18,13 @@ def torch():
     return t
 
 
-def _expand_and_compare(torch, dr, fr, K, T, seed, sample=None, calib=(0.67, -0.46), tag=""):
+def _expand_and_compare(torch, dr, fr, K, T, seed, sample=None, calib=(0.67, -0.46), tag="",
+                        sampler="gumbel"):
     from paper_2609_22098_amd import binding
     dd = binding.drafter_from_host(dr)
     P = len(fr["token"])
     parents = binding.parents_to_device(fr["token"], fr["depth"], fr["request"], fr["log_surv"], fr["path"])
-    out = binding.expand(dd, parents, P, K, T, seed, calib=calib)
+    out = binding.expand(dd, parents, P, K, T, seed, calib=calib, sampler=sampler)
     torch.cuda.synchronize()
     g = {k: v.cpu().numpy() for k, v in out.items() if not k.startswith("_")}
     assert np.all(g["diag"] == 0), "recomputed candidate runs differ from the streaming pass"
@@ -32,9 +33,9 @@ def _expand_and_compare(torch, dr, fr, K, T, seed, sample=None, calib=(0.67, -0.
     tally = Tally()
     for i in idx:
         ev = o.eval_node(om, int(fr["request"][i]), int(fr["token"][i]), int(fr["depth"][i]),
-                         int(fr["path"][i]), T, seed, K, want_z=False)
+                         int(fr["path"][i]), T, seed, K, want_z=False, sampler=sampler)
         compare_parent(g, i, ev, float(fr["log_surv"][i]), T, K, dr.dtype, tally, a=calib[0], b=calib[1],
-                       tag=f"{tag} parent {i}")
+                       tag=f"{tag} parent {i}", sampler=sampler)
     print(f"{tag}: compared {tally.compared} parents, near-ties {tally.near_ties}, "
           f"max rel err {tally.max_err:.2e}")
     assert not tally.failures, tally.failures[:5]
@@ -98,6 +99,63 @@ def test_serving_2048_parent_frontier(torch):
     sample = sorted(rng.choice(2048, 40, replace=False))
     _expand_and_compare(torch, dr, fr, 8, 0.7, seed=0, sample=sample, tag="serving T=0.7")
     _expand_and_compare(torch, dr, fr, 8, 0.0, seed=0, sample=sample[:16], tag="serving T=0")
+
+
+# ---------------------------------------------------------------- sequential draws
+
+@pytest.mark.parametrize("T", [1.0, 0.6])
+def test_sequential_tiny_workload_all_parents(torch, T):
+    """Sequential draws (one 4096-token segment, 64 blocks), fp32: every parent of a 3-per-depth
+    frontier of the tiny workload."""
+    dr = synth.make_workload_drafter(0, seed=0)
+    fr = synth.make_frontier(dr, per_depth=3, seed=1)
+    _expand_and_compare(torch, dr, fr, 4, T, seed=2, tag=f"sequential tiny T={T}", sampler="sequential")
+
+
+@pytest.mark.parametrize("dtype,r,V", [("f32", 16, 1000), ("f32", 32, 4097), ("bf16", 32, 8193),
+                                       ("bf16", 64, 100), ("f32", 64, 77), ("bf16", 128, 12000)])
+def test_sequential_ragged_shapes(torch, dtype, r, V):
+    """Sequential draws over ragged vocabularies: partial last block and segment, several
+    segments, vocabularies smaller than one block; K up to 12 (draws cross blocks and segments)."""
+    dr = synth.make_drafter(V, 5, r, R=3, dtype=dtype, u_sigma=1.0, planted=None, zipf=None,
+                            ew_sigma=0.2, seed=8)
+    fr = synth.make_frontier(dr, per_depth=3, seed=2)
+    keep = np.arange(37)
+    fr = {k: v[keep] for k, v in fr.items()}
+    _expand_and_compare(torch, dr, fr, min(12, V), 1.7, seed=4, tag=f"sequential ragged {dtype} r={r} V={V}",
+                        sampler="sequential")
+
+
+def test_sequential_v151936_r256_T1(torch):
+    """V=151936, r=256, bf16, T=1 (one sum serves lse0 and lseT): 24 sampled parents of 128."""
+    dr = synth.make_workload_drafter(2, seed=0)
+    fr = synth.make_frontier(dr, per_depth=8, seed=0)
+    rng = np.random.default_rng(2)
+    sample = sorted(rng.choice(128, 24, replace=False))
+    _expand_and_compare(torch, dr, fr, 8, 1.0, seed=1, sample=sample, tag="sequential v151936 r256 T=1",
+                        sampler="sequential")
+
+
+def test_sequential_serving_2048_parent_frontier(torch):
+    """The benchmark's launch: 64 requests, V=151936 (38 segments), r=64, bf16, T=0.7, 2048
+    parents; 48 sampled parents against the oracle."""
+    dr = synth.make_workload_drafter(3, seed=0)
+    fr = synth.make_frontier(dr, per_depth=2, seed=0)
+    rng = np.random.default_rng(3)
+    sample = sorted(rng.choice(2048, 48, replace=False))
+    _expand_and_compare(torch, dr, fr, 8, 0.7, seed=0, sample=sample, tag="sequential serving T=0.7",
+                        sampler="sequential")
+
+
+@pytest.mark.parametrize("T", [0.02, 0.2])
+def test_sequential_low_temperature(torch, T):
+    """Low temperatures: the remaining mass after the first draws is tiny next to the drawn
+    tokens' mass, so every level renormalises against its own maximum; all parents against the
+    oracle across three segments."""
+    dr = synth.make_drafter(9000, 4, 32, R=2, dtype="bf16", u_sigma=3.0, planted=None, zipf=None,
+                            ew_sigma=0.2, seed=9)
+    fr = synth.make_frontier(dr, per_depth=4, seed=5)
+    _expand_and_compare(torch, dr, fr, 8, T, seed=3, tag=f"sequential low T={T}", sampler="sequential")
 
 
 def test_deterministic_and_invalid_parents(torch):

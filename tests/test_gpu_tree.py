@@ -21,21 +21,21 @@ def torch():
     return t
 
 
-def _trees(dr, anchors, thetas, N, K, T, seed):
+def _trees(dr, anchors, thetas, N, K, T, seed, sampler="gumbel"):
     from paper_2609_22098_amd import binding
     dd = binding.drafter_from_host(dr)
-    tree = binding.build_tree(dd, anchors, thetas, N, K, T, seed)
+    tree = binding.build_tree(dd, anchors, thetas, N, K, T, seed, sampler=sampler)
     return dd, tree
 
 
-def _compare_all(dr, tree, anchors, thetas, N, K, T, seed, requests=None, tag=""):
+def _compare_all(dr, tree, anchors, thetas, N, K, T, seed, requests=None, tag="", sampler="gumbel"):
     om = o.Model(dr.U32, dr.E32, dr.W2_32)
     tally = Tally()
     refs = {}
     for q in (range(dr.R) if requests is None else requests):
-        ref = o.expand_tree(om, q, int(anchors[q]), float(thetas[q]), N, K, T, seed)
+        ref = o.expand_tree(om, q, int(anchors[q]), float(thetas[q]), N, K, T, seed, sampler=sampler)
         refs[q] = ref
-        compare_tree(tree, q, ref, float(thetas[q]), dr.dtype, tally, tag=f"{tag} request {q}")
+        compare_tree(tree, q, ref, float(thetas[q]), dr.dtype, tally, tag=f"{tag} request {q}", T=T)
     sizes = [int(tree.n[q]) for q in refs]
     print(f"{tag}: {tally.compared} trees, sizes {min(sizes)}..{max(sizes)}, near-ties {tally.near_ties}, "
           f"max rel err {tally.max_err:.2e}")
@@ -108,6 +108,29 @@ def test_serving_natural_trees(torch):
     _compare_all(dr, tree, anchors, thetas, w["N"], w["K"], 0.7, 0, tag="serving natural")
 
 
+@pytest.mark.parametrize("T,theta", [(1.0, 0.0), (0.5, 0.01)])
+def test_sequential_sharp_multi_request_trees(torch, T, theta):
+    """Sequential draws in whole trees: 6 requests, per-request theta, several waves."""
+    dr = synth.make_drafter(3000, 8, 32, R=6, dtype="bf16", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
+                            ew_sigma=0.3, seed=3, u_scale=3.0)
+    anchors, _, _ = synth.make_controls(6, dr.V, theta, seed=3)
+    thetas = np.array([theta, theta * 2, theta / 2, 0.0, theta, theta * 4], np.float32)
+    _, tree = _trees(dr, anchors, thetas, 40, 3, T, 9, sampler="sequential")
+    refs = _compare_all(dr, tree, anchors, thetas, 40, 3, T, 9, tag=f"sequential sharp T={T} theta={theta}",
+                        sampler="sequential")
+    assert max(int(r.depth.max()) for r in refs.values()) >= 3
+
+
+def test_sequential_serving_natural_trees(torch):
+    """The benchmark's trees with sequential draws: 64 requests, V=151936, T=0.7."""
+    w = synth.WORKLOADS[3]
+    dr = synth.make_workload_drafter(3, seed=0)
+    anchors, thetas, _ = synth.make_controls(dr.R, dr.V, w["theta"], seed=0)
+    _, tree = _trees(dr, anchors, thetas, w["N"], w["K"], 0.7, 0, sampler="sequential")
+    _compare_all(dr, tree, anchors, thetas, w["N"], w["K"], 0.7, 0, tag="sequential serving natural",
+                 sampler="sequential")
+
+
 # ---------------------------------------------------------------- verification
 
 def _prefixes(tree, q):
@@ -158,11 +181,12 @@ def test_verify_parity_multi_request(torch, T):
           f"accepted lengths {list(plen)}")
 
 
-def test_verify_losslessness_chi_square(torch):
+@pytest.mark.parametrize("sampler", ["gumbel", "sequential"])
+def test_verify_losslessness_chi_square(torch, sampler):
     """Proposition 1 on the GPU: 60000 replicate requests (independent Philox streams through the
     request field) build sampled trees and verify them against prefix-keyed target rows; the first
     emitted token follows softmax(target_root / T) and the token after an accepted child x follows
-    softmax(target_x / T)."""
+    softmax(target_x / T).  Both realisations of the draws."""
     from paper_2609_22098_amd import binding
     import itertools
     V, D, K, N, T, R = 6, 3, 3, 7, 1.0, 60000
@@ -177,7 +201,7 @@ def test_verify_losslessness_chi_square(torch):
             rows[pre] = rng.normal(size=V).astype(np.float32)
     dd = binding.drafter_from_host(dr)
     anchors = np.ones(R, np.int32)
-    tree = binding.build_tree(dd, anchors, np.zeros(R, np.float32), N, K, T, 99)
+    tree = binding.build_tree(dd, anchors, np.zeros(R, np.float32), N, K, T, 99, sampler=sampler)
     cap = N + 1
     tgt = np.zeros((R, cap, V), np.float32)
     for q in range(R):
