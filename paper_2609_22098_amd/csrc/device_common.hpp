@@ -80,16 +80,98 @@ __device__ __forceinline__ float log_phat(float lq, float a, float b) {
   return (x >= 0.0f) ? -log1pf(expf(-x)) : x - log1pf(expf(x));
 }
 
-// Wave-wide reductions (64 lanes) with a fixed butterfly order.
+// Cross-lane moves with DPP (data-parallel primitives): the source lane's
+// value moves inside the VALU operand path, without an LDS round trip.
+// CTRL: 0xB1 = quad_perm [1,0,3,2], 0x4E = quad_perm [2,3,0,1],
+// 0x141 = row_half_mirror (lane i <- 7 - i within 8), 0x140 = row_mirror
+// (i <- 15 - i within 16), 0x111 + (n - 1) = row_shr:n, 0x138 = wave_shr:1
+// (lane i <- i - 1 across the wave); lanes without a source read 0.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, true);
+}
+
+// Value of lane l (l wave-uniform), read through a scalar register.
+__device__ __forceinline__ float lane_f32(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+__device__ __forceinline__ int lane_i32(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+
+// Wave-wide (64 lanes) reductions in a fixed order: pairs, quads, halves of
+// a row, rows (all lanes of a row end equal), then the four rows in order.
+// Every lane gets the same value.
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  v = fmaxf(v, dpp_f32<0xB1>(v));
+  v = fmaxf(v, dpp_f32<0x4E>(v));
+  v = fmaxf(v, dpp_f32<0x141>(v));
+  v = fmaxf(v, dpp_f32<0x140>(v));
+  return fmaxf(fmaxf(lane_f32(v, 0), lane_f32(v, 16)), fmaxf(lane_f32(v, 32), lane_f32(v, 48)));
 }
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += dpp_f32<0xB1>(v);
+  v += dpp_f32<0x4E>(v);
+  v += dpp_f32<0x141>(v);
+  v += dpp_f32<0x140>(v);
+  return ((lane_f32(v, 0) + lane_f32(v, 16)) + lane_f32(v, 32)) + lane_f32(v, 48);
+}
+__device__ __forceinline__ int wave_sum_i32(int v) {
+  v += dpp_i32<0xB1>(v);
+  v += dpp_i32<0x4E>(v);
+  v += dpp_i32<0x141>(v);
+  v += dpp_i32<0x140>(v);
+  return ((lane_i32(v, 0) + lane_i32(v, 16)) + lane_i32(v, 32)) + lane_i32(v, 48);
+}
+
+// Exchanges across rows with the gfx950 permlane swaps (no LDS round trip):
+// xor16 gives lane i the value of lane i ^ 16, xor32 that of lane i ^ 32.
+__device__ __forceinline__ uint32_t xor16_u32(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return ((threadIdx.x >> 4) & 1) ? r[0] : r[1];
+}
+__device__ __forceinline__ uint32_t xor32_u32(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return ((threadIdx.x >> 5) & 1) ? r[0] : r[1];
+}
+__device__ __forceinline__ float xor16_f32(float v) { return __uint_as_float(xor16_u32(__float_as_uint(v))); }
+__device__ __forceinline__ float xor32_f32(float v) { return __uint_as_float(xor32_u32(__float_as_uint(v))); }
+__device__ __forceinline__ int xor16_i32(int v) { return (int)xor16_u32((uint32_t)v); }
+__device__ __forceinline__ int xor32_i32(int v) { return (int)xor32_u32((uint32_t)v); }
+
+// Sum over the four lanes n, n + 16, n + 32, n + 48, in one order for all four.
+__device__ __forceinline__ float cross_row_sum(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  const float s = __uint_as_float(a[0]) + __uint_as_float(a[1]);  // rows (0+1), (2+3)
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+__device__ __forceinline__ float cross_row_max(float v) {
+  const float m = fmaxf(v, xor16_f32(v));
+  return fmaxf(m, xor32_f32(m));
+}
+
+// Maximum over each row of 16 lanes (every lane of the row gets it).
+__device__ __forceinline__ float row_max(float v) {
+  v = fmaxf(v, dpp_f32<0xB1>(v));
+  v = fmaxf(v, dpp_f32<0x4E>(v));
+  v = fmaxf(v, dpp_f32<0x141>(v));
+  return fmaxf(v, dpp_f32<0x140>(v));
+}
+
+// Inclusive prefix sum over the 64 lanes: a four-step scan inside each row of
+// 16 (row_shr 1, 2, 4, 8), then the totals of the rows before.
+__device__ __forceinline__ float wave_incl_scan(float x) {
+  x += dpp_f32<0x111>(x);
+  x += dpp_f32<0x112>(x);
+  x += dpp_f32<0x114>(x);
+  x += dpp_f32<0x118>(x);
+  const float r0 = lane_f32(x, 15), r1 = lane_f32(x, 31), r2 = lane_f32(x, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  const float off = row == 0 ? 0.0f : row == 1 ? r0 : row == 2 ? r0 + r1 : (r0 + r1) + r2;
+  return x + off;
 }
 
 }  // namespace ts

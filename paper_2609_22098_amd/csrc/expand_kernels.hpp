@@ -92,7 +92,7 @@ struct MergeParams {
   const float* part_sT;
   RunSummaryPtr zs;
   RunSummaryPtr gs;
-  const float* blk;
+  float* blk;  // per-parent block table; the draws update their own parent's rows
   int nblk;
   ts_expand_out out;
 };
@@ -282,11 +282,8 @@ __device__ __forceinline__ void top_store(const RunSummaryPtr& d, size_t o, cons
 // parent (lanes n, n+16, n+32, n+48) hold the block's four runs.
 __device__ __forceinline__ float block_log_mass(float a, float ml) {
   const float l = a > 0.0f ? ml + __builtin_amdgcn_logf(a) : kNegInf;
-  float m = fmaxf(l, __shfl_xor(l, 16, 64));
-  m = fmaxf(m, __shfl_xor(m, 32, 64));
-  float s = m == kNegInf ? 0.0f : exp2_fast(l - m);
-  s += __shfl_xor(s, 16, 64);
-  s += __shfl_xor(s, 32, 64);
+  const float m = cross_row_max(l);
+  const float s = cross_row_sum(m == kNegInf ? 0.0f : exp2_fast(l - m));
   return m == kNegInf ? kNegInf : m + __builtin_amdgcn_logf(s);
 }
 
@@ -766,6 +763,7 @@ struct MergeLds {
   int item_k[kItemCap];  // key kind: 0 = z, 1 = Gumbel
   float item_e[kItemCap];  // expected run maximum (NaN if unknown)
   uint32_t whole[kMaxChunks / 32];
+  float seg_blk[40 * 64];  // sequential draws: the parent's block table when V <= 40 * 4096
 };
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -774,11 +772,7 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__device__ __forceinline__ int wave_sum_int(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
+__device__ __forceinline__ int wave_sum_int(int v) { return wave_sum_i32(v); }
 
 // A sorted list of at most K (key, token, aux) entries kept in registers:
 // lane j < cnt holds entry j; order: key desc, token asc.
@@ -799,9 +793,10 @@ __device__ __forceinline__ void reglist_insert(RegList& l, int K, float v, int i
   const bool ahead = lane < l.cnt && run_before(l.val, l.id, v, id);
   const int pos = __popcll(__ballot(ahead));
   if (pos >= K) return;
-  const float pv = __shfl_up(l.val, 1, 64);
-  const int pid = __shfl_up(l.id, 1, 64);
-  const float pa = __shfl_up(l.aux, 1, 64);
+  // the entries from pos on move up one lane (DPP wave_shr:1)
+  const float pv = dpp_f32<0x138>(l.val);
+  const int pid = dpp_i32<0x138>(l.id);
+  const float pa = dpp_f32<0x138>(l.aux);
   if (lane == pos) {
     l.val = v; l.id = id; l.aux = a;
   } else if (lane > pos && lane < K) {
@@ -892,18 +887,17 @@ __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* uro
       if (q == b) { tb = t[q]; kd = kind[q]; ex = expect[q]; }
     const bool live = b < nrun && tb + e < V;
     float rm = live ? kv : kNegInf;
-#pragma unroll
-    for (int o = 8; o >= 1; o >>= 1) rm = fmaxf(rm, __shfl_xor(rm, o, 64));
+    rm = row_max(rm);  // the run's 16 keys sit in one row of 16 lanes
     mism += __popcll(__ballot(live && e == 0 && !__builtin_isnan(ex) && rm != ex));
     const float th = kd ? thr[1] : thr[0];
     uint64_t mask = __ballot(live && kv >= th);
     while (mask) {
       const int src = __ffsll((unsigned long long)mask) - 1;
       mask &= mask - 1;
-      const float cv = __shfl(kv, src, 64);
-      const float cz = __shfl(L.bz[b][e], src, 64);
-      const int ct = __shfl(tb + e, src, 64);
-      const int ck = __shfl(kd, src, 64);
+      const float cv = lane_f32(kv, src);
+      const float cz = lane_f32(L.bz[b][e], src);
+      const int ct = lane_i32(tb + e, src);
+      const int ck = lane_i32(kd, src);
       if (ck == 0)
         reglist_insert(zl, p.K, cv, ct, cz);
       else
@@ -920,8 +914,11 @@ __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* uro
 // threshold.  A token whose key reaches the threshold lies in a run whose
 // maximum reaches it: one of its chunk's recorded runs, or, when the chunk's
 // rest maximum reaches it too, somewhere in the chunk (a whole-chunk item).
-__device__ __forceinline__ float select_items(const MergeParams& p, const RunSummaryPtr& sm,
-                                              int pidx, int kind, MergeLds& L, int& nitems) {
+// NE, NR: recorded-run and chunk-rest slots per lane (NE = 4 NR; S <= 64 NR).
+template <int NE, int NR>
+__device__ __forceinline__ float select_items_n(const MergeParams& p, const RunSummaryPtr& sm,
+                                                int pidx, int kind, MergeLds& L, int& nitems) {
+  constexpr int kEntrySlots = NE, kRestSlots = NR;
   const int lane = threadIdx.x & 63;
   const int S = p.S, K = p.K;
   const size_t pb = (size_t)pidx * S;
@@ -1021,20 +1018,15 @@ __device__ __forceinline__ float select_items(const MergeParams& p, const RunSum
   return thr;
 }
 
+__device__ __forceinline__ float select_items(const MergeParams& p, const RunSummaryPtr& sm,
+                                              int pidx, int kind, MergeLds& L, int& nitems) {
+  if (p.S <= 64) return select_items_n<4, 1>(p, sm, pidx, kind, L, nitems);
+  return select_items_n<kMaxChunks * kTopRuns / 64, kMaxChunks / 64>(p, sm, pidx, kind, L, nitems);
+}
+
 // ---------------------------------------------------------------- sequential draws
 
 constexpr int kSegSlots = (TS_MAX_V + 64 * kSegTokens - 1) / (64 * kSegTokens);  // segments per lane
-
-// Inclusive prefix sum over the 64 lanes (fixed order).
-__device__ __forceinline__ float wave_incl_scan(float x) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const float y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  return x;
-}
 
 // One categorical pick over items laid out as item = 64 * slot + lane with
 // masses m >= 0: the first item whose inclusive cumulative mass exceeds
@@ -1048,7 +1040,7 @@ __device__ __forceinline__ int wave_pick(const float (&m)[NS], float u) {
   for (int i = 0; i < NS; ++i) {
     const float x = wave_incl_scan(m[i]);
     c[i] = base + x;
-    base += __shfl(x, 63, 64);
+    base += lane_f32(x, 63);
   }
   const float t = u * base;
   int cnt = 0, last = -1;
@@ -1066,7 +1058,11 @@ __device__ __forceinline__ int wave_pick(const float (&m)[NS], float u) {
 // proportion to its remaining mass, from the words of one Philox call
 // (c0 = j, tag 4).  Masses are handled as base-2 logs relative to each
 // level's largest one, so removing drawn tokens never underflows the rest.
+// The parent's block table lives in LDS when it fits (V <= 40 * 4096), else
+// in its rows of the workspace; a drawn token's block is rewritten in place.
 // Draw j lands in lane j - 1 of gl (token, z).
+constexpr int kLdsSegs = 40;
+
 template <typename TE, int KS>
 __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const TE* urow,
                                           const typename Frag<TE>::type (&bcol)[KS], uint32_t pc1,
@@ -1076,38 +1072,53 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
   const int n = lane & 15, g = lane >> 4;
   const int V = p.V, nblk = p.nblk;
   const TE* W2 = static_cast<const TE*>(p.W2);
-  const float* blk = p.blk + (size_t)pidx * nblk;
+  float* gblk = p.blk + (size_t)pidx * nblk;
   constexpr int kBps = kSegTokens / kBlkTokens;  // blocks per segment (64)
+  const int nseg = (nblk + kBps - 1) / kBps;
+  const bool in_lds = nseg <= kLdsSegs;
 
-  // segment log-masses: lane l holds segment l + 64 i; the wave reduces one
-  // segment (its 64 blocks, one per lane) at a time, eight loads in flight
+  // Segment log-masses (lane l owns segment l + 64 i).  The wave reads the
+  // table one segment per load (lane = block offset, coalesced), keeps it in
+  // LDS when it fits, and reduces each segment with DPP.
   float segL[kSegSlots];
 #pragma unroll
   for (int i = 0; i < kSegSlots; ++i) segL[i] = kNegInf;
-  const int nseg = (nblk + kBps - 1) / kBps;
-#pragma unroll 1
-  for (int s0 = 0; s0 < nseg; s0 += 8) {
-    float x[8];
+  auto reduce_seg = [&](int sg, float x) {
+    const float m = wave_max(x);
+    const float sum = wave_sum(m == kNegInf ? 0.0f : exp2_fast(x - m));
+    const float l = m == kNegInf ? kNegInf : m + __builtin_amdgcn_logf(sum);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int b = (s0 + k) * kBps + lane;
-      x[k] = (s0 + k < nseg && b < nblk) ? blk[b] : kNegInf;
+    for (int i = 0; i < kSegSlots; ++i)
+      if (sg == 64 * i + lane) segL[i] = l;
+  };
+  if (in_lds) {
+    float x[kLdsSegs];
+#pragma unroll
+    for (int k = 0; k < kLdsSegs; ++k) {
+      const int b = k * kBps + lane;
+      x[k] = (k < nseg && b < nblk) ? gblk[b] : kNegInf;
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int sg = s0 + k;
-      const float m = wave_max(x[k]);
-      const float sum = wave_sum(m == kNegInf ? 0.0f : exp2_fast(x[k] - m));
-      const float l = m == kNegInf ? kNegInf : m + __builtin_amdgcn_logf(sum);
+    for (int k = 0; k < kLdsSegs; ++k)
+      if (k < nseg) L.seg_blk[k * kBps + lane] = x[k];
 #pragma unroll
-      for (int i = 0; i < kSegSlots; ++i)
-        if (sg < nseg && sg == 64 * i + lane) segL[i] = l;
+    for (int k = 0; k < kLdsSegs; ++k)
+      if (k < nseg) reduce_seg(k, x[k]);
+    wave_sync_lds();
+  } else {
+#pragma unroll 1
+    for (int s0 = 0; s0 < nseg; s0 += 8) {
+      float x[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int b = (s0 + k) * kBps + lane;
+        x[k] = (s0 + k < nseg && b < nblk) ? gblk[b] : kNegInf;
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (s0 + k < nseg) reduce_seg(s0 + k, x[k]);
     }
   }
-  // blocks whose mass changed (a token of theirs was drawn): lane k holds entry k
-  int ov_b = -1;
-  float ov_l = kNegInf;
-  int nov = 0;
   gl.cnt = 0;
 #pragma unroll 1
   for (int j = 1; j <= p.K; ++j) {
@@ -1124,12 +1135,8 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
     const int sg = wave_pick(ms, word_to_uniform(w0));
     // level 2: block within the segment (lane = block offset)
     const int b = sg * kBps + lane;
-    float lb = (sg >= 0 && b < nblk) ? blk[b] : kNegInf;
-    for (int k = 0; k < nov; ++k) {
-      const int ob = __shfl(ov_b, k, 64);
-      const float ol = __shfl(ov_l, k, 64);
-      if (ob == b) lb = ol;
-    }
+    const bool bin = sg >= 0 && b < nblk;
+    const float lb = bin ? (in_lds ? L.seg_blk[b] : gblk[b]) : kNegInf;
     const float mb = wave_max(lb);
     float m2[1];
     m2[0] = lb == kNegInf ? 0.0f : exp2_fast(lb - mb);
@@ -1137,9 +1144,14 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
     const int bsel = sg * kBps + bo;
     // level 3: token within the block; recompute its 64 logits (four runs of 16)
     const int t0 = bsel * kBlkTokens;
+    // all loads of the block first (one round trip), then the MFMAs
+    typename F::type wf[4][KS];
     f32x4 acc[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
+      const TE* wrow = W2 + (size_t)min(t0 + 16 * q + n, V - 1) * p.r;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) wf[q][kk] = F::load(wrow, kk * F::kPerStep, g);
       acc[q] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
       if (n == 0) {
 #pragma unroll
@@ -1148,10 +1160,11 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
           acc[q][e] = tok < V ? F::to_f32(urow[min(tok, V - 1)]) : kNegInf;
         }
       }
-      const TE* wrow = W2 + (size_t)min(t0 + 16 * q + n, V - 1) * p.r;
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) acc[q] = F::mma(F::load(wrow, kk * F::kPerStep, g), bcol[kk], acc[q]);
     }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) acc[q] = F::mma(wf[q][kk], bcol[kk], acc[q]);
     if (n == 0) {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -1163,14 +1176,14 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
     const float zy = L.bz[lane >> 4][lane & 15];
     wave_sync_lds();
     bool live = y < V && bo >= 0;
-    for (int k = 0; k < j - 1; ++k) live &= __shfl(gl.id, k, 64) != y;
+    for (int k = 0; k < j - 1; ++k) live &= lane_i32(gl.id, k) != y;
     const float xy = live ? zy * p.cT : kNegInf;
     const float mt = wave_max(xy);
     float m3[1];
     m3[0] = live ? exp2_fast(xy - mt) : 0.0f;
     const int to = wave_pick(m3, word_to_uniform(w2));
     const int tsel = t0 + to;
-    const float zsel = __shfl(zy, to < 0 ? 0 : to, 64);
+    const float zsel = lane_f32(zy, to < 0 ? 0 : to);
     if (lane == j - 1) {
       gl.id = to < 0 ? -1 : tsel;
       gl.aux = zsel;
@@ -1182,11 +1195,18 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
     const float mt2 = wave_max(left ? xy : kNegInf);
     const float rest3 = wave_sum(left ? exp2_fast(xy - mt2) : 0.0f);
     const float lnew = mt2 == kNegInf ? kNegInf : mt2 + __builtin_amdgcn_logf(rest3);
-    int slot = -1;
-    for (int k = 0; k < nov; ++k)
-      if (__shfl(ov_b, k, 64) == bsel) slot = k;
-    if (slot < 0) slot = nov++;
-    if (lane == slot) { ov_b = bsel; ov_l = lnew; }
+    if (lane == bo && bin) {
+      if (in_lds)
+        L.seg_blk[bsel] = lnew;
+      else
+        gblk[bsel] = lnew;
+    }
+    if (in_lds) {
+      wave_sync_lds();
+    } else {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
     const float lb2 = lane == bo ? lnew : lb;
     const float mb2 = wave_max(lb2);
     const float rest2 = wave_sum(lb2 == kNegInf ? 0.0f : exp2_fast(lb2 - mb2));
@@ -1333,10 +1353,10 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
     // bound of slot j: the first of the greedy order not drawn before j
     int bi = K - 1;
     for (int i = K - 1; i >= 0; --i) {
-      const int pid = __shfl(zl.id, i, 64);
+      const int pid = lane_i32(zl.id, i);
       bool used = false;
       for (int s2 = 0; s2 < K - 1; ++s2) {
-        const int gid = __shfl(gl.id, s2, 64);
+        const int gid = lane_i32(gl.id, s2);
         used |= (s2 < lane) && (gid == pid);
       }
       if (!used) bi = i;

@@ -147,6 +147,14 @@ def test_sequential_serving_2048_parent_frontier(torch):
                         sampler="sequential")
 
 
+def test_sequential_large_vocabulary(torch):
+    """V = 170000 (42 segments): the block table stays in the workspace instead of LDS."""
+    dr = synth.make_drafter(170000, 3, 32, R=1, dtype="bf16", u_sigma=1.5, planted=None, zipf=(6.0, 1.1),
+                            ew_sigma=0.1, seed=12)
+    fr = synth.make_frontier(dr, per_depth=4, seed=6)
+    _expand_and_compare(torch, dr, fr, 8, 0.8, seed=5, tag="sequential V=170000", sampler="sequential")
+
+
 @pytest.mark.parametrize("T", [0.02, 0.2])
 def test_sequential_low_temperature(torch, T):
     """Low temperatures: the remaining mass after the first draws is tiny next to the drawn
