@@ -280,6 +280,17 @@ __device__ __forceinline__ void top_store(const RunSummaryPtr& d, size_t o, cons
 // Base-2 log of the q_T mass of this step's 64-token block for the lane's
 // parent: a is the lane's run sum relative to 2^ml; the four lane groups of a
 // parent (lanes n, n+16, n+32, n+48) hold the block's four runs.
+// sum over j of 2^(v[j] * c - ref), as four interleaved partial sums
+// (short dependency chains), combined in a fixed order.
+__device__ __forceinline__ float sum16_exp2(const float (&v)[16], float c, float ref) {
+  float a[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) a[q] = exp2_fast(__builtin_fmaf(v[q], c, -ref));
+#pragma unroll
+  for (int j = 4; j < 16; ++j) a[j & 3] += exp2_fast(__builtin_fmaf(v[j], c, -ref));
+  return (a[0] + a[1]) + (a[2] + a[3]);
+}
+
 __device__ __forceinline__ float block_log_mass(float a, float ml) {
   const float l = a > 0.0f ? ml + __builtin_amdgcn_logf(a) : kNegInf;
   const float m = cross_row_max(l);
@@ -407,16 +418,13 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
       const float mref = fmaxf(mn, -1e30f);
       const float bref = fmaxf(bm, -1e30f);
       const float ml = mref * kLog2e, bl = bref * kLog2e;
-      float a0 = 0.0f;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) a0 += exp2_fast(__builtin_fmaf(v[j], kLog2e, -bl));
+      float a0 = sum16_exp2(v, kLog2e, bl);
       s0[nb] = __builtin_fmaf(s0[nb], exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -ml)),
                               a0 * exp2_fast(bl - ml));
       const float mlT = mref * p.cT, blT = bref * p.cT;
       float aT = 0.0f;
       if (SAMPLE && p.need_T) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) aT += exp2_fast(__builtin_fmaf(v[j], p.cT, -blT));
+        aT = sum16_exp2(v, p.cT, blT);
         sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)),
                                 aT * exp2_fast(blT - mlT));
       }
@@ -621,7 +629,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
 #pragma unroll
       for (int bb = 0; bb < 4; ++bb)
         acc[bb][nb] = f32x4{u.get(bb * 4), u.get(bb * 4 + 1), u.get(bb * 4 + 2), u.get(bb * 4 + 3)};
-      if (tl + 16 > V) {
+      if (t0 + 64 > V) {  // the vocabulary's last step only (a uniform branch)
 #pragma unroll
         for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
@@ -655,16 +663,13 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
       const float mref = fmaxf(mn, -1e30f);
       const float bref = fmaxf(bm, -1e30f);
       const float ml = mref * kLog2e, bl = bref * kLog2e;
-      float a0 = 0.0f;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) a0 += exp2_fast(__builtin_fmaf(v[j], kLog2e, -bl));
+      float a0 = sum16_exp2(v, kLog2e, bl);
       s0[nb] = __builtin_fmaf(s0[nb], exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -ml)),
                               a0 * exp2_fast(bl - ml));
       const float mlT = mref * p.cT, blT = bref * p.cT;
       float aT = 0.0f;
       if (SAMPLE && p.need_T) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) aT += exp2_fast(__builtin_fmaf(v[j], p.cT, -blT));
+        aT = sum16_exp2(v, p.cT, blT);
         sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)),
                                 aT * exp2_fast(blT - mlT));
       }
