@@ -126,6 +126,35 @@ __device__ __forceinline__ int wave_sum_i32(int v) {
   return ((lane_i32(v, 0) + lane_i32(v, 16)) + lane_i32(v, 32)) + lane_i32(v, 48);
 }
 
+// Eight independent wave reductions, interleaved stage by stage so their
+// latencies overlap; each result equals the single reduction's.
+__device__ __forceinline__ void wave_max8(float (&x)[8]) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) x[k] = fmaxf(x[k], dpp_f32<0xB1>(x[k]));
+#pragma unroll
+  for (int k = 0; k < 8; ++k) x[k] = fmaxf(x[k], dpp_f32<0x4E>(x[k]));
+#pragma unroll
+  for (int k = 0; k < 8; ++k) x[k] = fmaxf(x[k], dpp_f32<0x141>(x[k]));
+#pragma unroll
+  for (int k = 0; k < 8; ++k) x[k] = fmaxf(x[k], dpp_f32<0x140>(x[k]));
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    x[k] = fmaxf(fmaxf(lane_f32(x[k], 0), lane_f32(x[k], 16)), fmaxf(lane_f32(x[k], 32), lane_f32(x[k], 48)));
+}
+__device__ __forceinline__ void wave_sum8(float (&x)[8]) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) x[k] += dpp_f32<0xB1>(x[k]);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) x[k] += dpp_f32<0x4E>(x[k]);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) x[k] += dpp_f32<0x141>(x[k]);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) x[k] += dpp_f32<0x140>(x[k]);
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    x[k] = ((lane_f32(x[k], 0) + lane_f32(x[k], 16)) + lane_f32(x[k], 32)) + lane_f32(x[k], 48);
+}
+
 // Exchanges across rows with the gfx950 permlane swaps (no LDS round trip):
 // xor16 gives lane i the value of lane i ^ 16, xor32 that of lane i ^ 32.
 __device__ __forceinline__ uint32_t xor16_u32(uint32_t v) {

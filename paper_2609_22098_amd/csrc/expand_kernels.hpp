@@ -1083,18 +1083,29 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
   const bool in_lds = nseg <= kLdsSegs;
 
   // Segment log-masses (lane l owns segment l + 64 i).  The wave reads the
-  // table one segment per load (lane = block offset, coalesced), keeps it in
-  // LDS when it fits, and reduces each segment with DPP.
+  // table one segment per load (lane = block offset, coalesced); every load
+  // is issued before the first reduction (a global round trip costs about
+  // as much as all the arithmetic here).  The table is kept in LDS when it
+  // fits, and segments are reduced eight at a time.
   float segL[kSegSlots];
 #pragma unroll
   for (int i = 0; i < kSegSlots; ++i) segL[i] = kNegInf;
-  auto reduce_seg = [&](int sg, float x) {
-    const float m = wave_max(x);
-    const float sum = wave_sum(m == kNegInf ? 0.0f : exp2_fast(x - m));
-    const float l = m == kNegInf ? kNegInf : m + __builtin_amdgcn_logf(sum);
+  auto reduce8 = [&](int s0, const float (&xs)[8]) {
+    float m[8], e[8];
 #pragma unroll
-    for (int i = 0; i < kSegSlots; ++i)
-      if (sg == 64 * i + lane) segL[i] = l;
+    for (int k = 0; k < 8; ++k) m[k] = xs[k];
+    wave_max8(m);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) e[k] = m[k] == kNegInf ? 0.0f : exp2_fast(xs[k] - m[k]);
+    wave_sum8(e);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int sg = s0 + k;
+      const float l = m[k] == kNegInf ? kNegInf : m[k] + __builtin_amdgcn_logf(e[k]);
+#pragma unroll
+      for (int i = 0; i < kSegSlots; ++i)
+        if (sg < nseg && sg == 64 * i + lane) segL[i] = l;
+    }
   };
   if (in_lds) {
     float x[kLdsSegs];
@@ -1107,28 +1118,35 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
     for (int k = 0; k < kLdsSegs; ++k)
       if (k < nseg) L.seg_blk[k * kBps + lane] = x[k];
 #pragma unroll
-    for (int k = 0; k < kLdsSegs; ++k)
-      if (k < nseg) reduce_seg(k, x[k]);
+    for (int s0 = 0; s0 < kLdsSegs; s0 += 8) {
+      if (s0 >= nseg) break;
+      float xs[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) xs[k] = x[s0 + k];
+      reduce8(s0, xs);
+    }
     wave_sync_lds();
   } else {
 #pragma unroll 1
     for (int s0 = 0; s0 < nseg; s0 += 8) {
-      float x[8];
+      float xs[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int b = (s0 + k) * kBps + lane;
-        x[k] = (s0 + k < nseg && b < nblk) ? gblk[b] : kNegInf;
+        xs[k] = (s0 + k < nseg && b < nblk) ? gblk[b] : kNegInf;
       }
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (s0 + k < nseg) reduce_seg(s0 + k, x[k]);
+      reduce8(s0, xs);
     }
   }
+  // the words of every draw: lane j - 1 computes draw j's Philox call
+  uint32_t dw0 = (uint32_t)(lane + 1), dw1 = pc1, dw2 = pc2, dw3 = pc3;
+  philox10(dw0, dw1, dw2, dw3, p.keys);
   gl.cnt = 0;
 #pragma unroll 1
   for (int j = 1; j <= p.K; ++j) {
-    uint32_t w0 = (uint32_t)j, w1 = pc1, w2 = pc2, w3 = pc3;
-    philox10(w0, w1, w2, w3, p.keys);
+    const uint32_t w0 = (uint32_t)lane_i32((int)dw0, j - 1);
+    const uint32_t w1 = (uint32_t)lane_i32((int)dw1, j - 1);
+    const uint32_t w2 = (uint32_t)lane_i32((int)dw2, j - 1);
     // level 1: segment
     float ms[kSegSlots];
     float mx = kNegInf;
