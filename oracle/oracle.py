@@ -76,6 +76,8 @@ def _declare(L):
                                   _I, ctypes.POINTER(_Tree)]
     L.tso_draw_sequential.argtypes = [_P, _I, _D, _U64, _I, _I, _U64, _I, _P, _P]
     L.tso_draw_sequential.restype = None
+    L.tso_tree_mask.argtypes = [_P, _I, _I, _I, _P, _P]
+    L.tso_tree_mask.restype = _I
     L.tso_expand_tree.restype = _I
     L.tso_verify_greedy.argtypes = [ctypes.POINTER(_Tree), _P, _I, _P, _P, _P, _P]
     L.tso_verify_greedy.restype = _I
@@ -254,3 +256,15 @@ def residual_stages(p, qT, x):
     ratio = np.zeros(m); Z = np.zeros(m); pf = np.zeros(len(p))
     lib().tso_residual_stages(len(p), _ptr(p), _ptr(qT), m, _ptr(x), _ptr(ratio), _ptr(Z), _ptr(pf))
     return ratio, Z, pf
+
+
+def tree_mask(parent, n, cap, offset=0):
+    """Ancestor bitmask [cap][ceil(cap/32)] (uint32) and position ids [cap] of one tree."""
+    parent = np.ascontiguousarray(parent, dtype=np.int32)
+    W = (cap + 31) // 32
+    mask = np.zeros((cap, W), np.uint32)
+    pos = np.zeros(cap, np.int32)
+    rc = lib().tso_tree_mask(_ptr(parent), int(n), int(cap), int(offset), _ptr(mask), _ptr(pos))
+    if rc != 0:
+        raise ValueError("tso_tree_mask: malformed tree")
+    return mask, pos

@@ -9,6 +9,7 @@
  *   - without-replacement sibling draws at T>0    (§3.3 residual-proposal equation)
  *   - greedy verification by exact match          (§3.2 item 3; §3.3 first paragraph)
  *   - recursive rejection verification at T>0     (§3.3, Proposition 1)
+ *   - the tree attention mask and position ids    (§3.2 item 3; §5)
  *
  * Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may load
  * this library.  It shares no code with the HIP path and the HIP path never
@@ -682,5 +683,35 @@ int tso_verify_sample(const tso_model* m, int request, const tso_tree* t, const 
   *path_len = len;
   if (min_margin) *min_margin = margin;
   free(p); free(qT); free(q); free(z); free(drawn); free(kids);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Tree attention mask and position ids for the target's verification pass   */
+/* (§3.2 item 3: one forward over the flattened tree with a tree attention   */
+/* mask and per-depth position ids; §5: an ancestor bitmask per row).        */
+/* Row i (node 0 = the anchor) sees exactly the nodes on its root path,      */
+/* itself included: bit j of row i is set iff j is i or an ancestor of i.    */
+/* pos[i] = offset + depth(i), depth counted along the parent chain.         */
+/* Rows n+1 .. cap-1 are zero and get pos -1.  W = ceil(cap / 32) words.     */
+/* ------------------------------------------------------------------------- */
+int tso_tree_mask(const int32_t* parent, int n, int cap, int offset, uint32_t* mask, int32_t* pos) {
+  if (!parent || !mask || !pos || cap < 1 || n < 0 || n >= cap) return -1;
+  const int W = (cap + 31) / 32;
+  memset(mask, 0, sizeof(uint32_t) * (size_t)cap * W);
+  for (int i = 0; i < cap; ++i) pos[i] = -1;
+  for (int i = 0; i <= n; ++i) {
+    int depth = 0;
+    int a = i;
+    for (;;) {
+      mask[(size_t)i * W + (a >> 5)] |= 1u << (a & 31);
+      if (a == 0) break;
+      const int p = parent[a];
+      if (p < 0 || p >= a) return -1; /* parents precede their children */
+      a = p;
+      ++depth;
+    }
+    pos[i] = offset + depth;
+  }
   return 0;
 }

@@ -589,3 +589,55 @@ def test_single_child_acceptance_rate():
         acc += len(path)
     sd = math.sqrt(want * (1 - want) / n)
     assert abs(acc / n - want) < 5 * sd
+
+
+# ---------------------------------------------------------------- tree attention mask
+
+@pytest.mark.parametrize("T,sampler", [(0.0, "gumbel"), (1.0, "gumbel"), (0.7, "sequential")])
+def test_tree_mask_equals_path_prefix_relation(T, sampler):
+    """Bit j of row i is set iff node j's structural path id is a prefix of node i's (j is i
+    or an ancestor of i), and pos = offset + depth, on deep oracle trees."""
+    dr = synth.make_drafter(300, 8, 16, R=1, dtype="f32", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
+                            ew_sigma=0.3, seed=21, u_scale=3.0)
+    m = o.Model(dr.U32, dr.E32, dr.W2_32)
+    tree = o.expand_tree(m, 0, 5, 0.0, 40, 3, T, 4, sampler=sampler)
+    assert tree.depth.max() >= 3
+    cap = tree.n + 9  # unused rows at the end
+    parent = np.full(cap, -1, np.int32)
+    parent[: tree.n + 1] = tree.parent
+    mask, pos = o.tree_mask(parent, tree.n, cap, offset=100)
+    for i in range(cap):
+        for j in range(cap):
+            bit = (int(mask[i, j >> 5]) >> (j & 31)) & 1
+            if i > tree.n or j > tree.n:
+                want = 0
+            else:
+                dj = int(tree.depth[j])
+                low = (1 << (4 * dj)) - 1
+                want = int(dj <= tree.depth[i] and (int(tree.path[i]) & low) == int(tree.path[j]))
+            assert bit == want, (i, j)
+        assert pos[i] == (100 + tree.depth[i] if i <= tree.n else -1)
+
+
+def test_tree_mask_chain_and_star():
+    """A chain gives the lower-triangular all-ones mask with pos = offset + i; a star gives
+    {0, i} rows with pos = offset + 1 (offset 0 for the anchor)."""
+    n = 70
+    chain = np.arange(-1, n, dtype=np.int32)
+    mask, pos = o.tree_mask(chain, n, n + 1, offset=7)
+    dense = np.unpackbits(mask.view(np.uint8), axis=1, bitorder="little")[:, : n + 1]
+    assert np.array_equal(dense, np.tril(np.ones((n + 1, n + 1), np.uint8)))
+    assert list(pos) == [7 + i for i in range(n + 1)]
+    star = np.zeros(n + 1, np.int32)
+    star[0] = -1
+    mask, pos = o.tree_mask(star, n, n + 1)
+    dense = np.unpackbits(mask.view(np.uint8), axis=1, bitorder="little")[:, : n + 1]
+    want = np.eye(n + 1, dtype=np.uint8)
+    want[:, 0] = 1
+    assert np.array_equal(dense, want)
+    assert pos[0] == 0 and np.all(pos[1:] == 1)
+
+
+def test_tree_mask_rejects_a_parent_after_its_child():
+    with pytest.raises(ValueError):
+        o.tree_mask(np.array([-1, 0, 3, 1], np.int32), 3, 4)
