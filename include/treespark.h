@@ -10,6 +10,8 @@
  *                  (§3.2 Algorithm 1; §3.5)
  *   ts_verify      greedy exact-match or recursive-rejection verification
  *                  (§3.2 item 3; §3.3 and Proposition 1)
+ *   ts_tree_mask   the tree attention mask and position ids of the target's
+ *                  verification pass (§3.2 item 3; §5)
  *
  * Conventions shared by every call
  *   - Model tensors are DEVICE pointers owned by the caller, row-major:
@@ -213,6 +215,34 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target,
                   int32_t target_dtype, float T, uint64_t seed, int32_t* path_nodes,
                   int32_t* path_len, int32_t* bonus, void* workspace, size_t workspace_bytes,
                   void* stream);
+
+/* Largest tree (rows per request) the mask builder accepts. */
+#define TS_MAX_CAP 4096
+
+/* Words per mask row of a tree with cap rows: ceil(cap / 32) (0 if cap < 1). */
+int32_t ts_tree_mask_words(int32_t cap);
+
+/*
+ * ts_tree_mask: the tree attention mask and position ids of the target's
+ * verification forward over the flattened trees (§3.2 item 3: one target
+ * pass with a tree attention mask and per-depth position ids; §5: an
+ * ancestor bitmask per row).  Row i of request q (node 0 = the anchor) sees
+ * exactly the nodes on its root path, itself included: bit (j & 31) of word
+ * (j >> 5) of row i is set iff node j is i or an ancestor of i.
+ * pos[q][i] = pos_offset[q] + depth(i), the depth counted along the parent
+ * chain (pos_offset NULL reads as 0).  Rows i > n[q] are all zero and get
+ * pos -1.
+ *   parent [R][cap], n [R], pos_offset [R]: DEVICE inputs in the ts_tree
+ *       layout (parent[q][0] = -1 and 0 <= parent[q][i] < i for i >= 1);
+ *   mask [R][cap][ts_tree_mask_words(cap)] (uint32), pos [R][cap]: DEVICE
+ *       outputs, fully written.
+ * A parent chain that breaks the ordering rule stops at the break (nothing
+ * outside the arrays is read); n[q] < 0 gives an empty tree and
+ * n[q] >= cap is read as cap - 1.  Asynchronous on `stream`.  Host checks:
+ * null pointers, R >= 0, 1 <= cap <= TS_MAX_CAP.
+ */
+int32_t ts_tree_mask(const int32_t* parent, const int32_t* n, int32_t R, int32_t cap,
+                     const int32_t* pos_offset, uint32_t* mask, int32_t* pos, void* stream);
 
 /* Description of the last error on the calling thread ("" if none). */
 const char* ts_last_error(void);

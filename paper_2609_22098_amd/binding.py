@@ -21,7 +21,8 @@ TS_MAX_K, TS_MAX_D = 16, 16
 
 # Every symbol include/treespark.h declares.
 SAMPLERS = {"gumbel": 0, "sequential": 1}  # ts_sampler
-EXPORTED = ("ts_expand_workspace_size", "ts_expand", "ts_build_tree_workspace_size", "ts_build_tree",
+EXPORTED = ("ts_tree_mask_words", "ts_tree_mask",
+            "ts_expand_workspace_size", "ts_expand", "ts_build_tree_workspace_size", "ts_build_tree",
             "ts_verify_workspace_size", "ts_verify", "ts_last_error", "ts_version")
 
 
@@ -87,6 +88,10 @@ def lib():
         L.ts_verify_workspace_size.restype = SZ
         L.ts_verify.argtypes = [P, P, P, I32, F, U64, P, P, P, P, SZ, P]
         L.ts_verify.restype = I32
+        L.ts_tree_mask_words.argtypes = [I32]
+        L.ts_tree_mask_words.restype = I32
+        L.ts_tree_mask.argtypes = [P, P, I32, I32, P, P, P, P]
+        L.ts_tree_mask.restype = I32
         L.ts_last_error.restype = ctypes.c_char_p
         L.ts_version.restype = ctypes.c_char_p
         _lib = L
@@ -293,3 +298,30 @@ def verify(d: DeviceDrafter, tree: HostTree, target, T, seed, workspace=None, st
                          _stream(stream))
     _check(rc)
     return path, plen, bonus
+
+
+def tree_mask(parent, n, cap, pos_offset=None, stream=None):
+    """ts_tree_mask.  parent [R][cap] and n [R] int32 DEVICE tensors (ts_tree layout),
+    pos_offset optional [R] int32 device tensor.  Returns (mask [R][cap][W] int32 tensor holding
+    the uint32 words, pos [R][cap] int32), asynchronous on the stream."""
+    torch = _torch()
+    R = parent.shape[0]
+    assert tuple(parent.shape) == (R, cap) and parent.dtype == torch.int32 and parent.is_contiguous()
+    assert tuple(n.shape) == (R,) and n.dtype == torch.int32
+    W = lib().ts_tree_mask_words(cap)
+    mask = torch.empty((R, cap, W), dtype=torch.int32, device=parent.device)
+    pos = torch.empty((R, cap), dtype=torch.int32, device=parent.device)
+    off = ctypes.c_void_p(pos_offset.data_ptr()) if pos_offset is not None else None
+    rc = lib().ts_tree_mask(ctypes.c_void_p(parent.data_ptr()), ctypes.c_void_p(n.data_ptr()), R, cap, off,
+                            ctypes.c_void_p(mask.data_ptr()), ctypes.c_void_p(pos.data_ptr()), _stream(stream))
+    _check(rc)
+    return mask, pos
+
+
+def tree_mask_from_host(tree: HostTree, pos_offset=None, device="cuda", stream=None):
+    """Upload a HostTree's parents and sizes, then ts_tree_mask."""
+    torch = _torch()
+    parent = torch.from_numpy(np.ascontiguousarray(tree.parent, dtype=np.int32)).to(device)
+    n = torch.from_numpy(np.ascontiguousarray(tree.n, dtype=np.int32)).to(device)
+    off = None if pos_offset is None else torch.from_numpy(np.ascontiguousarray(pos_offset, np.int32)).to(device)
+    return tree_mask(parent, n, tree.cap, off, stream)

@@ -24,6 +24,9 @@ void launch_merge_t(const MergeParams& p, int mode, dim3 grid, dim3 block, hipSt
 // Verification.
 void launch_verify_argmax(const void* target, bool bf16, int V, const int* rows, int nrows,
                           int* argmax_out, float* gap_out, hipStream_t s);
+// Tree attention mask and position ids, one workgroup per request.
+void launch_tree_mask(const int32_t* parent, const int32_t* n, int R, int cap, const int32_t* pos_offset,
+                      uint32_t* mask, int32_t* pos, hipStream_t s);
 // One level of the T > 0 walk: pass A, stages 1..max(mmax, 1), bonus, resolve.
 void launch_verify_level(const VerifyPass& vp, bool bf16, int mmax, hipStream_t s);
 

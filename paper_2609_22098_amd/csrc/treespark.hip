@@ -774,4 +774,19 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
   return TS_OK;
 }
 
+int32_t ts_tree_mask_words(int32_t cap) { return cap < 1 ? 0 : (cap + 31) / 32; }
+
+int32_t ts_tree_mask(const int32_t* parent, const int32_t* n, int32_t R, int32_t cap,
+                     const int32_t* pos_offset, uint32_t* mask, int32_t* pos, void* stream) {
+  g_last_error.clear();
+  if (R < 0) return fail(TS_EINVAL, "R=%d is negative", R);
+  if (cap < 1 || cap > TS_MAX_CAP) return fail(TS_EINVAL, "cap=%d outside [1, %d]", cap, TS_MAX_CAP);
+  if (R == 0) return TS_OK;
+  if (!parent || !n || !mask || !pos) return fail(TS_EINVAL, "parent, n, mask or pos is NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  launch_tree_mask(parent, n, R, cap, pos_offset, mask, pos, s);
+  TS_HIP(hipGetLastError());
+  return TS_OK;
+}
+
 }  // extern "C"

@@ -20,7 +20,7 @@ def _declared():
 
 def test_library_exports_every_declared_symbol():
     declared = _declared()
-    assert len(declared) == 8
+    assert len(declared) == 10
     assert sorted(b.EXPORTED) == declared
     L = b.lib()
     for name in declared:
@@ -125,3 +125,15 @@ def test_verify_rejects_malformed_trees():
     assert call(tdt=9) == b.TS_EINVAL
     assert call(T=-0.5) == b.TS_EINVAL
     assert call(ws=4) == b.TS_ENOSPACE
+
+
+def test_tree_mask_rejects_bad_arguments():
+    L = b.lib()
+    assert L.ts_tree_mask_words(1) == 1 and L.ts_tree_mask_words(32) == 1 and L.ts_tree_mask_words(33) == 2
+    assert L.ts_tree_mask_words(0) == 0
+    assert L.ts_tree_mask(FAKE, FAKE, 2, 0, None, FAKE, FAKE, None) == b.TS_EINVAL
+    assert L.ts_tree_mask(FAKE, FAKE, 2, 4097, None, FAKE, FAKE, None) == b.TS_EINVAL
+    assert L.ts_tree_mask(FAKE, FAKE, -1, 8, None, FAKE, FAKE, None) == b.TS_EINVAL
+    assert L.ts_tree_mask(None, FAKE, 2, 8, None, FAKE, FAKE, None) == b.TS_EINVAL
+    assert L.ts_tree_mask(FAKE, FAKE, 2, 8, None, None, FAKE, None) == b.TS_EINVAL
+    assert L.ts_tree_mask(FAKE, FAKE, 0, 8, None, None, None, None) == b.TS_OK  # nothing to do
