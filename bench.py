@@ -9,7 +9,9 @@ the whole hot path over that batch:
      of every request): conditional logits on MFMA, log-sum-exp, top-k,
      Gumbel-top-k draws, child scoring;
   2. ts_build_tree: best-first trees for the 64 requests under their theta;
-  3. ts_verify: recursive-rejection verification of those trees at T=0.7.
+  3. ts_tree_mask: the trees' attention masks and position ids for the
+     target's verification pass;
+  4. ts_verify: recursive-rejection verification of those trees at T=0.7.
 value = node evaluations (frontier parents + tree-building parents) per
 second over the step.  The roofline object covers the dominant kernel (the
 streaming pass of ts_expand), timed with HIP events on its own stream.
@@ -119,7 +121,7 @@ def _largest_grid(pairs):
     return [v for gk, v in pairs if gk == g]
 
 
-def write_traffic(root, T):
+def write_traffic(root, T, sampler):
     """HBM bytes per launch of the streaming pass from FETCH_SIZE and WRITE_SIZE (KiB per
     dispatch), each scaled by what the same counter reads for a plain copy of known size."""
     with open(os.path.join(root, "copy_fetch", "copy.json")) as f:
@@ -134,7 +136,7 @@ def write_traffic(root, T):
     write = _largest_grid(_counter_per_dispatch(os.path.join(root, "write"), "WRITE_SIZE", EVAL_KERNEL))
     fb = float(np.mean(fetch)) * 1024.0 * scale["FETCH_SIZE"]
     wb = float(np.mean(write)) * 1024.0 * scale["WRITE_SIZE"]
-    rec = {"kernel": EVAL_KERNEL, "T": T, "kernel_source_hash": kernel_source_hash(),
+    rec = {"kernel": EVAL_KERNEL, "T": T, "sampler": sampler, "kernel_source_hash": kernel_source_hash(),
            "fetch_kib_per_dispatch": float(np.mean(fetch)), "write_kib_per_dispatch": float(np.mean(write)),
            "dispatches": [len(fetch), len(write)], "copy_bytes": copy_bytes,
            "copy_scale": scale, "fetch_bytes": fb, "write_bytes": wb, "bytes_per_launch": fb + wb}
@@ -143,20 +145,20 @@ def write_traffic(root, T):
     print(json.dumps(rec))
 
 
-def cpu_baseline(dr, fr, K, T, seed, seconds):
+def cpu_baseline(dr, fr, K, T, seed, seconds, sampler):
     from oracle import oracle
     om = oracle.Model(dr.U32, dr.E32, dr.W2_32)
     n, t0 = 0, time.perf_counter()
     while True:
         oracle.eval_node(om, int(fr["request"][n]), int(fr["token"][n]), int(fr["depth"][n]),
-                         int(fr["path"][n]), T, seed, K, want_z=False)
+                         int(fr["path"][n]), T, seed, K, want_z=False, sampler=sampler)
         n += 1
         el = time.perf_counter() - t0
         if (el >= seconds and n >= 4) or n == len(fr["token"]):
             break
     return {"value": n / el, "unit": "node-evals/s", "cores": 1, "kind": "oracle",
             "sample": f"first {n} of the 2048 frontier parents at T={T} (full-vocabulary fp64 "
-                      f"evaluation with Gumbel draws, one thread), {el:.1f} s"}
+                      f"evaluation with {sampler} draws, one thread), {el:.1f} s"}
 
 
 def main():
@@ -177,7 +179,7 @@ def main():
                          "(fetch, write, copy_fetch, copy_write); writes the traffic file and exits")
     args = ap.parse_args()
     if args.traffic_from:
-        write_traffic(args.traffic_from, args.T)
+        write_traffic(args.traffic_from, args.T, args.sampler)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the draft-tree step has no "
@@ -231,6 +233,7 @@ def main():
         if args.expand_only:
             return
         binding.build_tree(d, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler)
+        binding.tree_mask_from_host(tree)
         binding.verify(d, tree, tgt, T, seed, workspace=ws_v)
 
     for i in range(args.warmup):
@@ -255,11 +258,13 @@ def main():
             binding.expand(dd, parents, P, K, T, seed, outputs=outs, workspace=ws_e, sampler=sampler)
             torch.cuda.synchronize(); b = time.perf_counter()
             binding.build_tree(dd, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler)
+            binding.tree_mask_from_host(tree)
+            torch.cuda.synchronize()
             c = time.perf_counter()
             binding.verify(dd, tree, tgt, T, seed, workspace=ws_v)
             torch.cuda.synchronize(); e = time.perf_counter()
             te += b - a; tb += c - b; tv += e - c
-        phases = {"expand": te / 3e-3, "build_tree": tb / 3e-3, "verify": tv / 3e-3}
+        phases = {"expand": te / 3e-3, "build_tree_and_mask": tb / 3e-3, "verify": tv / 3e-3}
 
     # algorithmic bytes of the streaming pass: U rows touched once, W2 once, E rows
     rows = len(set(zip(fr["request"].tolist(), fr["depth"].tolist())))
@@ -270,7 +275,8 @@ def main():
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
             tr = json.load(f)
-        if tr.get("kernel_source_hash") == kernel_source_hash() and abs(tr.get("T", -1) - T) < 1e-9:
+        if (tr.get("kernel_source_hash") == kernel_source_hash() and abs(tr.get("T", -1) - T) < 1e-9
+                and tr.get("sampler") == args.sampler):
             traffic = tr.get("bytes_per_launch")
     evals_step = P + (0 if args.expand_only else tree_evals)
     result = {
@@ -287,9 +293,11 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w["name"] + (": ts_expand over the 2048-parent frontier" if args.expand_only else
-                                            ": 2048-parent ts_expand + best-first trees + T=0.7 verification"),
+                                            ": 2048-parent ts_expand + best-first trees + tree masks + "
+                                            "T=0.7 verification"),
                    "V": dr.V, "D": dr.D, "r": dr.r, "requests": dr.R, "frontier_parents": P, "K": K,
-                   "T": T, "N": N, "tree_evals_per_step": 0 if args.expand_only else tree_evals},
+                   "T": T, "N": N, "sampler": sampler,
+                   "tree_evals_per_step": 0 if args.expand_only else tree_evals},
         "roofline": {"bound": "hbm", "kernel": EVAL_KERNEL + " (streaming pass of ts_expand)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
@@ -301,7 +309,7 @@ def main():
     }
     if not args.no_cpu:
         log("timing the CPU oracle")
-        result["cpu_baseline"] = cpu_baseline(dr, fr, K, T, seed, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(dr, fr, K, T, seed, args.cpu_seconds, sampler)
     print(json.dumps(result), flush=True)
 
 

@@ -216,6 +216,46 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target,
                   int32_t* path_len, int32_t* bonus, void* workspace, size_t workspace_bytes,
                   void* stream);
 
+/* ------------------------------------------------------------------ serving
+ * Load-aware tree shaping (§4): a deployment measures a price ladder
+ * theta*(bs, T) once (Algorithm 2) and looks up each round's price from the
+ * active batch size and the temperature.  A rung with theta < 0 is the chain
+ * sentinel: the round runs the chain (K = 1, N = the block length b). */
+typedef struct {
+  int32_t bs_max;  /* the rung covers batches of at most bs_max requests */
+  float T;         /* sampling temperature of the rung */
+  float theta;     /* price; < 0 selects the chain */
+} ts_ladder_rung;
+
+typedef struct {
+  float theta;    /* price for ts_build_tree (0 for the chain: no stop) */
+  int32_t K;      /* sibling cap */
+  int32_t N;      /* node cap */
+  int32_t chain;  /* 1 if the chain sentinel was selected */
+} ts_round_policy;
+
+/*
+ * ts_ladder_lookup: the policy of one round.  Among the rungs, take the
+ * tabulated temperature nearest to T (ties: the lower one); among its rungs,
+ * the one with the smallest bs_max >= bs (if bs exceeds them all, the one
+ * with the largest bs_max).  A price >= 0 gives {theta, K, N, 0}; the chain
+ * sentinel gives {0, 1, block_len, 1}.  rungs is a HOST array of n rungs.
+ * Errors: NULL pointers, n < 1, bs < 1, T < 0 or not finite, K outside
+ * [1, TS_MAX_K], N < 0, block_len outside [1, TS_MAX_D].
+ */
+int32_t ts_ladder_lookup(const ts_ladder_rung* rungs, int32_t n, int32_t bs, float T, int32_t K,
+                         int32_t N, int32_t block_len, ts_round_policy* out);
+
+/*
+ * ts_ladder_default: the paper's measured A100 ladder with the interpolation
+ * it states (Table 2; §4 scheduler simulation): at T = 0, theta = 0.02 for
+ * bs <= 4, 0.05 for bs <= 8 and 0.15 above; at T = 0.5 and T = 1, theta = 0.05
+ * for bs <= 8 and the chain above.  It is specific to that deployment: a new
+ * one measures its own ladder.  Writes at most cap rungs to the HOST array
+ * rungs and returns the number of rungs of the ladder (7).
+ */
+int32_t ts_ladder_default(ts_ladder_rung* rungs, int32_t cap);
+
 /* Largest tree (rows per request) the mask builder accepts. */
 #define TS_MAX_CAP 4096
 

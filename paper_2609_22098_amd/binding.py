@@ -21,7 +21,7 @@ TS_MAX_K, TS_MAX_D = 16, 16
 
 # Every symbol include/treespark.h declares.
 SAMPLERS = {"gumbel": 0, "sequential": 1}  # ts_sampler
-EXPORTED = ("ts_tree_mask_words", "ts_tree_mask",
+EXPORTED = ("ts_ladder_lookup", "ts_ladder_default", "ts_tree_mask_words", "ts_tree_mask",
             "ts_expand_workspace_size", "ts_expand", "ts_build_tree_workspace_size", "ts_build_tree",
             "ts_verify_workspace_size", "ts_verify", "ts_last_error", "ts_version")
 
@@ -88,6 +88,10 @@ def lib():
         L.ts_verify_workspace_size.restype = SZ
         L.ts_verify.argtypes = [P, P, P, I32, F, U64, P, P, P, P, SZ, P]
         L.ts_verify.restype = I32
+        L.ts_ladder_lookup.argtypes = [P, I32, I32, F, I32, I32, I32, P]
+        L.ts_ladder_lookup.restype = I32
+        L.ts_ladder_default.argtypes = [P, I32]
+        L.ts_ladder_default.restype = I32
         L.ts_tree_mask_words.argtypes = [I32]
         L.ts_tree_mask_words.restype = I32
         L.ts_tree_mask.argtypes = [P, P, I32, I32, P, P, P, P]
@@ -325,3 +329,29 @@ def tree_mask_from_host(tree: HostTree, pos_offset=None, device="cuda", stream=N
     n = torch.from_numpy(np.ascontiguousarray(tree.n, dtype=np.int32)).to(device)
     off = None if pos_offset is None else torch.from_numpy(np.ascontiguousarray(pos_offset, np.int32)).to(device)
     return tree_mask(parent, n, tree.cap, off, stream)
+
+
+class LadderRung(ctypes.Structure):
+    _fields_ = [("bs_max", ctypes.c_int32), ("T", ctypes.c_float), ("theta", ctypes.c_float)]
+
+
+class RoundPolicy(ctypes.Structure):
+    _fields_ = [("theta", ctypes.c_float), ("K", ctypes.c_int32), ("N", ctypes.c_int32),
+                ("chain", ctypes.c_int32)]
+
+
+def ladder_default():
+    """The paper's measured A100 ladder: a list of (bs_max, T, theta) with theta < 0 = chain."""
+    n = lib().ts_ladder_default(None, 0)
+    arr = (LadderRung * n)()
+    lib().ts_ladder_default(arr, n)
+    return [(r.bs_max, r.T, r.theta) for r in arr]
+
+
+def ladder_lookup(rungs, bs, T, K, N, block_len):
+    """ts_ladder_lookup over a list of (bs_max, T, theta); returns (theta, K, N, chain)."""
+    arr = (LadderRung * len(rungs))(*[LadderRung(int(b), float(t), float(th)) for b, t, th in rungs])
+    out = RoundPolicy()
+    _check(lib().ts_ladder_lookup(arr, len(rungs), int(bs), float(T), int(K), int(N), int(block_len),
+                                  ctypes.byref(out)))
+    return out.theta, out.K, out.N, bool(out.chain)

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -772,6 +773,47 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     active.swap(next);
   }
   return TS_OK;
+}
+
+int32_t ts_ladder_lookup(const ts_ladder_rung* rungs, int32_t n, int32_t bs, float T, int32_t K,
+                         int32_t N, int32_t block_len, ts_round_policy* out) {
+  g_last_error.clear();
+  if (!rungs || !out) return fail(TS_EINVAL, "rungs or out is NULL");
+  if (n < 1) return fail(TS_EINVAL, "the ladder has no rungs");
+  if (bs < 1) return fail(TS_EINVAL, "batch size %d < 1", bs);
+  if (!(T >= 0.0f) || !std::isfinite(T)) return fail(TS_EINVAL, "T must be finite and >= 0");
+  if (K < 1 || K > TS_MAX_K) return fail(TS_EINVAL, "K=%d outside [1, %d]", K, TS_MAX_K);
+  if (N < 0) return fail(TS_EINVAL, "N=%d is negative", N);
+  if (block_len < 1 || block_len > TS_MAX_D) return fail(TS_EINVAL, "block length %d outside [1, %d]", block_len, TS_MAX_D);
+  // nearest tabulated temperature, ties to the lower one
+  float best_T = rungs[0].T;
+  for (int i = 1; i < n; ++i) {
+    const float d = std::fabs(rungs[i].T - T), db = std::fabs(best_T - T);
+    if (d < db || (d == db && rungs[i].T < best_T)) best_T = rungs[i].T;
+  }
+  int pick = -1, widest = -1;
+  for (int i = 0; i < n; ++i) {
+    if (rungs[i].T != best_T) continue;
+    if (widest < 0 || rungs[i].bs_max > rungs[widest].bs_max) widest = i;
+    if (rungs[i].bs_max >= bs && (pick < 0 || rungs[i].bs_max < rungs[pick].bs_max)) pick = i;
+  }
+  if (pick < 0) pick = widest;
+  if (rungs[pick].theta < 0.0f) {
+    *out = ts_round_policy{0.0f, 1, block_len, 1};
+  } else {
+    *out = ts_round_policy{rungs[pick].theta, K, N, 0};
+  }
+  return TS_OK;
+}
+
+int32_t ts_ladder_default(ts_ladder_rung* rungs, int32_t cap) {
+  static const ts_ladder_rung kLadder[] = {
+      {4, 0.0f, 0.02f}, {8, 0.0f, 0.05f}, {INT32_MAX, 0.0f, 0.15f},
+      {8, 0.5f, 0.05f}, {INT32_MAX, 0.5f, -1.0f},
+      {8, 1.0f, 0.05f}, {INT32_MAX, 1.0f, -1.0f}};
+  const int32_t count = (int32_t)(sizeof(kLadder) / sizeof(kLadder[0]));
+  for (int32_t i = 0; rungs && i < cap && i < count; ++i) rungs[i] = kLadder[i];
+  return count;
 }
 
 int32_t ts_tree_mask_words(int32_t cap) { return cap < 1 ? 0 : (cap + 31) / 32; }

@@ -20,7 +20,7 @@ def _declared():
 
 def test_library_exports_every_declared_symbol():
     declared = _declared()
-    assert len(declared) == 10
+    assert len(declared) == 12
     assert sorted(b.EXPORTED) == declared
     L = b.lib()
     for name in declared:
@@ -137,3 +137,44 @@ def test_tree_mask_rejects_bad_arguments():
     assert L.ts_tree_mask(None, FAKE, 2, 8, None, FAKE, FAKE, None) == b.TS_EINVAL
     assert L.ts_tree_mask(FAKE, FAKE, 2, 8, None, None, FAKE, None) == b.TS_EINVAL
     assert L.ts_tree_mask(FAKE, FAKE, 0, 8, None, None, None, None) == b.TS_OK  # nothing to do
+
+
+def _golden_ladder():
+    rows = []
+    with open(os.path.join(ROOT, "tests", "golden", "ladder.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                bs, T, want = line.split()
+                rows.append((int(bs), float(T), want))
+    return rows
+
+
+def test_default_ladder_matches_the_paper():
+    """The shipped ladder reproduces the paper's measured cells and its stated T=0 interpolation
+    (tests/golden/ladder.txt); the chain sentinel gives K=1, N=block length, theta=0."""
+    rungs = b.ladder_default()
+    assert len(rungs) == 7
+    for bs, T, want in _golden_ladder():
+        theta, K, N, chain = b.ladder_lookup(rungs, bs, T, K=8, N=64, block_len=16)
+        if want == "chain":
+            assert chain and (theta, K, N) == (0.0, 1, 16), (bs, T)
+        else:
+            assert not chain and K == 8 and N == 64 and abs(theta - float(want)) < 1e-7, (bs, T, theta)
+
+
+def test_ladder_lookup_rule_and_errors():
+    """Nearest tabulated temperature (ties to the lower one), smallest covering bs_max, the widest
+    rung above the table; bad arguments are rejected."""
+    rungs = [(2, 0.0, 0.1), (10, 0.0, 0.2), (4, 1.0, 0.3), (8, 1.0, -1.0)]
+    assert b.ladder_lookup(rungs, 1, 0.2, 4, 9, 5)[0] == pytest.approx(0.1)
+    assert b.ladder_lookup(rungs, 3, 0.2, 4, 9, 5)[0] == pytest.approx(0.2)
+    assert b.ladder_lookup(rungs, 50, 0.0, 4, 9, 5)[0] == pytest.approx(0.2)   # above the table
+    assert b.ladder_lookup(rungs, 3, 0.5, 4, 9, 5)[0] == pytest.approx(0.2)    # tie -> T = 0 rungs
+    assert b.ladder_lookup(rungs, 3, 0.8, 4, 9, 5)[0] == pytest.approx(0.3)
+    assert b.ladder_lookup(rungs, 6, 2.0, 4, 9, 5) == (0.0, 1, 5, True)
+    for args in [(0, 0.0, 4, 9, 5), (1, -1.0, 4, 9, 5), (1, 0.0, 0, 9, 5), (1, 0.0, 4, -1, 5),
+                 (1, 0.0, 4, 9, 17), (1, float("nan"), 4, 9, 5)]:
+        with pytest.raises(RuntimeError):
+            b.ladder_lookup(rungs, *args)
+    with pytest.raises(RuntimeError):
+        b.ladder_lookup([], 1, 0.0, 4, 9, 5)
