@@ -76,6 +76,8 @@ def _declare(L):
                                   _I, ctypes.POINTER(_Tree)]
     L.tso_draw_sequential.argtypes = [_P, _I, _D, _U64, _I, _I, _U64, _I, _P, _P]
     L.tso_draw_sequential.restype = None
+    L.tso_expand_forest.argtypes = [ctypes.POINTER(_Model), _I, _P, _P, _I, _I, _I, _D, _D, _D, _U64, _I, _P]
+    L.tso_expand_forest.restype = _I
     L.tso_tree_mask.argtypes = [_P, _I, _I, _I, _P, _P]
     L.tso_tree_mask.restype = _I
     L.tso_expand_tree.restype = _I
@@ -268,3 +270,31 @@ def tree_mask(parent, n, cap, offset=0):
     if rc != 0:
         raise ValueError("tso_tree_mask: malformed tree")
     return mask, pos
+
+
+def expand_forest(model: Model, anchors, thetas, N, budget, K, T, seed, a=0.67, b=-0.46, sampler="gumbel"):
+    """Trees of requests 0..R-1 (R = len(anchors)) under one global node budget (budget <= 0: none)."""
+    R = len(anchors)
+    cap = N + 1
+    trees = []
+    for _ in range(R):
+        arr = dict(token=np.zeros(cap, np.int32), parent=np.zeros(cap, np.int32),
+                   depth=np.zeros(cap, np.int32), rank=np.zeros(cap, np.int32),
+                   path=np.zeros(cap, np.uint64), log_surv=np.zeros(cap), log_q0=np.zeros(cap),
+                   log_qT=np.zeros(cap), key=np.zeros(cap), margin=np.zeros(cap),
+                   eval_gap=np.zeros(cap))
+        trees.append(Tree(0, 0, stop_key=float("nan"), **arr))
+    structs = (_Tree * R)(*[t.struct() for t in trees])
+    anc = np.ascontiguousarray(anchors, np.int32)
+    th = np.ascontiguousarray(thetas, np.float64)
+    rc = lib().tso_expand_forest(model.struct, R, _ptr(anc), _ptr(th), N, int(budget), K, float(a), float(b),
+                                 float(T), seed, SAMPLERS[sampler], structs)
+    if rc != 0:
+        raise ValueError("tso_expand_forest: invalid arguments")
+    for t, s in zip(trees, structs):
+        t.n, t.evals, t.stop_key = s.n, s.evals, s.stop_key
+        n1 = t.n + 1
+        for name in ("token", "parent", "depth", "rank", "path", "log_surv", "log_q0", "log_qT", "key",
+                     "margin", "eval_gap"):
+            setattr(t, name, getattr(t, name)[:n1].copy())
+    return trees

@@ -6,6 +6,7 @@
  *   - parent-conditioned drafter conditional      (§1 Eq. 1; §3.2 item 1)
  *   - calibrated edge acceptance p-hat            (§3.4 Eq. 3)
  *   - best-first expansion with slots, caps, theta (§3.2 Algorithm 1; §3.5)
+ *   - trees of many requests under one node budget (§4 per-request budgets)
  *   - without-replacement sibling draws at T>0    (§3.3 residual-proposal equation)
  *   - greedy verification by exact match          (§3.2 item 3; §3.3 first paragraph)
  *   - recursive rejection verification at T>0     (§3.3, Proposition 1)
@@ -713,5 +714,140 @@ int tso_tree_mask(const int32_t* parent, int n, int cap, int offset, uint32_t* m
     }
     pos[i] = offset + depth;
   }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Trees of R requests under one global node budget B (§4, per-request       */
+/* budget allocation): one heap over every request's slots, popped by        */
+/* (key desc, request asc, child depth asc, child path asc).  A popped slot  */
+/* of request q is dropped if q already has N nodes or stopped; a key below  */
+/* log(theta_q) stops q; otherwise the child is materialised in q's tree as  */
+/* in Algorithm 1.  Expansion ends when B nodes exist in all (B <= 0: no     */
+/* global budget) or the heap is empty.  trees[q] must hold N + 1 nodes.     */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+  int q, v, j;
+  double key;
+  int child_depth;
+  uint64_t child_path;
+} forest_slot;
+
+static int forest_before(const forest_slot* x, const forest_slot* y) {
+  if (x->key != y->key) return x->key > y->key;
+  if (x->q != y->q) return x->q < y->q;
+  if (x->child_depth != y->child_depth) return x->child_depth < y->child_depth;
+  return x->child_path < y->child_path;
+}
+
+int tso_expand_forest(const tso_model* m, int R, const int32_t* anchor, const double* theta, int N,
+                      int budget, int K, double a, double b, double T, uint64_t seed, int sampler,
+                      tso_tree* trees) {
+  if (!m || !anchor || !theta || !trees || R < 1 || R > m->R || N < 0 || K < 1 || K > 16 ||
+      K > m->V || m->D > 16 || T < 0.0)
+    return -1;
+  node_eval** ev = (node_eval**)calloc((size_t)R, sizeof(node_eval*));
+  forest_slot* heap = (forest_slot*)malloc(sizeof(forest_slot) * ((size_t)R * (2 * (size_t)N + 2)));
+  int* done = (int*)calloc((size_t)R, sizeof(int));
+  int nheap = 0, total = 0;
+  for (int q = 0; q < R; ++q) {
+    tso_tree* out = &trees[q];
+    if (anchor[q] < 0 || anchor[q] >= m->V || theta[q] < 0.0) { free(ev); free(heap); free(done); return -1; }
+    ev[q] = (node_eval*)calloc((size_t)N + 1, sizeof(node_eval));
+    out->token[0] = anchor[q]; out->parent[0] = -1; out->depth[0] = 0; out->rank[0] = 0;
+    out->path[0] = 0; out->log_surv[0] = 0.0; out->log_q0[0] = 0.0; out->log_qT[0] = NAN;
+    out->key[0] = 0.0; out->margin[0] = INFINITY;
+    for (int i = 0; i <= N; ++i) out->eval_gap[i] = NAN;
+    out->stop_key = NAN;
+    out->evals = 0;
+    out->n = 0;
+  }
+
+#define FOREST_EVAL(q, node)                                                                  \
+  do {                                                                                       \
+    node_eval* e_ = &ev[q][node];                                                            \
+    tso_tree* t_ = &trees[q];                                                                \
+    e_->K = K;                                                                               \
+    e_->pi = (int*)malloc(sizeof(int) * (size_t)K);                                          \
+    e_->pi_z = (double*)malloc(sizeof(double) * (size_t)(K + 1));                            \
+    e_->sigma = (int*)malloc(sizeof(int) * (size_t)K);                                       \
+    e_->sigma_g = (double*)malloc(sizeof(double) * (size_t)(K + 1));                         \
+    e_->sigma_z = (double*)malloc(sizeof(double) * (size_t)K);                               \
+    tso_eval(m, q, t_->token[node], t_->depth[node], t_->path[node], T, seed, sampler, K,     \
+             NULL, &e_->lse0, &e_->lseT, e_->pi, e_->pi_z, e_->sigma, e_->sigma_g,           \
+             e_->sigma_z);                                                                   \
+    double g_ = min_rel_gap(e_->pi_z, K + 1);                                                \
+    if (T > 0.0)                                                                             \
+      g_ = fmin(g_, sampler == 1 ? min_of(e_->sigma_g, K) : min_rel_gap(e_->sigma_g, K + 1)); \
+    t_->eval_gap[node] = g_;                                                                 \
+    t_->evals++;                                                                             \
+  } while (0)
+
+  if (N > 0 && m->D > 0) {
+    for (int q = 0; q < R; ++q) {
+      FOREST_EVAL(q, 0);
+      forest_slot s0;
+      int tok; double zc;
+      slot_values(&ev[q][0], 0.0, 1, T, 0, a, b, &tok, &zc, &s0.key);
+      s0.q = q; s0.v = 0; s0.j = 1; s0.child_depth = 1; s0.child_path = 0;
+      heap[nheap++] = s0;
+    }
+  }
+  while (nheap > 0 && (budget <= 0 || total < budget)) {
+    int best = 0;
+    for (int i = 1; i < nheap; ++i)
+      if (forest_before(&heap[i], &heap[best])) best = i;
+    forest_slot s = heap[best];
+    heap[best] = heap[--nheap];
+    const int q = s.q;
+    tso_tree* out = &trees[q];
+    if (done[q]) continue;
+    const double log_theta = theta[q] > 0.0 ? log(theta[q]) : -INFINITY;
+    if (s.key < log_theta) { done[q] = 1; out->stop_key = s.key; continue; }
+    double next_best = -INFINITY;
+    for (int i = 0; i < nheap; ++i)
+      if (heap[i].q == q && heap[i].key > next_best) next_best = heap[i].key;
+    const int v = s.v, j = s.j;
+    int tok; double zc, key;
+    slot_values(&ev[q][v], out->log_surv[v], j, T, 0, a, b, &tok, &zc, &key);
+    const int c = ++out->n;
+    ++total;
+    out->token[c] = tok;
+    out->parent[c] = v;
+    out->depth[c] = out->depth[v] + 1;
+    out->rank[c] = j;
+    out->path[c] = out->path[v] | ((uint64_t)(j - 1) << (4 * out->depth[v]));
+    out->log_q0[c] = zc - ev[q][v].lse0;
+    out->log_qT[c] = (T > 0.0) ? zc / T - ev[q][v].lseT : NAN;
+    out->log_surv[c] = out->log_surv[v] + tso_log_phat(out->log_q0[c], a, b);
+    out->key[c] = s.key;
+    out->margin[c] = s.key - next_best;
+    if (out->n == N) { done[q] = 1; continue; }
+    if (out->depth[c] < m->D) {
+      FOREST_EVAL(q, c);
+      forest_slot sc;
+      slot_values(&ev[q][c], out->log_surv[c], 1, T, 0, a, b, &tok, &zc, &sc.key);
+      sc.q = q; sc.v = c; sc.j = 1; sc.child_depth = out->depth[c] + 1; sc.child_path = out->path[c];
+      heap[nheap++] = sc;
+    }
+    if (j < K) {
+      forest_slot sv;
+      slot_values(&ev[q][v], out->log_surv[v], j + 1, T, 0, a, b, &tok, &zc, &sv.key);
+      sv.q = q; sv.v = v; sv.j = j + 1; sv.child_depth = out->depth[v] + 1;
+      sv.child_path = out->path[v] | ((uint64_t)j << (4 * out->depth[v]));
+      heap[nheap++] = sv;
+    }
+  }
+#undef FOREST_EVAL
+  for (int q = 0; q < R; ++q) {
+    for (int i = 0; i <= N; ++i) {
+      free(ev[q][i].pi); free(ev[q][i].pi_z); free(ev[q][i].sigma); free(ev[q][i].sigma_g);
+      free(ev[q][i].sigma_z);
+    }
+    free(ev[q]);
+  }
+  free(ev);
+  free(heap);
+  free(done);
   return 0;
 }

@@ -281,13 +281,14 @@ def _inverse_cdf_draws(q, K, seed, request, depth, path):
 
 
 def _universe_brute_force(model_arrays, V, D, r, anchor, theta, N, K, T, seed, a=A, b=B,
-                          sampler="gumbel"):
-    """Enumerate the full K-ary universe of slots with numpy and return the top-N keys >= log theta."""
+                          sampler="gumbel", request=0):
+    """Enumerate the full K-ary universe of slots with numpy and return the top-N keys >= log theta.
+    model_arrays holds this request's U rows as U[0]; request keys the random words."""
     U, E, W2 = model_arrays
     slots = []
 
     def philox_u(depth, path, tag, y):
-        ctr = [y >> 2, path & 0xFFFFFFFF, path >> 32, (0 << 12) | (depth << 4) | tag]
+        ctr = [y >> 2, path & 0xFFFFFFFF, path >> 32, (request << 12) | (depth << 4) | tag]
         w = o.philox4x32_10(ctr, [seed & 0xFFFFFFFF, seed >> 32])[y & 3]
         return ((int(w) >> 9) + 0.5) / 2**23
 
@@ -303,7 +304,7 @@ def _universe_brute_force(model_arrays, V, D, r, anchor, theta, N, K, T, seed, a
         lse0 = special.logsumexp(z)
         pi = list(np.lexsort((np.arange(V), -z))[:K])
         if T > 0 and sampler == "sequential":
-            sigma = _inverse_cdf_draws(special.softmax(z / T), K, seed, 0, depth, path)
+            sigma = _inverse_cdf_draws(special.softmax(z / T), K, seed, request, depth, path)
         elif T > 0:
             g = z / T - np.log(-np.log([philox_u(depth, path, 1, y) for y in range(V)]))
             sigma = list(np.lexsort((np.arange(V), -g))[:K])
@@ -641,3 +642,63 @@ def test_tree_mask_chain_and_star():
 def test_tree_mask_rejects_a_parent_after_its_child():
     with pytest.raises(ValueError):
         o.tree_mask(np.array([-1, 0, 3, 1], np.int32), 3, 4)
+
+
+# ---------------------------------------------------------------- global node budget
+
+def _forest_model(R=3, V=7, D=4, r=3, seed=17):
+    dr = synth.make_drafter(V, D, r, R=R, dtype="f32", u_sigma=2.0, planted=None, zipf=None,
+                            ew_sigma=0.8, seed=seed)
+    return dr, o.Model(dr.U32, dr.E32, dr.W2_32)
+
+
+@pytest.mark.parametrize("T,sampler", [(0.0, "gumbel"), (0.8, "gumbel"), (0.8, "sequential")])
+def test_forest_without_budget_equals_independent_trees(T, sampler):
+    """With no binding global budget every request's tree is its own Algorithm 1 tree."""
+    dr, m = _forest_model()
+    anchors, thetas = [1, 4, 6], [0.0, 0.03, 0.1]
+    trees = o.expand_forest(m, anchors, thetas, 12, 0, 3, T, 5, sampler=sampler)
+    for q in range(3):
+        ref = o.expand_tree(m, q, anchors[q], thetas[q], 12, 3, T, 5, sampler=sampler)
+        assert trees[q].n == ref.n
+        for name in ("token", "parent", "depth", "rank", "path"):
+            assert list(getattr(trees[q], name)) == list(getattr(ref, name)), (q, name)
+        assert np.allclose(trees[q].log_surv, ref.log_surv, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("budget,T", [(5, 0.0), (9, 0.0), (14, 0.7), (30, 1.0)])
+def test_forest_equals_global_top_b_of_the_universes(budget, T):
+    """Brute force: the budgeted trees are the global top-B slots of the requests' K-ary
+    universes, each request limited to its own top-N slots above its theta."""
+    R, V, D, r, K, N = 3, 7, 4, 3, 2, 8
+    dr, m = _forest_model(R, V, D, r)
+    anchors, thetas = [2, 5, 3], [0.0, 0.02, 0.0]
+    trees = o.expand_forest(m, anchors, thetas, N, budget, K, T, 11)
+    pool = []
+    for q in range(R):
+        U = dr.U32[q:q + 1]
+        slots = _universe_brute_force((U, dr.E32, dr.W2_32), V, D, r, anchors[q], thetas[q], N, K, T, 11,
+                                      request=q)
+        pool += [(s[0], q, s[1], s[2], s[3]) for s in slots]
+    pool.sort(key=lambda s: (-s[0], s[1], s[2], s[3]))
+    chosen = pool[:budget]
+    for q in range(R):
+        mine = [s for s in chosen if s[1] == q]
+        assert trees[q].n == len(mine), q
+        for i, s in enumerate(mine, start=1):
+            assert trees[q].key[i] == pytest.approx(s[0], rel=1e-12, abs=1e-12)
+            assert int(trees[q].path[i]) == s[3] and trees[q].token[i] == s[4]
+
+
+def test_forest_is_a_uniform_price():
+    """Section 4: under one marginal price the budget allocation is the theta rule: each budgeted
+    tree equals the request's own tree with theta' = max(theta, exp(key of the last node))."""
+    dr, m = _forest_model(R=4, V=9, D=5, r=3, seed=23)
+    anchors, thetas = [1, 2, 3, 4], [0.0, 0.01, 0.0, 0.05]
+    trees = o.expand_forest(m, anchors, thetas, 30, 17, 3, 0.0, 2)
+    last = min(t.key[1:t.n + 1].min() for t in trees if t.n > 0)
+    assert sum(t.n for t in trees) == 17
+    for q in range(4):
+        th = max(thetas[q], math.exp(last))
+        ref = o.expand_tree(m, q, anchors[q], th, 30, 3, 0.0, 2)
+        assert trees[q].n == ref.n and list(trees[q].token) == list(ref.token), q
