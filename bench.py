@@ -223,6 +223,7 @@ def main():
     log(f"frontier P={P}; natural trees: sizes {int(tree.n.min())}..{int(tree.n.max())}, "
         f"{tree_evals} evaluations")
 
+    mask_bufs = binding.TreeMaskBuffers(dr.R, N + 1)
     nsteps = args.steps + args.warmup
     ev = HipEvents(3 * nsteps)
 
@@ -233,7 +234,7 @@ def main():
         if args.expand_only:
             return
         binding.build_tree(d, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler)
-        binding.tree_mask_from_host(tree)
+        binding.tree_mask_from_host(tree, buffers=mask_bufs)
         binding.verify(d, tree, tgt, T, seed, workspace=ws_v)
 
     for i in range(args.warmup):
@@ -258,7 +259,7 @@ def main():
             binding.expand(dd, parents, P, K, T, seed, outputs=outs, workspace=ws_e, sampler=sampler)
             torch.cuda.synchronize(); b = time.perf_counter()
             binding.build_tree(dd, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler)
-            binding.tree_mask_from_host(tree)
+            binding.tree_mask_from_host(tree, buffers=mask_bufs)
             torch.cuda.synchronize()
             c = time.perf_counter()
             binding.verify(dd, tree, tgt, T, seed, workspace=ws_v)

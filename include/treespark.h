@@ -182,13 +182,21 @@ size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, f
  * slot for its next child until it has K children.  The result equals the
  * sequential heap of Algorithm 1; it is computed in breadth waves, each one
  * ts_expand call over all requests' pending parents.
+ * budget > 0 adds one node budget shared by all requests (§4, per-request
+ * budget allocation by greedy water-filling): the trees then hold the best
+ * `budget` nodes of all requests together in the order (key desc, request
+ * asc, child depth asc, child path asc), each request still at most N nodes
+ * and stopped by its own theta.  Under one marginal price this is the theta
+ * rule with theta_q raised to the key of the last node taken.  budget <= 0:
+ * no shared budget.
  * anchor [R], theta [R] are HOST arrays.  out->cap must be >= N + 1 and
  * out->R == d->R.  sampler is a ts_sampler (used at T > 0).  Synchronises
  * `stream` once per wave.
  */
 int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* theta, int32_t N,
-                      int32_t K, ts_calib calib, float T, uint64_t seed, int32_t sampler,
-                      ts_tree* out, void* workspace, size_t workspace_bytes, void* stream);
+                      int32_t budget, int32_t K, ts_calib calib, float T, uint64_t seed,
+                      int32_t sampler, ts_tree* out, void* workspace, size_t workspace_bytes,
+                      void* stream);
 
 size_t ts_verify_workspace_size(const ts_drafter* d, int32_t cap, float T);
 

@@ -82,7 +82,7 @@ def lib():
         L.ts_expand.restype = I32
         L.ts_build_tree_workspace_size.argtypes = [P, I32, I32, F]
         L.ts_build_tree_workspace_size.restype = SZ
-        L.ts_build_tree.argtypes = [P, P, P, I32, I32, Calib, F, U64, I32, P, P, SZ, P]
+        L.ts_build_tree.argtypes = [P, P, P, I32, I32, I32, Calib, F, U64, I32, P, P, SZ, P]
         L.ts_build_tree.restype = I32
         L.ts_verify_workspace_size.argtypes = [P, I32, F]
         L.ts_verify_workspace_size.restype = SZ
@@ -262,7 +262,8 @@ def build_tree_workspace_size(d: DeviceDrafter, N, K, T):
 
 
 def build_tree(d: DeviceDrafter, anchor, theta, N, K, T, seed, calib=(0.67, -0.46), workspace=None,
-               stream=None, tree=None, sampler="gumbel") -> HostTree:
+               stream=None, tree=None, sampler="gumbel", budget=0) -> HostTree:
+    """ts_build_tree: one tree per request; budget > 0 shares one node budget across requests."""
     torch = _torch()
     anchor = np.ascontiguousarray(anchor, dtype=np.int32)
     theta = np.ascontiguousarray(theta, dtype=np.float32)
@@ -272,7 +273,7 @@ def build_tree(d: DeviceDrafter, anchor, theta, N, K, T, seed, calib=(0.67, -0.4
         n = build_tree_workspace_size(d, N, K, T)
         workspace = torch.empty((max(n, 1),), dtype=torch.uint8, device=d.U.device)
     s = tree.struct()
-    rc = lib().ts_build_tree(d.ref(), anchor.ctypes.data, theta.ctypes.data, N, K, Calib(*calib),
+    rc = lib().ts_build_tree(d.ref(), anchor.ctypes.data, theta.ctypes.data, N, int(budget), K, Calib(*calib),
                              float(T), ctypes.c_uint64(seed), SAMPLERS[sampler], ctypes.byref(s),
                              ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream(stream))
     _check(rc)
@@ -304,17 +305,22 @@ def verify(d: DeviceDrafter, tree: HostTree, target, T, seed, workspace=None, st
     return path, plen, bonus
 
 
-def tree_mask(parent, n, cap, pos_offset=None, stream=None):
+def tree_mask(parent, n, cap, pos_offset=None, stream=None, out=None):
     """ts_tree_mask.  parent [R][cap] and n [R] int32 DEVICE tensors (ts_tree layout),
     pos_offset optional [R] int32 device tensor.  Returns (mask [R][cap][W] int32 tensor holding
-    the uint32 words, pos [R][cap] int32), asynchronous on the stream."""
+    the uint32 words, pos [R][cap] int32), asynchronous on the stream; out = (mask, pos) reuses
+    given output tensors."""
     torch = _torch()
     R = parent.shape[0]
     assert tuple(parent.shape) == (R, cap) and parent.dtype == torch.int32 and parent.is_contiguous()
     assert tuple(n.shape) == (R,) and n.dtype == torch.int32
     W = lib().ts_tree_mask_words(cap)
-    mask = torch.empty((R, cap, W), dtype=torch.int32, device=parent.device)
-    pos = torch.empty((R, cap), dtype=torch.int32, device=parent.device)
+    if out is None:
+        mask = torch.empty((R, cap, W), dtype=torch.int32, device=parent.device)
+        pos = torch.empty((R, cap), dtype=torch.int32, device=parent.device)
+    else:
+        mask, pos = out
+        assert tuple(mask.shape) == (R, cap, W) and tuple(pos.shape) == (R, cap)
     off = ctypes.c_void_p(pos_offset.data_ptr()) if pos_offset is not None else None
     rc = lib().ts_tree_mask(ctypes.c_void_p(parent.data_ptr()), ctypes.c_void_p(n.data_ptr()), R, cap, off,
                             ctypes.c_void_p(mask.data_ptr()), ctypes.c_void_p(pos.data_ptr()), _stream(stream))
@@ -322,13 +328,42 @@ def tree_mask(parent, n, cap, pos_offset=None, stream=None):
     return mask, pos
 
 
-def tree_mask_from_host(tree: HostTree, pos_offset=None, device="cuda", stream=None):
-    """Upload a HostTree's parents and sizes, then ts_tree_mask."""
+class TreeMaskBuffers:
+    """Reusable page-locked staging and device buffers for masks of HostTrees of one shape."""
+
+    def __init__(self, R, cap, device="cuda"):
+        torch = _torch()
+        self.R, self.cap = R, cap
+        self.host = torch.empty((R * (cap + 1),), dtype=torch.int32, pin_memory=True)
+        self.dev = torch.empty((R * (cap + 1),), dtype=torch.int32, device=device)
+        W = (cap + 31) // 32
+        self.out = (torch.empty((R, cap, W), dtype=torch.int32, device=device),
+                    torch.empty((R, cap), dtype=torch.int32, device=device))
+        self.copied = torch.cuda.Event()  # recorded after each copy out of the staging buffer
+        self.pending = False
+
+    def upload(self, tree: HostTree, stream=None):
+        torch = _torch()
+        if self.pending:
+            self.copied.synchronize()  # the previous copy has left the staging buffer
+        h = self.host.numpy()
+        h[: self.R * self.cap] = tree.parent.reshape(-1)
+        h[self.R * self.cap:] = tree.n
+        s = torch.cuda.current_stream() if stream is None else stream
+        with torch.cuda.stream(s):
+            self.dev.copy_(self.host, non_blocking=True)
+            self.copied.record(s)
+        self.pending = True
+        return self.dev[: self.R * self.cap].view(self.R, self.cap), self.dev[self.R * self.cap:]
+
+
+def tree_mask_from_host(tree: HostTree, pos_offset=None, device="cuda", stream=None, buffers=None):
+    """Upload a HostTree's parents and sizes (through page-locked staging), then ts_tree_mask."""
     torch = _torch()
-    parent = torch.from_numpy(np.ascontiguousarray(tree.parent, dtype=np.int32)).to(device)
-    n = torch.from_numpy(np.ascontiguousarray(tree.n, dtype=np.int32)).to(device)
+    buf = buffers or TreeMaskBuffers(tree.R, tree.cap, device)
+    parent, n = buf.upload(tree, stream)
     off = None if pos_offset is None else torch.from_numpy(np.ascontiguousarray(pos_offset, np.int32)).to(device)
-    return tree_mask(parent, n, tree.cap, off, stream)
+    return tree_mask(parent, n, tree.cap, off, stream, out=buf.out)
 
 
 class LadderRung(ctypes.Structure):

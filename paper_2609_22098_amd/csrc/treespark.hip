@@ -361,6 +361,21 @@ inline bool slot_before(const Slot& a, const Slot& b) {
   return a.path < b.path;
 }
 
+// A slot in the global order of a budget shared by all requests:
+// (key desc, request asc, child depth asc, child path asc).
+struct GlobalRef {
+  float key;
+  int q;
+  int depth;
+  uint64_t path;
+};
+inline bool global_before(const GlobalRef& a, const GlobalRef& b) {
+  if (a.key != b.key) return a.key > b.key;
+  if (a.q != b.q) return a.q < b.q;
+  if (a.depth != b.depth) return a.depth < b.depth;
+  return a.path < b.path;
+}
+
 struct BuildLayout {
   size_t off_par, off_out, off_exp, bytes;
   int Pmax;
@@ -465,8 +480,9 @@ size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, f
 }
 
 int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* theta, int32_t N,
-                      int32_t K, ts_calib calib, float T, uint64_t seed, int32_t sampler,
-                      ts_tree* out, void* workspace, size_t workspace_bytes, void* stream) {
+                      int32_t budget, int32_t K, ts_calib calib, float T, uint64_t seed,
+                      int32_t sampler, ts_tree* out, void* workspace, size_t workspace_bytes,
+                      void* stream) {
   g_last_error.clear();
   int32_t rc = check_drafter(d);
   if (rc != TS_OK) return rc;
@@ -541,24 +557,45 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
         known[par.request].push_back(sl);
       }
     }
-    // Next wave: children of slots that rank strictly above the N-th known slot
-    // (or all, if fewer than N are known), with key >= log(theta) and depth < D.
-    // Any slot of the final top-N descends from such a child, because a slot's
-    // key never exceeds the key of the slot whose pop created it.
+    // Next wave: children of the slots that can still be among the tree's
+    // nodes: key >= log(theta_q), strictly above the request's N-th such slot
+    // and, under a global budget B, strictly above the B-th best of all
+    // requests' top-N slots in the global order (key desc, request asc,
+    // depth asc, path asc).  Any node of the final trees descends from such
+    // a child, because a slot's key never exceeds the key of the slot whose
+    // pop created it.
     frontier.clear();
+    std::vector<Slot> nth(R);
+    std::vector<char> have_n(R, 0);
+    std::vector<GlobalRef> pool;
     for (int q = 0; q < R; ++q) {
-      std::vector<Slot>& ks = known[q];
-      const bool have_n = (int)ks.size() >= N;
-      Slot nth{};
-      if (have_n && N > 0) {
-        std::vector<Slot> tmp(ks);
-        std::nth_element(tmp.begin(), tmp.begin() + (N - 1), tmp.end(), slot_before);
-        nth = tmp[N - 1];
+      std::vector<Slot> el;
+      for (const Slot& sl : known[q])
+        if (sl.key >= log_theta[q]) el.push_back(sl);
+      if (N > 0 && (int)el.size() >= N) {
+        std::nth_element(el.begin(), el.begin() + (N - 1), el.end(), slot_before);
+        nth[q] = el[N - 1];
+        have_n[q] = 1;
       }
+      if (budget > 0) {
+        const int take = std::min<int>(N, (int)el.size());
+        if (take < (int)el.size()) el.resize(take);  // nth_element left the top N first
+        for (const Slot& sl : el) pool.push_back(GlobalRef{sl.key, q, sl.depth, sl.path});
+      }
+    }
+    bool have_g = false;
+    GlobalRef gth{};
+    if (budget > 0 && (int)pool.size() >= budget) {
+      std::nth_element(pool.begin(), pool.begin() + (budget - 1), pool.end(), global_before);
+      gth = pool[budget - 1];
+      have_g = true;
+    }
+    for (int q = 0; q < R; ++q) {
       const size_t first = frontier.size();
-      for (Slot& sl : ks) {
+      for (Slot& sl : known[q]) {
         if (sl.evaluated || sl.depth >= d->D || sl.key < log_theta[q]) continue;
-        if (have_n && !slot_before(sl, nth)) continue;
+        if (have_n[q] && !slot_before(sl, nth[q])) continue;
+        if (have_g && !global_before(GlobalRef{sl.key, q, sl.depth, sl.path}, gth)) continue;
         sl.evaluated = true;
         frontier.push_back(ts_parent{sl.token, sl.depth, q, sl.log_surv, sl.path});
       }
@@ -566,11 +603,29 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
                 [](const ts_parent& a, const ts_parent& b) { return a.depth < b.depth; });
     }
   }
-  // The tree: the first N known slots in pop order, stopping at a key below log(theta).
+  // The trees: each request's slots in pop order, at most N, stopping below
+  // log(theta_q); under a global budget, the best B of those in the global order.
+  std::vector<int> take(R, 0);
+  {
+    std::vector<GlobalRef> pool;
+    for (int q = 0; q < R; ++q) {
+      std::vector<Slot>& ks = known[q];
+      std::sort(ks.begin(), ks.end(), slot_before);
+      int t = 0;
+      while (t < (int)ks.size() && t < N && ks[t].key >= log_theta[q]) ++t;
+      take[q] = t;
+      if (budget > 0)
+        for (int i = 0; i < t; ++i) pool.push_back(GlobalRef{ks[i].key, q, ks[i].depth, ks[i].path});
+    }
+    if (budget > 0 && (int)pool.size() > budget) {
+      std::nth_element(pool.begin(), pool.begin() + budget, pool.end(), global_before);
+      std::fill(take.begin(), take.end(), 0);
+      for (int i = 0; i < budget; ++i) ++take[pool[i].q];  // a prefix of each request's order
+    }
+  }
   const int cap = out->cap;
   for (int q = 0; q < R; ++q) {
     std::vector<Slot>& ks = known[q];
-    std::sort(ks.begin(), ks.end(), slot_before);
     const size_t b = (size_t)q * cap;
     out->token[b] = anchor[q];
     out->parent[b] = -1;
@@ -585,7 +640,7 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
     node_of[0][0] = 0;
     int n = 0;
     for (const Slot& sl : ks) {
-      if (n >= N || sl.key < log_theta[q]) break;
+      if (n >= take[q]) break;
       const int pd = sl.depth - 1;
       const uint64_t ppath = sl.path & ((pd == 0) ? 0ull : ((1ull << (4 * pd)) - 1ull));
       const auto it = node_of[pd].find(ppath);

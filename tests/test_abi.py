@@ -84,7 +84,7 @@ def test_build_tree_rejects_bad_arguments():
     theta = np.array([0.0, 0.1], np.float32)
 
     def call(anchor=anchor, theta=theta, N=8, K=2, T=0.0, ws=1 << 30, st=s, sampler=1):
-        return L.ts_build_tree(ctypes.byref(d), anchor.ctypes.data, theta.ctypes.data, N, K,
+        return L.ts_build_tree(ctypes.byref(d), anchor.ctypes.data, theta.ctypes.data, N, 0, K,
                                b.Calib(0.67, -0.46), T, 0, sampler, ctypes.byref(st), FAKE, ws, None)
 
     assert call(anchor=np.array([1, 5000], np.int32)) == b.TS_EINVAL

@@ -223,3 +223,55 @@ def test_verify_losslessness_chi_square(torch, sampler):
     p2 = stats.chisquare(cnt, special.softmax(rows[(x1,)].astype(np.float64) / T) * cnt.sum()).pvalue
     print(f"chi-square p-values: first token {p1:.3g}, after x1={x1} ({int(cnt.sum())} samples) {p2:.3g}")
     assert p1 > 1e-3 and p2 > 1e-3
+
+
+# ---------------------------------------------------------------- shared node budget
+
+def _forest_compare(dr, tree, anchors, thetas, N, budget, K, T, seed, sampler, tag):
+    """GPU trees under a shared budget against the oracle's global heap.  A near-tie at the
+    budget's cut (the B-th and (B+1)-th keys within TIE) limits the check to tree prefixes."""
+    om = o.Model(dr.U32, dr.E32, dr.W2_32)
+    refs = o.expand_forest(om, anchors, thetas, N, budget, K, T, seed, sampler=sampler)
+    more = o.expand_forest(om, anchors, thetas, N, budget + 1, K, T, seed, sampler=sampler)
+    keys_b = sorted((k for r in refs for k in r.key[1:r.n + 1]), reverse=True)
+    keys_b1 = sorted((k for r in more for k in r.key[1:r.n + 1]), reverse=True)
+    cut_tie = (len(keys_b1) > len(keys_b) and len(keys_b) > 0
+               and keys_b[-1] - keys_b1[-1] <= TIE * max(1.0, abs(keys_b[-1])))
+    tally = Tally()
+    for q in range(dr.R):
+        if cut_tie:
+            ref = refs[q]
+            n = min(int(tree.n[q]), ref.n)
+            assert list(tree.token[q, :n + 1]) == list(ref.token[:n + 1]), (tag, q)
+        else:
+            compare_tree(tree, q, refs[q], float(thetas[q]), dr.dtype, tally, tag=f"{tag} request {q}", T=T)
+    total = int(tree.n.sum())
+    print(f"{tag}: {total} nodes (budget {budget}), cut near-tie {cut_tie}, near-ties {tally.near_ties}")
+    assert not tally.failures, tally.failures[:5]
+    if not cut_tie and budget > 0:
+        assert total == sum(r.n for r in refs)
+
+
+@pytest.mark.parametrize("budget,T,sampler", [(10, 0.0, "gumbel"), (40, 0.0, "gumbel"), (25, 1.0, "gumbel"),
+                                               (25, 0.5, "sequential"), (1000, 0.0, "gumbel")])
+def test_shared_budget_sharp_trees(torch, budget, T, sampler):
+    """6 requests with per-request theta share one node budget (or not, at 1000)."""
+    dr = synth.make_drafter(3000, 8, 32, R=6, dtype="bf16", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
+                            ew_sigma=0.3, seed=3, u_scale=3.0)
+    anchors, _, _ = synth.make_controls(6, dr.V, 0.0, seed=3)
+    thetas = np.array([0.0, 0.01, 0.0, 0.005, 0.0, 0.02], np.float32)
+    from paper_2609_22098_amd import binding
+    dd = binding.drafter_from_host(dr)
+    tree = binding.build_tree(dd, anchors, thetas, 24, 3, T, 9, sampler=sampler, budget=budget)
+    _forest_compare(dr, tree, anchors, thetas, 24, budget, 3, T, 9, sampler, f"budget {budget} T={T}")
+
+
+def test_shared_budget_serving(torch):
+    """The benchmark's 64 requests at theta = 0 (fixed budgets) sharing 300 nodes, T = 0.7."""
+    from paper_2609_22098_amd import binding
+    dr = synth.make_workload_drafter(3, seed=0)
+    anchors, _, _ = synth.make_controls(dr.R, dr.V, 0.0, seed=0)
+    thetas = np.zeros(dr.R, np.float32)
+    dd = binding.drafter_from_host(dr)
+    tree = binding.build_tree(dd, anchors, thetas, 16, 8, 0.7, 0, sampler="sequential", budget=300)
+    _forest_compare(dr, tree, anchors, thetas, 16, 300, 8, 0.7, 0, "sequential", "serving budget 300")
