@@ -64,8 +64,10 @@ struct ExpandParams {
   float* part_sT;  // [P][S] sum exp((z - m) / T)
   RunSummaryPtr zs;  // per (parent, chunk): the two best runs of z and the rest
   RunSummaryPtr gs;  // the same for the Gumbel keys (Gumbel draws)
-  float* blk;      // [P][nblk]: base-2 log of the q_T mass of each 64-token block (sequential draws)
+  float* blk;      // [P][blk_ld]: base-2 log of the q_T mass of each 64-token block (sequential
+                   // draws); rows padded to whole 64-byte lines
   int nblk;        // ceil(V / 64)
+  int blk_ld;      // row stride of blk: nblk rounded up to a multiple of 16
   float* z_out;    // optional [P][V]: the logits themselves (verification recompute)
 };
 
@@ -92,8 +94,8 @@ struct MergeParams {
   const float* part_sT;
   RunSummaryPtr zs;
   RunSummaryPtr gs;
-  float* blk;  // per-parent block table; the draws update their own parent's rows
-  int nblk;
+  float* blk;  // per-parent block table [P][blk_ld]; the draws update their own parent's rows
+  int nblk, blk_ld;
   ts_expand_out out;
 };
 
@@ -298,6 +300,35 @@ __device__ __forceinline__ float block_log_mass(float a, float ml) {
   return m == kNegInf ? kNegInf : m + __builtin_amdgcn_logf(s);
 }
 
+// Block-table stores of the streaming pass.  Blocks are grouped in windows of
+// 16 (one 64-byte line of a parent's row); lane group g keeps blocks 4g..4g+3
+// of the current window in registers, and at the window's end (or the chunk's)
+// the four lane groups of a parent store the line as four 16-byte pieces.  A
+// window cut by a chunk boundary stores only its own blocks, one by one.
+struct BlkWindow {
+  float h[4];
+  __device__ __forceinline__ void put(int bi, int g, float lb) {
+    const bool mine = g == ((bi >> 2) & 3);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) h[q] = (mine && q == (bi & 3)) ? lb : h[q];
+  }
+  // bi: the block just put; bfirst, blast: the chunk's first and last block
+  __device__ __forceinline__ void flush(float* row, int bi, int bfirst, int blast, int g) const {
+    if ((bi & 15) != 15 && bi != blast) return;
+    const int wb = bi & ~15;
+    float* dst = row + wb + 4 * g;
+    if (wb >= bfirst && (bi & 15) == 15) {
+      *reinterpret_cast<f32x4*>(dst) = f32x4{h[0], h[1], h[2], h[3]};
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int b = wb + 4 * g + q;
+        if (b >= bfirst && b <= bi) dst[q] = h[q];
+      }
+    }
+  }
+};
+
 template <typename TE, int KS, int NB, int MODE, bool STORE_Z>
 __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) {
   typedef Frag<TE> F;
@@ -355,6 +386,9 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
 
   float m0[NB], s0[NB], sT[NB];
   RunTop zt[NB], gt[NB];
+  BlkWindow bw[NB];
+  const int bfirst = chunk * (p.Vc >> 6);
+  const int blast = (min(chunk * p.Vc + p.Vc, V) - 1) >> 6;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     m0[nb] = kNegInf; s0[nb] = 0.0f; sT[nb] = 0.0f;
@@ -432,7 +466,9 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
       top_add(zt[nb], bm, run);
       if constexpr (SEQ) {
         const float lb = p.need_T ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
-        if (g == 0 && pidx[nb] < p.P) p.blk[(size_t)pidx[nb] * p.nblk + (t0 >> 6)] = lb;
+        const int bi = t0 >> 6;
+        bw[nb].put(bi, g, lb);
+        if (pidx[nb] < p.P) bw[nb].flush(p.blk + (size_t)pidx[nb] * p.blk_ld, bi, bfirst, blast, g);
       }
       if constexpr (GUMBEL) {
         float gm = kNegInf;
@@ -590,6 +626,9 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
 
   float m0[NB], s0[NB], sT[NB];
   RunTop zt[NB], gt[NB];
+  BlkWindow bw[NB];
+  const int bfirst = chunk * (p.Vc >> 6);
+  const int blast = (min(chunk * p.Vc + p.Vc, V) - 1) >> 6;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     m0[nb] = kNegInf; s0[nb] = 0.0f; sT[nb] = 0.0f;
@@ -677,7 +716,9 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
       top_add(zt[nb], bm, run);
       if constexpr (SEQ) {
         const float lb = p.need_T ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
-        if (g == 0 && pidx[nb] < p.P) p.blk[(size_t)pidx[nb] * p.nblk + (t0 >> 6)] = lb;
+        const int bi = t0 >> 6;
+        bw[nb].put(bi, g, lb);
+        if (pidx[nb] < p.P) bw[nb].flush(p.blk + (size_t)pidx[nb] * p.blk_ld, bi, bfirst, blast, g);
       }
       if constexpr (GUMBEL) {
         float gm = kNegInf;
@@ -1077,7 +1118,7 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
   const int n = lane & 15, g = lane >> 4;
   const int V = p.V, nblk = p.nblk;
   const TE* W2 = static_cast<const TE*>(p.W2);
-  float* gblk = p.blk + (size_t)pidx * nblk;
+  float* gblk = p.blk + (size_t)pidx * p.blk_ld;
   constexpr int kBps = kSegTokens / kBlkTokens;  // blocks per segment (64)
   const int nseg = (nblk + kBps - 1) / kBps;
   const bool in_lds = nseg <= kLdsSegs;

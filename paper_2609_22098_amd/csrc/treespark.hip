@@ -114,6 +114,7 @@ struct Plan {
   bool sample;  // T > 0: the merge takes lse of z/T and draws
   bool lds;     // LDS-staged bf16 streaming kernel
   int nblk;     // 64-token blocks of the vocabulary
+  int blk_ld;   // row stride of the block table (nblk rounded up to 16)
   size_t off_m, off_s0, off_sT, off_z[3], off_g[3], off_blk;
   size_t bytes;
 };
@@ -175,6 +176,7 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
   pl.sample = T > 0.0f && !store_z;
   pl.mode = !pl.sample ? kModeGreedy : sampler == TS_SAMPLER_SEQUENTIAL ? kModeSeq : kModeGumbel;
   pl.nblk = (d->V + kBlkTokens - 1) / kBlkTokens;
+  pl.blk_ld = ((pl.nblk + 15) / 16) * 16;
   pl.ks = d->dtype == TS_BF16 ? d->r / 32 : d->r / 4;
   pl.NB = P >= 512 ? 2 : 1;
 #ifdef TS_FORCE_NB
@@ -230,7 +232,7 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
       pl.off_g[2] = o; o += a;
     }
     if (pl.mode == kModeSeq || sizing_only) {
-      pl.off_blk = o; o += align256((size_t)std::max(P, 1) * pl.nblk * 4);
+      pl.off_blk = o; o += align256((size_t)std::max(P, 1) * pl.blk_ld * 4);
     }
   }
   pl.bytes = o;
@@ -304,6 +306,7 @@ ExpandParams eval_params(const ts_drafter* d, const ts_parent* parents, int P, f
   p.zs = summary_ptr(ws, pl.off_z);
   if (pl.mode == kModeGumbel) p.gs = summary_ptr(ws, pl.off_g);
   p.nblk = pl.nblk;
+  p.blk_ld = pl.blk_ld;
   if (pl.mode == kModeSeq) p.blk = reinterpret_cast<float*>(ws + pl.off_blk);
   p.z_out = z_out;
   return p;
@@ -336,6 +339,7 @@ int32_t run_expand(const ts_drafter* d, const ts_parent* parents, int P, ts_cali
   mp.gs = ep.gs;
   mp.blk = ep.blk;
   mp.nblk = ep.nblk;
+  mp.blk_ld = ep.blk_ld;
   mp.out = *out;
   launch_merge(d, mp, pl, s);
   TS_HIP(hipGetLastError());
