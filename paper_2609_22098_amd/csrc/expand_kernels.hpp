@@ -809,7 +809,28 @@ struct MergeLds {
   int item_k[kItemCap];  // key kind: 0 = z, 1 = Gumbel
   float item_e[kItemCap];  // expected run maximum (NaN if unknown)
   uint32_t whole[kMaxChunks / 32];
-  float seg_blk[40 * 64];  // sequential draws: the parent's block table when V <= 40 * 4096
+};
+
+// Sequential draws run on a wave of their own (the parent's second wave):
+// its scratch, and the draws it hands to the scoring wave.
+constexpr int kLdsSegs = 40;  // segments whose block table is kept in LDS
+struct DrawLds {
+  float bz[4][16];               // logits of the drawn block
+  float seg_blk[kLdsSegs * 64];  // the parent's block table when V <= 40 * 4096
+  int id[TS_MAX_K];              // draw j's token and logit at j - 1
+  float z[TS_MAX_K];
+};
+
+// Workgroup LDS of the merge: four parents of one wave each, or, for
+// sequential draws, one parent of two waves.
+template <bool SEQ>
+struct MergeShared {
+  MergeLds l[4];
+};
+template <>
+struct MergeShared<true> {
+  MergeLds l[1];
+  DrawLds d;
 };
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -1107,12 +1128,11 @@ __device__ __forceinline__ int wave_pick(const float (&m)[NS], float u) {
 // The parent's block table lives in LDS when it fits (V <= 40 * 4096), else
 // in its rows of the workspace; a drawn token's block is rewritten in place.
 // Draw j lands in lane j - 1 of gl (token, z).
-constexpr int kLdsSegs = 40;
 
 template <typename TE, int KS>
 __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const TE* urow,
                                           const typename Frag<TE>::type (&bcol)[KS], uint32_t pc1,
-                                          uint32_t pc2, uint32_t pc3, MergeLds& L, RegList& gl) {
+                                          uint32_t pc2, uint32_t pc3, DrawLds& L, RegList& gl) {
   typedef Frag<TE> F;
   const int lane = threadIdx.x & 63;
   const int n = lane & 15, g = lane >> 4;
@@ -1289,22 +1309,25 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   constexpr bool SAMPLE = MODE != kModeGreedy;
   constexpr bool GUMBEL = MODE == kModeGumbel;
   constexpr bool SEQ = MODE == kModeSeq;
-  __shared__ MergeLds lds[4];
+  // Sequential draws: one parent per workgroup; wave 1 draws while wave 0
+  // finds the greedy top-K, then wave 0 scores the children.
+  __shared__ MergeShared<SEQ> sh;
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   const int n = lane & 15, g = lane >> 4;
-  const int pidx = blockIdx.x * 4 + wv;
-  if (pidx >= p.P) return;
+  const int pidx = SEQ ? blockIdx.x : blockIdx.x * 4 + wv;
+  if (pidx >= p.P) return;  // uniform over the workgroup when SEQ
 #ifdef TS_DEBUG_RUNS
   const long long t_start = clock64();
 #endif
-  MergeLds& L = lds[wv];
+  MergeLds& L = sh.l[SEQ ? 0 : wv];
   const int K = p.K, V = p.V, S = p.S;
   const ts_parent par = p.parents[pidx];
   const bool ok = par.token >= 0 && par.token < V && par.depth >= 0 && par.depth < p.D &&
                   par.request >= 0 && par.request < p.R;
   const size_t ob = (size_t)pidx * K;
   if (!ok) {
+    if (SEQ && wv != 0) return;
     const float nan = __builtin_nanf("");
     if (lane < K) {
       p.out.child_token[ob + lane] = -1;
@@ -1321,6 +1344,27 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
       if (p.out.diag) p.out.diag[pidx] = 0;
     }
     return;
+  }
+  const TE* urow = static_cast<const TE*>(p.U) + ((size_t)par.request * p.D + par.depth) * (size_t)V;
+  const TE* erow = static_cast<const TE*>(p.E) + (size_t)par.token * p.r;
+  FT bcol[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) bcol[kk] = (n == 0) ? F::load(erow, kk * F::kPerStep, g) : F::zero();
+  const uint32_t pc1 = (uint32_t)par.path, pc2 = (uint32_t)(par.path >> 32);
+  const uint32_t pc3 = counter_word3(par.request, par.depth, 1u);
+
+  if constexpr (SEQ) {
+    if (wv == 1) {
+      RegList dl;
+      reglist_init(dl);
+      seq_draws<TE, KS>(p, pidx, urow, bcol, pc1, pc2, counter_word3(par.request, par.depth, 4u), sh.d, dl);
+      if (lane < K) {
+        sh.d.id[lane] = dl.id;
+        sh.d.z[lane] = dl.aux;
+      }
+      __syncthreads();
+      return;
+    }
   }
   const size_t pbase = (size_t)pidx * S;
 
@@ -1349,14 +1393,6 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   const float lse0 = M + logf(s);
   float lseT = __builtin_nanf("");
   if (SAMPLE) lseT = p.need_T ? M / p.T + logf(st) : lse0;
-
-  const TE* urow = static_cast<const TE*>(p.U) + ((size_t)par.request * p.D + par.depth) * (size_t)V;
-  const TE* erow = static_cast<const TE*>(p.E) + (size_t)par.token * p.r;
-  FT bcol[KS];
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) bcol[kk] = (n == 0) ? F::load(erow, kk * F::kPerStep, g) : F::zero();
-  const uint32_t pc1 = (uint32_t)par.path, pc2 = (uint32_t)(par.path >> 32);
-  const uint32_t pc3 = counter_word3(par.request, par.depth, 1u);
 
   int nitems = 0;
   float thr[2];
@@ -1406,8 +1442,15 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
     if (nr > 0)
       rescan_batch<TE, KS, GUMBEL>(p, urow, bcol, pc1, pc2, pc3, qt, qk, qe, nr, thr, L, zl, gl, mism);
   }
-  if constexpr (SEQ)
-    seq_draws<TE, KS>(p, pidx, urow, bcol, pc1, pc2, counter_word3(par.request, par.depth, 4u), L, gl);
+  if constexpr (SEQ) {
+    __syncthreads();  // the draws of wave 1
+    if (lane < K) {
+      gl.id = sh.d.id[lane];
+      gl.aux = sh.d.z[lane];
+      gl.val = 0.0f;
+    }
+    gl.cnt = K;
+  }
 
   // Child scoring: lane j handles slot j + 1 (Algorithm 1; §3.2 pre-draw bound; Eq. 3).
   const float lsp = par.log_surv;

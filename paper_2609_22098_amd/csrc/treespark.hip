@@ -271,7 +271,9 @@ void launch_eval(const ts_drafter* d, const ExpandParams& p, const Plan& pl, hip
 }
 
 void launch_merge(const ts_drafter* d, const MergeParams& p, const Plan& pl, hipStream_t s) {
-  const dim3 grid((p.P + 3) / 4), block(256);
+  // one parent per wave; sequential draws: one parent per workgroup of two waves
+  const bool seq = pl.mode == kModeSeq;
+  const dim3 grid(seq ? p.P : (p.P + 3) / 4), block(seq ? 128 : 256);
   if (d->dtype == TS_BF16) {
     switch (pl.ks) {
       case 1: launch_merge_t<uint16_t, 1>(p, pl.mode, grid, block, s); break;
