@@ -813,7 +813,8 @@ struct MergeLds {
 
 // Sequential draws run on a wave of their own (the parent's second wave):
 // its scratch, and the draws it hands to the scoring wave.
-constexpr int kLdsSegs = 40;  // segments whose block table is kept in LDS
+constexpr int kLdsSegs = 40;  // segments whose block table is kept in LDS (one per lane)
+static_assert(kLdsSegs <= 64, "one segment per lane");
 struct DrawLds {
   float bz[4][16];               // logits of the drawn block
   float seg_blk[kLdsSegs * 64];  // the parent's block table when V <= 40 * 4096
@@ -1178,15 +1179,27 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
 #pragma unroll
     for (int k = 0; k < kLdsSegs; ++k)
       if (k < nseg) L.seg_blk[k * kBps + lane] = x[k];
-#pragma unroll
-    for (int s0 = 0; s0 < kLdsSegs; s0 += 8) {
-      if (s0 >= nseg) break;
-      float xs[8];
-#pragma unroll
-      for (int k = 0; k < 8; ++k) xs[k] = x[s0 + k];
-      reduce8(s0, xs);
-    }
     wave_sync_lds();
+    // lane l reduces segment l from LDS (no cross-lane steps); the 16-byte
+    // pieces of its row are read in a lane-rotated order
+    if (lane < nseg) {
+      const f32x4* row = reinterpret_cast<const f32x4*>(L.seg_blk + lane * kBps);
+      f32x4 xv[kBps / 4];
+#pragma unroll
+      for (int i = 0; i < kBps / 4; ++i) xv[i] = row[(i + lane) & (kBps / 4 - 1)];
+      float m = kNegInf;
+#pragma unroll
+      for (int i = 0; i < kBps / 4; ++i)
+        m = fmaxf(fmaxf(m, fmaxf(xv[i][0], xv[i][1])), fmaxf(xv[i][2], xv[i][3]));
+      if (m != kNegInf) {
+        float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int i = 0; i < kBps / 4; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) a[e] += exp2_fast(xv[i][e] - m);
+        segL[0] = m + __builtin_amdgcn_logf((a[0] + a[1]) + (a[2] + a[3]));
+      }
+    }
   } else {
 #pragma unroll 1
     for (int s0 = 0; s0 < nseg; s0 += 8) {
