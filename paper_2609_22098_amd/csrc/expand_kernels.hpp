@@ -30,6 +30,7 @@
 // picking a 4096-token segment, a block in it and a token in it in proportion
 // to the remaining mass, recomputing only the chosen block.
 #pragma once
+#include <type_traits>
 
 #include "device_common.hpp"
 
@@ -293,11 +294,12 @@ __device__ __forceinline__ float sum16_exp2(const float (&v)[16], float c, float
   return (a[0] + a[1]) + (a[2] + a[3]);
 }
 
-__device__ __forceinline__ float block_log_mass(float a, float ml) {
-  const float l = a > 0.0f ? ml + __builtin_amdgcn_logf(a) : kNegInf;
-  const float m = cross_row_max(l);
-  const float s = cross_row_sum(m == kNegInf ? 0.0f : exp2_fast(l - m));
-  return m == kNegInf ? kNegInf : m + __builtin_amdgcn_logf(s);
+// a: this lane's run sum relative to 2^ref (ref finite); the run holding
+// the block's largest ref has a >= 1 unless the whole block is masked.
+__device__ __forceinline__ float block_log_mass(float a, float ref) {
+  const float m = cross_row_max(ref);
+  const float s = cross_row_sum(a * exp2_fast(ref - m));
+  return s > 0.0f ? m + __builtin_amdgcn_logf(s) : kNegInf;
 }
 
 // Block-table stores of the streaming pass.  Blocks are grouped in windows of
@@ -447,22 +449,25 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
 #pragma unroll
       for (int j = 1; j < 16; ++j) bm = fmaxf(bm, v[j]);
       // run sums are taken relative to the run's own maximum (a run far below
-      // the running maximum keeps its mass), then folded into the running sums
-      const float mn = fmaxf(m0[nb], bm);
-      const float mref = fmaxf(mn, -1e30f);
+      // the running maximum keeps its mass), then folded into the running
+      // sums, which are relative to the running maximum: of the two terms the
+      // one with the lower reference is scaled down (one exponential)
+      const float m0c = fmaxf(m0[nb], -1e30f);
       const float bref = fmaxf(bm, -1e30f);
-      const float ml = mref * kLog2e, bl = bref * kLog2e;
+      const bool run_high = bref > m0c;
+      const float gap = -__builtin_fabsf(m0c - bref);
+      const float bl = bref * kLog2e;
       float a0 = sum16_exp2(v, kLog2e, bl);
-      s0[nb] = __builtin_fmaf(s0[nb], exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -ml)),
-                              a0 * exp2_fast(bl - ml));
-      const float mlT = mref * p.cT, blT = bref * p.cT;
+      const float f0 = exp2_fast(gap * kLog2e);
+      s0[nb] = run_high ? __builtin_fmaf(s0[nb], f0, a0) : __builtin_fmaf(a0, f0, s0[nb]);
+      const float blT = bref * p.cT;
       float aT = 0.0f;
       if (SAMPLE && p.need_T) {
         aT = sum16_exp2(v, p.cT, blT);
-        sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)),
-                                aT * exp2_fast(blT - mlT));
+        const float fT = exp2_fast(gap * p.cT);
+        sT[nb] = run_high ? __builtin_fmaf(sT[nb], fT, aT) : __builtin_fmaf(aT, fT, sT[nb]);
       }
-      m0[nb] = mn;
+      m0[nb] = fmaxf(m0[nb], bm);
       top_add(zt[nb], bm, run);
       if constexpr (SEQ) {
         const float lb = p.need_T ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
@@ -655,7 +660,10 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
       }
   };
 
-  auto compute = [&](const u32x4* wb, const u32x4* ub, int t0, int step) {
+  // mask_tag: std::true_type for the vocabulary's last, partial step only; a
+  // separate instantiation keeps the masking out of every other step.
+  auto compute = [&](const u32x4* wb, const u32x4* ub, int t0, int step, auto mask_tag) {
+    constexpr bool kMask = decltype(mask_tag)::value;
     const int tl = t0 + g * 16;
     f32x4 acc[4][NB];
 #pragma unroll
@@ -668,7 +676,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
 #pragma unroll
       for (int bb = 0; bb < 4; ++bb)
         acc[bb][nb] = f32x4{u.get(bb * 4), u.get(bb * 4 + 1), u.get(bb * 4 + 2), u.get(bb * 4 + 3)};
-      if (t0 + 64 > V) {  // the vocabulary's last step only (a uniform branch)
+      if constexpr (kMask) {  // tokens past the vocabulary: z = -inf
 #pragma unroll
         for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
@@ -697,22 +705,25 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
 #pragma unroll
       for (int j = 1; j < 16; ++j) bm = fmaxf(bm, v[j]);
       // run sums are taken relative to the run's own maximum (a run far below
-      // the running maximum keeps its mass), then folded into the running sums
-      const float mn = fmaxf(m0[nb], bm);
-      const float mref = fmaxf(mn, -1e30f);
+      // the running maximum keeps its mass), then folded into the running
+      // sums, which are relative to the running maximum: of the two terms the
+      // one with the lower reference is scaled down (one exponential)
+      const float m0c = fmaxf(m0[nb], -1e30f);
       const float bref = fmaxf(bm, -1e30f);
-      const float ml = mref * kLog2e, bl = bref * kLog2e;
+      const bool run_high = bref > m0c;
+      const float gap = -__builtin_fabsf(m0c - bref);
+      const float bl = bref * kLog2e;
       float a0 = sum16_exp2(v, kLog2e, bl);
-      s0[nb] = __builtin_fmaf(s0[nb], exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -ml)),
-                              a0 * exp2_fast(bl - ml));
-      const float mlT = mref * p.cT, blT = bref * p.cT;
+      const float f0 = exp2_fast(gap * kLog2e);
+      s0[nb] = run_high ? __builtin_fmaf(s0[nb], f0, a0) : __builtin_fmaf(a0, f0, s0[nb]);
+      const float blT = bref * p.cT;
       float aT = 0.0f;
       if (SAMPLE && p.need_T) {
         aT = sum16_exp2(v, p.cT, blT);
-        sT[nb] = __builtin_fmaf(sT[nb], exp2_fast(__builtin_fmaf(m0[nb], p.cT, -mlT)),
-                                aT * exp2_fast(blT - mlT));
+        const float fT = exp2_fast(gap * p.cT);
+        sT[nb] = run_high ? __builtin_fmaf(sT[nb], fT, aT) : __builtin_fmaf(aT, fT, sT[nb]);
       }
-      m0[nb] = mn;
+      m0[nb] = fmaxf(m0[nb], bm);
       top_add(zt[nb], bm, run);
       if constexpr (SEQ) {
         const float lb = p.need_T ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
@@ -731,7 +742,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const int j = i * 4 + q;
-            const float key = (tl + j < V) ? gumbel_key2(v[j], p.cT, w[q]) : kNegInf;
+            const float key = gumbel_key2(v[j], p.cT, w[q]);  // -inf past the vocabulary
             gm = fmaxf(gm, key);
           }
         }
@@ -749,14 +760,24 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
     __syncthreads();
     const bool more1 = t0 + 64 < tend;
     if (more1) issue(w1, u1, t0 + 64);
-    if (active) compute(w0, u0, t0, step);
+    if (active) {
+      if (t0 + 64 > V)
+        compute(w0, u0, t0, step, std::true_type{});
+      else
+        compute(w0, u0, t0, step, std::false_type{});
+    }
     if (!more1) break;
     t0 += 64; ++step;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     const bool more2 = t0 + 64 < tend;
     if (more2) issue(w0, u0, t0 + 64);
-    if (active) compute(w1, u1, t0, step);
+    if (active) {
+      if (t0 + 64 > V)
+        compute(w1, u1, t0, step, std::true_type{});
+      else
+        compute(w1, u1, t0, step, std::false_type{});
+    }
     if (!more2) break;
     t0 += 64; ++step;
   }
