@@ -7,14 +7,17 @@ synthetic inputs (see paper_2609_22098_amd/synth.py).  One step is one pass of
 the whole hot path over that batch:
   1. ts_expand over the 2048-parent serving frontier (2 parents at every depth
      of every request): conditional logits on MFMA, log-sum-exp, top-k,
-     Gumbel-top-k draws, child scoring;
+     k draws without replacement (sequential sampler by default), child
+     scoring;
   2. ts_build_tree: best-first trees for the 64 requests under their theta;
   3. ts_tree_mask: the trees' attention masks and position ids for the
      target's verification pass;
   4. ts_verify: recursive-rejection verification of those trees at T=0.7.
 value = node evaluations (frontier parents + tree-building parents) per
 second over the step.  The roofline object covers the dominant kernel (the
-streaming pass of ts_expand), timed with HIP events on its own stream.
+streaming pass of ts_expand), timed with HIP events on its own stream, against
+the roofline that binds it (HBM bytes or VALU issue slots; the other one is
+reported as roofline_other).
 
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1]
 """
@@ -35,6 +38,11 @@ sys.path.insert(0, ROOT)
 
 METRIC = "parent-conditioned node evals/sec at V=151936 + achieved HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+# VALU issue peak: 256 CUs x 4 SIMDs x 32 fp32 lanes per cycle x 2.4 GHz (the
+# 157.3 TFLOP/s fp32 vector figure counts an FMA as two); transcendentals
+# (v_exp_f32, v_log_f32) issue at a quarter of that rate.
+VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12
+TRANS_WEIGHT = 4
 KERNEL_SOURCES = ("paper_2609_22098_amd/csrc/expand_kernels.hpp",
                   "paper_2609_22098_amd/csrc/device_common.hpp")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "expand_eval_serving_traffic.json")
@@ -272,6 +280,13 @@ def main():
     alg_bytes = rows * dr.V * 2 + dr.V * dr.r * 2 + P * dr.r * 2
     eval_s = float(eval_ms.mean()) / 1e3
     achieved = alg_bytes / eval_s / 1e9
+    # algorithmic VALU work per (parent, token) element, in full-rate issue
+    # slots: a running max, and per temperature one FMA (scale and shift), one
+    # exp2 (TRANS_WEIGHT slots) and one add; two temperatures when T != 0, 1
+    n_temps = 2 if (T > 0 and T != 1.0) else 1
+    slots_per_elem = 1 + n_temps * (2 + TRANS_WEIGHT)
+    alg_ops = slots_per_elem * P * dr.V
+    achieved_ops = alg_ops / eval_s / 1e12
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
@@ -293,21 +308,29 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": w["name"] + (": ts_expand over the 2048-parent frontier" if args.expand_only else
+        "config": {"workload": w["name"].replace("-T0.7", f"-T{T:g}") + (": ts_expand over the 2048-parent frontier" if args.expand_only else
                                             ": 2048-parent ts_expand + best-first trees + tree masks + "
-                                            "T=0.7 verification"),
+                                            f"T={T:g} verification"),
                    "V": dr.V, "D": dr.D, "r": dr.r, "requests": dr.R, "frontier_parents": P, "K": K,
                    "T": T, "N": N, "sampler": sampler,
                    "tree_evals_per_step": 0 if args.expand_only else tree_evals},
-        "roofline": {"bound": "hbm", "kernel": EVAL_KERNEL + " (streaming pass of ts_expand)",
-                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": float(eval_ms.mean())},
+        "roofline": None,
         "expand_ms": {"eval": float(eval_ms.mean()), "merge": float(merge_ms.mean()),
                       "eval_p10": float(np.percentile(eval_ms, 10)), "eval_p90": float(np.percentile(eval_ms, 90))},
         "expand_node_evals_per_s": P / ((eval_ms.mean() + merge_ms.mean()) / 1e3),
         "phases_ms": phases,
     }
+    kernel = EVAL_KERNEL + " (streaming pass of ts_expand)"
+    hbm = {"bound": "hbm", "kernel": kernel, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+           "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "alg_bytes_per_launch": alg_bytes,
+           "avg_launch_ms": float(eval_ms.mean())}
+    alu = {"bound": "alu", "kernel": kernel, "achieved": achieved_ops, "peak": VALU_PEAK_TOPS,
+           "unit": "T VALU slots/s", "frac": achieved_ops / VALU_PEAK_TOPS, "traffic": traffic,
+           "alg_slots_per_launch": alg_ops, "slots_per_element": slots_per_elem,
+           "avg_launch_ms": float(eval_ms.mean())}
+    # the binding roofline is the one with the longer floor, i.e. the larger fraction
+    result["roofline"] = alu if alu["frac"] > hbm["frac"] else hbm
+    result["roofline_other"] = hbm if alu["frac"] > hbm["frac"] else alu
     if not args.no_cpu:
         log("timing the CPU oracle")
         result["cpu_baseline"] = cpu_baseline(dr, fr, K, T, seed, args.cpu_seconds, sampler)

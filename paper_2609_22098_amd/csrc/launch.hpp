@@ -2,7 +2,7 @@
 // instantiated in its own translation unit so the kernels compile in parallel.
 #pragma once
 
-#include "expand_kernels.hpp"
+#include "merge_kernels.hpp"
 #include "verify_kernels.hpp"
 
 namespace ts {

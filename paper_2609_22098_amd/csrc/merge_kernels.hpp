@@ -1,0 +1,755 @@
+// Pass 2 of the parent-conditioned expansion (ts_expand): merge of the
+// per-chunk partials of pass 1, exact top-k, the sequential draws and child
+// scoring.  The pass-1 kernels, the shared parameter blocks and the MFMA
+// fragment helpers are in expand_kernels.hpp.
+#pragma once
+#include "expand_kernels.hpp"
+
+namespace ts {
+
+struct MergeParams {
+  const void* U;
+  const void* E;
+  const void* W2;
+  int R, D, V, r;
+  const ts_parent* parents;
+  int P;
+  int Vc, S;
+  int K;
+  float T, cT;
+  int need_T;
+  float calib_a, calib_b;
+  PhiloxKeys keys;
+  const float* part_m;
+  const float* part_s0;
+  const float* part_sT;
+  RunSummaryPtr zs;
+  RunSummaryPtr gs;
+  float* blk;  // per-parent block table [P][blk_ld]; the draws update their own parent's rows
+  int nblk, blk_ld;
+  ts_expand_out out;
+};
+
+// ---------------------------------------------------------------- pass 2
+
+constexpr int kMaxChunks = 256;                              // chunks per parent
+constexpr int kEntrySlots = kMaxChunks * kTopRuns / 64;      // recorded runs per lane
+constexpr int kRestSlots = kMaxChunks / 64;                  // chunk rests per lane
+constexpr int kBatch = 8;                                    // runs recomputed together
+constexpr int kItemCap = 256;                                // candidate items per parent
+
+struct MergeLds {
+  float bz[kBatch][16];  // logits of a batch of recomputed runs
+  float bk[kBatch][16];  // their keys (z, or the Gumbel keys)
+  int item_t[kItemCap];  // run start token, or -(chunk+1) for a whole chunk
+  int item_k[kItemCap];  // key kind: 0 = z, 1 = Gumbel
+  float item_e[kItemCap];  // expected run maximum (NaN if unknown)
+  uint32_t whole[kMaxChunks / 32];
+};
+
+// Sequential draws run on a wave of their own (the parent's second wave):
+// its scratch, and the draws it hands to the scoring wave.
+constexpr int kLdsSegs = 40;  // segments whose block table is kept in LDS (one per lane)
+static_assert(kLdsSegs <= 64, "one segment per lane");
+struct DrawLds {
+  float bz[4][16];               // logits of the drawn block
+  float seg_blk[kLdsSegs * 64];  // the parent's block table when V <= 40 * 4096
+  int id[TS_MAX_K];              // draw j's token and logit at j - 1
+  float z[TS_MAX_K];
+};
+
+// Workgroup LDS of the merge: four parents of one wave each, or, for
+// sequential draws, one parent of two waves.
+template <bool SEQ>
+struct MergeShared {
+  MergeLds l[4];
+};
+template <>
+struct MergeShared<true> {
+  MergeLds l[1];
+  DrawLds d;
+};
+
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ int wave_sum_int(int v) { return wave_sum_i32(v); }
+
+// A sorted list of at most K (key, token, aux) entries kept in registers:
+// lane j < cnt holds entry j; order: key desc, token asc.
+struct RegList {
+  float val;
+  int id;
+  float aux;
+  int cnt;
+};
+
+__device__ __forceinline__ void reglist_init(RegList& l) {
+  l.val = kNegInf; l.id = 0x7FFFFFFF; l.aux = 0.0f; l.cnt = 0;
+}
+
+// Insert a candidate (uniform across the wave).
+__device__ __forceinline__ void reglist_insert(RegList& l, int K, float v, int id, float a) {
+  const int lane = threadIdx.x & 63;
+  const bool ahead = lane < l.cnt && run_before(l.val, l.id, v, id);
+  const int pos = __popcll(__ballot(ahead));
+  if (pos >= K) return;
+  // the entries from pos on move up one lane (DPP wave_shr:1)
+  const float pv = dpp_f32<0x138>(l.val);
+  const int pid = dpp_i32<0x138>(l.id);
+  const float pa = dpp_f32<0x138>(l.aux);
+  if (lane == pos) {
+    l.val = v; l.id = id; l.aux = a;
+  } else if (lane > pos && lane < K) {
+    l.val = pv; l.id = pid; l.aux = pa;
+  }
+  l.cnt = min(l.cnt + 1, K);
+}
+
+// Recompute up to kBatch runs of 16 tokens [t, t+16) for one parent with the
+// MFMA sequence of pass 1 (same operands in the same K positions, same
+// accumulator start), so the values are bit-identical to the streaming pass.
+// The parent sits in column 0; lanes 0, 16, 32, 48 get tokens t + g*4 + [0,4).
+// Runs of kind 1 also get their Gumbel keys.  All lanes then check the keys
+// against the kind's threshold; candidates go into the kind's list.  A run
+// whose expected maximum is known counts a mismatch if the recomputed one differs.
+template <typename TE, int KS, bool SAMPLE>
+__device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* urow,
+                                             const typename Frag<TE>::type (&bcol)[KS],
+                                             uint32_t pc1, uint32_t pc2, uint32_t pc3,
+                                             const int (&t)[kBatch], const int (&kind)[kBatch],
+                                             const float (&expect)[kBatch], int nrun,
+                                             const float (&thr)[2], MergeLds& L, RegList& zl,
+                                             RegList& gl, int& mism) {
+  typedef Frag<TE> F;
+  const int lane = threadIdx.x & 63;
+  const int n = lane & 15, g = lane >> 4;
+  const int V = p.V;
+  const TE* W2 = static_cast<const TE*>(p.W2);
+  f32x4 acc[kBatch];
+#pragma unroll
+  for (int b = 0; b < kBatch; ++b) {
+    const int tb = b < nrun ? t[b] : 0;
+    acc[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    if (n == 0) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int tok = tb + g * 4 + e;
+        acc[b][e] = tok < V ? F::to_f32(urow[min(tok, V - 1)]) : kNegInf;
+      }
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < kBatch; ++b) {
+    const int tb = b < nrun ? t[b] : 0;
+    const TE* wrow = W2 + (size_t)min(tb + n, V - 1) * p.r;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) acc[b] = F::mma(F::load(wrow, kk * F::kPerStep, g), bcol[kk], acc[b]);
+  }
+  if (n == 0) {
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int tb = b < nrun ? t[b] : 0;
+      float k4[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) k4[e] = acc[b][e];
+      if constexpr (SAMPLE) {
+        if (b < nrun && kind[b] == 1) {
+          // tokens tb + g*4 + [0,4) are exactly one Philox call
+          uint32_t c0 = (uint32_t)(tb + g * 4) >> 2, c1 = pc1, c2 = pc2, c3 = pc3;
+          philox10(c0, c1, c2, c3, p.keys);
+          const uint32_t w[4] = {c0, c1, c2, c3};
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            k4[e] = (tb + g * 4 + e < V) ? gumbel_key2(acc[b][e], p.cT, w[e]) : kNegInf;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        L.bz[b][g * 4 + e] = acc[b][e];
+        L.bk[b][g * 4 + e] = k4[e];
+      }
+    }
+  }
+  wave_sync_lds();
+#ifdef TS_DEBUG_RUNS
+  mism += nrun * 1000;
+#endif
+  // lane l checks key j = l + 64 h of the batch (run j / 16, token j % 16)
+#pragma unroll
+  for (int h = 0; h < kBatch / 4; ++h) {
+    const int j = lane + 64 * h;
+    const int b = j >> 4, e = j & 15;
+    const float kv = L.bk[b][e];
+    int tb = 0, kd = 0;
+    float ex = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q)
+      if (q == b) { tb = t[q]; kd = kind[q]; ex = expect[q]; }
+    const bool live = b < nrun && tb + e < V;
+    float rm = live ? kv : kNegInf;
+    rm = row_max(rm);  // the run's 16 keys sit in one row of 16 lanes
+    mism += __popcll(__ballot(live && e == 0 && !__builtin_isnan(ex) && rm != ex));
+    const float th = kd ? thr[1] : thr[0];
+    uint64_t mask = __ballot(live && kv >= th);
+    while (mask) {
+      const int src = __ffsll((unsigned long long)mask) - 1;
+      mask &= mask - 1;
+      const float cv = lane_f32(kv, src);
+      const float cz = lane_f32(L.bz[b][e], src);
+      const int ct = lane_i32(tb + e, src);
+      const int ck = lane_i32(kd, src);
+      if (ck == 0)
+        reglist_insert(zl, p.K, cv, ct, cz);
+      else
+        reglist_insert(gl, p.K, cv, ct, cz);
+    }
+  }
+  wave_sync_lds();
+}
+
+// Threshold and candidate items for one key kind.  The threshold is the
+// K-th largest recorded run maximum (counting equal values with their
+// multiplicity): those are maxima of K distinct runs, hence of K distinct
+// tokens, so the K-th largest key over the vocabulary is at least the
+// threshold.  A token whose key reaches the threshold lies in a run whose
+// maximum reaches it: one of its chunk's recorded runs, or, when the chunk's
+// rest maximum reaches it too, somewhere in the chunk (a whole-chunk item).
+// NE, NR: recorded-run and chunk-rest slots per lane (NE = 4 NR; S <= 64 NR).
+template <int NE, int NR>
+__device__ __forceinline__ float select_items_n(const MergeParams& p, const RunSummaryPtr& sm,
+                                                int pidx, int kind, MergeLds& L, int& nitems) {
+  constexpr int kEntrySlots = NE, kRestSlots = NR;
+  const int lane = threadIdx.x & 63;
+  const int S = p.S, K = p.K;
+  const size_t pb = (size_t)pidx * S;
+  float ev[kEntrySlots];
+  int er[kEntrySlots];
+  float rv[kRestSlots];
+#pragma unroll
+  for (int i = 0; i < kEntrySlots; ++i) {
+    const int e = i * 64 + lane;
+    const bool in = (e >> 2) < S;
+    ev[i] = in ? sm.m[pb * kTopRuns + e] : kNegInf;
+    er[i] = in ? sm.r[pb * kTopRuns + e] : 0;
+  }
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) {
+    const int c = i * 64 + lane;
+    rv[i] = c < S ? sm.rest[pb + c] : kNegInf;
+  }
+  uint32_t taken = 0u;
+  float thr = kNegInf;
+  int picked = 0;
+  for (int round = 0; round < K; ++round) {
+    float lm = kNegInf;
+#pragma unroll
+    for (int i = 0; i < kEntrySlots; ++i)
+      if (!(taken & (1u << i))) lm = fmaxf(lm, ev[i]);
+    const float m = wave_max(lm);
+    if (m == kNegInf) break;
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < kEntrySlots; ++i)
+      if (!(taken & (1u << i)) && ev[i] == m) { taken |= 1u << i; ++c; }
+    picked += wave_sum_int(c);
+    if (picked >= K) { thr = m; break; }
+  }
+  if (picked < K) thr = kNegInf;  // fewer than K runs recorded: every token is a candidate
+
+  // whole chunks
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) {
+    const uint64_t wm = __ballot(rv[i] >= thr);
+    if (lane == 0) {
+      L.whole[2 * i] = (uint32_t)wm;
+      L.whole[2 * i + 1] = (uint32_t)(wm >> 32);
+    }
+  }
+  wave_sync_lds();
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int base = nitems;
+  // recorded runs of chunks that are not whole
+#pragma unroll
+  for (int i = 0; i < kEntrySlots; ++i) {
+    const int e = i * 64 + lane;
+    const int c = e >> 2;
+    const bool in = c < S;
+    const bool wh = in && ((L.whole[c >> 5] >> (c & 31)) & 1u);
+    const bool cand = in && !wh && ev[i] >= thr;
+    const uint64_t mask = __ballot(cand);
+    const int off = base + __popcll(mask & lt);
+    if (cand && off < kItemCap) {
+      const int run = er[i];
+      L.item_t[off] = c * p.Vc + (run >> 2) * 64 + (run & 3) * 16;
+      L.item_k[off] = kind;
+      L.item_e[off] = ev[i];
+    }
+    base += __popcll(mask);
+  }
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) {
+    const int c = i * 64 + lane;
+    const bool cand = c < S && rv[i] >= thr;
+    const uint64_t mask = __ballot(cand);
+    const int off = base + __popcll(mask & lt);
+    if (cand && off < kItemCap) {
+      L.item_t[off] = -(c + 1);
+      L.item_k[off] = kind;
+      L.item_e[off] = __builtin_nanf("");
+    }
+    base += __popcll(mask);
+  }
+  if (base > kItemCap) {
+    // too many candidates (heavy ties): rescan every chunk of this kind
+    base = nitems;
+    for (int c0 = 0; c0 < S; c0 += 64) {
+      const int c = c0 + lane;
+      if (c < S && base + c - c0 < kItemCap) {
+        L.item_t[base + c - c0] = -(c + 1);
+        L.item_k[base + c - c0] = kind;
+        L.item_e[base + c - c0] = __builtin_nanf("");
+      }
+      base += min(64, S - c0);
+    }
+    thr = kNegInf;
+  }
+  nitems = min(base, kItemCap);
+  wave_sync_lds();
+  return thr;
+}
+
+__device__ __forceinline__ float select_items(const MergeParams& p, const RunSummaryPtr& sm,
+                                              int pidx, int kind, MergeLds& L, int& nitems) {
+  if (p.S <= 64) return select_items_n<4, 1>(p, sm, pidx, kind, L, nitems);
+  return select_items_n<kMaxChunks * kTopRuns / 64, kMaxChunks / 64>(p, sm, pidx, kind, L, nitems);
+}
+
+// ---------------------------------------------------------------- sequential draws
+
+constexpr int kSegSlots = (TS_MAX_V + 64 * kSegTokens - 1) / (64 * kSegTokens);  // segments per lane
+
+// One categorical pick over items laid out as item = 64 * slot + lane with
+// masses m >= 0: the first item whose inclusive cumulative mass exceeds
+// u * total (never a zero-mass item); rounding at the top end falls back to
+// the last item with mass.  Returns -1 only if every mass is zero.
+template <int NS>
+__device__ __forceinline__ int wave_pick(const float (&m)[NS], float u) {
+  float c[NS];
+  float base = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    const float x = wave_incl_scan(m[i]);
+    c[i] = base + x;
+    base += lane_f32(x, 63);
+  }
+  const float t = u * base;
+  int cnt = 0, last = -1;
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    cnt += __popcll(__ballot(c[i] <= t));
+    const uint64_t pos = __ballot(m[i] > 0.0f);
+    if (pos) last = 64 * i + 63 - __clzll((long long)pos);
+  }
+  return cnt > last ? last : cnt;
+}
+
+// K draws without replacement from q_T, one after another (§3.3 residual
+// proposal): draw j picks a segment, a block in it and a token in it, each in
+// proportion to its remaining mass, from the words of one Philox call
+// (c0 = j, tag 4).  Masses are handled as base-2 logs relative to each
+// level's largest one, so removing drawn tokens never underflows the rest.
+// The parent's block table lives in LDS when it fits (V <= 40 * 4096), else
+// in its rows of the workspace; a drawn token's block is rewritten in place.
+// Draw j lands in lane j - 1 of gl (token, z).
+
+template <typename TE, int KS>
+__device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const TE* urow,
+                                          const typename Frag<TE>::type (&bcol)[KS], uint32_t pc1,
+                                          uint32_t pc2, uint32_t pc3, DrawLds& L, RegList& gl) {
+  typedef Frag<TE> F;
+  const int lane = threadIdx.x & 63;
+  const int n = lane & 15, g = lane >> 4;
+  const int V = p.V, nblk = p.nblk;
+  const TE* W2 = static_cast<const TE*>(p.W2);
+  float* gblk = p.blk + (size_t)pidx * p.blk_ld;
+  constexpr int kBps = kSegTokens / kBlkTokens;  // blocks per segment (64)
+  const int nseg = (nblk + kBps - 1) / kBps;
+  const bool in_lds = nseg <= kLdsSegs;
+
+  // Segment log-masses (lane l owns segment l + 64 i).  The wave reads the
+  // table one segment per load (lane = block offset, coalesced); every load
+  // is issued before the first reduction (a global round trip costs about
+  // as much as all the arithmetic here).  The table is kept in LDS when it
+  // fits, and segments are reduced eight at a time.
+  float segL[kSegSlots];
+#pragma unroll
+  for (int i = 0; i < kSegSlots; ++i) segL[i] = kNegInf;
+  auto reduce8 = [&](int s0, const float (&xs)[8]) {
+    float m[8], e[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) m[k] = xs[k];
+    wave_max8(m);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) e[k] = m[k] == kNegInf ? 0.0f : exp2_fast(xs[k] - m[k]);
+    wave_sum8(e);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int sg = s0 + k;
+      const float l = m[k] == kNegInf ? kNegInf : m[k] + __builtin_amdgcn_logf(e[k]);
+#pragma unroll
+      for (int i = 0; i < kSegSlots; ++i)
+        if (sg < nseg && sg == 64 * i + lane) segL[i] = l;
+    }
+  };
+  if (in_lds) {
+    float x[kLdsSegs];
+#pragma unroll
+    for (int k = 0; k < kLdsSegs; ++k) {
+      const int b = k * kBps + lane;
+      x[k] = (k < nseg && b < nblk) ? gblk[b] : kNegInf;
+    }
+#pragma unroll
+    for (int k = 0; k < kLdsSegs; ++k)
+      if (k < nseg) L.seg_blk[k * kBps + lane] = x[k];
+    wave_sync_lds();
+    // lane l reduces segment l from LDS (no cross-lane steps); the 16-byte
+    // pieces of its row are read in a lane-rotated order
+    if (lane < nseg) {
+      const f32x4* row = reinterpret_cast<const f32x4*>(L.seg_blk + lane * kBps);
+      f32x4 xv[kBps / 4];
+#pragma unroll
+      for (int i = 0; i < kBps / 4; ++i) xv[i] = row[(i + lane) & (kBps / 4 - 1)];
+      float m = kNegInf;
+#pragma unroll
+      for (int i = 0; i < kBps / 4; ++i)
+        m = fmaxf(fmaxf(m, fmaxf(xv[i][0], xv[i][1])), fmaxf(xv[i][2], xv[i][3]));
+      if (m != kNegInf) {
+        float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int i = 0; i < kBps / 4; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) a[e] += exp2_fast(xv[i][e] - m);
+        segL[0] = m + __builtin_amdgcn_logf((a[0] + a[1]) + (a[2] + a[3]));
+      }
+    }
+  } else {
+#pragma unroll 1
+    for (int s0 = 0; s0 < nseg; s0 += 8) {
+      float xs[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int b = (s0 + k) * kBps + lane;
+        xs[k] = (s0 + k < nseg && b < nblk) ? gblk[b] : kNegInf;
+      }
+      reduce8(s0, xs);
+    }
+  }
+  // the words of every draw: lane j - 1 computes draw j's Philox call
+  uint32_t dw0 = (uint32_t)(lane + 1), dw1 = pc1, dw2 = pc2, dw3 = pc3;
+  philox10(dw0, dw1, dw2, dw3, p.keys);
+  gl.cnt = 0;
+#pragma unroll 1
+  for (int j = 1; j <= p.K; ++j) {
+    const uint32_t w0 = (uint32_t)lane_i32((int)dw0, j - 1);
+    const uint32_t w1 = (uint32_t)lane_i32((int)dw1, j - 1);
+    const uint32_t w2 = (uint32_t)lane_i32((int)dw2, j - 1);
+    // level 1: segment
+    float ms[kSegSlots];
+    float mx = kNegInf;
+#pragma unroll
+    for (int i = 0; i < kSegSlots; ++i) mx = fmaxf(mx, segL[i]);
+    mx = wave_max(mx);
+#pragma unroll
+    for (int i = 0; i < kSegSlots; ++i) ms[i] = segL[i] == kNegInf ? 0.0f : exp2_fast(segL[i] - mx);
+    const int sg = wave_pick(ms, word_to_uniform(w0));
+    // level 2: block within the segment (lane = block offset)
+    const int b = sg * kBps + lane;
+    const bool bin = sg >= 0 && b < nblk;
+    const float lb = bin ? (in_lds ? L.seg_blk[b] : gblk[b]) : kNegInf;
+    const float mb = wave_max(lb);
+    float m2[1];
+    m2[0] = lb == kNegInf ? 0.0f : exp2_fast(lb - mb);
+    const int bo = wave_pick(m2, word_to_uniform(w1));
+    const int bsel = sg * kBps + bo;
+    // level 3: token within the block; recompute its 64 logits (four runs of 16)
+    const int t0 = bsel * kBlkTokens;
+    // all loads of the block first (one round trip), then the MFMAs
+    typename F::type wf[4][KS];
+    f32x4 acc[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const TE* wrow = W2 + (size_t)min(t0 + 16 * q + n, V - 1) * p.r;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) wf[q][kk] = F::load(wrow, kk * F::kPerStep, g);
+      acc[q] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      if (n == 0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int tok = t0 + 16 * q + g * 4 + e;
+          acc[q][e] = tok < V ? F::to_f32(urow[min(tok, V - 1)]) : kNegInf;
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) acc[q] = F::mma(wf[q][kk], bcol[kk], acc[q]);
+    if (n == 0) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) L.bz[q][g * 4 + e] = acc[q][e];
+    }
+    wave_sync_lds();
+    const int y = t0 + lane;
+    const float zy = L.bz[lane >> 4][lane & 15];
+    wave_sync_lds();
+    bool live = y < V && bo >= 0;
+    for (int k = 0; k < j - 1; ++k) live &= lane_i32(gl.id, k) != y;
+    const float xy = live ? zy * p.cT : kNegInf;
+    const float mt = wave_max(xy);
+    float m3[1];
+    m3[0] = live ? exp2_fast(xy - mt) : 0.0f;
+    const int to = wave_pick(m3, word_to_uniform(w2));
+    const int tsel = t0 + to;
+    const float zsel = lane_f32(zy, to < 0 ? 0 : to);
+    if (lane == j - 1) {
+      gl.id = to < 0 ? -1 : tsel;
+      gl.aux = zsel;
+      gl.val = 0.0f;
+    }
+    // the block and the segment lose the drawn token's mass; both sums are
+    // taken relative to the largest value left, so nothing underflows
+    const bool left = live && lane != to;
+    const float mt2 = wave_max(left ? xy : kNegInf);
+    const float rest3 = wave_sum(left ? exp2_fast(xy - mt2) : 0.0f);
+    const float lnew = mt2 == kNegInf ? kNegInf : mt2 + __builtin_amdgcn_logf(rest3);
+    if (lane == bo && bin) {
+      if (in_lds)
+        L.seg_blk[bsel] = lnew;
+      else
+        gblk[bsel] = lnew;
+    }
+    if (in_lds) {
+      wave_sync_lds();
+    } else {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+    const float lb2 = lane == bo ? lnew : lb;
+    const float mb2 = wave_max(lb2);
+    const float rest2 = wave_sum(lb2 == kNegInf ? 0.0f : exp2_fast(lb2 - mb2));
+    const float snew = mb2 == kNegInf ? kNegInf : mb2 + __builtin_amdgcn_logf(rest2);
+#pragma unroll
+    for (int i = 0; i < kSegSlots; ++i)
+      if (sg == 64 * i + lane) segL[i] = snew;
+  }
+  gl.cnt = p.K;
+}
+
+template <typename TE, int KS, int MODE>
+__global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) {
+  typedef Frag<TE> F;
+  typedef typename F::type FT;
+  constexpr bool SAMPLE = MODE != kModeGreedy;
+  constexpr bool GUMBEL = MODE == kModeGumbel;
+  constexpr bool SEQ = MODE == kModeSeq;
+  // Sequential draws: one parent per workgroup; wave 1 draws while wave 0
+  // finds the greedy top-K, then wave 0 scores the children.
+  __shared__ MergeShared<SEQ> sh;
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int n = lane & 15, g = lane >> 4;
+  const int pidx = SEQ ? blockIdx.x : blockIdx.x * 4 + wv;
+  if (pidx >= p.P) return;  // uniform over the workgroup when SEQ
+#ifdef TS_DEBUG_RUNS
+  const long long t_start = clock64();
+#endif
+  MergeLds& L = sh.l[SEQ ? 0 : wv];
+  const int K = p.K, V = p.V, S = p.S;
+  const ts_parent par = p.parents[pidx];
+  const bool ok = par.token >= 0 && par.token < V && par.depth >= 0 && par.depth < p.D &&
+                  par.request >= 0 && par.request < p.R;
+  const size_t ob = (size_t)pidx * K;
+  if (!ok) {
+    if (SEQ && wv != 0) return;
+    const float nan = __builtin_nanf("");
+    if (lane < K) {
+      p.out.child_token[ob + lane] = -1;
+      p.out.child_log_q0[ob + lane] = nan;
+      p.out.child_log_surv[ob + lane] = nan;
+      p.out.slot_key[ob + lane] = nan;
+      if (p.out.child_log_qT) p.out.child_log_qT[ob + lane] = nan;
+      if (p.out.rank_token) p.out.rank_token[ob + lane] = -1;
+      if (p.out.rank_log_q0) p.out.rank_log_q0[ob + lane] = nan;
+    }
+    if (lane == 0) {
+      if (p.out.lse0) p.out.lse0[pidx] = nan;
+      if (p.out.lseT) p.out.lseT[pidx] = nan;
+      if (p.out.diag) p.out.diag[pidx] = 0;
+    }
+    return;
+  }
+  const TE* urow = static_cast<const TE*>(p.U) + ((size_t)par.request * p.D + par.depth) * (size_t)V;
+  const TE* erow = static_cast<const TE*>(p.E) + (size_t)par.token * p.r;
+  FT bcol[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) bcol[kk] = (n == 0) ? F::load(erow, kk * F::kPerStep, g) : F::zero();
+  const uint32_t pc1 = (uint32_t)par.path, pc2 = (uint32_t)(par.path >> 32);
+  const uint32_t pc3 = counter_word3(par.request, par.depth, 1u);
+
+  if constexpr (SEQ) {
+    if (wv == 1) {
+      RegList dl;
+      reglist_init(dl);
+      seq_draws<TE, KS>(p, pidx, urow, bcol, pc1, pc2, counter_word3(par.request, par.depth, 4u), sh.d, dl);
+      if (lane < K) {
+        sh.d.id[lane] = dl.id;
+        sh.d.z[lane] = dl.aux;
+      }
+      __syncthreads();
+      return;
+    }
+  }
+  const size_t pbase = (size_t)pidx * S;
+
+  // log-sum-exp over chunks: each lane folds its chunks in index order, then a fixed butterfly.
+  float pm[kRestSlots], ps[kRestSlots], pt[kRestSlots];
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) {
+    const int c = i * 64 + lane;
+    pm[i] = c < S ? p.part_m[pbase + c] : kNegInf;
+    ps[i] = c < S ? p.part_s0[pbase + c] : 0.0f;
+    pt[i] = (SAMPLE && p.need_T && c < S) ? p.part_sT[pbase + c] : 0.0f;
+  }
+  float M = kNegInf;
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) M = fmaxf(M, pm[i]);
+  M = wave_max(M);
+  const float Mref = fmaxf(M, -1e30f);
+  float s = 0.0f, st = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kRestSlots; ++i) {
+    s += ps[i] * exp2_fast(__builtin_fmaf(pm[i], kLog2e, -Mref * kLog2e));
+    if (SAMPLE && p.need_T) st += pt[i] * exp2_fast(__builtin_fmaf(pm[i], p.cT, -Mref * p.cT));
+  }
+  s = wave_sum(s);
+  st = wave_sum(st);
+  const float lse0 = M + logf(s);
+  float lseT = __builtin_nanf("");
+  if (SAMPLE) lseT = p.need_T ? M / p.T + logf(st) : lse0;
+
+  int nitems = 0;
+  float thr[2];
+  thr[0] = select_items(p, p.zs, pidx, 0, L, nitems);
+  thr[1] = kNegInf;
+  if constexpr (GUMBEL) thr[1] = select_items(p, p.gs, pidx, 1, L, nitems);
+
+  RegList zl, gl;
+  reglist_init(zl);
+  reglist_init(gl);
+  int mism = 0;
+  const float nan = __builtin_nanf("");
+  int it = 0, sub = 0;
+#pragma unroll 1
+  while (it < nitems) {
+    int qt[kBatch], qk[kBatch];
+    float qe[kBatch];
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) { qt[q] = 0; qk[q] = 0; qe[q] = nan; }
+    int nr = 0;
+#pragma unroll 1
+    while (nr < kBatch && it < nitems) {
+      const int code = L.item_t[it];
+      const int kd = L.item_k[it];
+      int t;
+      float e;
+      if (code < 0) {
+        const int cc = -code - 1;
+        const int cbeg = cc * p.Vc;
+        const int nruns = ((min(cbeg + p.Vc, V) - cbeg + 63) / 64) * 4;
+        t = cbeg + (sub >> 2) * 64 + (sub & 3) * 16;
+        e = nan;
+        if (++sub == nruns) { sub = 0; ++it; }
+        if (t >= V) continue;
+      } else {
+        t = code;
+        e = L.item_e[it];
+        ++it;
+      }
+#pragma unroll
+      for (int q = kBatch - 1; q > 0; --q) { qt[q] = qt[q - 1]; qk[q] = qk[q - 1]; qe[q] = qe[q - 1]; }
+      qt[0] = t;
+      qk[0] = kd;
+      qe[0] = e;
+      ++nr;
+    }
+    if (nr > 0)
+      rescan_batch<TE, KS, GUMBEL>(p, urow, bcol, pc1, pc2, pc3, qt, qk, qe, nr, thr, L, zl, gl, mism);
+  }
+  if constexpr (SEQ) {
+    __syncthreads();  // the draws of wave 1
+    if (lane < K) {
+      gl.id = sh.d.id[lane];
+      gl.aux = sh.d.z[lane];
+      gl.val = 0.0f;
+    }
+    gl.cnt = K;
+  }
+
+  // Child scoring: lane j handles slot j + 1 (Algorithm 1; §3.2 pre-draw bound; Eq. 3).
+  const float lsp = par.log_surv;
+  const float a = p.calib_a, bb = p.calib_b;
+  float zb = 0.0f;
+  if constexpr (SAMPLE) {
+    // bound of slot j: the first of the greedy order not drawn before j
+    int bi = K - 1;
+    for (int i = K - 1; i >= 0; --i) {
+      const int pid = lane_i32(zl.id, i);
+      bool used = false;
+      for (int s2 = 0; s2 < K - 1; ++s2) {
+        const int gid = lane_i32(gl.id, s2);
+        used |= (s2 < lane) && (gid == pid);
+      }
+      if (!used) bi = i;
+    }
+    zb = __shfl(zl.val, bi, 64);
+  }
+  if (lane < K) {
+    const int j = lane;
+    const float zpi = zl.val;
+    if (p.out.rank_token) p.out.rank_token[ob + j] = zl.id;
+    if (p.out.rank_log_q0) p.out.rank_log_q0[ob + j] = zpi - lse0;
+    if constexpr (!SAMPLE) {
+      const float lq0 = zpi - lse0;
+      const float ls = lsp + log_phat(lq0, a, bb);
+      p.out.child_token[ob + j] = zl.id;
+      p.out.child_log_q0[ob + j] = lq0;
+      p.out.child_log_surv[ob + j] = ls;
+      p.out.slot_key[ob + j] = ls;
+      if (p.out.child_log_qT) p.out.child_log_qT[ob + j] = __builtin_nanf("");
+    } else {
+      const float zc = gl.aux;
+      const float lq0 = zc - lse0;
+      p.out.child_token[ob + j] = gl.id;
+      p.out.child_log_q0[ob + j] = lq0;
+      p.out.child_log_surv[ob + j] = lsp + log_phat(lq0, a, bb);
+      p.out.slot_key[ob + j] = lsp + log_phat(zb - lse0, a, bb);
+      if (p.out.child_log_qT) p.out.child_log_qT[ob + j] = zc / p.T - lseT;
+    }
+  }
+  if (lane == 0) {
+    if (p.out.lse0) p.out.lse0[pidx] = lse0;
+    if (p.out.lseT) p.out.lseT[pidx] = lseT;
+#ifdef TS_DEBUG_RUNS
+    if (p.out.rank_log_q0) p.out.rank_log_q0[ob + K - 1] = (float)(clock64() - t_start);
+#endif
+    if (p.out.diag) p.out.diag[pidx] = mism;
+  }
+}
+
+}  // namespace ts
