@@ -9,9 +9,11 @@ the whole hot path over that batch:
      of every request): conditional logits on MFMA, log-sum-exp, top-k,
      k draws without replacement (sequential sampler by default), child
      scoring;
-  2. ts_build_tree: best-first trees for the 64 requests under their theta;
+  2. ts_build_tree: best-first trees for the 64 requests under their theta
+     (waves on the device; the trees come back to the host and stay on the
+     device);
   3. ts_tree_mask: the trees' attention masks and position ids for the
-     target's verification pass;
+     target's verification pass, from the device copy of the trees;
   4. ts_verify: recursive-rejection verification of those trees at T=0.7.
 value = node evaluations (frontier parents + tree-building parents) per
 second over the step.  The roofline object covers the dominant kernel (the
@@ -231,7 +233,11 @@ def main():
     log(f"frontier P={P}; natural trees: sizes {int(tree.n.min())}..{int(tree.n.max())}, "
         f"{tree_evals} evaluations")
 
-    mask_bufs = binding.TreeMaskBuffers(dr.R, N + 1)
+    # the trees also stay on the device, where ts_tree_mask reads them
+    dtree = binding.DeviceTree(dr.R, N + 1)
+    W = binding.lib().ts_tree_mask_words(N + 1)
+    mask_out = (torch.empty((dr.R, N + 1, W), dtype=torch.int32, device="cuda"),
+                torch.empty((dr.R, N + 1), dtype=torch.int32, device="cuda"))
     nsteps = args.steps + args.warmup
     ev = HipEvents(3 * nsteps)
 
@@ -241,8 +247,9 @@ def main():
                        sampler=sampler)
         if args.expand_only:
             return
-        binding.build_tree(d, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler)
-        binding.tree_mask_from_host(tree, buffers=mask_bufs)
+        binding.build_tree(d, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler,
+                           device_tree=dtree)
+        binding.tree_mask(dtree.parent, dtree.n, N + 1, out=mask_out)
         binding.verify(d, tree, tgt, T, seed, workspace=ws_v)
 
     for i in range(args.warmup):
@@ -266,8 +273,9 @@ def main():
             torch.cuda.synchronize(); a = time.perf_counter()
             binding.expand(dd, parents, P, K, T, seed, outputs=outs, workspace=ws_e, sampler=sampler)
             torch.cuda.synchronize(); b = time.perf_counter()
-            binding.build_tree(dd, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler)
-            binding.tree_mask_from_host(tree, buffers=mask_bufs)
+            binding.build_tree(dd, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler,
+                               device_tree=dtree)
+            binding.tree_mask(dtree.parent, dtree.n, N + 1, out=mask_out)
             torch.cuda.synchronize()
             c = time.perf_counter()
             binding.verify(dd, tree, tgt, T, seed, workspace=ws_v)

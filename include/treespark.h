@@ -171,6 +171,11 @@ typedef struct {
   int32_t* evals;      /* [R] optional (may be NULL): parents evaluated for the request */
 } ts_tree;
 
+/* Limits of the device-resident waves of ts_build_tree (larger trees use
+ * the host-driven waves). */
+#define TS_DEVICE_WAVES_MAX_N 512
+#define TS_DEVICE_WAVES_MAX_CHILDREN 1024
+
 size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, float T);
 
 /*
@@ -181,7 +186,7 @@ size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, f
  * when N nodes exist; a node at depth D gets no slot; a node re-offers a
  * slot for its next child until it has K children.  The result equals the
  * sequential heap of Algorithm 1; it is computed in breadth waves, each one
- * ts_expand call over all requests' pending parents.
+ * expansion over all requests' pending parents.
  * budget > 0 adds one node budget shared by all requests (§4, per-request
  * budget allocation by greedy water-filling): the trees then hold the best
  * `budget` nodes of all requests together in the order (key desc, request
@@ -189,14 +194,23 @@ size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, f
  * and stopped by its own theta.  Under one marginal price this is the theta
  * rule with theta_q raised to the key of the last node taken.  budget <= 0:
  * no shared budget.
- * anchor [R], theta [R] are HOST arrays.  out->cap must be >= N + 1 and
- * out->R == d->R.  sampler is a ts_sampler (used at T > 0).  Synchronises
- * `stream` once per wave.
+ * Where the waves run: with budget <= 0, 1 <= N <= TS_DEVICE_WAVES_MAX_N and
+ * max(1, N - 1) * K <= TS_DEVICE_WAVES_MAX_CHILDREN the waves and the tree
+ * assembly run on the device (a control kernel per wave keeps each request's
+ * best N slots and writes the next frontier; the host only reads each wave's
+ * size, one wave ahead of the GPU); otherwise the host keeps the slots and
+ * launches each wave.  Both give the same trees.
+ * anchor [R], theta [R] are HOST arrays.  out is a HOST tree: out->cap must
+ * be >= N + 1 and out->R == d->R; rows past n[q] are written with token and
+ * parent -1, depth and rank 0, path 0 and NaN values.  device_out (may be
+ * NULL) is a tree with the same R and cap whose arrays are DEVICE memory: it
+ * receives the same tree (for ts_tree_mask without a host round trip).
+ * sampler is a ts_sampler (used at T > 0).  Synchronises `stream`.
  */
 int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* theta, int32_t N,
                       int32_t budget, int32_t K, ts_calib calib, float T, uint64_t seed,
-                      int32_t sampler, ts_tree* out, void* workspace, size_t workspace_bytes,
-                      void* stream);
+                      int32_t sampler, ts_tree* out, const ts_tree* device_out, void* workspace,
+                      size_t workspace_bytes, void* stream);
 
 size_t ts_verify_workspace_size(const ts_drafter* d, int32_t cap, float T);
 

@@ -82,7 +82,7 @@ def lib():
         L.ts_expand.restype = I32
         L.ts_build_tree_workspace_size.argtypes = [P, I32, I32, F]
         L.ts_build_tree_workspace_size.restype = SZ
-        L.ts_build_tree.argtypes = [P, P, P, I32, I32, I32, Calib, F, U64, I32, P, P, SZ, P]
+        L.ts_build_tree.argtypes = [P, P, P, I32, I32, I32, Calib, F, U64, I32, P, P, P, SZ, P]
         L.ts_build_tree.restype = I32
         L.ts_verify_workspace_size.argtypes = [P, I32, F]
         L.ts_verify_workspace_size.restype = SZ
@@ -257,13 +257,35 @@ class HostTree:
         return Tree(self.R, self.cap, *[getattr(self, f).ctypes.data for f, _ in Tree._fields_[2:]])
 
 
+class DeviceTree:
+    """A tree in the ts_tree layout held in device memory (torch tensors; path as int64)."""
+
+    _INT = ("token", "parent", "depth", "rank")
+    _FLT = ("log_surv", "log_q0", "log_qT", "key")
+
+    def __init__(self, R, cap, device="cuda"):
+        torch = _torch()
+        self.R, self.cap = R, cap
+        self.n = torch.zeros(R, dtype=torch.int32, device=device)
+        self.evals = torch.zeros(R, dtype=torch.int32, device=device)
+        for f in self._INT:
+            setattr(self, f, torch.zeros((R, cap), dtype=torch.int32, device=device))
+        self.path = torch.zeros((R, cap), dtype=torch.int64, device=device)
+        for f in self._FLT:
+            setattr(self, f, torch.zeros((R, cap), dtype=torch.float32, device=device))
+
+    def struct(self):
+        return Tree(self.R, self.cap, *[getattr(self, f).data_ptr() for f, _ in Tree._fields_[2:]])
+
+
 def build_tree_workspace_size(d: DeviceDrafter, N, K, T):
     return lib().ts_build_tree_workspace_size(d.ref(), N, K, float(T))
 
 
 def build_tree(d: DeviceDrafter, anchor, theta, N, K, T, seed, calib=(0.67, -0.46), workspace=None,
-               stream=None, tree=None, sampler="gumbel", budget=0) -> HostTree:
-    """ts_build_tree: one tree per request; budget > 0 shares one node budget across requests."""
+               stream=None, tree=None, sampler="gumbel", budget=0, device_tree=None) -> HostTree:
+    """ts_build_tree: one tree per request; budget > 0 shares one node budget across requests.
+    device_tree (a DeviceTree of the same R and cap) also receives the tree in device memory."""
     torch = _torch()
     anchor = np.ascontiguousarray(anchor, dtype=np.int32)
     theta = np.ascontiguousarray(theta, dtype=np.float32)
@@ -273,8 +295,13 @@ def build_tree(d: DeviceDrafter, anchor, theta, N, K, T, seed, calib=(0.67, -0.4
         n = build_tree_workspace_size(d, N, K, T)
         workspace = torch.empty((max(n, 1),), dtype=torch.uint8, device=d.U.device)
     s = tree.struct()
+    ds = None
+    if device_tree is not None:
+        assert (device_tree.R, device_tree.cap) == (tree.R, tree.cap)
+        ds = device_tree.struct()
     rc = lib().ts_build_tree(d.ref(), anchor.ctypes.data, theta.ctypes.data, N, int(budget), K, Calib(*calib),
                              float(T), ctypes.c_uint64(seed), SAMPLERS[sampler], ctypes.byref(s),
+                             ctypes.byref(ds) if ds is not None else None,
                              ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream(stream))
     _check(rc)
     return tree

@@ -70,7 +70,15 @@ struct ExpandParams {
   int nblk;        // ceil(V / 64)
   int blk_ld;      // row stride of blk: nblk rounded up to a multiple of 16
   float* z_out;    // optional [P][V]: the logits themselves (verification recompute)
+  const int* P_dev;  // optional: the parent count in device memory (device-resident
+                     // tree waves); the grid and P are then an upper bound
 };
+
+// Parents of a launch: P, or the count the device holds (<= P).
+template <typename Params>
+__device__ __forceinline__ int launch_parents(const Params& p) {
+  return p.P_dev ? min(*p.P_dev, p.P) : p.P;
+}
 
 // Sampling modes of a launch: greedy (T = 0), Gumbel-top-k draws, sequential draws.
 enum : int { kModeGreedy = 0, kModeGumbel = 1, kModeSeq = 2 };
@@ -329,8 +337,9 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
   const int chunk = (b & 7) + 8 * (kx / p.n_pgroups);
   const int pgroup = kx % p.n_pgroups;
   if (chunk >= p.S) return;
+  const int P = launch_parents(p);
   const int pb = pgroup * p.wpg + wv;
-  if (pb >= p.n_pblocks) return;
+  if (pb * 16 * NB >= P) return;
 
   const TE* U = static_cast<const TE*>(p.U);
   const TE* E = static_cast<const TE*>(p.E);
@@ -348,7 +357,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
     pidx[nb] = (pb * NB + nb) * 16 + n;
     int tok = 0, dep = 0, req = 0;
     uint64_t path = 0;
-    if (pidx[nb] < p.P) {
+    if (pidx[nb] < P) {
       const ts_parent par = p.parents[pidx[nb]];
       if (par.token >= 0 && par.token < V && par.depth >= 0 && par.depth < p.D &&
           par.request >= 0 && par.request < p.R) {
@@ -416,7 +425,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[bb * 4 + e] = acc[bb][nb][e];
       if constexpr (STORE_Z) {
-        if (pidx[nb] < p.P) {
+        if (pidx[nb] < P) {
           float* zo = p.z_out + (size_t)pidx[nb] * V;
 #pragma unroll
           for (int j = 0; j < 16; ++j)
@@ -451,7 +460,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
         const float lb = p.need_T ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
         const int bi = t0 >> 6;
         bw[nb].put(bi, g, lb);
-        if (pidx[nb] < p.P) bw[nb].flush(p.blk + (size_t)pidx[nb] * p.blk_ld, bi, bfirst, blast, g);
+        if (pidx[nb] < P) bw[nb].flush(p.blk + (size_t)pidx[nb] * p.blk_ld, bi, bfirst, blast, g);
       }
       if constexpr (GUMBEL) {
         float gm = kNegInf;
@@ -527,7 +536,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
       top_combine(zc, top_shfl_xor(zc, o));
       if constexpr (GUMBEL) top_combine(gc, top_shfl_xor(gc, o));
     }
-    if (g == 0 && pidx[nb] < p.P) {
+    if (g == 0 && pidx[nb] < P) {
       const size_t o = (size_t)pidx[nb] * p.S + chunk;
       p.part_m[o] = M;
       p.part_s0[o] = s;
@@ -574,8 +583,10 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
   const int chunk = (b & 7) + 8 * (kx / p.n_pgroups);
   const int pgroup = kx % p.n_pgroups;
   if (chunk >= p.S) return;  // uniform over the workgroup
+  const int P = launch_parents(p);
+  if (pgroup * 4 * 16 * NB >= P) return;  // uniform: no parent in this workgroup
   const int pb = pgroup * 4 + wv;
-  const bool active = pb < p.n_pblocks;  // idle waves still load W2 and join the barriers
+  const bool active = pb * 16 * NB < P;  // idle waves still load W2 and join the barriers
 
   const uint16_t* U = static_cast<const uint16_t*>(p.U);
   const uint16_t* E = static_cast<const uint16_t*>(p.E);
@@ -591,7 +602,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
     pidx[nb] = (pb * NB + nb) * 16 + n;
     int tok = 0, dep = 0, req = 0;
     uint64_t path = 0;
-    if (active && pidx[nb] < p.P) {
+    if (active && pidx[nb] < P) {
       const ts_parent par = p.parents[pidx[nb]];
       if (par.token >= 0 && par.token < V && par.depth >= 0 && par.depth < p.D &&
           par.request >= 0 && par.request < p.R) {
@@ -707,7 +718,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
         const float lb = p.need_T ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
         const int bi = t0 >> 6;
         bw[nb].put(bi, g, lb);
-        if (pidx[nb] < p.P) bw[nb].flush(p.blk + (size_t)pidx[nb] * p.blk_ld, bi, bfirst, blast, g);
+        if (pidx[nb] < P) bw[nb].flush(p.blk + (size_t)pidx[nb] * p.blk_ld, bi, bfirst, blast, g);
       }
       if constexpr (GUMBEL) {
         float gm = kNegInf;
@@ -782,7 +793,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
       top_combine(zc, top_shfl_xor(zc, o));
       if constexpr (GUMBEL) top_combine(gc, top_shfl_xor(gc, o));
     }
-    if (g == 0 && pidx[nb] < p.P) {
+    if (g == 0 && pidx[nb] < P) {
       const size_t o = (size_t)pidx[nb] * p.S + chunk;
       p.part_m[o] = M;
       p.part_s0[o] = s;

@@ -4,6 +4,7 @@
 
 #include "merge_kernels.hpp"
 #include "verify_kernels.hpp"
+#include "wave_params.hpp"
 
 namespace ts {
 
@@ -27,6 +28,11 @@ void launch_verify_argmax(const void* target, bool bf16, int V, const int* rows,
 // Tree attention mask and position ids, one workgroup per request.
 void launch_tree_mask(const int32_t* parent, const int32_t* n, int R, int cap, const int32_t* pos_offset,
                       uint32_t* mask, int32_t* pos, hipStream_t s);
+// Device-resident tree waves: set-up, the control step after wave w's
+// expansion (one workgroup per request), the trees.
+void launch_wave_init(const WaveParams& wp, hipStream_t s);
+void launch_wave_control(const WaveParams& wp, int w, hipStream_t s);
+void launch_wave_tree(const WaveParams& wp, const WaveTreeOut& o, hipStream_t s);
 // One level of the T > 0 walk: pass A, stages 1..max(mmax, 1), bonus, resolve.
 void launch_verify_level(const VerifyPass& vp, bool bf16, int mmax, hipStream_t s);
 

@@ -28,6 +28,7 @@ struct MergeParams {
   float* blk;  // per-parent block table [P][blk_ld]; the draws update their own parent's rows
   int nblk, blk_ld;
   ts_expand_out out;
+  const int* P_dev;  // optional device-held parent count (<= P), as in ExpandParams
 };
 
 // ---------------------------------------------------------------- pass 2
@@ -565,7 +566,7 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   const int wv = threadIdx.x >> 6;
   const int n = lane & 15, g = lane >> 4;
   const int pidx = SEQ ? blockIdx.x : blockIdx.x * 4 + wv;
-  if (pidx >= p.P) return;  // uniform over the workgroup when SEQ
+  if (pidx >= launch_parents(p)) return;  // uniform over the workgroup when SEQ
 #ifdef TS_DEBUG_RUNS
   const long long t_start = clock64();
 #endif

@@ -170,15 +170,20 @@ int eval_blocks_per_cu(int dtype, int ks, int nb, int mode, bool store_z, bool l
 // sampler, so it assumes the largest chunk count and room for both samplers.
 static_assert(TS_MAX_V <= kMaxChunks * 4096, "the merge holds kMaxChunks chunks of <= 4096 tokens");
 
+// max_chunks: the most chunks the vocabulary allows (the plan of a launch
+// whose parent count is only bounded on the host: parallelism comes from the
+// chunks, and workgroups beyond the parents the device holds exit at once).
 Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = false,
-               bool sizing_only = false) {
+               bool sizing_only = false, bool max_chunks = false) {
   Plan pl{};
   pl.sample = T > 0.0f && !store_z;
   pl.mode = !pl.sample ? kModeGreedy : sampler == TS_SAMPLER_SEQUENTIAL ? kModeSeq : kModeGumbel;
   pl.nblk = (d->V + kBlkTokens - 1) / kBlkTokens;
   pl.blk_ld = ((pl.nblk + 15) / 16) * 16;
   pl.ks = d->dtype == TS_BF16 ? d->r / 32 : d->r / 4;
-  pl.NB = P >= 512 ? 2 : 1;
+  // two parent blocks per wave pay off only when the parents fill them; a
+  // bound on a device-held count (max_chunks) usually overstates them
+  pl.NB = (P >= 512 && !max_chunks) ? 2 : 1;
 #ifdef TS_FORCE_NB
   pl.NB = TS_FORCE_NB;
 #endif
@@ -191,7 +196,7 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
   // whole rounds (all workgroups of a round finish together), chunks of
   // 256..4096 tokens, at most kMaxChunks per parent.
   int vc;
-  if (sizing_only) {
+  if (sizing_only || max_chunks) {
     vc = 256;
   } else {
     const int concurrent = device_cus() *
@@ -315,12 +320,15 @@ ExpandParams eval_params(const ts_drafter* d, const ts_parent* parents, int P, f
 }
 
 // Both passes of one expansion; all arguments already checked.
+// P_dev (optional): the device holds the parent count (<= P); P then sizes
+// the grids and the plan takes the most chunks.
 int32_t run_expand(const ts_drafter* d, const ts_parent* parents, int P, ts_calib calib, int k,
                    float T, uint64_t seed, int sampler, const ts_expand_out* out, char* ws,
-                   hipStream_t s) {
+                   hipStream_t s, const int* P_dev = nullptr) {
   if (P == 0) return TS_OK;
-  const Plan pl = make_plan(d, P, T, sampler);
-  const ExpandParams ep = eval_params(d, parents, P, T, seed, pl, ws, nullptr);
+  const Plan pl = make_plan(d, P, T, sampler, false, false, P_dev != nullptr);
+  ExpandParams ep = eval_params(d, parents, P, T, seed, pl, ws, nullptr);
+  ep.P_dev = P_dev;
   hipEvent_t* ev = reinterpret_cast<hipEvent_t*>(out->events);
   if (ev) TS_HIP(hipEventRecord(ev[0], s));
   launch_eval(d, ep, pl, s);
@@ -343,6 +351,7 @@ int32_t run_expand(const ts_drafter* d, const ts_parent* parents, int P, ts_cali
   mp.nblk = ep.nblk;
   mp.blk_ld = ep.blk_ld;
   mp.out = *out;
+  mp.P_dev = P_dev;
   launch_merge(d, mp, pl, s);
   TS_HIP(hipGetLastError());
   if (ev) TS_HIP(hipEventRecord(ev[2], s));
@@ -382,21 +391,205 @@ inline bool global_before(const GlobalRef& a, const GlobalRef& b) {
   return a.path < b.path;
 }
 
+// A tree in the ts_tree layout packed into one block (device staging and
+// its host copy): n [R], evals [R], err, then token, parent, depth, rank
+// [R][cap] int32, path [R][cap] uint64, log_surv, log_q0, log_qT, key
+// [R][cap] float.
+struct TreeBlock {
+  size_t n, evals, err, token, parent, depth, rank, path, log_surv, log_q0, log_qT, key, bytes;
+};
+
+TreeBlock tree_block(int R, int cap) {
+  TreeBlock t{};
+  const size_t rc = (size_t)R * cap;
+  size_t o = 0;
+  t.n = o; o += align256((size_t)R * 4);
+  t.evals = o; o += align256((size_t)R * 4);
+  t.err = o; o += 256;
+  t.token = o; o += align256(rc * 4);
+  t.parent = o; o += align256(rc * 4);
+  t.depth = o; o += align256(rc * 4);
+  t.rank = o; o += align256(rc * 4);
+  t.path = o; o += align256(rc * 8);
+  t.log_surv = o; o += align256(rc * 4);
+  t.log_q0 = o; o += align256(rc * 4);
+  t.log_qT = o; o += align256(rc * 4);
+  t.key = o; o += align256(rc * 4);
+  t.bytes = o;
+  return t;
+}
+
 struct BuildLayout {
-  size_t off_par, off_out, off_exp, bytes;
+  size_t off_par, off_out, off_exp;
+  // device-resident waves
+  size_t off_par2, off_list, off_lsize, off_evals, off_pcount, off_span, off_anchor, off_ltheta, off_tree;
+  size_t bytes;
   int Pmax;
 };
 
 BuildLayout build_layout(const ts_drafter* d, int N, int K, float T) {
   BuildLayout b{};
-  b.Pmax = d->R * std::max(N, 1);
+  const int R = d->R;
+  b.Pmax = R * std::max(N, 1);
   const size_t pk = align256((size_t)b.Pmax * K * 4);
   size_t o = 0;
   b.off_par = o; o += align256((size_t)b.Pmax * sizeof(ts_parent));
   b.off_out = o; o += 5 * pk;  // child token, log q0, log qT, log S, key: [P][K] each, packed
   b.off_exp = o; o += expand_ws_max(d, b.Pmax, T);
+  b.off_par2 = o; o += align256((size_t)b.Pmax * sizeof(ts_parent));
+  b.off_list = o; o += align256((size_t)R * std::max(N, 1) * sizeof(WaveSlot));
+  b.off_lsize = o; o += align256((size_t)R * 4);
+  b.off_evals = o; o += align256((size_t)R * 4);
+  b.off_pcount = o; o += align256((size_t)(d->D + 2) * 4);
+  b.off_span = o; o += 2 * align256((size_t)R * sizeof(WaveSpan));
+  b.off_anchor = o; o += align256((size_t)R * 4);
+  b.off_ltheta = o; o += align256((size_t)R * 4);
+  b.off_tree = o; o += tree_block(R, N + 1).bytes;
   b.bytes = o;
   return b;
+}
+
+// The waves run on the device when the per-request lists fit the control
+// kernel and no budget is shared across requests.
+bool device_waves(int N, int K, int budget) {
+  return N >= 1 && budget <= 0 && N <= kWaveMaxN && std::max(1, N - 1) * K <= kWaveMaxNew;
+}
+
+WaveTreeOut tree_out_of(const ts_tree* t) {
+  WaveTreeOut o{};
+  o.cap = t->cap;
+  o.n = t->n; o.token = t->token; o.parent = t->parent; o.depth = t->depth; o.rank = t->rank;
+  o.path = t->path; o.log_surv = t->log_surv; o.log_q0 = t->log_q0; o.log_qT = t->log_qT;
+  o.key = t->key; o.evals = t->evals;
+  return o;
+}
+
+hipEvent_t* wave_events(int n) {
+  thread_local std::vector<hipEvent_t> ev;
+  while ((int)ev.size() < n) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
+    ev.push_back(e);
+  }
+  return ev.data();
+}
+
+// ts_build_tree with the waves on the device (no budget; N, K within the
+// control kernel's limits).  Wave w + 1 is queued before the host learns
+// its size (its kernels read the size the control step wrote), so the GPU
+// never waits for the host between waves; the host reads each wave's size
+// through an event and stops queueing at the first empty wave.
+int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std::vector<float>& log_theta,
+                          int N, int K, ts_calib calib, float T, uint64_t seed, int sampler, ts_tree* out,
+                          const ts_tree* device_out, char* ws, const BuildLayout& bl, hipStream_t s) {
+  const int R = d->R, D = d->D, cap = out->cap;
+  const TreeBlock tb = tree_block(R, cap);
+  char* hs = nullptr;
+  const size_t hs_up = align256((size_t)R * 8), hs_cnt = align256((size_t)(D + 2) * 4);
+  int32_t rc = host_stage(hs_up + hs_cnt + tb.bytes, &hs);
+  if (rc != TS_OK) return rc;
+  hipEvent_t* ev = wave_events(D + 2);
+  if (!ev) return fail(TS_EHIP, "hipEventCreate failed");
+  std::memcpy(hs, anchor, (size_t)R * 4);
+  std::memcpy(hs + (size_t)R * 4, log_theta.data(), (size_t)R * 4);
+  TS_HIP(hipMemcpyAsync(ws + bl.off_anchor, hs, (size_t)R * 4, hipMemcpyHostToDevice, s));
+  TS_HIP(hipMemcpyAsync(ws + bl.off_ltheta, hs + (size_t)R * 4, (size_t)R * 4, hipMemcpyHostToDevice, s));
+  volatile int32_t* hcnt = reinterpret_cast<volatile int32_t*>(hs + hs_up);
+  char* htree = hs + hs_up + hs_cnt;
+
+  WaveParams wp{};
+  wp.R = R; wp.N = N; wp.K = K; wp.D = D;
+  wp.anchor = reinterpret_cast<const int32_t*>(ws + bl.off_anchor);
+  wp.log_theta = reinterpret_cast<const float*>(ws + bl.off_ltheta);
+  wp.list = reinterpret_cast<WaveSlot*>(ws + bl.off_list);
+  wp.lsize = reinterpret_cast<int*>(ws + bl.off_lsize);
+  wp.evals = reinterpret_cast<int*>(ws + bl.off_evals);
+  wp.pcount = reinterpret_cast<int*>(ws + bl.off_pcount);
+  wp.err = reinterpret_cast<int*>(ws + bl.off_tree + tree_block(R, cap).err);
+  wp.par[0] = reinterpret_cast<ts_parent*>(ws + bl.off_par);
+  wp.par[1] = reinterpret_cast<ts_parent*>(ws + bl.off_par2);
+  wp.span[0] = reinterpret_cast<WaveSpan*>(ws + bl.off_span);
+  wp.span[1] = reinterpret_cast<WaveSpan*>(ws + bl.off_span + align256((size_t)R * sizeof(WaveSpan)));
+  const size_t nk = (size_t)bl.Pmax * K;
+  char* dout = ws + bl.off_out;
+  ts_expand_out eo{};
+  eo.child_token = reinterpret_cast<int32_t*>(dout);
+  eo.child_log_q0 = reinterpret_cast<float*>(dout + align256(nk * 4));
+  eo.child_log_qT = reinterpret_cast<float*>(dout + 2 * align256(nk * 4));
+  eo.child_log_surv = reinterpret_cast<float*>(dout + 3 * align256(nk * 4));
+  eo.slot_key = reinterpret_cast<float*>(dout + 4 * align256(nk * 4));
+  wp.child_token = eo.child_token;
+  wp.child_log_q0 = eo.child_log_q0;
+  wp.child_log_qT = eo.child_log_qT;
+  wp.child_log_surv = eo.child_log_surv;
+  wp.slot_key = eo.slot_key;
+  launch_wave_init(wp, s);
+  TS_HIP(hipGetLastError());
+
+  // queue wave w: expansion of par[w & 1] (at most Pub parents; the device
+  // holds the count), the control step, and the next wave's size to the host
+  auto queue_wave = [&](int w, int Pub) -> int32_t {
+    int32_t r = run_expand(d, wp.par[w & 1], Pub, calib, K, T, seed, sampler, &eo, ws + bl.off_exp, s,
+                           wp.pcount + w);
+    if (r != TS_OK) return r;
+    launch_wave_control(wp, w, s);
+    TS_HIP(hipGetLastError());
+    TS_HIP(hipMemcpyAsync((void*)(hcnt + w + 1), wp.pcount + w + 1, 4, hipMemcpyDeviceToHost, s));
+    TS_HIP(hipEventRecord(ev[w + 1], s));
+    return TS_OK;
+  };
+  const int per_req = std::max(0, N - 1);  // children a request can send to the next wave
+  int Pw = R;                              // size of wave w, known
+  if ((rc = queue_wave(0, R)) != TS_OK) return rc;
+  for (int w = 0;; ++w) {
+    const long long ub = std::min<long long>((long long)Pw * K, (long long)R * per_req);
+    if (w + 1 < D && ub > 0)
+      if ((rc = queue_wave(w + 1, (int)ub)) != TS_OK) return rc;
+    TS_HIP(hipEventSynchronize(ev[w + 1]));
+    const int Pn = hcnt[w + 1];
+    if (Pn <= 0 || w + 1 >= D || ub == 0) break;
+    if (Pn > ub) return fail(TS_EINTERNAL, "wave %d has %d parents, more than the bound %lld", w + 1, Pn, ub);
+    Pw = Pn;
+  }
+
+  // the trees: staging block, one copy to the host, and the caller's device arrays
+  char* dt = ws + bl.off_tree;
+  ts_tree st{};
+  st.R = R; st.cap = cap;
+  st.n = reinterpret_cast<int32_t*>(dt + tb.n);
+  st.evals = reinterpret_cast<int32_t*>(dt + tb.evals);
+  st.token = reinterpret_cast<int32_t*>(dt + tb.token);
+  st.parent = reinterpret_cast<int32_t*>(dt + tb.parent);
+  st.depth = reinterpret_cast<int32_t*>(dt + tb.depth);
+  st.rank = reinterpret_cast<int32_t*>(dt + tb.rank);
+  st.path = reinterpret_cast<uint64_t*>(dt + tb.path);
+  st.log_surv = reinterpret_cast<float*>(dt + tb.log_surv);
+  st.log_q0 = reinterpret_cast<float*>(dt + tb.log_q0);
+  st.log_qT = reinterpret_cast<float*>(dt + tb.log_qT);
+  st.key = reinterpret_cast<float*>(dt + tb.key);
+  launch_wave_tree(wp, tree_out_of(&st), s);
+  TS_HIP(hipGetLastError());
+  if (device_out) {
+    launch_wave_tree(wp, tree_out_of(device_out), s);
+    TS_HIP(hipGetLastError());
+  }
+  TS_HIP(hipMemcpyAsync(htree, dt, tb.bytes, hipMemcpyDeviceToHost, s));
+  TS_HIP(hipStreamSynchronize(s));
+  if (*reinterpret_cast<const int32_t*>(htree + tb.err) != 0)
+    return fail(TS_EINTERNAL, "a tree slot has no materialised parent");
+  const size_t rcn = (size_t)R * cap;
+  std::memcpy(out->n, htree + tb.n, (size_t)R * 4);
+  if (out->evals) std::memcpy(out->evals, htree + tb.evals, (size_t)R * 4);
+  std::memcpy(out->token, htree + tb.token, rcn * 4);
+  std::memcpy(out->parent, htree + tb.parent, rcn * 4);
+  std::memcpy(out->depth, htree + tb.depth, rcn * 4);
+  std::memcpy(out->rank, htree + tb.rank, rcn * 4);
+  std::memcpy(out->path, htree + tb.path, rcn * 8);
+  std::memcpy(out->log_surv, htree + tb.log_surv, rcn * 4);
+  std::memcpy(out->log_q0, htree + tb.log_q0, rcn * 4);
+  std::memcpy(out->log_qT, htree + tb.log_qT, rcn * 4);
+  std::memcpy(out->key, htree + tb.key, rcn * 4);
+  return TS_OK;
 }
 
 struct VerifyLayout {
@@ -487,8 +680,8 @@ size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, f
 
 int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* theta, int32_t N,
                       int32_t budget, int32_t K, ts_calib calib, float T, uint64_t seed,
-                      int32_t sampler, ts_tree* out, void* workspace, size_t workspace_bytes,
-                      void* stream) {
+                      int32_t sampler, ts_tree* out, const ts_tree* device_out, void* workspace,
+                      size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   int32_t rc = check_drafter(d);
   if (rc != TS_OK) return rc;
@@ -500,6 +693,11 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
       !out->log_surv || !out->log_q0 || !out->log_qT || !out->key)
     return fail(TS_EINVAL, "a tree array is NULL");
   if (out->R != d->R || out->cap < N + 1) return fail(TS_EINVAL, "tree has R=%d cap=%d, need R=%d cap>=%d", out->R, out->cap, d->R, N + 1);
+  if (device_out && (device_out->R != out->R || device_out->cap != out->cap || !device_out->n ||
+                     !device_out->token || !device_out->parent || !device_out->depth || !device_out->rank ||
+                     !device_out->path || !device_out->log_surv || !device_out->log_q0 ||
+                     !device_out->log_qT || !device_out->key))
+    return fail(TS_EINVAL, "device_out must have the R and cap of out and no NULL array");
   if (!std::isfinite(calib.a) || !std::isfinite(calib.b)) return fail(TS_EINVAL, "calibration must be finite");
   const int R = d->R;
   for (int q = 0; q < R; ++q) {
@@ -519,6 +717,8 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
 
   std::vector<float> log_theta(R);
   for (int q = 0; q < R; ++q) log_theta[q] = theta[q] > 0.0f ? logf(theta[q]) : -INFINITY;
+  if (device_waves(N, K, budget))
+    return build_tree_device(d, anchor, log_theta, N, K, calib, T, seed, sampler, out, device_out, ws, bl, s);
   std::vector<std::vector<Slot>> known(R);
   std::vector<ts_parent> frontier;
   std::vector<int32_t> evals(R, 0);
@@ -665,6 +865,33 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
     }
     out->n[q] = n;
     if (out->evals) out->evals[q] = evals[q];
+    for (int c = n + 1; c < cap; ++c) {  // rows past the tree, as the device waves leave them
+      out->token[b + c] = -1;
+      out->parent[b + c] = -1;
+      out->depth[b + c] = 0;
+      out->rank[b + c] = 0;
+      out->path[b + c] = 0;
+      out->log_surv[b + c] = NAN;
+      out->log_q0[b + c] = NAN;
+      out->log_qT[b + c] = NAN;
+      out->key[b + c] = NAN;
+    }
+  }
+  if (device_out) {
+    const size_t rcn = (size_t)R * cap;
+    const hipMemcpyKind h2d = hipMemcpyHostToDevice;
+    TS_HIP(hipMemcpyAsync(device_out->n, out->n, (size_t)R * 4, h2d, s));
+    if (device_out->evals && out->evals) TS_HIP(hipMemcpyAsync(device_out->evals, out->evals, (size_t)R * 4, h2d, s));
+    TS_HIP(hipMemcpyAsync(device_out->token, out->token, rcn * 4, h2d, s));
+    TS_HIP(hipMemcpyAsync(device_out->parent, out->parent, rcn * 4, h2d, s));
+    TS_HIP(hipMemcpyAsync(device_out->depth, out->depth, rcn * 4, h2d, s));
+    TS_HIP(hipMemcpyAsync(device_out->rank, out->rank, rcn * 4, h2d, s));
+    TS_HIP(hipMemcpyAsync(device_out->path, out->path, rcn * 8, h2d, s));
+    TS_HIP(hipMemcpyAsync(device_out->log_surv, out->log_surv, rcn * 4, h2d, s));
+    TS_HIP(hipMemcpyAsync(device_out->log_q0, out->log_q0, rcn * 4, h2d, s));
+    TS_HIP(hipMemcpyAsync(device_out->log_qT, out->log_qT, rcn * 4, h2d, s));
+    TS_HIP(hipMemcpyAsync(device_out->key, out->key, rcn * 4, h2d, s));
+    TS_HIP(hipStreamSynchronize(s));
   }
   return TS_OK;
 }

@@ -1,0 +1,59 @@
+// Parameter blocks of the device-resident tree waves (kernels in wave_kernels.hpp).
+#pragma once
+
+#include "device_common.hpp"
+
+namespace ts {
+
+constexpr int kWaveThreads = 256;
+constexpr int kWaveMaxN = TS_DEVICE_WAVES_MAX_N;  // list capacity per request (N)
+constexpr int kWaveMaxNew = TS_DEVICE_WAVES_MAX_CHILDREN;  // children of a request in one wave
+
+struct WaveSlot {  // 32 bytes
+  float key;       // slot key: the pop priority
+  int depth;       // depth of the child the slot creates
+  uint64_t path;   // the child's structural path id
+  int token;
+  float log_surv, log_q0, log_qT;
+};
+
+struct WaveSpan {  // a request's rows in a wave's frontier
+  int off, cnt;
+};
+
+struct WaveParams {
+  int R, N, K, D;
+  const int32_t* anchor;   // [R] root tokens
+  const float* log_theta;  // [R] log(theta_q), -inf for theta = 0
+  WaveSlot* list;          // [R][N] best known slots with key >= log(theta), pop order
+  int* lsize;              // [R] entries of list in use
+  int* evals;              // [R] parents evaluated so far
+  int* pcount;             // [D + 2] frontier size of each wave (wave w: pcount[w])
+  int* err;                // tree assembly: slots whose parent is not listed
+  ts_parent* par[2];       // frontier of wave w in par[w & 1]
+  WaveSpan* span[2];       // [R] rows of each request in par[w & 1]
+  // outputs of the current wave's expansion, [P][K] row-major
+  const int32_t* child_token;
+  const float* child_log_q0;
+  const float* child_log_qT;
+  const float* child_log_surv;
+  const float* slot_key;
+};
+
+// A tree in the ts_tree layout, device arrays.
+struct WaveTreeOut {
+  int cap;
+  int32_t* n;
+  int32_t* token;
+  int32_t* parent;
+  int32_t* depth;
+  int32_t* rank;
+  uint64_t* path;
+  float* log_surv;
+  float* log_q0;
+  float* log_qT;
+  float* key;
+  int32_t* evals;  // may be null
+};
+
+}  // namespace ts

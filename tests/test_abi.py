@@ -83,9 +83,10 @@ def test_build_tree_rejects_bad_arguments():
     anchor = np.array([1, 2], np.int32)
     theta = np.array([0.0, 0.1], np.float32)
 
-    def call(anchor=anchor, theta=theta, N=8, K=2, T=0.0, ws=1 << 30, st=s, sampler=1):
+    def call(anchor=anchor, theta=theta, N=8, K=2, T=0.0, ws=1 << 30, st=s, sampler=1, dev=None):
         return L.ts_build_tree(ctypes.byref(d), anchor.ctypes.data, theta.ctypes.data, N, 0, K,
-                               b.Calib(0.67, -0.46), T, 0, sampler, ctypes.byref(st), FAKE, ws, None)
+                               b.Calib(0.67, -0.46), T, 0, sampler, ctypes.byref(st),
+                               ctypes.byref(dev) if dev is not None else None, FAKE, ws, None)
 
     assert call(anchor=np.array([1, 5000], np.int32)) == b.TS_EINVAL
     assert call(theta=np.array([0.0, -0.1], np.float32)) == b.TS_EINVAL
@@ -96,6 +97,11 @@ def test_build_tree_rejects_bad_arguments():
     assert call(ws=8) == b.TS_ENOSPACE
     bad = b.HostTree.empty(3, 9).struct()
     assert call(st=bad) == b.TS_EINVAL
+    # a device tree must match out's R and cap and have every array
+    assert call(dev=b.HostTree.empty(2, 10).struct()) == b.TS_EINVAL
+    nulls = b.HostTree.empty(2, 9).struct()
+    nulls.key = None
+    assert call(dev=nulls) == b.TS_EINVAL
 
 
 def test_verify_rejects_malformed_trees():

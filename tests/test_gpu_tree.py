@@ -7,7 +7,7 @@ from scipy import special, stats
 
 from oracle import oracle as o
 from paper_2609_22098_amd import synth
-from helpers import TIE, Tally, compare_tree
+from helpers import TIE, Tally, close, compare_tree, tree_compare_limit, value_tol
 
 pytestmark = pytest.mark.gpu
 
@@ -183,13 +183,13 @@ def test_verify_parity_multi_request(torch, T):
 
 @pytest.mark.parametrize("sampler", ["gumbel", "sequential"])
 def test_verify_losslessness_chi_square(torch, sampler):
-    """Proposition 1 on the GPU: 60000 replicate requests (independent Philox streams through the
+    """Proposition 1 on the GPU: 1e5 replicate requests (independent Philox streams through the
     request field) build sampled trees and verify them against prefix-keyed target rows; the first
     emitted token follows softmax(target_root / T) and the token after an accepted child x follows
     softmax(target_x / T).  Both realisations of the draws."""
     from paper_2609_22098_amd import binding
     import itertools
-    V, D, K, N, T, R = 6, 3, 3, 7, 1.0, 60000
+    V, D, K, N, T, R = 6, 3, 3, 7, 1.0, 100_000
     base = synth.make_drafter(V, D, 16, R=1, dtype="f32", u_sigma=0.8, planted=None, zipf=None,
                               ew_sigma=0.6, seed=41)
     U = np.repeat(base.U32, R, axis=0)
@@ -275,3 +275,73 @@ def test_shared_budget_serving(torch):
     dd = binding.drafter_from_host(dr)
     tree = binding.build_tree(dd, anchors, thetas, 16, 8, 0.7, 0, sampler="sequential", budget=300)
     _forest_compare(dr, tree, anchors, thetas, 16, 300, 8, 0.7, 0, "sequential", "serving budget 300")
+
+
+# ---------------------------------------------------------------- where the waves run
+
+@pytest.mark.parametrize("T,sampler", [(0.0, "gumbel"), (1.0, "sequential"), (0.5, "gumbel")])
+def test_device_waves_equal_host_waves(torch, T, sampler):
+    """The device-resident waves (no budget) and the host-driven waves (a shared budget too large to
+    bind) build the same trees: topology identical up to the oracle's first near-tie, values within
+    the rounding of their different vocabulary chunkings; both match the oracle."""
+    from paper_2609_22098_amd import binding
+    dr = synth.make_drafter(3000, 8, 32, R=6, dtype="bf16", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
+                            ew_sigma=0.3, seed=3, u_scale=3.0)
+    anchors, _, _ = synth.make_controls(6, dr.V, 0.0, seed=3)
+    thetas = np.array([0.0, 0.01, 0.0, 0.005, 0.0, 0.02], np.float32)
+    N, K, seed = 24, 3, 9
+    dd = binding.drafter_from_host(dr)
+    dev = binding.build_tree(dd, anchors, thetas, N, K, T, seed, sampler=sampler)
+    host = binding.build_tree(dd, anchors, thetas, N, K, T, seed, sampler=sampler, budget=dr.R * N + 1)
+    om = o.Model(dr.U32, dr.E32, dr.W2_32)
+    tol = value_tol(dr.dtype)
+    for q in range(dr.R):
+        ref = o.expand_tree(om, q, int(anchors[q]), float(thetas[q]), N, K, T, seed, sampler=sampler)
+        limit, ties = tree_compare_limit(ref, float(thetas[q]), T)
+        if ties == 0:
+            assert int(dev.n[q]) == int(host.n[q]) == ref.n
+        upto = min(limit, int(dev.n[q]) + 1, int(host.n[q]) + 1)
+        for f in ("token", "parent", "depth", "rank", "path"):
+            assert list(getattr(dev, f)[q, :upto]) == list(getattr(host, f)[q, :upto]), (q, f)
+        for f in ("log_surv", "log_q0", "key"):
+            for c in range(1, upto):
+                assert close(getattr(dev, f)[q, c], getattr(host, f)[q, c], tol), (q, f, c)
+        assert int(dev.evals[q]) == int(host.evals[q]) or ties > 0
+    _compare_all(dr, dev, anchors, thetas, N, K, T, seed, tag=f"device waves T={T}", sampler=sampler)
+
+
+def test_device_tree_output_and_mask(torch):
+    """device_tree receives the same tree as the host copy, and ts_tree_mask on it equals the mask of
+    the uploaded host tree (the serving workload, T = 0.7, sequential draws)."""
+    from paper_2609_22098_amd import binding
+    w = synth.WORKLOADS[3]
+    dr = synth.make_workload_drafter(3, seed=0)
+    anchors, thetas, _ = synth.make_controls(dr.R, dr.V, w["theta"], seed=0)
+    dd = binding.drafter_from_host(dr)
+    cap = w["N"] + 1
+    dtree = binding.DeviceTree(dr.R, cap)
+    tree = binding.build_tree(dd, anchors, thetas, w["N"], w["K"], 0.7, 0, sampler="sequential",
+                              device_tree=dtree)
+    assert np.array_equal(dtree.n.cpu().numpy(), tree.n)
+    assert np.array_equal(dtree.evals.cpu().numpy(), tree.evals)
+    for f in ("token", "parent", "depth", "rank"):
+        assert np.array_equal(getattr(dtree, f).cpu().numpy(), getattr(tree, f)), f
+    assert np.array_equal(dtree.path.cpu().numpy().view(np.uint64), tree.path)
+    for f in ("log_surv", "log_q0", "log_qT", "key"):
+        assert np.array_equal(getattr(dtree, f).cpu().numpy(), getattr(tree, f), equal_nan=True), f
+    m_dev, p_dev = binding.tree_mask(dtree.parent, dtree.n, cap)
+    m_host, p_host = binding.tree_mask_from_host(tree)
+    torch.cuda.synchronize()
+    assert torch.equal(m_dev, m_host) and torch.equal(p_dev, p_host)
+    print(f"device tree: sizes {int(tree.n.min())}..{int(tree.n.max())}, evaluations {int(tree.evals.sum())}")
+
+
+def test_host_waves_beyond_device_limits(torch):
+    """N = 600 exceeds the device waves' list capacity, so the host drives the waves; the tiny
+    workload (V=4096, D=8, fp32), K=3, theta=0, T=1, against the oracle."""
+    dr = synth.make_workload_drafter(0, seed=0)
+    anchors, _, _ = synth.make_controls(1, dr.V, 0.0, seed=0)
+    thetas = np.zeros(1, np.float32)
+    _, tree = _trees(dr, anchors, thetas, 600, 3, 1.0, 4, sampler="sequential")
+    _compare_all(dr, tree, anchors, thetas, 600, 3, 1.0, 4, tag="host waves N=600", sampler="sequential")
+    assert tree.n[0] == 600
