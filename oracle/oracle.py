@@ -5,7 +5,8 @@ cpu_baseline leg may import this module.  It shares no code with the HIP path.
 
 Every function works on numpy arrays in host memory.  Float inputs are the
 exact values the GPU path sees (bf16 inputs are passed as the float32 values
-they represent); the arithmetic is fp64.
+they represent); the arithmetic is fp64.  The calibration functions (greedy
+labels and the two-scalar Platt fit of §3.4 Eq. 3) are written here in numpy.
 """
 from __future__ import annotations
 
@@ -298,3 +299,72 @@ def expand_forest(model: Model, anchors, thetas, N, budget, K, T, seed, a=0.67, 
                      "margin", "eval_gap"):
             setattr(t, name, getattr(t, name)[:n1].copy())
     return trees
+
+
+# ---------------------------------------------------------------- calibration (§3.4 Eq. 3)
+
+def logit_q0(log_q0):
+    """logit q0 = log q0 - log(1 - q0) from log q0, fp64; +inf where q0 == 1."""
+    lq = np.asarray(log_q0, dtype=np.float64)
+    out = np.full(lq.shape, np.inf)
+    m = lq < 0.0
+    l = lq[m]
+    # log(1 - q0) = log1mexp(log q0), two-branch form (Maechler 2012)
+    l1m = np.where(l > -np.log(2.0), np.log(-np.expm1(np.minimum(l, -1e-300))), np.log1p(-np.exp(l)))
+    out[m] = l - l1m
+    return out
+
+
+def calib_labels(parent, token, n, target):
+    """The greedy labels of one tree (§3.4): the verifier shows, for every node, whether its token is
+    the target's greedy choice at its parent.  y[i] = 1 iff token[i] is the argmax (smallest id on
+    ties) of the target row of parent[i]; sel[i] = 1 iff every edge on the root path of parent[i]
+    has y = 1 (the ancestors-accepted population the two scalars are fitted on).  Row 0 and rows
+    past n: y = -1, sel = 0.  Parents precede their children."""
+    cap = len(parent)
+    y = np.full(cap, -1, np.int32)
+    sel = np.zeros(cap, np.int32)
+    greedy = [int(np.argmax(np.asarray(target[i], dtype=np.float64))) for i in range(n + 1)]
+    path_ok = np.zeros(cap, bool)  # every edge on the root path of node i accepted
+    path_ok[0] = True
+    for i in range(1, n + 1):
+        p = int(parent[i])
+        y[i] = 1 if int(token[i]) == greedy[p] else 0
+        sel[i] = 1 if path_ok[p] else 0
+        path_ok[i] = path_ok[p] and y[i] == 1
+    return y, sel
+
+
+def _nll(a, b, x, y):
+    z = a * x + b
+    return float(np.sum(np.logaddexp(0.0, z) - y * z))
+
+
+def platt_fit(x, y, max_iter=100, tol=1e-10):
+    """Maximum-likelihood (a, b) of y ~ Bernoulli(sigmoid(a x + b)): the two-scalar map of Eq. 3.
+    Newton's method on the log-likelihood from (0, 0); a step that raises the negative
+    log-likelihood is halved until it does not.  fp64.  Returns (a, b, mean negative
+    log-likelihood, Newton steps taken)."""
+    x = np.asarray(x, dtype=np.float64)
+    y = np.asarray(y, dtype=np.float64)
+    a = b = 0.0
+    f = _nll(a, b, x, y)
+    steps = 0
+    for steps in range(1, max_iter + 1):
+        p = 1.0 / (1.0 + np.exp(-(a * x + b)))
+        r = p - y
+        w = p * (1.0 - p)
+        g = np.array([np.sum(r * x), np.sum(r)])
+        H = np.array([[np.sum(w * x * x), np.sum(w * x)], [np.sum(w * x), np.sum(w)]])
+        da, db = np.linalg.solve(H, g)
+        t = 1.0
+        while True:
+            fa, fb = a - t * da, b - t * db
+            fc = _nll(fa, fb, x, y)
+            if fc <= f or t < 2.0 ** -30:
+                break
+            t *= 0.5
+        a, b, f = fa, fb, fc
+        if max(abs(t * da), abs(t * db)) < tol:
+            break
+    return a, b, f / max(len(x), 1), steps

@@ -702,3 +702,74 @@ def test_forest_is_a_uniform_price():
         th = max(thetas[q], math.exp(last))
         ref = o.expand_tree(m, q, anchors[q], th, 30, 3, 0.0, 2)
         assert trees[q].n == ref.n and list(trees[q].token) == list(ref.token), q
+
+
+# ---------------------------------------------------------------- calibration fit (§3.4 Eq. 3)
+
+def test_logit_q0_closed_forms():
+    """logit q0 = log(q0 / (1 - q0)): 0 at q0 = 1/2, log 9 at 0.9, -log 999 at 0.001, +inf at 1;
+    the two branches of log(1 - q0) meet at q0 = 1/2."""
+    lq = np.log(np.array([0.5, 0.9, 0.001, 1.0, 0.5 - 1e-12, 0.5 + 1e-12]))
+    got = o.logit_q0(lq)
+    assert got[0] == pytest.approx(0.0, abs=1e-15)
+    assert got[1] == pytest.approx(math.log(9.0), rel=1e-13)
+    assert got[2] == pytest.approx(-math.log(999.0), rel=1e-13)
+    assert got[3] == math.inf
+    assert abs(got[4]) < 1e-11 and abs(got[5]) < 1e-11
+
+
+def test_calib_labels_on_a_hand_tree():
+    """Root 0; nodes 1, 2 under the root, 3 under 1, 4 under 3, 5 under 2.  The target's greedy
+    choices: row 0 -> token of node 1, row 1 -> not the token of node 3, row 3 -> token of node 4,
+    row 2 -> token of node 5 (a tie broken toward the smaller id).  Accepted edges: 1, 4, 5;
+    ancestors-accepted edges: 1, 2 (root children) and 3 (under the accepted 1)."""
+    parent = np.array([-1, 0, 0, 1, 3, 2, -1], np.int32)
+    token = np.array([9, 4, 6, 2, 7, 1, -1], np.int32)
+    V = 10
+    target = np.zeros((7, V))
+    target[0, 4] = 3.0             # greedy 4 = token of node 1
+    target[1, 5] = 2.0             # greedy 5, node 3 has token 2
+    target[3, 7] = 1.0             # greedy 7 = token of node 4
+    target[2, 1] = target[2, 8] = 5.0  # tie: smallest id 1 = token of node 5
+    y, sel = o.calib_labels(parent, token, 5, target)
+    assert list(y) == [-1, 1, 0, 0, 1, 1, -1]
+    assert list(sel) == [0, 1, 1, 1, 0, 0, 0]
+
+
+def test_platt_fit_saturated_closed_form():
+    """Two distinct inputs with acceptance frequencies f1, f2: the maximum-likelihood map passes
+    through both, a = (logit f1 - logit f2) / (x1 - x2), b = logit f1 - a x1."""
+    x1, x2, n1, k1, n2, k2 = 1.5, -0.5, 400, 300, 600, 150
+    x = np.r_[np.full(n1, x1), np.full(n2, x2)]
+    y = np.r_[np.ones(k1), np.zeros(n1 - k1), np.ones(k2), np.zeros(n2 - k2)]
+    lg = lambda f: math.log(f / (1 - f))
+    a_ref = (lg(k1 / n1) - lg(k2 / n2)) / (x1 - x2)
+    b_ref = lg(k1 / n1) - a_ref * x1
+    a, b, _, _ = o.platt_fit(x, y)
+    assert a == pytest.approx(a_ref, rel=1e-9) and b == pytest.approx(b_ref, rel=1e-9)
+
+
+def test_platt_fit_equals_unpenalised_logistic_regression():
+    """The fit is the unpenalised logistic regression of y on x (scikit-learn's solver), and the score
+    equations sum(p - y) = 0, sum((p - y) x) = 0 hold at it."""
+    from sklearn.linear_model import LogisticRegression
+    rng = np.random.default_rng(5)
+    x = rng.normal(-1.0, 2.5, 20000)
+    y = (rng.random(20000) < 1.0 / (1.0 + np.exp(-(0.8 * x + 0.3)))).astype(float)
+    a, b, nll, steps = o.platt_fit(x, y)
+    m = LogisticRegression(penalty=None, tol=1e-12, max_iter=10000).fit(x[:, None], y)
+    assert a == pytest.approx(float(m.coef_[0, 0]), rel=1e-6)
+    assert b == pytest.approx(float(m.intercept_[0]), rel=1e-6, abs=1e-8)
+    p = 1.0 / (1.0 + np.exp(-(a * x + b)))
+    assert abs(np.sum(p - y)) < 1e-7 * len(x) and abs(np.sum((p - y) * x)) < 1e-7 * len(x)
+    assert steps < 20 and 0.0 < nll < math.log(2.0)
+
+
+def test_platt_fit_recovers_the_papers_coefficients():
+    """Labels drawn from the paper's map sigma(0.67 logit q0 - 0.46) over 2e5 edges give back
+    (0.67, -0.46) within five standard errors (about 0.005 each here)."""
+    rng = np.random.default_rng(11)
+    x = rng.normal(0.5, 2.0, 200_000)
+    y = (rng.random(len(x)) < 1.0 / (1.0 + np.exp(-(0.67 * x - 0.46)))).astype(float)
+    a, b, _, _ = o.platt_fit(x, y)
+    assert abs(a - 0.67) < 0.025 and abs(b + 0.46) < 0.03
