@@ -306,6 +306,54 @@ int32_t ts_tree_mask_words(int32_t cap);
 int32_t ts_tree_mask(const int32_t* parent, const int32_t* n, int32_t R, int32_t cap,
                      const int32_t* pos_offset, uint32_t* mask, int32_t* pos, void* stream);
 
+/*
+ * Calibration of the edge-acceptance estimate (§3.4 Eq. 3): the labels a
+ * greedy (T = 0) round produces, and the two-scalar Platt fit
+ * p-hat = sigmoid(a logit q0 + b).  In a greedy round the verifier shows, for
+ * every materialised node, whether its token is the target's greedy choice
+ * at its parent; the fit uses the edges whose ancestors were all accepted
+ * (the population that path-survival products condition on).  A deployment
+ * fits the two scalars once per drafter-target pair.
+ */
+
+/* Bytes of device workspace ts_calib_labels needs for R requests of capacity cap. */
+size_t ts_calib_labels_workspace_size(int32_t R, int32_t cap);
+
+/*
+ * ts_calib_labels: tree is a HOST tree (ts_build_tree's out) of R requests
+ * and capacity cap; target is a DEVICE array [R][cap][V] of target_dtype
+ * (row i: the target's next-token logits after node i's root path).  For
+ * every request q and node 1 <= i <= n[q] it writes, to DEVICE arrays
+ * [R][cap]:
+ *   x[q][i]   = logit q0 = log q0 - log(1 - q0) of the node (from
+ *               tree->log_q0; +inf where q0 == 1);
+ *   y[q][i]   = 1 if the node's token is the argmax (smallest id on ties) of
+ *               the target row of its parent, else 0;
+ *   sel[q][i] = 1 if every edge on the root path of its parent has y = 1.
+ * Row 0 and rows past n[q] get x NaN, y -1, sel 0.  Host checks: null
+ * pointers, R >= 1, the tree's shape (0 <= n < cap, parents before
+ * children, tokens in [0, V)), target_dtype, workspace size.  Synchronises
+ * `stream`.
+ */
+int32_t ts_calib_labels(const ts_tree* tree, const void* target, int32_t target_dtype, int32_t V, float* x,
+                        int32_t* y, int32_t* sel, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * ts_calib_fit: the maximum-likelihood (a, b) of y ~ Bernoulli(sigmoid(a x +
+ * b)) over the samples i < n with sel[i] = 1, y[i] in {0, 1} and x[i]
+ * finite (x, y, sel: DEVICE arrays in the ts_calib_labels layout, flattened).
+ * Newton's method from (0, 0); a step that raises the negative
+ * log-likelihood is halved until it does not; at most max_iter steps,
+ * stopping when a step moves both scalars by less than tol.  Sums are fp64
+ * in a fixed order.  out: DEVICE float[4] = {a, b, mean negative
+ * log-likelihood, steps}; a, b and the likelihood are NaN when no sample
+ * takes part or the curvature is singular (a single input value), and a
+ * separable sample keeps growing until max_iter.  Asynchronous on
+ * `stream`.  Host checks: null pointers, n >= 0, max_iter >= 1, tol > 0.
+ */
+int32_t ts_calib_fit(const float* x, const int32_t* y, const int32_t* sel, int32_t n, int32_t max_iter,
+                     double tol, float* out, void* stream);
+
 /* Description of the last error on the calling thread ("" if none). */
 const char* ts_last_error(void);
 

@@ -23,7 +23,8 @@ TS_MAX_K, TS_MAX_D = 16, 16
 SAMPLERS = {"gumbel": 0, "sequential": 1}  # ts_sampler
 EXPORTED = ("ts_ladder_lookup", "ts_ladder_default", "ts_tree_mask_words", "ts_tree_mask",
             "ts_expand_workspace_size", "ts_expand", "ts_build_tree_workspace_size", "ts_build_tree",
-            "ts_verify_workspace_size", "ts_verify", "ts_last_error", "ts_version")
+            "ts_verify_workspace_size", "ts_verify", "ts_calib_labels_workspace_size", "ts_calib_labels",
+            "ts_calib_fit", "ts_last_error", "ts_version")
 
 
 class TreeSparkError(RuntimeError):
@@ -88,6 +89,12 @@ def lib():
         L.ts_verify_workspace_size.restype = SZ
         L.ts_verify.argtypes = [P, P, P, I32, F, U64, P, P, P, P, SZ, P]
         L.ts_verify.restype = I32
+        L.ts_calib_labels_workspace_size.argtypes = [I32, I32]
+        L.ts_calib_labels_workspace_size.restype = SZ
+        L.ts_calib_labels.argtypes = [P, P, I32, I32, P, P, P, P, SZ, P]
+        L.ts_calib_labels.restype = I32
+        L.ts_calib_fit.argtypes = [P, P, P, I32, I32, ctypes.c_double, P, P]
+        L.ts_calib_fit.restype = I32
         L.ts_ladder_lookup.argtypes = [P, I32, I32, F, I32, I32, I32, P]
         L.ts_ladder_lookup.restype = I32
         L.ts_ladder_default.argtypes = [P, I32]
@@ -391,6 +398,45 @@ def tree_mask_from_host(tree: HostTree, pos_offset=None, device="cuda", stream=N
     parent, n = buf.upload(tree, stream)
     off = None if pos_offset is None else torch.from_numpy(np.ascontiguousarray(pos_offset, np.int32)).to(device)
     return tree_mask(parent, n, tree.cap, off, stream, out=buf.out)
+
+
+def calib_labels(tree: HostTree, target, workspace=None, stream=None):
+    """ts_calib_labels: greedy labels of a round's trees.  target: device tensor [R][cap][V]
+    (float32 or bfloat16).  Returns device tensors (x [R][cap] float32 = logit q0,
+    y [R][cap] int32, sel [R][cap] int32)."""
+    torch = _torch()
+    R, cap = tree.R, tree.cap
+    assert target.dim() == 3 and tuple(target.shape[:2]) == (R, cap) and target.is_contiguous()
+    dev = target.device
+    x = torch.empty((R, cap), dtype=torch.float32, device=dev)
+    y = torch.empty((R, cap), dtype=torch.int32, device=dev)
+    sel = torch.empty((R, cap), dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty((lib().ts_calib_labels_workspace_size(R, cap),), dtype=torch.uint8, device=dev)
+    s = tree.struct()
+    rc = lib().ts_calib_labels(ctypes.byref(s), ctypes.c_void_p(target.data_ptr()), _dtype_code(target),
+                               int(target.shape[2]), ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()),
+                               ctypes.c_void_p(sel.data_ptr()), ctypes.c_void_p(workspace.data_ptr()),
+                               workspace.numel(), _stream(stream))
+    _check(rc)
+    return x, y, sel
+
+
+def calib_fit(x, y, sel, max_iter=100, tol=1e-10, stream=None):
+    """ts_calib_fit over device tensors x (float32), y, sel (int32) of equal size.
+    Returns (a, b, mean negative log-likelihood, steps) as Python numbers."""
+    torch = _torch()
+    n = x.numel()
+    assert y.numel() == n and sel.numel() == n
+    assert x.dtype == torch.float32 and y.dtype == torch.int32 and sel.dtype == torch.int32
+    assert x.is_contiguous() and y.is_contiguous() and sel.is_contiguous()
+    out = torch.empty(4, dtype=torch.float32, device=x.device)
+    rc = lib().ts_calib_fit(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()),
+                            ctypes.c_void_p(sel.data_ptr()), n, int(max_iter), float(tol),
+                            ctypes.c_void_p(out.data_ptr()), _stream(stream))
+    _check(rc)
+    a, b, nll, steps = out.cpu().tolist()
+    return a, b, nll, int(steps)
 
 
 class LadderRung(ctypes.Structure):

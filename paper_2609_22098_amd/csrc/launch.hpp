@@ -33,6 +33,12 @@ void launch_tree_mask(const int32_t* parent, const int32_t* n, int R, int cap, c
 void launch_wave_init(const WaveParams& wp, hipStream_t s);
 void launch_wave_control(const WaveParams& wp, int w, hipStream_t s);
 void launch_wave_tree(const WaveParams& wp, const WaveTreeOut& o, hipStream_t s);
+// Calibration: greedy labels of host-built trees, and the two-scalar fit.
+void launch_calib_labels(const int32_t* parent, const int32_t* token, const float* log_q0, const int32_t* n,
+                         int R, int cap, const int32_t* greedy, const int32_t* off, float* x, int32_t* y,
+                         int32_t* sel, hipStream_t s);
+void launch_calib_fit(const float* x, const int32_t* y, const int32_t* sel, int n, int max_iter, double tol,
+                      float* out, hipStream_t s);
 // One level of the T > 0 walk: pass A, stages 1..max(mmax, 1), bonus, resolve.
 void launch_verify_level(const VerifyPass& vp, bool bf16, int mmax, hipStream_t s);
 

@@ -1104,6 +1104,96 @@ int32_t ts_ladder_default(ts_ladder_rung* rungs, int32_t cap) {
   return count;
 }
 
+// ---------------------------------------------------------------- calibration
+
+namespace {
+struct CalibLayout {
+  size_t parent, token, log_q0, n, rows, off, upload, greedy, gap, bytes;
+};
+CalibLayout calib_layout(int R, int cap) {
+  CalibLayout c{};
+  const size_t rc = (size_t)R * cap;
+  size_t o = 0;
+  c.parent = o; o += align256(rc * 4);
+  c.token = o; o += align256(rc * 4);
+  c.log_q0 = o; o += align256(rc * 4);
+  c.n = o; o += align256((size_t)R * 4);
+  c.rows = o; o += align256(rc * 4);
+  c.off = o; o += align256((size_t)R * 4);
+  c.upload = o;  // everything above is one host-to-device copy
+  c.greedy = o; o += align256(rc * 4);
+  c.gap = o; o += align256(rc * 4);
+  c.bytes = o;
+  return c;
+}
+}  // namespace
+
+size_t ts_calib_labels_workspace_size(int32_t R, int32_t cap) {
+  if (R < 1 || cap < 1) return 0;
+  return calib_layout(R, cap).bytes;
+}
+
+int32_t ts_calib_labels(const ts_tree* tree, const void* target, int32_t target_dtype, int32_t V, float* x,
+                        int32_t* y, int32_t* sel, void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (!tree || !target || !x || !y || !sel) return fail(TS_EINVAL, "tree, target or an output is NULL");
+  if (!tree->n || !tree->token || !tree->parent || !tree->log_q0) return fail(TS_EINVAL, "a tree array is NULL");
+  if (tree->R < 1 || tree->cap < 1) return fail(TS_EINVAL, "tree R=%d cap=%d", tree->R, tree->cap);
+  if (V < 1) return fail(TS_EINVAL, "V=%d", V);
+  if (target_dtype != TS_F32 && target_dtype != TS_BF16) return fail(TS_EINVAL, "unknown target dtype %d", target_dtype);
+  const int R = tree->R, cap = tree->cap;
+  for (int q = 0; q < R; ++q) {
+    const int nq = tree->n[q];
+    if (nq < 0 || nq >= cap) return fail(TS_EINVAL, "tree n[%d]=%d outside [0, cap)", q, nq);
+    for (int i = 1; i <= nq; ++i) {
+      const size_t o = (size_t)q * cap + i;
+      if (tree->parent[o] < 0 || tree->parent[o] >= i || tree->token[o] < 0 || tree->token[o] >= V)
+        return fail(TS_EINVAL, "tree of request %d is malformed at node %d", q, i);
+    }
+  }
+  const CalibLayout cl = calib_layout(R, cap);
+  if (!workspace || workspace_bytes < cl.bytes)
+    return fail(TS_ENOSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, cl.bytes);
+  char* hs = nullptr;
+  int32_t rc = host_stage(cl.upload, &hs);
+  if (rc != TS_OK) return rc;
+  const size_t rcn = (size_t)R * cap;
+  std::memcpy(hs + cl.parent, tree->parent, rcn * 4);
+  std::memcpy(hs + cl.token, tree->token, rcn * 4);
+  std::memcpy(hs + cl.log_q0, tree->log_q0, rcn * 4);
+  std::memcpy(hs + cl.n, tree->n, (size_t)R * 4);
+  int32_t* rows = reinterpret_cast<int32_t*>(hs + cl.rows);
+  int32_t* off = reinterpret_cast<int32_t*>(hs + cl.off);
+  int nrows = 0;
+  for (int q = 0; q < R; ++q) {
+    off[q] = nrows;
+    for (int i = 0; i <= tree->n[q]; ++i) rows[nrows++] = q * cap + i;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  TS_HIP(hipMemcpyAsync(ws, hs, cl.upload, hipMemcpyHostToDevice, s));
+  int32_t* greedy = reinterpret_cast<int32_t*>(ws + cl.greedy);
+  launch_verify_argmax(target, target_dtype == TS_BF16, V, reinterpret_cast<const int*>(ws + cl.rows), nrows,
+                       greedy, reinterpret_cast<float*>(ws + cl.gap), s);
+  TS_HIP(hipGetLastError());
+  launch_calib_labels(reinterpret_cast<const int32_t*>(ws + cl.parent), reinterpret_cast<const int32_t*>(ws + cl.token),
+                      reinterpret_cast<const float*>(ws + cl.log_q0), reinterpret_cast<const int32_t*>(ws + cl.n), R,
+                      cap, greedy, reinterpret_cast<const int32_t*>(ws + cl.off), x, y, sel, s);
+  TS_HIP(hipGetLastError());
+  TS_HIP(hipStreamSynchronize(s));
+  return TS_OK;
+}
+
+int32_t ts_calib_fit(const float* x, const int32_t* y, const int32_t* sel, int32_t n, int32_t max_iter,
+                     double tol, float* out, void* stream) {
+  g_last_error.clear();
+  if (!x || !y || !sel || !out) return fail(TS_EINVAL, "an array is NULL");
+  if (n < 0 || max_iter < 1 || !(tol > 0.0)) return fail(TS_EINVAL, "n=%d max_iter=%d tol=%g", n, max_iter, tol);
+  launch_calib_fit(x, y, sel, n, max_iter, tol, out, static_cast<hipStream_t>(stream));
+  TS_HIP(hipGetLastError());
+  return TS_OK;
+}
+
 int32_t ts_tree_mask_words(int32_t cap) { return cap < 1 ? 0 : (cap + 31) / 32; }
 
 int32_t ts_tree_mask(const int32_t* parent, const int32_t* n, int32_t R, int32_t cap,

@@ -20,7 +20,7 @@ def _declared():
 
 def test_library_exports_every_declared_symbol():
     declared = _declared()
-    assert len(declared) == 12
+    assert len(declared) == 15
     assert sorted(b.EXPORTED) == declared
     L = b.lib()
     for name in declared:
@@ -184,3 +184,30 @@ def test_ladder_lookup_rule_and_errors():
             b.ladder_lookup(rungs, *args)
     with pytest.raises(RuntimeError):
         b.ladder_lookup([], 1, 0.0, 4, 9, 5)
+
+
+def test_calib_entry_points_reject_bad_arguments():
+    L = b.lib()
+    tree = b.HostTree.empty(2, 5)
+    tree.n[:] = [1, 0]
+    tree.parent[0, :2] = [-1, 0]
+    tree.token[0, :2] = [3, 4]
+    s = tree.struct()
+    x = y = sel = out = FAKE
+    ws = L.ts_calib_labels_workspace_size(2, 5)
+    assert ws > 0 and L.ts_calib_labels_workspace_size(0, 5) == 0
+
+    def labels(st=s, dtype=b.TS_F32, V=10, wsb=ws):
+        return L.ts_calib_labels(ctypes.byref(st), FAKE, dtype, V, x, y, sel, FAKE, wsb, None)
+
+    assert labels(V=4) == b.TS_EINVAL            # token 4 outside [0, V)
+    assert labels(dtype=7) == b.TS_EINVAL
+    assert labels(wsb=8) == b.TS_ENOSPACE
+    bad = b.HostTree.empty(2, 5)
+    bad.n[:] = [2, 0]
+    bad.parent[0, :3] = [-1, 0, 2]                # a parent that is not before its child
+    assert labels(st=bad.struct()) == b.TS_EINVAL
+    assert L.ts_calib_fit(None, y, sel, 4, 10, 1e-9, out, None) == b.TS_EINVAL
+    assert L.ts_calib_fit(x, y, sel, -1, 10, 1e-9, out, None) == b.TS_EINVAL
+    assert L.ts_calib_fit(x, y, sel, 4, 0, 1e-9, out, None) == b.TS_EINVAL
+    assert L.ts_calib_fit(x, y, sel, 4, 10, 0.0, out, None) == b.TS_EINVAL
