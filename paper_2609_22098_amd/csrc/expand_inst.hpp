@@ -17,10 +17,14 @@ struct EvalKernels {
     else
       return expand_eval_kernel<TE, KS, NB, MODE, false>;
   }
+  // mode: kModeGreedy, kModeGumbel or kModeSeq, with kModeNeedT for T != 1
+  // (the LDS kernel has a variant for it; the other takes it from the params)
   static auto get(int mode) {
     decltype(pick<0>()) k = pick<0>();
-    if (mode == kModeGumbel) k = pick<kModeGumbel>();
-    if (mode == kModeSeq) k = pick<kModeSeq>();
+    const bool nt = LDS && (mode & kModeNeedT);
+    const int base = mode & 3;
+    if (base == kModeGumbel) k = nt ? pick<(LDS ? kModeGumbel | kModeNeedT : kModeGumbel)>() : pick<kModeGumbel>();
+    if (base == kModeSeq) k = nt ? pick<(LDS ? kModeSeq | kModeNeedT : kModeSeq)>() : pick<kModeSeq>();
     return k;
   }
 };

@@ -81,7 +81,9 @@ __device__ __forceinline__ int launch_parents(const Params& p) {
 }
 
 // Sampling modes of a launch: greedy (T = 0), Gumbel-top-k draws, sequential draws.
-enum : int { kModeGreedy = 0, kModeGumbel = 1, kModeSeq = 2 };
+// The LDS streaming kernel also takes kModeNeedT in its mode (T != 1: a second
+// sum for log-sum-exp of z / T), so that both sums are computed together.
+enum : int { kModeGreedy = 0, kModeGumbel = 1, kModeSeq = 2, kModeNeedT = 4 };
 constexpr int kSegTokens = 4096;  // tokens per segment of the sequential draws
 constexpr int kBlkTokens = 64;    // tokens per block
 
@@ -278,6 +280,25 @@ __device__ __forceinline__ float sum16_exp2(const float (&v)[16], float c, float
 #pragma unroll
   for (int j = 4; j < 16; ++j) a[j & 3] += exp2_fast(__builtin_fmaf(v[j], c, -ref));
   return (a[0] + a[1]) + (a[2] + a[3]);
+}
+
+// The two sums of one run (scales c0, c1; references r0, r1) interleaved:
+// eight independent chains, each summed in the order of sum16_exp2.
+__device__ __forceinline__ void sum16_exp2_x2(const float (&v)[16], float c0, float r0, float c1, float r1,
+                                              float& s0, float& s1) {
+  float a[4], b[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    a[q] = exp2_fast(__builtin_fmaf(v[q], c0, -r0));
+    b[q] = exp2_fast(__builtin_fmaf(v[q], c1, -r1));
+  }
+#pragma unroll
+  for (int j = 4; j < 16; ++j) {
+    a[j & 3] += exp2_fast(__builtin_fmaf(v[j], c0, -r0));
+    b[j & 3] += exp2_fast(__builtin_fmaf(v[j], c1, -r1));
+  }
+  s0 = (a[0] + a[1]) + (a[2] + a[3]);
+  s1 = (b[0] + b[1]) + (b[2] + b[3]);
 }
 
 // a: this lane's run sum relative to 2^ref (ref finite); the run holding
@@ -571,9 +592,11 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
   __shared__ __attribute__((aligned(16))) u32x4 u0[4 * kU];
   __shared__ __attribute__((aligned(16))) u32x4 u1[4 * kU];
   const int lane = threadIdx.x & 63;
-  constexpr bool SAMPLE = MODE != kModeGreedy;  // T > 0: lse of z/T and K draws
-  constexpr bool GUMBEL = MODE == kModeGumbel;
-  constexpr bool SEQ = MODE == kModeSeq;
+  constexpr int BASE = MODE & 3;
+  constexpr bool SAMPLE = BASE != kModeGreedy;  // T > 0: lse of z/T and K draws
+  constexpr bool GUMBEL = BASE == kModeGumbel;
+  constexpr bool SEQ = BASE == kModeSeq;
+  constexpr bool NT = SAMPLE && (MODE & kModeNeedT) != 0;  // T != 1: a separate sum for z/T
   const int wv = threadIdx.x >> 6;
   const int n = lane & 15;
   const int g = lane >> 4;
@@ -702,20 +725,22 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
       const bool run_high = bref > m0c;
       const float gap = -__builtin_fabsf(m0c - bref);
       const float bl = bref * kLog2e;
-      float a0 = sum16_exp2(v, kLog2e, bl);
+      const float blT = bref * p.cT;
+      float a0, aT = 0.0f;
+      if constexpr (NT)
+        sum16_exp2_x2(v, kLog2e, bl, p.cT, blT, a0, aT);
+      else
+        a0 = sum16_exp2(v, kLog2e, bl);
       const float f0 = exp2_fast(gap * kLog2e);
       s0[nb] = run_high ? __builtin_fmaf(s0[nb], f0, a0) : __builtin_fmaf(a0, f0, s0[nb]);
-      const float blT = bref * p.cT;
-      float aT = 0.0f;
-      if (SAMPLE && p.need_T) {
-        aT = sum16_exp2(v, p.cT, blT);
+      if constexpr (NT) {
         const float fT = exp2_fast(gap * p.cT);
         sT[nb] = run_high ? __builtin_fmaf(sT[nb], fT, aT) : __builtin_fmaf(aT, fT, sT[nb]);
       }
       m0[nb] = fmaxf(m0[nb], bm);
       top_add(zt[nb], bm, run);
       if constexpr (SEQ) {
-        const float lb = p.need_T ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
+        const float lb = NT ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
         const int bi = t0 >> 6;
         bw[nb].put(bi, g, lb);
         if (pidx[nb] < P) bw[nb].flush(p.blk + (size_t)pidx[nb] * p.blk_ld, bi, bfirst, blast, g);
@@ -782,7 +807,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
     s += __shfl_xor(s, 16, 64);
     s += __shfl_xor(s, 32, 64);
     float st = 0.0f;
-    if (SAMPLE && p.need_T) {
+    if constexpr (NT) {
       st = sT[nb] * exp2_fast(__builtin_fmaf(m0[nb], p.cT, -Mref * p.cT));
       st += __shfl_xor(st, 16, 64);
       st += __shfl_xor(st, 32, 64);

@@ -178,6 +178,8 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
   Plan pl{};
   pl.sample = T > 0.0f && !store_z;
   pl.mode = !pl.sample ? kModeGreedy : sampler == TS_SAMPLER_SEQUENTIAL ? kModeSeq : kModeGumbel;
+  // the streaming kernel's mode: with the separate z / T sum when T != 1
+  const int eval_mode = pl.mode | (pl.sample && T != 1.0f ? kModeNeedT : 0);
   pl.nblk = (d->V + kBlkTokens - 1) / kBlkTokens;
   pl.blk_ld = ((pl.nblk + 15) / 16) * 16;
   pl.ks = d->dtype == TS_BF16 ? d->r / 32 : d->r / 4;
@@ -200,7 +202,7 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
     vc = 256;
   } else {
     const int concurrent = device_cus() *
-        eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, pl.mode, store_z, pl.lds, 64 * pl.wpg);
+        eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, eval_mode, store_z, pl.lds, 64 * pl.wpg);
     const int s_min = (d->V + 4095) / 4096;
     const int rounds = std::max(1, (pl.n_pgroups * s_min + concurrent - 1) / concurrent);
     const int s_want = std::max(1, (rounds * concurrent + pl.n_pgroups - 1) / pl.n_pgroups);
@@ -219,7 +221,7 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
   if (!sizing_only)
     fprintf(stderr, "[plan] P=%d NB=%d lds=%d wpg=%d n_pgroups=%d Vc=%d S=%d grid=%d bpc=%d cus=%d\n", P,
             pl.NB, (int)pl.lds, pl.wpg, pl.n_pgroups, pl.Vc, pl.S, pl.S8 * pl.n_pgroups,
-            eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, pl.mode, store_z, pl.lds, 64 * pl.wpg), device_cus());
+            eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, eval_mode, store_z, pl.lds, 64 * pl.wpg), device_cus());
 #endif
   const size_t a = align256((size_t)std::max(P, 1) * pl.S * 4);
   const size_t a4 = align256((size_t)std::max(P, 1) * pl.S * 4 * kTopRuns);
@@ -259,18 +261,19 @@ size_t expand_ws_max(const ts_drafter* d, int Pmax, float T, bool store_z = fals
 void launch_eval(const ts_drafter* d, const ExpandParams& p, const Plan& pl, hipStream_t s) {
   const dim3 grid(pl.S8 * pl.n_pgroups), block(64 * pl.wpg);
   const bool z = p.z_out != nullptr;
+  const int mode = pl.mode | (p.need_T && pl.mode != kModeGreedy ? kModeNeedT : 0);
   if (d->dtype == TS_BF16) {
     switch (pl.ks) {
-      case 1: launch_eval_t<uint16_t, 1>(p, pl.NB, pl.mode, z, pl.lds, grid, block, s); break;
-      case 2: launch_eval_t<uint16_t, 2>(p, pl.NB, pl.mode, z, pl.lds, grid, block, s); break;
-      case 4: launch_eval_t<uint16_t, 4>(p, pl.NB, pl.mode, z, pl.lds, grid, block, s); break;
-      default: launch_eval_t<uint16_t, 8>(p, pl.NB, pl.mode, z, pl.lds, grid, block, s); break;
+      case 1: launch_eval_t<uint16_t, 1>(p, pl.NB, mode, z, pl.lds, grid, block, s); break;
+      case 2: launch_eval_t<uint16_t, 2>(p, pl.NB, mode, z, pl.lds, grid, block, s); break;
+      case 4: launch_eval_t<uint16_t, 4>(p, pl.NB, mode, z, pl.lds, grid, block, s); break;
+      default: launch_eval_t<uint16_t, 8>(p, pl.NB, mode, z, pl.lds, grid, block, s); break;
     }
   } else {
     switch (pl.ks) {
-      case 4: launch_eval_t<float, 4>(p, pl.NB, pl.mode, z, false, grid, block, s); break;
-      case 8: launch_eval_t<float, 8>(p, pl.NB, pl.mode, z, false, grid, block, s); break;
-      default: launch_eval_t<float, 16>(p, pl.NB, pl.mode, z, false, grid, block, s); break;
+      case 4: launch_eval_t<float, 4>(p, pl.NB, mode, z, false, grid, block, s); break;
+      case 8: launch_eval_t<float, 8>(p, pl.NB, mode, z, false, grid, block, s); break;
+      default: launch_eval_t<float, 16>(p, pl.NB, mode, z, false, grid, block, s); break;
     }
   }
 }
