@@ -367,8 +367,8 @@ __device__ __forceinline__ int wave_pick(const float (&m)[NS], float u) {
 // in its rows of the workspace; a drawn token's block is rewritten in place.
 // Draw j lands in lane j - 1 of gl (token, z).
 
-template <typename TE, int KS>
-__device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const TE* urow,
+template <typename TE, int KS, int NSEG>
+__device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, const TE* urow,
                                           const typename Frag<TE>::type (&bcol)[KS], uint32_t pc1,
                                           uint32_t pc2, uint32_t pc3, DrawLds& L, RegList& gl) {
   typedef Frag<TE> F;
@@ -386,9 +386,9 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
   // is issued before the first reduction (a global round trip costs about
   // as much as all the arithmetic here).  The table is kept in LDS when it
   // fits, and segments are reduced eight at a time.
-  float segL[kSegSlots];
+  float segL[NSEG];
 #pragma unroll
-  for (int i = 0; i < kSegSlots; ++i) segL[i] = kNegInf;
+  for (int i = 0; i < NSEG; ++i) segL[i] = kNegInf;
   auto reduce8 = [&](int s0, const float (&xs)[8]) {
     float m[8], e[8];
 #pragma unroll
@@ -402,7 +402,7 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
       const int sg = s0 + k;
       const float l = m[k] == kNegInf ? kNegInf : m[k] + __builtin_amdgcn_logf(e[k]);
 #pragma unroll
-      for (int i = 0; i < kSegSlots; ++i)
+      for (int i = 0; i < NSEG; ++i)
         if (sg < nseg && sg == 64 * i + lane) segL[i] = l;
     }
   };
@@ -459,13 +459,13 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
     const uint32_t w1 = (uint32_t)lane_i32((int)dw1, j - 1);
     const uint32_t w2 = (uint32_t)lane_i32((int)dw2, j - 1);
     // level 1: segment
-    float ms[kSegSlots];
+    float ms[NSEG];
     float mx = kNegInf;
 #pragma unroll
-    for (int i = 0; i < kSegSlots; ++i) mx = fmaxf(mx, segL[i]);
+    for (int i = 0; i < NSEG; ++i) mx = fmaxf(mx, segL[i]);
     mx = wave_max(mx);
 #pragma unroll
-    for (int i = 0; i < kSegSlots; ++i) ms[i] = segL[i] == kNegInf ? 0.0f : exp2_fast(segL[i] - mx);
+    for (int i = 0; i < NSEG; ++i) ms[i] = segL[i] == kNegInf ? 0.0f : exp2_fast(segL[i] - mx);
     const int sg = wave_pick(ms, word_to_uniform(w0));
     // level 2: block within the segment (lane = block offset)
     const int b = sg * kBps + lane;
@@ -546,10 +546,23 @@ __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const 
     const float rest2 = wave_sum(lb2 == kNegInf ? 0.0f : exp2_fast(lb2 - mb2));
     const float snew = mb2 == kNegInf ? kNegInf : mb2 + __builtin_amdgcn_logf(rest2);
 #pragma unroll
-    for (int i = 0; i < kSegSlots; ++i)
+    for (int i = 0; i < NSEG; ++i)
       if (sg == 64 * i + lane) segL[i] = snew;
   }
   gl.cnt = p.K;
+}
+
+// The draws with NSEG segment slots per lane: one when the vocabulary has at
+// most 64 segments (V <= 64 * 4096), so level 1 is a single scan.
+template <typename TE, int KS>
+__device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const TE* urow,
+                                          const typename Frag<TE>::type (&bcol)[KS], uint32_t pc1,
+                                          uint32_t pc2, uint32_t pc3, DrawLds& L, RegList& gl) {
+  const int nseg = (p.nblk + kSegTokens / kBlkTokens - 1) / (kSegTokens / kBlkTokens);
+  if (nseg <= 64)
+    seq_draws_n<TE, KS, 1>(p, pidx, urow, bcol, pc1, pc2, pc3, L, gl);
+  else
+    seq_draws_n<TE, KS, kSegSlots>(p, pidx, urow, bcol, pc1, pc2, pc3, L, gl);
 }
 
 template <typename TE, int KS, int MODE>
