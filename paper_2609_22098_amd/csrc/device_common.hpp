@@ -177,9 +177,26 @@ __device__ __forceinline__ float cross_row_sum(float v) {
   const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(s), false, false);
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
+// max(a, b) as the median of (a, b, +inf): one v_med3_f32, which needs no
+// NaN-quieting of its operands (the inputs here are never NaN).
+// +inf from a register the compiler cannot see into, so that it keeps the
+// median instruction instead of turning it back into a max (which would
+// first quiet both operands).
+__device__ __forceinline__ float opaque_inf() {
+  float r;
+  asm("v_mov_b32 %0, 0x7f800000" : "=v"(r));
+  return r;
+}
+__device__ __forceinline__ float max2_med3(float a, float b) {
+  return __builtin_amdgcn_fmed3f(a, b, opaque_inf());
+}
+// Maximum over the four lanes n, n + 16, n + 32, n + 48 (each swap hands a
+// lane both values of its pair, as in cross_row_sum).
 __device__ __forceinline__ float cross_row_max(float v) {
-  const float m = fmaxf(v, xor16_f32(v));
-  return fmaxf(m, xor32_f32(m));
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  const float m = max2_med3(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  return max2_med3(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 // Maximum over each row of 16 lanes (every lane of the row gets it).

@@ -198,21 +198,23 @@ __device__ __forceinline__ void top_init(RunTop& t) {
 }
 
 // Add one run.  Runs arrive in increasing index order within a lane, so a
-// strict comparison keeps the earlier run ahead on ties.
+// strict comparison keeps the earlier run ahead on ties.  With the list
+// sorted (m[0] >= .. >= m[3] >= rest), the new i-th entry is the median of
+// m[i-1], m[i] and v, and the new rest that of m[3], rest and v.
 __device__ __forceinline__ void top_add(RunTop& t, float v, int run) {
-  float cv = v;
-  int cr = run;
+  static_assert(kTopRuns == 4, "unrolled for four entries");
+  bool c[kTopRuns];
 #pragma unroll
-  for (int i = 0; i < kTopRuns; ++i) {
-    const bool sw = cv > t.m[i];
-    const float om = t.m[i];
-    const int orr = t.r[i];
-    t.m[i] = sw ? cv : om;
-    t.r[i] = sw ? cr : orr;
-    cv = sw ? om : cv;
-    cr = sw ? orr : cr;
+  for (int i = 0; i < kTopRuns; ++i) c[i] = v > t.m[i];
+  t.rest = __builtin_amdgcn_fmed3f(t.m[3], t.rest, v);
+#pragma unroll
+  for (int i = kTopRuns - 1; i >= 1; --i) {
+    t.m[i] = __builtin_amdgcn_fmed3f(t.m[i - 1], t.m[i], v);
+    const int x = c[i] ? run : t.r[i];
+    t.r[i] = c[i - 1] ? t.r[i - 1] : x;
   }
-  t.rest = fmaxf(t.rest, cv);  // whatever fell off the end
+  t.m[0] = max2_med3(t.m[0], v);
+  t.r[0] = c[0] ? run : t.r[0];
 }
 
 __device__ __forceinline__ void cswap(float& a, int& ar, float& b, int& br) {
@@ -453,9 +455,9 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
             if (tl + j < V) zo[tl + j] = v[j];
         }
       }
-      float bm = v[0];
+      float bm = max2_med3(v[0], v[1]);
 #pragma unroll
-      for (int j = 1; j < 16; ++j) bm = fmaxf(bm, v[j]);
+      for (int j = 2; j < 16; ++j) bm = fmaxf(bm, v[j]);
       // run sums are taken relative to the run's own maximum (a run far below
       // the running maximum keeps its mass), then folded into the running
       // sums, which are relative to the running maximum: of the two terms the
@@ -713,9 +715,9 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
       for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[bb * 4 + e] = acc[bb][nb][e];
-      float bm = v[0];
+      float bm = max2_med3(v[0], v[1]);
 #pragma unroll
-      for (int j = 1; j < 16; ++j) bm = fmaxf(bm, v[j]);
+      for (int j = 2; j < 16; ++j) bm = fmaxf(bm, v[j]);
       // run sums are taken relative to the run's own maximum (a run far below
       // the running maximum keeps its mass), then folded into the running
       // sums, which are relative to the running maximum: of the two terms the
