@@ -769,11 +769,28 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
 
   const int tbeg = chunk * p.Vc;
   const int tend = min(tbeg + p.Vc, V);
+  // Issue priority falls as the wave walks its chunk (3 in the first quarter,
+  // then 2, 1, 0), so that on a SIMD the waves that are behind are served
+  // first.  With equal priorities the oldest wave wins every arbitration:
+  // the waves of a SIMD finish one after another and the last one runs
+  // alone, with nothing to hide its latencies.
+  const int nsteps = (tend - tbeg + 63) >> 6;
+  int prio_next = (nsteps + 3) >> 2, prio_q = 0;
+  __builtin_amdgcn_s_setprio(3);
+  auto lower_priority = [&](int done) {
+    if (done < prio_next) return;
+    ++prio_q;
+    prio_next = (nsteps * (prio_q + 1) + 3) >> 2;
+    if (prio_q == 1) __builtin_amdgcn_s_setprio(2);
+    else if (prio_q == 2) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(0);
+  };
   int t0 = tbeg, step = 0;
   issue(w0, u0, t0);
   for (;;) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    lower_priority(step);
     const bool more1 = t0 + 64 < tend;
     if (more1) issue(w1, u1, t0 + 64);
     if (active) {
@@ -786,6 +803,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
     t0 += 64; ++step;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    lower_priority(step);
     const bool more2 = t0 + 64 < tend;
     if (more2) issue(w0, u0, t0 + 64);
     if (active) {
