@@ -106,6 +106,7 @@ def copy_calibration(gib, args_out=""):
 
 
 EVAL_KERNEL = "expand_eval_lds_kernel"
+EVAL_FRONTIER = "expand_eval_lds_kernel<2, 2,"  # rank 64 (KS = 2), two parent blocks per wave
 
 
 def _counter_per_dispatch(run_dir, counter, name_part):
@@ -141,9 +142,10 @@ def write_traffic(root, T, sampler):
         vals = _counter_per_dispatch(os.path.join(root, sub), counter, "")
         kib = max(v for _, v in vals)  # the copy is by far the largest dispatch of its run
         scale[counter] = copy_bytes / (kib * 1024.0)
-    # the serving frontier's launch is the largest-grid launch of the streaming pass in a step
-    fetch = _largest_grid(_counter_per_dispatch(os.path.join(root, "fetch"), "FETCH_SIZE", EVAL_KERNEL))
-    write = _largest_grid(_counter_per_dispatch(os.path.join(root, "write"), "WRITE_SIZE", EVAL_KERNEL))
+    # the serving frontier's launch: two parent blocks per wave (the tree waves'
+    # launches take one, and their upper-bound grids can be larger), rank 64
+    fetch = _largest_grid(_counter_per_dispatch(os.path.join(root, "fetch"), "FETCH_SIZE", EVAL_FRONTIER))
+    write = _largest_grid(_counter_per_dispatch(os.path.join(root, "write"), "WRITE_SIZE", EVAL_FRONTIER))
     fb = float(np.mean(fetch)) * 1024.0 * scale["FETCH_SIZE"]
     wb = float(np.mean(write)) * 1024.0 * scale["WRITE_SIZE"]
     rec = {"kernel": EVAL_KERNEL, "T": T, "sampler": sampler, "kernel_source_hash": kernel_source_hash(),
