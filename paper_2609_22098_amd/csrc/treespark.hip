@@ -55,7 +55,8 @@ int32_t host_stage(size_t bytes, char** out) {
     st.p = nullptr;
     st.n = 0;
     void* q = nullptr;
-    TS_HIP(hipHostMalloc(&q, bytes, hipHostMallocDefault));
+    // coherent: kernels read and write parts of it directly
+    TS_HIP(hipHostMalloc(&q, bytes, hipHostMallocCoherent));
     st.p = static_cast<char*>(q);
     st.n = bytes;
   }
@@ -425,7 +426,7 @@ TreeBlock tree_block(int R, int cap) {
 struct BuildLayout {
   size_t off_par, off_out, off_exp;
   // device-resident waves
-  size_t off_par2, off_list, off_lsize, off_evals, off_pcount, off_span, off_anchor, off_ltheta, off_tree;
+  size_t off_par2, off_list, off_lsize, off_evals, off_pcount, off_done, off_span, off_anchor, off_ltheta, off_tree;
   size_t bytes;
   int Pmax;
 };
@@ -444,6 +445,7 @@ BuildLayout build_layout(const ts_drafter* d, int N, int K, float T) {
   b.off_lsize = o; o += align256((size_t)R * 4);
   b.off_evals = o; o += align256((size_t)R * 4);
   b.off_pcount = o; o += align256((size_t)(d->D + 2) * 4);
+  b.off_done = o; o += align256((size_t)(d->D + 2) * 4);
   b.off_span = o; o += 2 * align256((size_t)R * sizeof(WaveSpan));
   b.off_anchor = o; o += align256((size_t)R * 4);
   b.off_ltheta = o; o += align256((size_t)R * 4);
@@ -493,10 +495,9 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   if (rc != TS_OK) return rc;
   hipEvent_t* ev = wave_events(D + 2);
   if (!ev) return fail(TS_EHIP, "hipEventCreate failed");
+  // roots and thresholds stay in the pinned buffer: the init kernel reads them
   std::memcpy(hs, anchor, (size_t)R * 4);
   std::memcpy(hs + (size_t)R * 4, log_theta.data(), (size_t)R * 4);
-  TS_HIP(hipMemcpyAsync(ws + bl.off_anchor, hs, (size_t)R * 4, hipMemcpyHostToDevice, s));
-  TS_HIP(hipMemcpyAsync(ws + bl.off_ltheta, hs + (size_t)R * 4, (size_t)R * 4, hipMemcpyHostToDevice, s));
   volatile int32_t* hcnt = reinterpret_cast<volatile int32_t*>(hs + hs_up);
   char* htree = hs + hs_up + hs_cnt;
 
@@ -504,6 +505,12 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   wp.R = R; wp.N = N; wp.K = K; wp.D = D;
   wp.anchor = reinterpret_cast<const int32_t*>(ws + bl.off_anchor);
   wp.log_theta = reinterpret_cast<const float*>(ws + bl.off_ltheta);
+  wp.anchor_host = reinterpret_cast<const int32_t*>(hs);
+  wp.log_theta_host = reinterpret_cast<const float*>(hs + (size_t)R * 4);
+  wp.anchor_w = reinterpret_cast<int32_t*>(ws + bl.off_anchor);
+  wp.log_theta_w = reinterpret_cast<float*>(ws + bl.off_ltheta);
+  wp.done = reinterpret_cast<int*>(ws + bl.off_done);
+  wp.host_count = hcnt;
   wp.list = reinterpret_cast<WaveSlot*>(ws + bl.off_list);
   wp.lsize = reinterpret_cast<int*>(ws + bl.off_lsize);
   wp.evals = reinterpret_cast<int*>(ws + bl.off_evals);
@@ -530,14 +537,14 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   TS_HIP(hipGetLastError());
 
   // queue wave w: expansion of par[w & 1] (at most Pub parents; the device
-  // holds the count), the control step, and the next wave's size to the host
+  // holds the count) and the control step, which also writes the next
+  // wave's size into hcnt; an event marks its end
   auto queue_wave = [&](int w, int Pub) -> int32_t {
     int32_t r = run_expand(d, wp.par[w & 1], Pub, calib, K, T, seed, sampler, &eo, ws + bl.off_exp, s,
                            wp.pcount + w);
     if (r != TS_OK) return r;
     launch_wave_control(wp, w, s);
     TS_HIP(hipGetLastError());
-    TS_HIP(hipMemcpyAsync((void*)(hcnt + w + 1), wp.pcount + w + 1, 4, hipMemcpyDeviceToHost, s));
     TS_HIP(hipEventRecord(ev[w + 1], s));
     return TS_OK;
   };
@@ -596,7 +603,7 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
 }
 
 struct VerifyLayout {
-  size_t off_rows, off_arg, off_gap, off_items, off_res, off_par, off_z, off_exp;
+  size_t off_rows, off_arg, off_gap, off_items, off_par, off_z, off_exp;
   size_t off_pa, off_zp, off_bp, off_cst, off_rec, bytes;
   int max_chunks;
 };
@@ -622,7 +629,6 @@ VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
     v.off_gap = o; o += align256(rows * 4);
   } else {
     v.off_items = o; o += align256((size_t)d->R * sizeof(VerifyItem));
-    v.off_res = o; o += align256((size_t)d->R * sizeof(VerifyResult));
     v.off_par = o; o += align256((size_t)d->R * sizeof(ts_parent));
     v.off_z = o; o += align256((size_t)d->R * d->V * 4);
     v.off_exp = o; o += expand_ws_max(d, d->R, T, true);
@@ -982,7 +988,6 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
 
   // T > 0: one level of the walk per iteration, batched over the requests still walking.
   VerifyItem* ditems = reinterpret_cast<VerifyItem*>(ws + vl.off_items);
-  VerifyResult* dres = reinterpret_cast<VerifyResult*>(ws + vl.off_res);
   ts_parent* dpar = reinterpret_cast<ts_parent*>(ws + vl.off_par);
   float* zbuf = reinterpret_cast<float*>(ws + vl.off_z);
   const PhiloxKeys keys = philox_keys(seed);
@@ -1042,12 +1047,11 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     vp.bp = reinterpret_cast<VBonusPart*>(ws + vl.off_bp);
     vp.consts = reinterpret_cast<VConst*>(ws + vl.off_cst);
     vp.recs = reinterpret_cast<VRec*>(ws + vl.off_rec);
-    vp.results = dres;
+    vp.results = const_cast<VerifyResult*>(res);  // pinned: the resolve kernel writes it
     int mmax = 0;
     for (const VerifyItem& it : items) mmax = std::max(mmax, it.m);
     launch_verify_level(vp, target_dtype == TS_BF16, mmax, s);
     TS_HIP(hipGetLastError());
-    TS_HIP(hipMemcpyAsync(hs + hs_items + hs_par, dres, ni * sizeof(VerifyResult), hipMemcpyDeviceToHost, s));
     TS_HIP(hipStreamSynchronize(s));
     std::vector<int> next;
     for (int i = 0; i < ni; ++i) {

@@ -161,7 +161,7 @@ struct VerifyPass {
   VBonusPart* bp;      // [nitems][nchunks]
   VConst* consts;      // [nitems]: written by the stage-1 launch
   VRec* recs;          // [TS_MAX_K][nitems]: record after the launch of stage j, at j - 1
-  VerifyResult* results;
+  VerifyResult* results;  // [nitems], pinned host memory
 };
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
@@ -567,7 +567,10 @@ __global__ __launch_bounds__(64) void verify_resolve_kernel(VerifyPass vp, int J
     r.bonus = id;
     r.margin = fminf(r.margin, gap);
   }
-  if (lane == 0) vp.results[it] = r;
+  if (lane == 0) {
+    vp.results[it] = r;  // pinned host memory
+    __threadfence_system();
+  }
 }
 
 }  // namespace ts

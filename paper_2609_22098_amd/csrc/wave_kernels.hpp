@@ -46,17 +46,24 @@ __device__ __forceinline__ int wave_block_excl_scan(int v, int* tmp, int& total)
   return incl - v;
 }
 
-// Wave 0: every request's root is the one parent; lists empty.
+// Wave 0: every request's root is the one parent; lists empty.  The roots
+// and thresholds are read from the host's pinned buffer (no upload copy).
 __global__ __launch_bounds__(kWaveThreads) void wave_init_kernel(const WaveParams wp) {
   const int q = blockIdx.x * kWaveThreads + threadIdx.x;
   if (q == 0) {
-    for (int i = 0; i < wp.D + 2; ++i) wp.pcount[i] = i == 0 ? wp.R : 0;
+    for (int i = 0; i < wp.D + 2; ++i) {
+      wp.pcount[i] = i == 0 ? wp.R : 0;
+      wp.done[i] = 0;
+    }
     *wp.err = 0;
   }
   if (q >= wp.R) return;
+  const int32_t a = wp.anchor_host[q];
+  wp.anchor_w[q] = a;
+  wp.log_theta_w[q] = wp.log_theta_host[q];
   wp.lsize[q] = 0;
   wp.evals[q] = 0;
-  wp.par[0][q] = ts_parent{wp.anchor[q], 0, q, 0.0f, 0ull};
+  wp.par[0][q] = ts_parent{a, 0, q, 0.0f, 0ull};
   wp.span[0][q] = WaveSpan{q, 1};
 }
 
@@ -145,6 +152,13 @@ __global__ __launch_bounds__(kWaveThreads) void wave_control_kernel(const WavePa
     const int base = nc > 0 ? atomicAdd(&wp.pcount[w + 1], nc) : 0;
     base_sh = base;
     wp.span[(w + 1) & 1][q] = WaveSpan{base, nc};
+    // the last workgroup to finish hands the next wave's size to the host
+    __threadfence();
+    if (atomicAdd(&wp.done[w + 1], 1) == wp.R - 1) {
+      __threadfence();
+      wp.host_count[w + 1] = atomicAdd(&wp.pcount[w + 1], 0);
+      __threadfence_system();
+    }
   }
   __syncthreads();
   ts_parent* out = wp.par[(w + 1) & 1] + base_sh;

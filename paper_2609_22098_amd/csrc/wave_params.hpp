@@ -25,6 +25,16 @@ struct WaveParams {
   int R, N, K, D;
   const int32_t* anchor;   // [R] root tokens
   const float* log_theta;  // [R] log(theta_q), -inf for theta = 0
+  // the two arrays above as the host wrote them (pinned host memory, read by
+  // the init step, which writes them to anchor_w and log_theta_w: the same
+  // buffers as anchor and log_theta)
+  const int32_t* anchor_host;
+  const float* log_theta_host;
+  int32_t* anchor_w;
+  float* log_theta_w;
+  int* done;                     // [D + 2] control workgroups finished after wave w - 1
+  volatile int32_t* host_count;  // [D + 2] pinned host memory: pcount[w], written by the
+                                 // last control workgroup of wave w - 1
   WaveSlot* list;          // [R][N] best known slots with key >= log(theta), pop order
   int* lsize;              // [R] entries of list in use
   int* evals;              // [R] parents evaluated so far
