@@ -426,7 +426,7 @@ TreeBlock tree_block(int R, int cap) {
 struct BuildLayout {
   size_t off_par, off_out, off_exp;
   // device-resident waves
-  size_t off_par2, off_list, off_lsize, off_evals, off_pcount, off_done, off_span, off_anchor, off_ltheta, off_tree;
+  size_t off_par2, off_list, off_lsize, off_evals, off_pcount, off_done, off_span, off_anchor, off_ltheta;
   size_t bytes;
   int Pmax;
 };
@@ -449,7 +449,6 @@ BuildLayout build_layout(const ts_drafter* d, int N, int K, float T) {
   b.off_span = o; o += 2 * align256((size_t)R * sizeof(WaveSpan));
   b.off_anchor = o; o += align256((size_t)R * 4);
   b.off_ltheta = o; o += align256((size_t)R * 4);
-  b.off_tree = o; o += tree_block(R, N + 1).bytes;
   b.bytes = o;
   return b;
 }
@@ -515,7 +514,6 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   wp.lsize = reinterpret_cast<int*>(ws + bl.off_lsize);
   wp.evals = reinterpret_cast<int*>(ws + bl.off_evals);
   wp.pcount = reinterpret_cast<int*>(ws + bl.off_pcount);
-  wp.err = reinterpret_cast<int*>(ws + bl.off_tree + tree_block(R, cap).err);
   wp.par[0] = reinterpret_cast<ts_parent*>(ws + bl.off_par);
   wp.par[1] = reinterpret_cast<ts_parent*>(ws + bl.off_par2);
   wp.span[0] = reinterpret_cast<WaveSpan*>(ws + bl.off_span);
@@ -562,8 +560,10 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
     Pw = Pn;
   }
 
-  // the trees: staging block, one copy to the host, and the caller's device arrays
-  char* dt = ws + bl.off_tree;
+  // the trees: written straight into the pinned block, and into the caller's
+  // device arrays
+  char* dt = htree;
+  *reinterpret_cast<volatile int32_t*>(htree + tb.err) = 0;
   ts_tree st{};
   st.R = R; st.cap = cap;
   st.n = reinterpret_cast<int32_t*>(dt + tb.n);
@@ -577,15 +577,16 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   st.log_q0 = reinterpret_cast<float*>(dt + tb.log_q0);
   st.log_qT = reinterpret_cast<float*>(dt + tb.log_qT);
   st.key = reinterpret_cast<float*>(dt + tb.key);
-  launch_wave_tree(wp, tree_out_of(&st), s);
+  WaveTreeOut ho = tree_out_of(&st);
+  ho.err = reinterpret_cast<int32_t*>(htree + tb.err);
+  launch_wave_tree(wp, ho, s);
   TS_HIP(hipGetLastError());
   if (device_out) {
     launch_wave_tree(wp, tree_out_of(device_out), s);
     TS_HIP(hipGetLastError());
   }
-  TS_HIP(hipMemcpyAsync(htree, dt, tb.bytes, hipMemcpyDeviceToHost, s));
   TS_HIP(hipStreamSynchronize(s));
-  if (*reinterpret_cast<const int32_t*>(htree + tb.err) != 0)
+  if (*reinterpret_cast<const volatile int32_t*>(htree + tb.err) != 0)
     return fail(TS_EINTERNAL, "a tree slot has no materialised parent");
   const size_t rcn = (size_t)R * cap;
   std::memcpy(out->n, htree + tb.n, (size_t)R * 4);
@@ -603,7 +604,7 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
 }
 
 struct VerifyLayout {
-  size_t off_rows, off_arg, off_gap, off_items, off_par, off_z, off_exp;
+  size_t off_rows, off_arg, off_gap, off_items, off_z, off_exp;
   size_t off_pa, off_zp, off_bp, off_cst, off_rec, bytes;
   int max_chunks;
 };
@@ -629,7 +630,6 @@ VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
     v.off_gap = o; o += align256(rows * 4);
   } else {
     v.off_items = o; o += align256((size_t)d->R * sizeof(VerifyItem));
-    v.off_par = o; o += align256((size_t)d->R * sizeof(ts_parent));
     v.off_z = o; o += align256((size_t)d->R * d->V * 4);
     v.off_exp = o; o += expand_ws_max(d, d->R, T, true);
     v.max_chunks = (d->V + kVChunkQuantum - 1) / kVChunkQuantum;
@@ -988,7 +988,6 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
 
   // T > 0: one level of the walk per iteration, batched over the requests still walking.
   VerifyItem* ditems = reinterpret_cast<VerifyItem*>(ws + vl.off_items);
-  ts_parent* dpar = reinterpret_cast<ts_parent*>(ws + vl.off_par);
   float* zbuf = reinterpret_cast<float*>(ws + vl.off_z);
   const PhiloxKeys keys = philox_keys(seed);
   std::vector<int> cur(R, 0), active(R);
@@ -1023,20 +1022,23 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     const int ni = (int)items.size();
     if (!zpar.empty()) {
       const int P = (int)zpar.size();
+      // the recompute reads its parents from the pinned buffer
       std::memcpy(hs + hs_items, zpar.data(), P * sizeof(ts_parent));
-      TS_HIP(hipMemcpyAsync(dpar, hs + hs_items, P * sizeof(ts_parent), hipMemcpyHostToDevice, s));
       const Plan pl = make_plan(d, P, T, TS_SAMPLER_GUMBEL, true);
-      const ExpandParams ep = eval_params(d, dpar, P, T, seed, pl, ws + vl.off_exp, zbuf);
+      const ExpandParams ep =
+          eval_params(d, reinterpret_cast<const ts_parent*>(hs + hs_items), P, T, seed, pl, ws + vl.off_exp, zbuf);
       launch_eval(d, ep, pl, s);
       TS_HIP(hipGetLastError());
     }
+    // pass A reads the items from the pinned buffer and stages them in ditems
     std::memcpy(hs, items.data(), ni * sizeof(VerifyItem));
-    TS_HIP(hipMemcpyAsync(ditems, hs, ni * sizeof(VerifyItem), hipMemcpyHostToDevice, s));
     VerifyPass vp{};
     vp.target = target;
     vp.cap = cap;
     vp.V = V;
     vp.items = ditems;
+    vp.items_host = reinterpret_cast<const VerifyItem*>(hs);
+    vp.items_w = ditems;
     vp.nitems = ni;
     vp.zbuf = zbuf;
     vp.c = kLog2e / T;

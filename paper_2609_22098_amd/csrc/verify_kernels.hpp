@@ -150,7 +150,9 @@ struct VRec;
 struct VerifyPass {
   const void* target;  // [R][cap][V]
   int cap, V;
-  const VerifyItem* items;
+  const VerifyItem* items;       // [nitems], device copy (staged by pass A)
+  const VerifyItem* items_host;  // [nitems], pinned host memory: read by pass A only
+  VerifyItem* items_w;           // the device copy, written by pass A
   int nitems;
   const float* zbuf;   // recomputed draft logits, row items[i].zrow
   float c;             // log2(e) / T
@@ -347,9 +349,19 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
   __shared__ double redd[4];
   __shared__ int loc[TS_MAX_K];
   __shared__ int cnt;
+  __shared__ VerifyItem sitem;
+  static_assert(sizeof(VerifyItem) % 4 == 0 && sizeof(VerifyItem) / 4 <= kVerifyThreads, "item words");
   const int it = blockIdx.x / vp.nchunks, ck = blockIdx.x % vp.nchunks;
   if (it >= vp.nitems) return;
-  const VerifyItem& item = vp.items[it];
+  // the item from the host's pinned buffer; chunk 0 also stages it for the
+  // level's later kernels
+  if (threadIdx.x < (int)(sizeof(VerifyItem) / 4)) {
+    const int32_t w = reinterpret_cast<const int32_t*>(vp.items_host + it)[threadIdx.x];
+    reinterpret_cast<int32_t*>(&sitem)[threadIdx.x] = w;
+    if (ck == 0) reinterpret_cast<int32_t*>(vp.items_w + it)[threadIdx.x] = w;
+  }
+  __syncthreads();
+  const VerifyItem& item = sitem;
   const int y0 = ck * vp.chunk, y1 = min(vp.V, y0 + vp.chunk);
   const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
   const float* zrow = item.m > 0 ? vp.zbuf + (size_t)item.zrow * vp.V : nullptr;

@@ -55,7 +55,6 @@ __global__ __launch_bounds__(kWaveThreads) void wave_init_kernel(const WaveParam
       wp.pcount[i] = i == 0 ? wp.R : 0;
       wp.done[i] = 0;
     }
-    *wp.err = 0;
   }
   if (q >= wp.R) return;
   const int32_t a = wp.anchor_host[q];
@@ -210,7 +209,7 @@ __global__ __launch_bounds__(kWaveThreads) void wave_tree_kernel(const WaveParam
             break;
           }
       }
-      if (parent < 0) atomicAdd(wp.err, 1);
+      if (parent < 0 && o.err) *o.err = 1;
       tok = sl.token;
       depth = sl.depth;
       rank = (int)((sl.path >> (4 * pd)) & 15ull) + 1;

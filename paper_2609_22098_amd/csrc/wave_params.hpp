@@ -39,7 +39,6 @@ struct WaveParams {
   int* lsize;              // [R] entries of list in use
   int* evals;              // [R] parents evaluated so far
   int* pcount;             // [D + 2] frontier size of each wave (wave w: pcount[w])
-  int* err;                // tree assembly: slots whose parent is not listed
   ts_parent* par[2];       // frontier of wave w in par[w & 1]
   WaveSpan* span[2];       // [R] rows of each request in par[w & 1]
   // outputs of the current wave's expansion, [P][K] row-major
@@ -64,6 +63,7 @@ struct WaveTreeOut {
   float* log_qT;
   float* key;
   int32_t* evals;  // may be null
+  int32_t* err;    // may be null: set to 1 when a slot's parent is not listed
 };
 
 }  // namespace ts
