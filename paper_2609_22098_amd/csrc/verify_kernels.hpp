@@ -35,6 +35,40 @@ __device__ __forceinline__ float target_at(const TT* row, int y) {
     return row[y];
 }
 
+// Target values (as float) and draft logits of tokens b .. b+3.  A quad that
+// lies wholly before y1 in rows whose length is a multiple of 4 (vec) is read
+// with one vector load per row; otherwise token by token, and tokens at or
+// past y1 read as 0 (the callers skip them).  zrow may be null (z reads 0).
+template <typename TT>
+__device__ __forceinline__ void load_quad(const TT* trow, const float* zrow, int b, int y1, bool vec,
+                                          float (&t)[4], float (&z)[4]) {
+  if (vec && b + 4 <= y1) {
+    if constexpr (sizeof(TT) == 2) {
+      const uint2 w = *reinterpret_cast<const uint2*>(trow + b);
+      t[0] = __uint_as_float(w.x << 16);
+      t[1] = __uint_as_float(w.x & 0xFFFF0000u);
+      t[2] = __uint_as_float(w.y << 16);
+      t[3] = __uint_as_float(w.y & 0xFFFF0000u);
+    } else {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(trow + b);
+      t[0] = v[0]; t[1] = v[1]; t[2] = v[2]; t[3] = v[3];
+    }
+    if (zrow) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(zrow + b);
+      z[0] = v[0]; z[1] = v[1]; z[2] = v[2]; z[3] = v[3];
+    } else {
+      z[0] = z[1] = z[2] = z[3] = 0.0f;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int y = b + e;
+      t[e] = y < y1 ? target_at(trow, y) : 0.0f;
+      z[e] = (zrow && y < y1) ? zrow[y] : 0.0f;
+    }
+  }
+}
+
 // Block-wide (256 threads) reductions with a fixed order: a wave butterfly,
 // then the four wave results in wave order.
 __device__ __forceinline__ float block_sum(float v, float* red) {
@@ -366,14 +400,16 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
   const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
   const float* zrow = item.m > 0 ? vp.zbuf + (size_t)item.zrow * vp.V : nullptr;
   const int nloc = item.m > 0 ? chunk_children(item, item.m, y0, y1, loc, &cnt) : 0;
+  const bool vec = (vp.V & 3) == 0;
   float mt = kNegInf, mz = kNegInf;
   for (int b = y0 + 4 * threadIdx.x; b < y1; b += kVChunkQuantum) {
+    float tq[4], zq[4];
+    load_quad(trow, zrow, b, y1, vec, tq, zq);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int y = b + e;
-      if (y < y1) {
-        mt = fmaxf(mt, target_at(trow, y) * vp.c);
-        if (zrow) mz = fmaxf(mz, zrow[y] * vp.c);
+      if (b + e < y1) {
+        mt = fmaxf(mt, tq[e] * vp.c);
+        if (zrow) mz = fmaxf(mz, zq[e] * vp.c);
       }
     }
   }
@@ -381,12 +417,14 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
   mz = block_max(mz, red);
   float st = 0.0f, snc = 0.0f;
   for (int b = y0 + 4 * threadIdx.x; b < y1; b += kVChunkQuantum) {
+    float tq[4], zq[4];
+    load_quad(trow, zrow, b, y1, vec, tq, zq);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int y = b + e;
       if (y < y1) {
-        st += exp2_fast(target_at(trow, y) * vp.c - mt);
-        if (zrow && !(nloc && is_listed(y, loc, nloc))) snc += exp2_fast(zrow[y] * vp.c - mz);
+        st += exp2_fast(tq[e] * vp.c - mt);
+        if (zrow && !(nloc && is_listed(y, loc, nloc))) snc += exp2_fast(zq[e] * vp.c - mz);
       }
     }
   }
@@ -450,14 +488,17 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stage_kernel(VerifyPass
   const float* zrow = vp.zbuf + (size_t)item.zrow * vp.V;
   const int nloc = chunk_children(item, j, y0, y1, loc, &cnt);
   const float Lt = j == 1 ? shc.Lt : C.Lt, Lz = j == 1 ? shc.Lz : C.Lz;
+  const bool vec = (vp.V & 3) == 0;
   float acc = 0.0f;
   for (int b = y0 + 4 * threadIdx.x; b < y1; b += kVChunkQuantum) {
+    float tq[4], zq[4];
+    load_quad(trow, zrow, b, y1, vec, tq, zq);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int y = b + e;
       if (y < y1 && !(nloc && is_listed(y, loc, nloc))) {
-        const float p = exp2_fast(target_at(trow, y) * vp.c - Lt);
-        const float q = exp2_fast(zrow[y] * vp.c - Lz);
+        const float p = exp2_fast(tq[e] * vp.c - Lt);
+        const float q = exp2_fast(zq[e] * vp.c - Lz);
         acc += fmaxf(rec.alpha * p - rec.betap * q, 0.0f);
       }
     }
@@ -499,20 +540,23 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_bonus_kernel(VerifyPass
   const uint32_t c3 = counter_word3(item.request, item.depth, 3u);
   float bv = kNegInf, sv = kNegInf;
   int bi = 0x7FFFFFFF;
+  const bool vec = (vp.V & 3) == 0;
   for (int b = y0 + 4 * threadIdx.x; b < y1; b += kVChunkQuantum) {
     uint32_t w0 = (uint32_t)b >> 2, w1 = pc1, w2 = pc2, w3 = c3;
     philox10(w0, w1, w2, w3, vp.keys);
+    float tq[4], zq[4];
+    load_quad(trow, zrow, b, y1, vec, tq, zq);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int y = b + e;
       if (y >= y1) break;
       float l2r;
       if (!zrow) {
-        l2r = target_at(trow, y) * vp.c - Lt;
+        l2r = tq[e] * vp.c - Lt;
       } else {
         if (nloc && is_listed(y, loc, nloc)) continue;
-        const float p = exp2_fast(target_at(trow, y) * vp.c - Lt);
-        const float q = exp2_fast(zrow[y] * vp.c - Lz);
+        const float p = exp2_fast(tq[e] * vp.c - Lt);
+        const float q = exp2_fast(zq[e] * vp.c - Lz);
         const float r = v.alpha * p - v.beta * q;
         if (!(r > 0.0f)) continue;
         l2r = __builtin_amdgcn_logf(r);
