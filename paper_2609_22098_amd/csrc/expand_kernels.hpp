@@ -450,9 +450,15 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
       if constexpr (STORE_Z) {
         if (pidx[nb] < P) {
           float* zo = p.z_out + (size_t)pidx[nb] * V;
+          if ((V & 3) == 0 && tl + 16 <= V) {  // 16-byte aligned: four vector stores
 #pragma unroll
-          for (int j = 0; j < 16; ++j)
-            if (tl + j < V) zo[tl + j] = v[j];
+            for (int j = 0; j < 16; j += 4)
+              *reinterpret_cast<f32x4*>(zo + tl + j) = f32x4{v[j], v[j + 1], v[j + 2], v[j + 3]};
+          } else {
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+              if (tl + j < V) zo[tl + j] = v[j];
+          }
         }
       }
       float bm = max2_med3(v[0], v[1]);
