@@ -261,7 +261,15 @@ class HostTree:
         return self.token.shape[1]
 
     def struct(self):
-        return Tree(self.R, self.cap, *[getattr(self, f).ctypes.data for f, _ in Tree._fields_[2:]])
+        """The ts_tree view of the arrays.  Built once and reused while the same array
+        objects are attached (taking an array's address costs microseconds)."""
+        arrs = tuple(getattr(self, f) for f, _ in Tree._fields_[2:])
+        cached = self.__dict__.get("_struct")
+        if cached is not None and len(cached[0]) == len(arrs) and all(a is b for a, b in zip(cached[0], arrs)):
+            return cached[1]
+        st = Tree(self.R, self.cap, *[a.ctypes.data for a in arrs])
+        self.__dict__["_struct"] = (arrs, st)
+        return st
 
 
 class DeviceTree:
