@@ -39,6 +39,26 @@ __device__ __forceinline__ float target_at(const TT* row, int y) {
 // lies wholly before y1 in rows whose length is a multiple of 4 (vec) is read
 // with one vector load per row; otherwise token by token, and tokens at or
 // past y1 read as 0 (the callers skip them).  zrow may be null (z reads 0).
+template <bool HZ, typename TT>
+__device__ __forceinline__ void load_quad_vec(const TT* trow, const float* zrow, int b, float (&t)[4],
+                                              float (&z)[4]) {
+  if constexpr (sizeof(TT) == 2) {
+    const uint2 w = *reinterpret_cast<const uint2*>(trow + b);
+    t[0] = __uint_as_float(w.x << 16);
+    t[1] = __uint_as_float(w.x & 0xFFFF0000u);
+    t[2] = __uint_as_float(w.y << 16);
+    t[3] = __uint_as_float(w.y & 0xFFFF0000u);
+  } else {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(trow + b);
+    t[0] = v[0]; t[1] = v[1]; t[2] = v[2]; t[3] = v[3];
+  }
+  if constexpr (HZ) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(zrow + b);
+    z[0] = v[0]; z[1] = v[1]; z[2] = v[2]; z[3] = v[3];
+  } else {
+    z[0] = z[1] = z[2] = z[3] = 0.0f;
+  }
+}
 template <typename TT>
 __device__ __forceinline__ void load_quad(const TT* trow, const float* zrow, int b, int y1, bool vec,
                                           float (&t)[4], float (&z)[4]) {
@@ -67,6 +87,45 @@ __device__ __forceinline__ void load_quad(const TT* trow, const float* zrow, int
       z[e] = (zrow && y < y1) ? zrow[y] : 0.0f;
     }
   }
+}
+
+// One workgroup's pass over the tokens [y0, y1) of a target row and a draft
+// row (zrow may be null): thread t takes the quad y0 + 4t + 1024 s in sweep
+// s, in sweep order, and calls f(b, t[4], z[4], nv) with the quad's first
+// token b and its nv tokens before y1.  Sweeps whose quads are all whole
+// (vec: rows of a multiple of 4 tokens) are read four at a time, every load
+// issued before any use, so a workgroup waits for memory about once per four
+// sweeps.
+template <bool HZ, typename TT, typename F>
+__device__ __forceinline__ void sweep_rows(const TT* trow, const float* zrow, int y0, int y1, bool vec, F&& f) {
+  constexpr int kQ = kVerifyThreads * 4;  // tokens per sweep
+  const int b0 = y0 + 4 * threadIdx.x;
+  const int nfull = vec ? (y1 - y0) / kQ : 0;
+  int sw = 0;
+  for (; sw + 4 <= nfull; sw += 4) {
+    float t[4][4], z[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) load_quad_vec<HZ>(trow, zrow, b0 + (sw + u) * kQ, t[u], z[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) f(b0 + (sw + u) * kQ, t[u], z[u], 4);
+  }
+  for (; sw < nfull; ++sw) {
+    float t[4], z[4];
+    load_quad_vec<HZ>(trow, zrow, b0 + sw * kQ, t, z);
+    f(b0 + sw * kQ, t, z, 4);
+  }
+  for (int b = b0 + sw * kQ; b < y1; b += kQ) {
+    float t[4], z[4];
+    load_quad(trow, zrow, b, y1, vec, t, z);
+    f(b, t, z, min(4, y1 - b));
+  }
+}
+template <typename TT, typename F>
+__device__ __forceinline__ void sweep_chunk(const TT* trow, const float* zrow, int y0, int y1, bool vec, F&& f) {
+  if (zrow)
+    sweep_rows<true>(trow, zrow, y0, y1, vec, f);
+  else
+    sweep_rows<false>(trow, zrow, y0, y1, vec, f);
 }
 
 // Block-wide (256 threads) reductions with a fixed order: a wave butterfly,
@@ -402,32 +461,27 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
   const int nloc = item.m > 0 ? chunk_children(item, item.m, y0, y1, loc, &cnt) : 0;
   const bool vec = (vp.V & 3) == 0;
   float mt = kNegInf, mz = kNegInf;
-  for (int b = y0 + 4 * threadIdx.x; b < y1; b += kVChunkQuantum) {
-    float tq[4], zq[4];
-    load_quad(trow, zrow, b, y1, vec, tq, zq);
+  sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      if (b + e < y1) {
+      if (e < nv) {
         mt = fmaxf(mt, tq[e] * vp.c);
         if (zrow) mz = fmaxf(mz, zq[e] * vp.c);
       }
     }
-  }
+  });
   mt = block_max(mt, red);
   mz = block_max(mz, red);
   float st = 0.0f, snc = 0.0f;
-  for (int b = y0 + 4 * threadIdx.x; b < y1; b += kVChunkQuantum) {
-    float tq[4], zq[4];
-    load_quad(trow, zrow, b, y1, vec, tq, zq);
+  sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int y = b + e;
-      if (y < y1) {
+      if (e < nv) {
         st += exp2_fast(tq[e] * vp.c - mt);
-        if (zrow && !(nloc && is_listed(y, loc, nloc))) snc += exp2_fast(zq[e] * vp.c - mz);
+        if (zrow && !(nloc && is_listed(b + e, loc, nloc))) snc += exp2_fast(zq[e] * vp.c - mz);
       }
     }
-  }
+  });
   const double dst = block_sum_f64((double)st, redd);
   const double dsnc = block_sum_f64((double)snc, redd);
   if (threadIdx.x == 0) {
@@ -490,19 +544,16 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stage_kernel(VerifyPass
   const float Lt = j == 1 ? shc.Lt : C.Lt, Lz = j == 1 ? shc.Lz : C.Lz;
   const bool vec = (vp.V & 3) == 0;
   float acc = 0.0f;
-  for (int b = y0 + 4 * threadIdx.x; b < y1; b += kVChunkQuantum) {
-    float tq[4], zq[4];
-    load_quad(trow, zrow, b, y1, vec, tq, zq);
+  sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int y = b + e;
-      if (y < y1 && !(nloc && is_listed(y, loc, nloc))) {
+      if (e < nv && !(nloc && is_listed(b + e, loc, nloc))) {
         const float p = exp2_fast(tq[e] * vp.c - Lt);
         const float q = exp2_fast(zq[e] * vp.c - Lz);
         acc += fmaxf(rec.alpha * p - rec.betap * q, 0.0f);
       }
     }
-  }
+  });
   const double z = block_sum_f64((double)acc, redd);
   if (threadIdx.x == 0) vp.zp[((size_t)(j - 1) * vp.nitems + it) * vp.nchunks + ck] = z;
 }
@@ -541,15 +592,13 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_bonus_kernel(VerifyPass
   float bv = kNegInf, sv = kNegInf;
   int bi = 0x7FFFFFFF;
   const bool vec = (vp.V & 3) == 0;
-  for (int b = y0 + 4 * threadIdx.x; b < y1; b += kVChunkQuantum) {
+  sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
     uint32_t w0 = (uint32_t)b >> 2, w1 = pc1, w2 = pc2, w3 = c3;
     philox10(w0, w1, w2, w3, vp.keys);
-    float tq[4], zq[4];
-    load_quad(trow, zrow, b, y1, vec, tq, zq);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int y = b + e;
-      if (y >= y1) break;
+      if (e >= nv) break;
       float l2r;
       if (!zrow) {
         l2r = tq[e] * vp.c - Lt;
@@ -566,7 +615,7 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_bonus_kernel(VerifyPass
       if (key > bv) { sv = bv; bv = key; bi = y; }
       else if (key > sv) sv = key;
     }
-  }
+  });
   float vb = bv;
   int id = bi;
   block_argmax(vb, id, redv, redi);
