@@ -22,7 +22,8 @@
  *       W2 [V][r]     W2 of the Markov head: row v = W2[v], so the transition
  *                     bias is B(x, v) = <W1[x], W2[v]> (§3.1); as an r x V
  *                     matrix W this is W2 transposed
- *     All three share one dtype (TS_F32 or TS_BF16).  Accumulation is fp32.
+ *     All three share one dtype (TS_F32 or TS_BF16) and start at 16-byte
+     aligned addresses (TS_EINVAL otherwise).  Accumulation is fp32.
  *   - The library never frees, retains or writes caller tensors other than
  *     the documented outputs.  It allocates no device memory: scratch comes
  *     from the caller's workspace (sizes from the *_workspace_size calls).

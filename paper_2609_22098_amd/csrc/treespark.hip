@@ -72,6 +72,9 @@ int32_t check_drafter(const ts_drafter* d) {
   if (d->R <= 0 || d->D <= 0 || d->V <= 0 || d->r <= 0)
     return fail(TS_EINVAL, "drafter sizes must be positive (R=%d D=%d V=%d r=%d)", d->R, d->D, d->V, d->r);
   if (d->dtype != TS_F32 && d->dtype != TS_BF16) return fail(TS_EINVAL, "unknown dtype %d", d->dtype);
+  if (((reinterpret_cast<uintptr_t>(d->U) | reinterpret_cast<uintptr_t>(d->E) |
+        reinterpret_cast<uintptr_t>(d->W2)) & 15) != 0)
+    return fail(TS_EINVAL, "U, E and W2 must start at 16-byte aligned addresses");
   if (d->D > TS_MAX_D) return fail(TS_EUNSUPPORTED, "D=%d exceeds %d (4-bit path digits)", d->D, TS_MAX_D);
   if (d->R >= TS_MAX_R) return fail(TS_EUNSUPPORTED, "R=%d exceeds %d", d->R, TS_MAX_R - 1);
   if (d->V > TS_MAX_V) return fail(TS_EUNSUPPORTED, "V=%d exceeds %d", d->V, TS_MAX_V);

@@ -176,11 +176,42 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(const TT*
   const TT* row = target + (size_t)rows[i] * V;
   float bv = kNegInf, sv = kNegInf;
   int bi = 0x7FFFFFFF;
-  for (int y = threadIdx.x; y < V; y += kVerifyThreads) {
-    const float t = target_at(row, y);
+  auto take = [&](float t, int y) {
     if (t > bv) { sv = bv; bv = t; bi = y; }
     else if (t > sv) sv = t;
+  };
+  // 16-byte groups of G tokens (rows 16-byte aligned: V a multiple of G),
+  // four groups in flight per thread; each thread scans its tokens in
+  // increasing order, so ties keep the smallest id
+  constexpr int G = 16 / (int)sizeof(TT);
+  constexpr int kStep = kVerifyThreads * G;
+  int y0 = 0;
+  if (V % G == 0 && (reinterpret_cast<uintptr_t>(target) & 15) == 0) {
+    const int nfull = V / kStep;
+    int sw = 0;
+    for (; sw < nfull; sw += 4) {
+      u32x4 w[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (sw + u < nfull) w[u] = *reinterpret_cast<const u32x4*>(row + (sw + u) * kStep + G * threadIdx.x);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (sw + u >= nfull) break;
+        const int yb = (sw + u) * kStep + G * threadIdx.x;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if constexpr (sizeof(TT) == 2) {
+            take(__uint_as_float(w[u][k] << 16), yb + 2 * k);
+            take(__uint_as_float(w[u][k] & 0xFFFF0000u), yb + 2 * k + 1);
+          } else {
+            take(__uint_as_float(w[u][k]), yb + k);
+          }
+        }
+      }
+    }
+    y0 = nfull * kStep;
   }
+  for (int y = y0 + threadIdx.x; y < V; y += kVerifyThreads) take(target_at(row, y), y);
   float v = bv;
   int id = bi;
   block_argmax(v, id, redv, redi);
@@ -258,6 +289,13 @@ struct VerifyPass {
   VRec* recs;          // [TS_MAX_K][nitems]: record after the launch of stage j, at j - 1
   VerifyResult* results;  // [nitems], pinned host memory
 };
+
+// Rows can be read in aligned quads: a multiple of 4 tokens long, the target
+// at a 4-token-aligned address (the logits live in the workspace).
+template <typename TT>
+__device__ __forceinline__ bool vector_rows(const VerifyPass& vp) {
+  return (vp.V & 3) == 0 && (reinterpret_cast<uintptr_t>(vp.target) & (4 * sizeof(TT) - 1)) == 0;
+}
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
@@ -459,7 +497,7 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
   const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
   const float* zrow = item.m > 0 ? vp.zbuf + (size_t)item.zrow * vp.V : nullptr;
   const int nloc = item.m > 0 ? chunk_children(item, item.m, y0, y1, loc, &cnt) : 0;
-  const bool vec = (vp.V & 3) == 0;
+  const bool vec = vector_rows<TT>(vp);
   float mt = kNegInf, mz = kNegInf;
   sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
 #pragma unroll
@@ -542,7 +580,7 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stage_kernel(VerifyPass
   const float* zrow = vp.zbuf + (size_t)item.zrow * vp.V;
   const int nloc = chunk_children(item, j, y0, y1, loc, &cnt);
   const float Lt = j == 1 ? shc.Lt : C.Lt, Lz = j == 1 ? shc.Lz : C.Lz;
-  const bool vec = (vp.V & 3) == 0;
+  const bool vec = vector_rows<TT>(vp);
   float acc = 0.0f;
   sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
 #pragma unroll
@@ -591,7 +629,7 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_bonus_kernel(VerifyPass
   const uint32_t c3 = counter_word3(item.request, item.depth, 3u);
   float bv = kNegInf, sv = kNegInf;
   int bi = 0x7FFFFFFF;
-  const bool vec = (vp.V & 3) == 0;
+  const bool vec = vector_rows<TT>(vp);
   sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
     uint32_t w0 = (uint32_t)b >> 2, w1 = pc1, w2 = pc2, w3 = c3;
     philox10(w0, w1, w2, w3, vp.keys);

@@ -48,6 +48,11 @@ def test_expand_rejects_bad_arguments():
     assert _expand(_drafter(r=24)) == b.TS_EUNSUPPORTED
     assert _expand(_drafter(r=16, dtype=b.TS_BF16)) == b.TS_EUNSUPPORTED
     assert _expand(_drafter(dtype=7)) == b.TS_EINVAL
+    # model tensors must start 16-byte aligned (the kernels read them in 16-byte pieces)
+    bad = _drafter()
+    bad.W2 = FAKE + 8
+    assert _expand(bad) == b.TS_EINVAL
+    assert b"aligned" in L.ts_last_error()
     assert _expand(_drafter(), k=0) == b.TS_EINVAL
     assert _expand(_drafter(), k=17) == b.TS_EUNSUPPORTED
     assert _expand(_drafter(V=3), k=4) == b.TS_EINVAL
