@@ -29,21 +29,30 @@ __device__ __forceinline__ bool wslot_before(const WaveSlot& a, const WaveSlot& 
   return a.path < b.path;
 }
 
-// Exclusive scan of one int per thread of the workgroup; tmp: kWaveThreads ints of LDS.
+// Exclusive scan of one int per thread of the workgroup (total: the sum of
+// all): a shuffle scan inside each wave, then the wave totals in wave order.
+// tmp: at least kWaveThreads / 64 ints of LDS.
 __device__ __forceinline__ int wave_block_excl_scan(int v, int* tmp, int& total) {
-  const int t = threadIdx.x;
-  tmp[t] = v;
-  __syncthreads();
-  for (int o = 1; o < kWaveThreads; o <<= 1) {
-    const int x = t >= o ? tmp[t - o] : 0;
-    __syncthreads();
-    tmp[t] += x;
-    __syncthreads();
+  constexpr int kW = kWaveThreads / 64;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
   }
-  total = tmp[kWaveThreads - 1];
-  const int incl = tmp[t];
+  __syncthreads();  // tmp free (a previous scan's readers are done)
+  if (lane == 63) tmp[wv] = x;
   __syncthreads();
-  return incl - v;
+  int before = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < kW; ++w) {
+    const int tw = tmp[w];
+    before += w < wv ? tw : 0;
+    total += tw;
+  }
+  return before + x - v;
 }
 
 // Wave 0: every request's root is the one parent; lists empty.  The roots
