@@ -498,20 +498,26 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
   const float* zrow = item.m > 0 ? vp.zbuf + (size_t)item.zrow * vp.V : nullptr;
   const int nloc = item.m > 0 ? chunk_children(item, item.m, y0, y1, loc, &cnt) : 0;
   const bool vec = vector_rows<TT>(vp);
-  float mt = kNegInf, mz = kNegInf;
+  // one sweep: running maxima, and sums relative to them (rescaled when a
+  // maximum rises); the draft sum leaves the children out, its maximum does not
+  float mt = kNegInf, mz = kNegInf, st = 0.0f, snc = 0.0f;
   sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
+    float qt = kNegInf, qz = kNegInf;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       if (e < nv) {
-        mt = fmaxf(mt, tq[e] * vp.c);
-        if (zrow) mz = fmaxf(mz, zq[e] * vp.c);
+        qt = fmaxf(qt, tq[e] * vp.c);
+        if (zrow) qz = fmaxf(qz, zq[e] * vp.c);
       }
     }
-  });
-  mt = block_max(mt, red);
-  mz = block_max(mz, red);
-  float st = 0.0f, snc = 0.0f;
-  sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
+    if (qt > mt) {
+      if (st > 0.0f) st *= exp2_fast(mt - qt);
+      mt = qt;
+    }
+    if (qz > mz) {
+      if (snc > 0.0f) snc *= exp2_fast(mz - qz);
+      mz = qz;
+    }
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       if (e < nv) {
@@ -520,6 +526,12 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
       }
     }
   });
+  // to the workgroup's maxima
+  const float Mt = block_max(mt, red), Mz = block_max(mz, red);
+  st = st > 0.0f ? st * exp2_fast(mt - Mt) : 0.0f;
+  snc = snc > 0.0f ? snc * exp2_fast(mz - Mz) : 0.0f;
+  mt = Mt;
+  mz = Mz;
   const double dst = block_sum_f64((double)st, redd);
   const double dsnc = block_sum_f64((double)snc, redd);
   if (threadIdx.x == 0) {
