@@ -131,6 +131,76 @@ def test_sequential_serving_natural_trees(torch):
                  sampler="sequential")
 
 
+@pytest.fixture(scope="module")
+def chain_workload(torch):
+    """The high-load workload's shapes: V=151936, D=16, r=128, bf16, theta swept geometrically from
+    0.01 to 0.5 over the requests (one drafter for both temperatures).  64 of its 256 requests, the
+    same sweep: generating all 256 requests' inputs takes over a minute of host time."""
+    w = synth.WORKLOADS[4]
+    dr = synth.make_workload_drafter(4, seed=0, R=64)
+    anchors, thetas, _ = synth.make_controls(dr.R, dr.V, w["theta"], seed=0)
+    from paper_2609_22098_amd import binding
+    return w, dr, anchors, thetas, binding.drafter_from_host(dr)
+
+
+@pytest.mark.parametrize("T", [0.0, 1.0])
+def test_chain_collapse_theta_sweep(torch, chain_workload, T):
+    """All trees of the high-load workload in one call; 12 requests across the theta sweep
+    against the oracle.  With the deployed calibration (a=0.67, b=-0.46) an edge estimate of
+    at least 0.4 needs q0 >= 0.52, so at theta >= 0.4 no node can keep two children: those
+    trees are chains (one node per depth)."""
+    from paper_2609_22098_amd import binding
+    w, dr, anchors, thetas, dd = chain_workload
+    N, K = w["N"], w["K"]
+    tree = binding.build_tree(dd, anchors, thetas, N, K, T, 0)
+    picks = sorted(set(np.linspace(0, dr.R - 1, 12).round().astype(int).tolist()))
+    _compare_all(dr, tree, anchors, thetas, N, K, T, 0, requests=picks, tag=f"chain T={T}")
+    sizes = tree.n.astype(int)
+    print(f"chain T={T}: tree sizes {sizes.min()}..{sizes.max()}, mean {sizes.mean():.1f}; "
+          f"theta {float(thetas[0]):.3f}: {int(sizes[0])} nodes, theta {float(thetas[-1]):.3f}: {int(sizes[-1])}")
+    high = np.where(thetas >= 0.4)[0]
+    assert len(high) > 0
+    for q in high:
+        n = int(tree.n[q])
+        kids = np.bincount(tree.parent[q, 1:n + 1], minlength=n + 1) if n else np.zeros(1, int)
+        assert kids.max(initial=0) <= 1, f"request {q} (theta {float(thetas[q]):.3f}) is not a chain"
+        assert n <= dr.D
+    # the low end of the sweep keeps more nodes than the high end
+    assert sizes[: dr.R // 4].mean() > sizes[-dr.R // 4:].mean()
+
+    # verification of the compared requests against target rows U + N(0, 1) (other rows zero)
+    cap = N + 1
+    tgt = np.zeros((dr.R, cap, dr.V), np.uint16)
+    tgt32 = {}
+    for q in picks:
+        n1 = int(tree.n[q]) + 1
+        st, v = synth.make_target_rows(dr, q, tree.depth[q, :n1], w["target_sigma"], seed=4)
+        tgt[q, :n1] = st
+        tgt32[q] = v
+    target = torch.from_numpy(tgt).view(torch.bfloat16).cuda()
+    path, plen, bonus = binding.verify(dd, tree, target, T, 77)
+    om = o.Model(dr.U32, dr.E32, dr.W2_32)
+    ties = 0
+    for q in picks:
+        n1 = int(tree.n[q]) + 1
+        ot = o.Tree(int(tree.n[q]), 0, tree.token[q, :n1].copy(), tree.parent[q, :n1].copy(),
+                    tree.depth[q, :n1].copy(), tree.rank[q, :n1].copy(), tree.path[q, :n1].copy(),
+                    tree.log_surv[q, :n1].astype(np.float64), tree.log_q0[q, :n1].astype(np.float64),
+                    tree.log_qT[q, :n1].astype(np.float64), tree.key[q, :n1].astype(np.float64),
+                    np.zeros(n1), np.zeros(n1), float("nan"))
+        if T == 0:
+            rp, rb, gap = o.verify_greedy(ot, tgt32[q])
+        else:
+            rp, rb, gap = o.verify_sample(om, q, ot, tgt32[q], T, 77)
+        if gap <= 1e-4:
+            ties += 1
+            continue
+        assert list(path[q, :plen[q]]) == list(rp), (q, path[q, :plen[q]], rp)
+        assert bonus[q] == rb, (q, bonus[q], rb)
+    print(f"chain verify T={T}: {len(picks) - ties} requests compared, near-ties {ties}, "
+          f"accepted lengths {[int(plen[q]) for q in picks]}")
+
+
 # ---------------------------------------------------------------- verification
 
 def _prefixes(tree, q):
