@@ -348,7 +348,15 @@ template <typename TT>
 __device__ VConst verify_consts(const VerifyPass& vp, const VerifyItem& item, int it) {
   const int lane = threadIdx.x & 63;
   const int nc = vp.nchunks;
+  const int m = item.m;
   const VPartA* pa = vp.pa + (size_t)it * nc;
+  // child `lane`'s target value and draft logit, loaded alongside the partials
+  const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
+  const float* zrow = m > 0 ? vp.zbuf + (size_t)item.zrow * vp.V : nullptr;
+  const bool mine = lane < m;
+  const int ctok = mine ? item.child_tok[lane] : 0;
+  const float tv = mine ? target_at(trow, ctok) : 0.0f;
+  const float wzl = mine ? zrow[ctok] * vp.c : 0.0f;
   float mt = kNegInf, mz = kNegInf;
   for (int k = lane; k < nc; k += 64) {
     mt = fmaxf(mt, pa[k].mt);
@@ -359,51 +367,55 @@ __device__ VConst verify_consts(const VerifyPass& vp, const VerifyItem& item, in
   double st = 0.0, snc = 0.0;
   for (int k = lane; k < nc; k += 64) {
     st += pa[k].st * (double)exp2_fast(pa[k].mt - mt);
-    if (item.m > 0) snc += pa[k].snc * (double)exp2_fast(pa[k].mz - mz);
+    if (m > 0) snc += pa[k].snc * (double)exp2_fast(pa[k].mz - mz);
   }
   st = wave_sum_f64(st);
   snc = wave_sum_f64(snc);
   VConst C;
   C.Lt = mt + (float)log2(st);
   C.Lz = 0.0f;
-  const int m = item.m;
 #pragma unroll
   for (int k = 0; k < TS_MAX_K; ++k) {
     C.lp[k] = 0.0f; C.lq[k] = 0.0f; C.lR[k] = 0.0f; C.invR[k] = 0.0f; C.lu[k] = 0.0f;
   }
   if (m == 0) return C;
-  const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
-  const float* zrow = vp.zbuf + (size_t)item.zrow * vp.V;
-  // suffix sums of the proposal mass: suf[s] = non-children + children s..m-1
-  float wz[TS_MAX_K];
-  double suf[TS_MAX_K + 1];
-  {
-    double acc = snc;
-    suf[TS_MAX_K] = acc;
+  // suffix sums of the proposal mass, suf[s] = non-children + children s..m-1,
+  // added in the fixed order s = m-1 .. 0 from the children's terms of every lane
+  const double el = mine ? (double)exp2_fast(wzl - mz) : 0.0;
+  const uint64_t elb = __builtin_bit_cast(uint64_t, el);
+  double acc = snc, my_suf = snc;
 #pragma unroll
-    for (int s = TS_MAX_K - 1; s >= 0; --s) {
-      wz[s] = 0.0f;
-      if (s < m) {
-        wz[s] = zrow[item.child_tok[s]] * vp.c;
-        acc += (double)exp2_fast(wz[s] - mz);
-      }
-      suf[s] = acc;
+  for (int s = TS_MAX_K - 1; s >= 0; --s) {
+    if (s < m) {
+      const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)elb, s);
+      const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(elb >> 32), s);
+      acc += __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+      if (lane == s) my_suf = acc;
     }
   }
-  C.Lz = mz + (float)log2(suf[0]);
-  const uint32_t pc1 = (uint32_t)item.path, pc2 = (uint32_t)(item.path >> 32);
-  const uint32_t c3 = counter_word3(item.request, item.depth, 2u);
+  const double suf0 = acc;
+  C.Lz = mz + (float)log2(suf0);
+  // lane s: child s's terms
+  float lp = 0.0f, lq = 0.0f, lR = 0.0f, invR = 0.0f, lu = 0.0f;
+  if (mine) {
+    const double Rs = my_suf / suf0;
+    lp = tv * vp.c - C.Lt;
+    lq = wzl - C.Lz;
+    lR = (float)log2(Rs);
+    invR = (float)(1.0 / Rs);
+    uint32_t w0 = (uint32_t)(lane + 1), w1 = (uint32_t)item.path, w2 = (uint32_t)(item.path >> 32),
+             w3 = counter_word3(item.request, item.depth, 2u);
+    philox10(w0, w1, w2, w3, vp.keys);
+    lu = __builtin_amdgcn_logf(word_to_uniform(w0));
+  }
 #pragma unroll
   for (int s = 0; s < TS_MAX_K; ++s) {
     if (s < m) {
-      const double Rs = suf[s] / suf[0];
-      C.lp[s] = target_at(trow, item.child_tok[s]) * vp.c - C.Lt;
-      C.lq[s] = wz[s] - C.Lz;
-      C.lR[s] = (float)log2(Rs);
-      C.invR[s] = (float)(1.0 / Rs);
-      uint32_t w0 = (uint32_t)(s + 1), w1 = pc1, w2 = pc2, w3 = c3;
-      philox10(w0, w1, w2, w3, vp.keys);
-      C.lu[s] = __builtin_amdgcn_logf(word_to_uniform(w0));
+      C.lp[s] = lane_f32(lp, s);
+      C.lq[s] = lane_f32(lq, s);
+      C.lR[s] = lane_f32(lR, s);
+      C.invR[s] = lane_f32(invR, s);
+      C.lu[s] = lane_f32(lu, s);
     }
   }
   return C;
