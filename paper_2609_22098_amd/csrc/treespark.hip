@@ -606,6 +606,44 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   return TS_OK;
 }
 
+// The children of every tree node, in creation order, as flat per-request
+// lists: node p of request q has count(q, p) children starting at
+// first(q, p).  The arrays are kept per thread and reused, so indexing a
+// tree allocates nothing once they have grown to its size.
+struct KidIndex {
+  std::vector<int> off;   // [R][cap + 1]: start of node p's children in list
+  std::vector<int> list;  // [R][cap]: child ids, grouped by parent
+  int cap = 0;
+  const int* first(int q, int p) const { return list.data() + (size_t)q * cap + off[(size_t)q * (cap + 1) + p]; }
+  int count(int q, int p) const {
+    const size_t o = (size_t)q * (cap + 1) + p;
+    return off[o + 1] - off[o];
+  }
+};
+
+// Builds the index of a tree whose parents were checked (0 <= parent[i] < i).
+const KidIndex& kid_index(const ts_tree* t) {
+  thread_local KidIndex k;
+  const int R = t->R, cap = t->cap;
+  k.cap = cap;
+  k.off.assign((size_t)R * (cap + 1), 0);
+  k.list.resize((size_t)R * cap);
+  for (int q = 0; q < R; ++q) {
+    const int n = t->n[q];
+    int* off = k.off.data() + (size_t)q * (cap + 1);
+    const int32_t* par = t->parent + (size_t)q * cap;
+    for (int i = 1; i <= n; ++i) ++off[par[i] + 1];
+    for (int p = 0; p < cap; ++p) off[p + 1] += off[p];
+    // fill in increasing id order, which is creation order; off[p] ends at
+    // the start of node p + 1 and is moved back afterwards
+    int* list = k.list.data() + (size_t)q * cap;
+    for (int i = 1; i <= n; ++i) list[off[par[i]]++] = i;
+    for (int p = cap; p > 0; --p) off[p] = off[p - 1];
+    off[0] = 0;
+  }
+  return k;
+}
+
 struct VerifyLayout {
   size_t off_rows, off_arg, off_gap, off_items, off_z, off_exp;
   size_t off_pa, off_zp, off_bp, off_cst, off_rec, bytes;
@@ -947,11 +985,7 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
   char* ws = static_cast<char*>(workspace);
 
   // children of every node in creation order (= draw order)
-  std::vector<std::vector<std::vector<int>>> kids(R);
-  for (int q = 0; q < R; ++q) {
-    kids[q].assign(tree->n[q] + 1, {});
-    for (int i = 1; i <= tree->n[q]; ++i) kids[q][tree->parent[(size_t)q * cap + i]].push_back(i);
-  }
+  const KidIndex& kids = kid_index(tree);
   for (int q = 0; q < R; ++q) path_len[q] = 0;
 
   if (T == 0.0f) {
@@ -977,8 +1011,9 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
       for (;;) {
         const int gtok = arg[base + cur];
         int next = -1;
-        for (int c : kids[q][cur])
-          if (tree->token[(size_t)q * cap + c] == gtok) { next = c; break; }
+        const int* ch = kids.first(q, cur);
+        for (int j = 0, m = kids.count(q, cur); j < m; ++j)
+          if (tree->token[(size_t)q * cap + ch[j]] == gtok) { next = ch[j]; break; }
         if (next < 0 || len >= TS_MAX_D) { bonus[q] = gtok; break; }
         path_nodes[(size_t)q * TS_MAX_D + len++] = next;
         cur = next;
@@ -1012,8 +1047,8 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
       it.node = cur[q];
       it.depth = tree->depth[o];
       it.path = tree->path[o];
-      const std::vector<int>& ch = kids[q][cur[q]];
-      it.m = (int)std::min<size_t>(ch.size(), TS_MAX_K);
+      const int* ch = kids.first(q, cur[q]);
+      it.m = std::min(kids.count(q, cur[q]), TS_MAX_K);
       for (int j = 0; j < it.m; ++j) it.child_tok[j] = tree->token[(size_t)q * cap + ch[j]];
       it.zrow = -1;
       if (it.m > 0) {
@@ -1062,7 +1097,7 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     for (int i = 0; i < ni; ++i) {
       const int q = items[i].request;
       if (res[i].accepted > 0 && path_len[q] < TS_MAX_D) {
-        const int c = kids[q][cur[q]][res[i].accepted - 1];
+        const int c = kids.first(q, cur[q])[res[i].accepted - 1];
         path_nodes[(size_t)q * TS_MAX_D + path_len[q]++] = c;
         cur[q] = c;
         next.push_back(q);
