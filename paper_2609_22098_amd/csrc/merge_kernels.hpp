@@ -110,6 +110,51 @@ __device__ __forceinline__ void reglist_insert(RegList& l, int K, float v, int i
   l.cnt = min(l.cnt + 1, K);
 }
 
+// The accumulator seeds of a lane's four tokens tok0 + [0, 4): their U
+// values, -inf at or past V.  Every load reads a clamped index inside the
+// row and none sits under a condition, so all of a batch's loads are in
+// flight together (a conditional load becomes a branch that waits for its
+// own value); the tail select comes afterwards.
+template <typename TE>
+__device__ __forceinline__ void u_seeds(const TE* urow, int tok0, int V, float (&u)[4]) {
+  TE raw[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) raw[e] = urow[min(tok0 + e, V - 1)];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) u[e] = tok0 + e < V ? Frag<TE>::to_f32(raw[e]) : kNegInf;
+}
+// The same four seeds with one vector load, for a group that starts at a
+// multiple of 4 inside a row of V % 4 == 0 tokens (the row then starts 8-byte
+// aligned for bf16, 16-byte for f32) and ends at or before V.
+__device__ __forceinline__ void u_seeds4(const uint16_t* p, float (&u)[4]) {
+  const uint2 w = *reinterpret_cast<const uint2*>(p);
+  u[0] = __uint_as_float(w.x << 16);
+  u[1] = __uint_as_float(w.x & 0xFFFF0000u);
+  u[2] = __uint_as_float(w.y << 16);
+  u[3] = __uint_as_float(w.y & 0xFFFF0000u);
+}
+__device__ __forceinline__ void u_seeds4(const float* p, float (&u)[4]) {
+  const float4 v = *reinterpret_cast<const float4*>(p);
+  u[0] = v.x;
+  u[1] = v.y;
+  u[2] = v.z;
+  u[3] = v.w;
+}
+
+// All ones on the lanes where keep holds, zero elsewhere, through an empty
+// asm: masking a value with it (keep_or_zero) cannot be turned back into a
+// branch on keep, which would move the loads behind the value into that
+// branch, each waiting for its own result.
+__device__ __forceinline__ uint32_t opaque_mask(bool keep) {
+  uint32_t m = keep ? 0xFFFFFFFFu : 0u;
+  asm("" : "+v"(m));
+  return m;
+}
+// v where the mask is all ones, +0 where it is zero.
+__device__ __forceinline__ float keep_or_zero(float v, uint32_t mask) {
+  return __uint_as_float(__float_as_uint(v) & mask);
+}
+
 // Recompute up to kBatch runs of 16 tokens [t, t+16) for one parent with the
 // MFMA sequence of pass 1 (same operands in the same K positions, same
 // accumulator start), so the values are bit-identical to the streaming pass.
@@ -131,24 +176,49 @@ __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* uro
   const int V = p.V;
   const TE* W2 = static_cast<const TE*>(p.W2);
   f32x4 acc[kBatch];
+  const uint32_t col0 = opaque_mask(n == 0);
+  // whole aligned runs take vector seed loads (uniform over the wave)
+  bool vec = (V & 3) == 0;
 #pragma unroll
   for (int b = 0; b < kBatch; ++b) {
     const int tb = b < nrun ? t[b] : 0;
-    acc[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    if (n == 0) {
+    vec = vec && (tb & 3) == 0 && tb + 16 <= V;
+  }
+  // in two halves: all loads of a half first (one round trip), then its MFMAs
+  constexpr int kHalf = kBatch / 2;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int tok = tb + g * 4 + e;
-        acc[b][e] = tok < V ? F::to_f32(urow[min(tok, V - 1)]) : kNegInf;
+  for (int h = 0; h < 2; ++h) {
+    typename F::type wf[kHalf][KS];
+    float u[kHalf][4];
+#pragma unroll
+    for (int i = 0; i < kHalf; ++i) {
+      const int b = h * kHalf + i;
+      const int tb = b < nrun ? t[b] : 0;
+      const TE* wrow = W2 + (size_t)min(tb + n, V - 1) * p.r;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) wf[i][kk] = F::load(wrow, kk * F::kPerStep, g);
+    }
+    if (vec) {
+#pragma unroll
+      for (int i = 0; i < kHalf; ++i) {
+        const int b = h * kHalf + i;
+        u_seeds4(urow + (b < nrun ? t[b] : 0) + g * 4, u[i]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < kHalf; ++i) {
+        const int b = h * kHalf + i;
+        u_seeds(urow, (b < nrun ? t[b] : 0) + g * 4, V, u[i]);
       }
     }
-  }
 #pragma unroll
-  for (int b = 0; b < kBatch; ++b) {
-    const int tb = b < nrun ? t[b] : 0;
-    const TE* wrow = W2 + (size_t)min(tb + n, V - 1) * p.r;
+    for (int i = 0; i < kHalf; ++i) {
+      const int b = h * kHalf + i;
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) acc[b] = F::mma(F::load(wrow, kk * F::kPerStep, g), bcol[kk], acc[b]);
+      for (int e = 0; e < 4; ++e) acc[b][e] = keep_or_zero(u[i][e], col0);
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) acc[b] = F::mma(wf[i][kk], bcol[kk], acc[b]);
+    }
   }
   if (n == 0) {
 #pragma unroll
@@ -481,20 +551,25 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     // all loads of the block first (one round trip), then the MFMAs
     typename F::type wf[4][KS];
     f32x4 acc[4];
+    const uint32_t col0 = opaque_mask(n == 0);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const TE* wrow = W2 + (size_t)min(t0 + 16 * q + n, V - 1) * p.r;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) wf[q][kk] = F::load(wrow, kk * F::kPerStep, g);
-      acc[q] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-      if (n == 0) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int tok = t0 + 16 * q + g * 4 + e;
-          acc[q][e] = tok < V ? F::to_f32(urow[min(tok, V - 1)]) : kNegInf;
-        }
-      }
     }
+    float u[4][4];
+    if ((V & 3) == 0 && t0 + 4 * 16 <= V) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) u_seeds4(urow + t0 + 16 * q + g * 4, u[q]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) u_seeds(urow, t0 + 16 * q + g * 4, V, u[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[q][e] = keep_or_zero(u[q][e], col0);
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
