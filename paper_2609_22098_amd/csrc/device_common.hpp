@@ -190,6 +190,28 @@ __device__ __forceinline__ float opaque_inf() {
 __device__ __forceinline__ float max2_med3(float a, float b) {
   return __builtin_amdgcn_fmed3f(a, b, opaque_inf());
 }
+// All ones on the lanes where keep holds, zero elsewhere, through an empty
+// asm.  A choice between a loaded value and a constant written as a select
+// may be turned back into a branch on the condition, with the load moved
+// into it and waited for on its own; a mask the compiler cannot see into
+// keeps such loads unconditional, so that they are in flight together.
+__device__ __forceinline__ uint32_t opaque_mask(bool keep) {
+  uint32_t m = keep ? 0xFFFFFFFFu : 0u;
+  asm("" : "+v"(m));
+  return m;
+}
+// v where the mask is all ones, `other` where it is zero.
+__device__ __forceinline__ float keep_or(float v, uint32_t mask, float other) {
+  return __uint_as_float((__float_as_uint(v) & mask) | (__float_as_uint(other) & ~mask));
+}
+__device__ __forceinline__ int keep_or(int v, uint32_t mask, int other) {
+  return (int)(((uint32_t)v & mask) | ((uint32_t)other & ~mask));
+}
+// v where the mask is all ones, +0 where it is zero.
+__device__ __forceinline__ float keep_or_zero(float v, uint32_t mask) {
+  return __uint_as_float(__float_as_uint(v) & mask);
+}
+
 // Maximum over the four lanes n, n + 16, n + 32, n + 48 (each swap hands a
 // lane both values of its pair, as in cross_row_sum).
 __device__ __forceinline__ float cross_row_max(float v) {

@@ -143,12 +143,18 @@ struct URun<uint16_t> {
     w[0] = a[0]; w[1] = a[1]; w[2] = a[2]; w[3] = a[3];
     w[4] = b[0]; w[5] = b[1]; w[6] = b[2]; w[7] = b[3];
   }
+  // Tokens at or past V read as bf16 -inf (0xFF80).  Every load reads a
+  // clamped index and the tail is masked after, so the loads are in flight
+  // together.
   __device__ __forceinline__ void load_masked(const uint16_t* row, int t, int V) {
+    uint32_t raw[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) raw[i] = row[min(t + i, V - 1)];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int y0 = t + 2 * i, y1 = y0 + 1;
-      const uint32_t lo = y0 < V ? row[min(y0, V - 1)] : 0xFF80u;  // bf16 -inf
-      const uint32_t hi = y1 < V ? row[min(y1, V - 1)] : 0xFF80u;
+      const uint32_t m0 = opaque_mask(t + 2 * i < V), m1 = opaque_mask(t + 2 * i + 1 < V);
+      const uint32_t lo = (raw[2 * i] & m0) | (0xFF80u & ~m0);
+      const uint32_t hi = (raw[2 * i + 1] & m1) | (0xFF80u & ~m1);
       w[i] = lo | (hi << 16);
     }
   }
@@ -169,10 +175,13 @@ struct URun<float> {
     }
   }
   __device__ __forceinline__ void load_masked(const float* row, int t, int V) {
+    float raw[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) raw[i] = row[min(t + i, V - 1)];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const float v = row[min(t + i, V - 1)];
-      f[i] = (t + i < V) ? v : kNegInf;
+      const uint32_t m = opaque_mask(t + i < V);
+      f[i] = __uint_as_float((__float_as_uint(raw[i]) & m) | (0xFF800000u & ~m));
     }
   }
   __device__ __forceinline__ float get(int i) const { return f[i]; }

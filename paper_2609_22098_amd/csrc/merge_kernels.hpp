@@ -54,7 +54,7 @@ constexpr int kLdsSegs = 40;  // segments whose block table is kept in LDS (one 
 static_assert(kLdsSegs <= 64, "one segment per lane");
 struct DrawLds {
   float bz[4][16];               // logits of the drawn block
-  float seg_blk[kLdsSegs * 64];  // the parent's block table when V <= 40 * 4096
+  alignas(16) float seg_blk[kLdsSegs * 64];  // the parent's block table when V <= 40 * 4096
   int id[TS_MAX_K];              // draw j's token and logit at j - 1
   float z[TS_MAX_K];
 };
@@ -139,20 +139,6 @@ __device__ __forceinline__ void u_seeds4(const float* p, float (&u)[4]) {
   u[1] = v.y;
   u[2] = v.z;
   u[3] = v.w;
-}
-
-// All ones on the lanes where keep holds, zero elsewhere, through an empty
-// asm: masking a value with it (keep_or_zero) cannot be turned back into a
-// branch on keep, which would move the loads behind the value into that
-// branch, each waiting for its own result.
-__device__ __forceinline__ uint32_t opaque_mask(bool keep) {
-  uint32_t m = keep ? 0xFFFFFFFFu : 0u;
-  asm("" : "+v"(m));
-  return m;
-}
-// v where the mask is all ones, +0 where it is zero.
-__device__ __forceinline__ float keep_or_zero(float v, uint32_t mask) {
-  return __uint_as_float(__float_as_uint(v) & mask);
 }
 
 // Recompute up to kBatch runs of 16 tokens [t, t+16) for one parent with the
@@ -300,19 +286,20 @@ __device__ __forceinline__ float select_items_n(const MergeParams& p, const RunS
   float ev[kEntrySlots];
   int er[kEntrySlots];
   float rv[kRestSlots];
+  // Every load reads a clamped index, so all are in flight together.  A slot
+  // past the last chunk holds a copy of a real entry: it starts out taken in
+  // the threshold rounds below, and every later use checks the chunk range.
+  uint32_t taken = 0u;
 #pragma unroll
   for (int i = 0; i < kEntrySlots; ++i) {
     const int e = i * 64 + lane;
-    const bool in = (e >> 2) < S;
-    ev[i] = in ? sm.m[pb * kTopRuns + e] : kNegInf;
-    er[i] = in ? sm.r[pb * kTopRuns + e] : 0;
+    const size_t ec = pb * kTopRuns + min(e, S * kTopRuns - 1);
+    ev[i] = sm.m[ec];
+    er[i] = sm.r[ec];
+    taken |= (e >> 2) < S ? 0u : 1u << i;
   }
 #pragma unroll
-  for (int i = 0; i < kRestSlots; ++i) {
-    const int c = i * 64 + lane;
-    rv[i] = c < S ? sm.rest[pb + c] : kNegInf;
-  }
-  uint32_t taken = 0u;
+  for (int i = 0; i < kRestSlots; ++i) rv[i] = sm.rest[pb + min(i * 64 + lane, S - 1)];
   float thr = kNegInf;
   int picked = 0;
   for (int round = 0; round < K; ++round) {
@@ -477,15 +464,16 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     }
   };
   if (in_lds) {
-    float x[kLdsSegs];
-#pragma unroll
-    for (int k = 0; k < kLdsSegs; ++k) {
-      const int b = k * kBps + lane;
-      x[k] = (k < nseg && b < nblk) ? gblk[b] : kNegInf;
-    }
-#pragma unroll
-    for (int k = 0; k < kLdsSegs; ++k)
-      if (k < nseg) L.seg_blk[k * kBps + lane] = x[k];
+    // the row goes straight to LDS (no registers): each direct load moves
+    // 256 entries, 16 bytes per lane; a piece past the row's stride reads
+    // its last 16 bytes instead, and every entry at or past nblk (the last
+    // segment's tail) is set to -inf once the loads have landed
+    const int nent = nseg * kBps;
+    const int npc = (nent + 255) / 256;
+    for (int pc = 0; pc < npc; ++pc)
+      lds_dma16(gblk + min(pc * 256 + lane * 4, p.blk_ld - 4), reinterpret_cast<u32x4*>(L.seg_blk + pc * 256));
+    __builtin_amdgcn_s_waitcnt(0);
+    for (int b = nblk + lane; b < nent; b += 64) L.seg_blk[b] = kNegInf;
     wave_sync_lds();
     // lane l reduces segment l from LDS (no cross-lane steps); the 16-byte
     // pieces of its row are read in a lane-rotated order
@@ -514,7 +502,7 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int b = (s0 + k) * kBps + lane;
-        xs[k] = (s0 + k < nseg && b < nblk) ? gblk[b] : kNegInf;
+        xs[k] = keep_or(gblk[min(b, nblk - 1)], opaque_mask(s0 + k < nseg && b < nblk), kNegInf);
       }
       reduce8(s0, xs);
     }
@@ -711,9 +699,14 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
 #pragma unroll
   for (int i = 0; i < kRestSlots; ++i) {
     const int c = i * 64 + lane;
-    pm[i] = c < S ? p.part_m[pbase + c] : kNegInf;
-    ps[i] = c < S ? p.part_s0[pbase + c] : 0.0f;
-    pt[i] = (SAMPLE && p.need_T && c < S) ? p.part_sT[pbase + c] : 0.0f;
+    // clamped loads, masked after: all of them in flight together (without
+    // the z/T sums, their loads read the z sums and are masked out)
+    const size_t cc = pbase + min(c, S - 1);
+    const uint32_t in = opaque_mask(c < S);
+    const bool has_T = SAMPLE && p.need_T;
+    pm[i] = keep_or(p.part_m[cc], in, kNegInf);
+    ps[i] = keep_or_zero(p.part_s0[cc], in);
+    pt[i] = keep_or_zero((has_T ? p.part_sT : p.part_s0)[cc], in & opaque_mask(has_T));
   }
   float M = kNegInf;
 #pragma unroll

@@ -352,11 +352,13 @@ __device__ VConst verify_consts(const VerifyPass& vp, const VerifyItem& item, in
   const VPartA* pa = vp.pa + (size_t)it * nc;
   // child `lane`'s target value and draft logit, loaded alongside the partials
   const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
-  const float* zrow = m > 0 ? vp.zbuf + (size_t)item.zrow * vp.V : nullptr;
-  const bool mine = lane < m;
-  const int ctok = mine ? item.child_tok[lane] : 0;
-  const float tv = mine ? target_at(trow, ctok) : 0.0f;
-  const float wzl = mine ? zrow[ctok] * vp.c : 0.0f;
+  // loaded on every lane from valid addresses (a lane past m reads token 0
+  // of the item's rows, logit row 0 when there is none) and masked after
+  const uint32_t mine = opaque_mask(lane < m);
+  const int ctok = item.child_tok[min(lane, TS_MAX_K - 1)] & (int)mine;
+  const float* zrow = vp.zbuf + (size_t)max(item.zrow, 0) * vp.V;
+  const float tv = keep_or_zero(target_at(trow, ctok), mine);
+  const float wzl = keep_or_zero(zrow[ctok] * vp.c, mine);
   float mt = kNegInf, mz = kNegInf;
   for (int k = lane; k < nc; k += 64) {
     mt = fmaxf(mt, pa[k].mt);
@@ -458,10 +460,16 @@ __device__ __forceinline__ S share(const S& v, S* sh) {
 __device__ __forceinline__ int chunk_children(const VerifyItem& item, int n, int y0, int y1, int* loc,
                                               int* cnt) {
   if (threadIdx.x == 0) {
+    // every slot is loaded (the array is whole in each item) and stored, so
+    // the loads are in flight together; slots at or past n do not count
+    int x[TS_MAX_K];
+#pragma unroll
+    for (int s = 0; s < TS_MAX_K; ++s) x[s] = item.child_tok[s];
     int k = 0;
-    for (int s = 0; s < n; ++s) {
-      const int x = item.child_tok[s];
-      if (x >= y0 && x < y1) loc[k++] = x;
+#pragma unroll
+    for (int s = 0; s < TS_MAX_K; ++s) {
+      loc[k] = x[s];
+      k += (s < n && x[s] >= y0 && x[s] < y1) ? 1 : 0;
     }
     *cnt = k;
   }
