@@ -85,7 +85,9 @@ __device__ __forceinline__ float log_phat(float lq, float a, float b) {
 // CTRL: 0xB1 = quad_perm [1,0,3,2], 0x4E = quad_perm [2,3,0,1],
 // 0x141 = row_half_mirror (lane i <- 7 - i within 8), 0x140 = row_mirror
 // (i <- 15 - i within 16), 0x111 + (n - 1) = row_shr:n, 0x138 = wave_shr:1
-// (lane i <- i - 1 across the wave); lanes without a source read 0.
+// (lane i <- i - 1 across the wave), 0x142 = row_bcast:15 (lane 15 of a row
+// to every lane of the next row), 0x143 = row_bcast:31 (lane 31 to rows 2
+// and 3); lanes without a source read 0.
 template <int CTRL>
 __device__ __forceinline__ float dpp_f32(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
@@ -229,17 +231,25 @@ __device__ __forceinline__ float row_max(float v) {
   return fmaxf(v, dpp_f32<0x140>(v));
 }
 
+// DPP move with a row mask: rows outside `rows` keep 0 (the added term).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_rows_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xF, false));
+}
+
 // Inclusive prefix sum over the 64 lanes: a four-step scan inside each row of
-// 16 (row_shr 1, 2, 4, 8), then the totals of the rows before.
+// 16 (row_shr 1, 2, 4, 8), then the row totals passed on with the GFX9 row
+// broadcasts: lane 15 of each even row to the odd row after it (rows 1 and
+// 3), then lane 31 to rows 2 and 3.  With non-negative inputs every step
+// adds non-negative terms, so the sums never decrease along the lanes.
 __device__ __forceinline__ float wave_incl_scan(float x) {
   x += dpp_f32<0x111>(x);
   x += dpp_f32<0x112>(x);
   x += dpp_f32<0x114>(x);
   x += dpp_f32<0x118>(x);
-  const float r0 = lane_f32(x, 15), r1 = lane_f32(x, 31), r2 = lane_f32(x, 47);
-  const int row = (threadIdx.x & 63) >> 4;
-  const float off = row == 0 ? 0.0f : row == 1 ? r0 : row == 2 ? r0 + r1 : (r0 + r1) + r2;
-  return x + off;
+  x += dpp_rows_f32<0x142, 0xA>(x);
+  x += dpp_rows_f32<0x143, 0xC>(x);
+  return x;
 }
 
 }  // namespace ts
