@@ -223,6 +223,16 @@ __device__ __forceinline__ float cross_row_max(float v) {
   return max2_med3(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
+// wave_max for inputs that are never NaN: each step is one v_med3 with
+// +inf, without the NaN-quieting of both operands that fmaxf needs.
+__device__ __forceinline__ float wave_max_fin(float v) {
+  v = max2_med3(v, dpp_f32<0xB1>(v));
+  v = max2_med3(v, dpp_f32<0x4E>(v));
+  v = max2_med3(v, dpp_f32<0x141>(v));
+  v = max2_med3(v, dpp_f32<0x140>(v));
+  return max2_med3(max2_med3(lane_f32(v, 0), lane_f32(v, 16)), max2_med3(lane_f32(v, 32), lane_f32(v, 48)));
+}
+
 // Maximum over each row of 16 lanes (every lane of the row gets it).
 __device__ __forceinline__ float row_max(float v) {
   v = fmaxf(v, dpp_f32<0xB1>(v));

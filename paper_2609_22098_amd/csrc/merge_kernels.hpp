@@ -422,7 +422,8 @@ __device__ __forceinline__ int wave_pick(const float (&m)[NS], float u) {
 // level's largest one, so removing drawn tokens never underflows the rest.
 // The parent's block table lives in LDS when it fits (V <= 40 * 4096), else
 // in its rows of the workspace; a drawn token's block is rewritten in place.
-// Draw j lands in lane j - 1 of gl (token, z).
+// Draw j lands in lane j - 1 of gl (token, z).  Every value here is finite
+// or -inf (never NaN), so maxima take the median form.
 
 template <typename TE, int KS, int NSEG>
 __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, const TE* urow,
@@ -485,7 +486,7 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
       float m = kNegInf;
 #pragma unroll
       for (int i = 0; i < kBps / 4; ++i)
-        m = fmaxf(fmaxf(m, fmaxf(xv[i][0], xv[i][1])), fmaxf(xv[i][2], xv[i][3]));
+        m = max2_med3(max2_med3(m, max2_med3(xv[i][0], xv[i][1])), max2_med3(xv[i][2], xv[i][3]));
       if (m != kNegInf) {
         float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
@@ -521,7 +522,7 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     float mx = kNegInf;
 #pragma unroll
     for (int i = 0; i < NSEG; ++i) mx = fmaxf(mx, segL[i]);
-    mx = wave_max(mx);
+    mx = wave_max_fin(mx);
 #pragma unroll
     for (int i = 0; i < NSEG; ++i) ms[i] = segL[i] == kNegInf ? 0.0f : exp2_fast(segL[i] - mx);
     const int sg = wave_pick(ms, word_to_uniform(w0));
@@ -529,7 +530,7 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     const int b = sg * kBps + lane;
     const bool bin = sg >= 0 && b < nblk;
     const float lb = bin ? (in_lds ? L.seg_blk[b] : gblk[b]) : kNegInf;
-    const float mb = wave_max(lb);
+    const float mb = wave_max_fin(lb);
     float m2[1];
     m2[0] = lb == kNegInf ? 0.0f : exp2_fast(lb - mb);
     const int bo = wave_pick(m2, word_to_uniform(w1));
@@ -575,7 +576,7 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     bool live = y < V && bo >= 0;
     for (int k = 0; k < j - 1; ++k) live &= lane_i32(gl.id, k) != y;
     const float xy = live ? zy * p.cT : kNegInf;
-    const float mt = wave_max(xy);
+    const float mt = wave_max_fin(xy);
     float m3[1];
     m3[0] = live ? exp2_fast(xy - mt) : 0.0f;
     const int to = wave_pick(m3, word_to_uniform(w2));
@@ -589,7 +590,7 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     // the block and the segment lose the drawn token's mass; both sums are
     // taken relative to the largest value left, so nothing underflows
     const bool left = live && lane != to;
-    const float mt2 = wave_max(left ? xy : kNegInf);
+    const float mt2 = wave_max_fin(left ? xy : kNegInf);
     const float rest3 = wave_sum(left ? exp2_fast(xy - mt2) : 0.0f);
     const float lnew = mt2 == kNegInf ? kNegInf : mt2 + __builtin_amdgcn_logf(rest3);
     if (lane == bo && bin) {
@@ -605,7 +606,7 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
     const float lb2 = lane == bo ? lnew : lb;
-    const float mb2 = wave_max(lb2);
+    const float mb2 = wave_max_fin(lb2);
     const float rest2 = wave_sum(lb2 == kNegInf ? 0.0f : exp2_fast(lb2 - mb2));
     const float snew = mb2 == kNegInf ? kNegInf : mb2 + __builtin_amdgcn_logf(rest2);
 #pragma unroll
