@@ -53,7 +53,6 @@ struct MergeLds {
 constexpr int kLdsSegs = 40;  // segments whose block table is kept in LDS (one per lane)
 static_assert(kLdsSegs <= 64, "one segment per lane");
 struct DrawLds {
-  float bz[4][16];               // logits of the drawn block
   alignas(16) float seg_blk[kLdsSegs * 64];  // the parent's block table when V <= 40 * 4096
   int id[TS_MAX_K];              // draw j's token and logit at j - 1
   float z[TS_MAX_K];
@@ -427,7 +426,7 @@ __device__ __forceinline__ int wave_pick(const float (&m)[NS], float u) {
 
 template <typename TE, int KS, int NSEG>
 __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, const TE* urow,
-                                          const typename Frag<TE>::type (&bcol)[KS], uint32_t pc1,
+                                          const typename Frag<TE>::type (&erow_all)[KS], uint32_t pc1,
                                           uint32_t pc2, uint32_t pc3, DrawLds& L, RegList& gl) {
   typedef Frag<TE> F;
   const int lane = threadIdx.x & 63;
@@ -535,44 +534,41 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     m2[0] = lb == kNegInf ? 0.0f : exp2_fast(lb - mb);
     const int bo = wave_pick(m2, word_to_uniform(w1));
     const int bsel = sg * kBps + bo;
-    // level 3: token within the block; recompute its 64 logits (four runs of 16)
+    // level 3: token within the block; recompute its 64 logits (four runs of
+    // 16).  The operands are the streaming pass's with their roles swapped:
+    // E in every row of A, the run's W2 rows as the columns of B, so run q's
+    // logit of token t0 + 16 q + n lands in lane n + 16 i for every row
+    // group i (the matrix core gives the same values bit for bit either
+    // way).  Lane y takes run y / 16 and so holds token t0 + y; its seed is
+    // that token's U (-inf past V), the other runs' results on it are unused.
+    // Every load is issued before the MFMAs (one round trip).
     const int t0 = bsel * kBlkTokens;
-    // all loads of the block first (one round trip), then the MFMAs
+    const int y = t0 + lane;
     typename F::type wf[4][KS];
-    f32x4 acc[4];
-    const uint32_t col0 = opaque_mask(n == 0);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const TE* wrow = W2 + (size_t)min(t0 + 16 * q + n, V - 1) * p.r;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) wf[q][kk] = F::load(wrow, kk * F::kPerStep, g);
     }
-    float u[4][4];
-    if ((V & 3) == 0 && t0 + 4 * 16 <= V) {
+    const float useed = keep_or(F::to_f32(urow[min(y, V - 1)]), opaque_mask(y < V), kNegInf);
+    f32x4 acc[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) u_seeds4(urow + t0 + 16 * q + g * 4, u[q]);
-    } else {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) u_seeds(urow, t0 + 16 * q + g * 4, V, u[q]);
-    }
+    for (int q = 0; q < 4; ++q) acc[q] = f32x4{useed, useed, useed, useed};
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc[q][e] = keep_or_zero(u[q][e], col0);
+      for (int kk = 0; kk < KS; ++kk) acc[q] = F::mma(erow_all[kk], wf[q][kk], acc[q]);
+    // the four registers of a run's result hold the same value (every row of
+    // A is E); all four are read, so none of them is handed to another value
+    // while the matrix core may still be writing it (with only one register
+    // read, the compiler reused the other three a few wait states after the
+    // MFMA and the loaded W2 row came from a clobbered address)
+    float zq[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) acc[q] = F::mma(wf[q][kk], bcol[kk], acc[q]);
-    if (n == 0) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) L.bz[q][g * 4 + e] = acc[q][e];
-    }
-    wave_sync_lds();
-    const int y = t0 + lane;
-    const float zy = L.bz[lane >> 4][lane & 15];
-    wave_sync_lds();
+      zq[q] = max2_med3(__builtin_amdgcn_fmed3f(acc[q][0], acc[q][1], acc[q][2]), acc[q][3]);
+    const float zy = g == 0 ? zq[0] : g == 1 ? zq[1] : g == 2 ? zq[2] : zq[3];
     bool live = y < V && bo >= 0;
     for (int k = 0; k < j - 1; ++k) live &= lane_i32(gl.id, k) != y;
     const float xy = live ? zy * p.cT : kNegInf;
@@ -620,13 +616,13 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
 // most 64 segments (V <= 64 * 4096), so level 1 is a single scan.
 template <typename TE, int KS>
 __device__ __forceinline__ void seq_draws(const MergeParams& p, int pidx, const TE* urow,
-                                          const typename Frag<TE>::type (&bcol)[KS], uint32_t pc1,
+                                          const typename Frag<TE>::type (&erow_all)[KS], uint32_t pc1,
                                           uint32_t pc2, uint32_t pc3, DrawLds& L, RegList& gl) {
   const int nseg = (p.nblk + kSegTokens / kBlkTokens - 1) / (kSegTokens / kBlkTokens);
   if (nseg <= 64)
-    seq_draws_n<TE, KS, 1>(p, pidx, urow, bcol, pc1, pc2, pc3, L, gl);
+    seq_draws_n<TE, KS, 1>(p, pidx, urow, erow_all, pc1, pc2, pc3, L, gl);
   else
-    seq_draws_n<TE, KS, kSegSlots>(p, pidx, urow, bcol, pc1, pc2, pc3, L, gl);
+    seq_draws_n<TE, KS, kSegSlots>(p, pidx, urow, erow_all, pc1, pc2, pc3, L, gl);
 }
 
 template <typename TE, int KS, int MODE>
@@ -682,9 +678,14 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
 
   if constexpr (SEQ) {
     if (wv == 1) {
+      // the parent's E fragment on every lane: the A operand of the draws'
+      // block recompute
+      FT eall[KS];
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) eall[kk] = F::load(erow, kk * F::kPerStep, g);
       RegList dl;
       reglist_init(dl);
-      seq_draws<TE, KS>(p, pidx, urow, bcol, pc1, pc2, counter_word3(par.request, par.depth, 4u), sh.d, dl);
+      seq_draws<TE, KS>(p, pidx, urow, eall, pc1, pc2, counter_word3(par.request, par.depth, 4u), sh.d, dl);
       if (lane < K) {
         sh.d.id[lane] = dl.id;
         sh.d.z[lane] = dl.aux;
