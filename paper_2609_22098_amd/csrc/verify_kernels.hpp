@@ -424,22 +424,38 @@ __device__ VConst verify_consts(const VerifyPass& vp, const VerifyItem& item, in
 }
 
 // Record after the launch of stage j >= 2 from the record of stage j - 1.
-__device__ VRec verify_advance(const VerifyPass& vp, const VConst& C, const VRec& prev, int m, int it, int j) {
-  if (prev.status != kRejected) return prev;
+// Total Z of stage s for item it from its chunk partials (one whole wave; every
+// lane gets it, summed in a fixed order).  The partials are read whatever the
+// item's state, so the loads go out with the record's (unused unless the
+// record is a pending rejection at stage s).
+__device__ __forceinline__ double stage_z(const VerifyPass& vp, int it, int s) {
   const int lane = threadIdx.x & 63;
-  const double* zs = vp.zp + ((size_t)(prev.stage - 1) * vp.nitems + it) * vp.nchunks;
+  const double* zs = vp.zp + ((size_t)(s - 1) * vp.nitems + it) * vp.nchunks;
   double Z = 0.0;
   for (int k = lane; k < vp.nchunks; k += 64) Z += zs[k];
-  Z = wave_sum_f64(Z);
+  return wave_sum_f64(Z);
+}
+
+// Child j's acceptance constants (index j - 1 of the item's constants).
+struct VChild {
+  float lp, lq, lR, invR, lu;
+};
+__device__ __forceinline__ VChild child_consts(const VConst& C, int k) {
+  return VChild{C.lp[k], C.lq[k], C.lR[k], C.invR[k], C.lu[k]};
+}
+
+// The record for stage j from the one after stage j - 1: a pending rejection
+// divides alpha and beta by its stage's total Z and tests child j (or, past
+// the last child, ends the walk with the residual); any other state carries
+// over.
+__device__ __forceinline__ VRec verify_advance(const VRec& prev, double Z, const VChild& c, int m, int j) {
+  if (prev.status != kRejected) return prev;
   float alpha = prev.alpha, beta = prev.beta;
   if (Z > 0.0) {
     alpha = (float)(alpha / Z);
     beta = (float)(prev.betap / Z);
   }
-  if (j <= m) {
-    const int k = j - 1;
-    return stage_test(C.lp[k], C.lq[k], C.lR[k], C.invR[k], C.lu[k], j, alpha, beta, prev.margin);
-  }
+  if (j <= m) return stage_test(c.lp, c.lq, c.lR, c.invR, c.lu, j, alpha, beta, prev.margin);
   VRec r = prev;
   r.alpha = alpha;
   r.beta = beta;
@@ -571,15 +587,19 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
 template <typename TT>
 __global__ __launch_bounds__(kVerifyThreads) void verify_stage_kernel(VerifyPass vp, int j) {
   __shared__ VRec shr;
-  __shared__ VConst shc;
+  __shared__ float shL[2];
   __shared__ double redd[4];
   __shared__ int loc[TS_MAX_K];
   __shared__ int cnt;
+  __shared__ VerifyItem sitem;
   const int it = blockIdx.x / vp.nchunks, ck = blockIdx.x % vp.nchunks;
   if (it >= vp.nitems) return;
   const VerifyItem& item = vp.items[it];
+  constexpr int kItemWords = (int)(sizeof(VerifyItem) / 4);
   VRec rec;
   if (j == 1) {
+    if (threadIdx.x < kItemWords)
+      reinterpret_cast<int32_t*>(&sitem)[threadIdx.x] = reinterpret_cast<const int32_t*>(vp.items + it)[threadIdx.x];
     VConst C;
     if (threadIdx.x < 64) {
       C = verify_consts<TT>(vp, item, it);
@@ -593,25 +613,57 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stage_kernel(VerifyPass
                          __builtin_huge_valf());
       }
       if (ck == 0 && threadIdx.x == 0) vp.consts[it] = C;
+      if (threadIdx.x == 0) {
+        shL[0] = C.Lt;
+        shL[1] = C.Lz;
+      }
     }
-    C = share(C, &shc);
     rec = share(rec, &shr);
   } else {
+    // Wave 0 issues every load of the scalar step before using any (one
+    // round trip): a word of the item, the previous record, stage j - 1's Z
+    // partials (at clamped indices, masked after), child j's constants and
+    // the normalisers.  The empty asm consumes them all at one point, so
+    // none of the loads is moved behind a use.
     if (threadIdx.x < 64) {
+      const int lane = threadIdx.x;
+      const int nc = vp.nchunks;
+      constexpr int kZq = 4;  // partials per lane loaded up front (256 chunks)
+      const int32_t iw = reinterpret_cast<const int32_t*>(vp.items + it)[min(lane, kItemWords - 1)];
       const VRec prev = vp.recs[(size_t)(j - 2) * vp.nitems + it];
-      rec = prev;
-      if (prev.status == kRejected) rec = verify_advance(vp, vp.consts[it], prev, item.m, it, j);
+      const double* zs = vp.zp + ((size_t)(j - 2) * vp.nitems + it) * nc;
+      double zq[kZq];
+#pragma unroll
+      for (int q = 0; q < kZq; ++q) zq[q] = zs[min(lane + 64 * q, nc - 1)];
+      const VConst& C = vp.consts[it];
+      const VChild c = child_consts(C, j - 1);
+      const float Lt = C.Lt, Lz = C.Lz;
+      asm volatile("" ::"v"(iw), "v"(prev.alpha), "v"(prev.beta), "v"(prev.betap), "v"(prev.margin),
+                   "v"(prev.status), "v"(prev.stage), "v"(zq[0]), "v"(zq[1]), "v"(zq[2]), "v"(zq[3]),
+                   "v"(c.lp), "v"(c.lq), "v"(c.lR), "v"(c.invR), "v"(c.lu), "v"(Lt), "v"(Lz));
+      if (lane < kItemWords) reinterpret_cast<int32_t*>(&sitem)[lane] = iw;
+      // stage j - 1's total Z, in the order chunk k = lane, lane + 64, ...
+      double Z = 0.0;
+#pragma unroll
+      for (int q = 0; q < kZq; ++q) Z += lane + 64 * q < nc ? zq[q] : 0.0;
+      for (int k = lane + 64 * kZq; k < nc; k += 64) Z += zs[k];
+      Z = wave_sum_f64(Z);
+      if (lane == 0) {
+        shL[0] = Lt;
+        shL[1] = Lz;
+      }
+      const int m = __builtin_amdgcn_readlane(iw, (int)(offsetof(VerifyItem, m) / 4));  // the item's child count
+      rec = verify_advance(prev, Z, c, m, j);
     }
     rec = share(rec, &shr);
   }
   if (ck == 0 && threadIdx.x == 0) vp.recs[(size_t)(j - 1) * vp.nitems + it] = rec;
   if (rec.status != kRejected || rec.stage != j) return;
-  const VConst& C = vp.consts[it];
   const int y0 = ck * vp.chunk, y1 = min(vp.V, y0 + vp.chunk);
-  const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
-  const float* zrow = vp.zbuf + (size_t)item.zrow * vp.V;
-  const int nloc = chunk_children(item, j, y0, y1, loc, &cnt);
-  const float Lt = j == 1 ? shc.Lt : C.Lt, Lz = j == 1 ? shc.Lz : C.Lz;
+  const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)sitem.request * vp.cap + sitem.node) * vp.V;
+  const float* zrow = vp.zbuf + (size_t)sitem.zrow * vp.V;
+  const int nloc = chunk_children(sitem, j, y0, y1, loc, &cnt);
+  const float Lt = shL[0], Lz = shL[1];
   const bool vec = vector_rows<TT>(vp);
   float acc = 0.0f;
   sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
@@ -630,10 +682,11 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stage_kernel(VerifyPass
 
 // Final record of an item after the last stage launch (stage J): a pending
 // rejection at J is folded into the residual.
+// Every item has at most J children, so the fold never tests a child.
 __device__ __forceinline__ VRec verify_final(const VerifyPass& vp, const VerifyItem& item, int it, int J) {
   const VRec prev = vp.recs[(size_t)(J - 1) * vp.nitems + it];
-  if (prev.status != kRejected) return prev;
-  return verify_advance(vp, vp.consts[it], prev, item.m, it, J + 1);
+  const double Z = stage_z(vp, it, J);
+  return verify_advance(prev, Z, VChild{}, item.m, J + 1);
 }
 
 // Bonus: when every child was rejected (or there is none), the chunk's best
