@@ -32,7 +32,7 @@ void launch_tree_mask(const int32_t* parent, const int32_t* n, int R, int cap, c
 // expansion (one workgroup per request), the trees.
 void launch_wave_init(const WaveParams& wp, hipStream_t s);
 void launch_wave_control(const WaveParams& wp, int w, hipStream_t s);
-void launch_wave_tree(const WaveParams& wp, const WaveTreeOut& o, hipStream_t s);
+void launch_wave_tree(const WaveParams& wp, const WaveTreeOut& o, const WaveTreeOut& o2, hipStream_t s);
 // Calibration: greedy labels of host-built trees, and the two-scalar fit.
 void launch_calib_labels(const int32_t* parent, const int32_t* token, const float* log_q0, const int32_t* n,
                          int R, int cap, const int32_t* greedy, const int32_t* off, float* x, int32_t* y,

@@ -582,12 +582,9 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   st.key = reinterpret_cast<float*>(dt + tb.key);
   WaveTreeOut ho = tree_out_of(&st);
   ho.err = reinterpret_cast<int32_t*>(htree + tb.err);
-  launch_wave_tree(wp, ho, s);
+  // one launch writes the host's copy and, when given, the device copy
+  launch_wave_tree(wp, ho, device_out ? tree_out_of(device_out) : WaveTreeOut{}, s);
   TS_HIP(hipGetLastError());
-  if (device_out) {
-    launch_wave_tree(wp, tree_out_of(device_out), s);
-    TS_HIP(hipGetLastError());
-  }
   TS_HIP(hipStreamSynchronize(s));
   if (*reinterpret_cast<const volatile int32_t*>(htree + tb.err) != 0)
     return fail(TS_EINTERNAL, "a tree slot has no materialised parent");

@@ -177,9 +177,25 @@ __global__ __launch_bounds__(kWaveThreads) void wave_control_kernel(const WavePa
     }
 }
 
+// One tree row into one output.
+__device__ __forceinline__ void put_tree_row(const WaveTreeOut& o, size_t i, int32_t tok, int32_t parent, int32_t depth,
+                                             int32_t rank, uint64_t path, float ls, float lq0, float lqT, float key) {
+  o.token[i] = tok;
+  o.parent[i] = parent;
+  o.depth[i] = depth;
+  o.rank[i] = rank;
+  o.path[i] = path;
+  o.log_surv[i] = ls;
+  o.log_q0[i] = lq0;
+  o.log_qT[i] = lqT;
+  o.key[i] = key;
+}
+
 // The trees: node 0 is the root, nodes 1..n the list in pop order; rows past
-// n get parent -1, token -1 and NaN values.
-__global__ __launch_bounds__(kWaveThreads) void wave_tree_kernel(const WaveParams wp, const WaveTreeOut o) {
+// n get parent -1, token -1 and NaN values.  Written to o, and to o2 as well
+// when o2.n is not null (one pass for the host's copy and a device copy).
+__global__ __launch_bounds__(kWaveThreads) void wave_tree_kernel(const WaveParams wp, const WaveTreeOut o,
+                                                                 const WaveTreeOut o2) {
   __shared__ int dep[kWaveMaxN + 1];
   __shared__ uint64_t pth[kWaveMaxN + 1];
   const int q = blockIdx.x, t = threadIdx.x;
@@ -228,19 +244,16 @@ __global__ __launch_bounds__(kWaveThreads) void wave_tree_kernel(const WaveParam
       lqT = sl.log_qT;
       key = sl.key;
     }
-    o.token[b + c] = tok;
-    o.parent[b + c] = parent;
-    o.depth[b + c] = depth;
-    o.rank[b + c] = rank;
-    o.path[b + c] = path;
-    o.log_surv[b + c] = ls;
-    o.log_q0[b + c] = lq0;
-    o.log_qT[b + c] = lqT;
-    o.key[b + c] = key;
+    put_tree_row(o, b + c, tok, parent, depth, rank, path, ls, lq0, lqT, key);
+    if (o2.n) put_tree_row(o2, b + c, tok, parent, depth, rank, path, ls, lq0, lqT, key);
   }
   if (t == 0) {
     o.n[q] = s;
     if (o.evals) o.evals[q] = wp.evals[q];
+    if (o2.n) {
+      o2.n[q] = s;
+      if (o2.evals) o2.evals[q] = wp.evals[q];
+    }
   }
 }
 

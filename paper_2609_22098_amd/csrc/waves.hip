@@ -15,8 +15,8 @@ void launch_wave_control(const WaveParams& wp, int w, hipStream_t s) {
   hipLaunchKernelGGL(wave_control_kernel, dim3(wp.R), dim3(kWaveThreads), 0, s, wp, w);
 }
 
-void launch_wave_tree(const WaveParams& wp, const WaveTreeOut& o, hipStream_t s) {
-  hipLaunchKernelGGL(wave_tree_kernel, dim3(wp.R), dim3(kWaveThreads), 0, s, wp, o);
+void launch_wave_tree(const WaveParams& wp, const WaveTreeOut& o, const WaveTreeOut& o2, hipStream_t s) {
+  hipLaunchKernelGGL(wave_tree_kernel, dim3(wp.R), dim3(kWaveThreads), 0, s, wp, o, o2);
 }
 
 }  // namespace ts
