@@ -194,8 +194,8 @@ def main():
         write_traffic(args.traffic_from, args.T, args.sampler)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the draft-tree step has no "
-              f"multi-GPU path in this build.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the draft-tree step runs on "
+              f"a single GPU (how it would shard is described in the design notes).", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -53,7 +53,7 @@ extern "C" {
 typedef enum {
   TS_OK = 0,
   TS_EINVAL = -1,        /* bad argument (null pointer, size out of range, ...) */
-  TS_EUNSUPPORTED = -2,  /* valid but not supported by this build (see limits) */
+  TS_EUNSUPPORTED = -2,  /* valid but beyond the library's limits (below) */
   TS_EHIP = -3,          /* a HIP runtime call failed */
   TS_ENOSPACE = -4,      /* workspace smaller than the *_workspace_size result */
   TS_EINTERNAL = -5      /* an internal consistency check failed */
@@ -75,7 +75,7 @@ typedef enum { TS_F32 = 0, TS_BF16 = 1 } ts_dtype;
  * The sampler does not matter at T = 0. */
 typedef enum { TS_SAMPLER_GUMBEL = 0, TS_SAMPLER_SEQUENTIAL = 1 } ts_sampler;
 
-/* Limits of this build: K <= TS_MAX_K siblings, D <= TS_MAX_D (the path id
+/* Limits of the library: K <= TS_MAX_K siblings, D <= TS_MAX_D (the path id
  * holds 4 bits per level), R < 2^20 requests, V <= TS_MAX_V; the rank r is
  * one of 32, 64, 128, 256 for bf16 and one of 16, 32, 64 for fp32. */
 #define TS_MAX_K 16
