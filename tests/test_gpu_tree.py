@@ -251,6 +251,48 @@ def test_verify_parity_multi_request(torch, T):
           f"accepted lengths {list(plen)}")
 
 
+@pytest.mark.parametrize("T", [0.7, 1.0])
+def test_verify_parity_many_chunks(torch, T):
+    """ts_verify against the oracle walk with a 300000-token vocabulary and two requests: each
+    level item spans 293 chunks, more than the 256 whose Z partials a stage loads up front, so
+    the stages also sum the rest in the same order."""
+    from paper_2609_22098_amd import binding
+    R, V = 2, 300000
+    dr = synth.make_drafter(V, 3, 32, R=R, dtype="bf16", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
+                            ew_sigma=0.3, seed=9, u_scale=2.0)
+    anchors, _, _ = synth.make_controls(R, dr.V, 0.0, seed=9)
+    thetas = np.full(R, 0.001, np.float32)
+    N, K = 6, 3
+    dd, tree = _trees(dr, anchors, thetas, N, K, T, 4)
+    cap = N + 1
+    tgt = np.zeros((R, cap, dr.V), np.uint16)
+    tgt32 = np.zeros((R, cap, dr.V), np.float32)
+    for q in range(R):
+        n1 = int(tree.n[q]) + 1
+        s, v = synth.make_target_rows(dr, q, tree.depth[q, :n1], 1.0, seed=3)
+        tgt[q, :n1], tgt32[q, :n1] = s, v
+    target = torch.from_numpy(tgt).view(torch.bfloat16).cuda()
+    path, plen, bonus = binding.verify(dd, tree, target, T, 41)
+    om = o.Model(dr.U32, dr.E32, dr.W2_32)
+    compared = 0
+    for q in range(R):
+        n1 = int(tree.n[q]) + 1
+        ot = o.Tree(int(tree.n[q]), 0, tree.token[q, :n1].copy(), tree.parent[q, :n1].copy(),
+                    tree.depth[q, :n1].copy(), tree.rank[q, :n1].copy(), tree.path[q, :n1].copy(),
+                    tree.log_surv[q, :n1].astype(np.float64), tree.log_q0[q, :n1].astype(np.float64),
+                    tree.log_qT[q, :n1].astype(np.float64), tree.key[q, :n1].astype(np.float64),
+                    np.zeros(n1), np.zeros(n1), float("nan"))
+        rp, rb, gap = o.verify_sample(om, q, ot, tgt32[q, :n1], T, 41)
+        if gap <= 1e-4:
+            continue
+        compared += 1
+        assert list(path[q, :plen[q]]) == list(rp), (q, path[q, :plen[q]], rp)
+        assert bonus[q] == rb, (q, bonus[q], rb)
+    assert compared > 0
+    print(f"verify V={V} T={T}: {compared} of {R} requests compared, tree sizes {list(tree.n)}, "
+          f"accepted lengths {list(plen)}")
+
+
 @pytest.mark.parametrize("sampler", ["gumbel", "sequential"])
 def test_verify_losslessness_chi_square(torch, sampler):
     """Proposition 1 on the GPU: 1e5 replicate requests (independent Philox streams through the
