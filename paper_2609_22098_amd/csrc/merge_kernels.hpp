@@ -463,15 +463,21 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
         if (sg < nseg && sg == 64 * i + lane) segL[i] = l;
     }
   };
+  // the row goes straight to LDS (no registers): each direct load moves 256
+  // entries, 16 bytes per lane; a piece past the row's stride reads its last
+  // 16 bytes instead, and every entry at or past nblk (the last segment's
+  // tail) is set to -inf once the loads have landed
+  const int nent = nseg * kBps;
   if (in_lds) {
-    // the row goes straight to LDS (no registers): each direct load moves
-    // 256 entries, 16 bytes per lane; a piece past the row's stride reads
-    // its last 16 bytes instead, and every entry at or past nblk (the last
-    // segment's tail) is set to -inf once the loads have landed
-    const int nent = nseg * kBps;
     const int npc = (nent + 255) / 256;
     for (int pc = 0; pc < npc; ++pc)
       lds_dma16(gblk + min(pc * 256 + lane * 4, p.blk_ld - 4), reinterpret_cast<u32x4*>(L.seg_blk + pc * 256));
+  }
+  // the words of every draw (lane j - 1 computes draw j's Philox call), while
+  // the table loads are in flight
+  uint32_t dw0 = (uint32_t)(lane + 1), dw1 = pc1, dw2 = pc2, dw3 = pc3;
+  philox10(dw0, dw1, dw2, dw3, p.keys);
+  if (in_lds) {
     __builtin_amdgcn_s_waitcnt(0);
     for (int b = nblk + lane; b < nent; b += 64) L.seg_blk[b] = kNegInf;
     wave_sync_lds();
@@ -507,9 +513,6 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
       reduce8(s0, xs);
     }
   }
-  // the words of every draw: lane j - 1 computes draw j's Philox call
-  uint32_t dw0 = (uint32_t)(lane + 1), dw1 = pc1, dw2 = pc2, dw3 = pc3;
-  philox10(dw0, dw1, dw2, dw3, p.keys);
   gl.cnt = 0;
 #pragma unroll 1
   for (int j = 1; j <= p.K; ++j) {
@@ -678,6 +681,9 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
 
   if constexpr (SEQ) {
     if (wv == 1) {
+      // the draws are the longer of the two chains: their wave issues first
+      // when both waves of a SIMD are ready
+      __builtin_amdgcn_s_setprio(2);
       // the parent's E fragment on every lane: the A operand of the draws'
       // block recompute
       FT eall[KS];
