@@ -242,17 +242,20 @@ def main():
                 torch.empty((dr.R, N + 1), dtype=torch.int32, device="cuda"))
     nsteps = args.steps + args.warmup
     ev = HipEvents(3 * nsteps)
+    # a serving loop holds its stream and output buffers across rounds
+    stream = torch.cuda.current_stream()
+    vout = (np.zeros((dr.R, binding.TS_MAX_D), np.int32), np.zeros(dr.R, np.int32), np.zeros(dr.R, np.int32))
 
     def step(i):
         d = drafters[i % 2]
         binding.expand(d, parents, P, K, T, seed, outputs=outs, workspace=ws_e, events=ev.address(3 * i),
-                       sampler=sampler)
+                       sampler=sampler, stream=stream)
         if args.expand_only:
             return
         binding.build_tree(d, anchors, thetas, N, K, T, seed, workspace=ws_b, tree=tree, sampler=sampler,
-                           device_tree=dtree)
-        binding.tree_mask(dtree.parent, dtree.n, N + 1, out=mask_out)
-        binding.verify(d, tree, tgt, T, seed, workspace=ws_v)
+                           device_tree=dtree, stream=stream)
+        binding.tree_mask(dtree.parent, dtree.n, N + 1, out=mask_out, stream=stream)
+        binding.verify(d, tree, tgt, T, seed, workspace=ws_v, stream=stream, out=vout)
 
     for i in range(args.warmup):
         step(i)

@@ -326,15 +326,22 @@ def verify_workspace_size(d: DeviceDrafter, cap, T):
     return lib().ts_verify_workspace_size(d.ref(), cap, float(T))
 
 
-def verify(d: DeviceDrafter, tree: HostTree, target, T, seed, workspace=None, stream=None):
+def verify(d: DeviceDrafter, tree: HostTree, target, T, seed, workspace=None, stream=None, out=None):
     """ts_verify.  target: device tensor [R][cap][V] (float32 or bfloat16).
-    Returns (path_nodes [R][16], path_len [R], bonus [R]) as numpy arrays."""
+    Returns (path_nodes [R][16], path_len [R], bonus [R]) as numpy arrays; out = (path_nodes,
+    path_len, bonus) reuses given int32 arrays of those shapes."""
     torch = _torch()
     R, cap = tree.R, tree.cap
     assert tuple(target.shape) == (R, cap, d.V) and target.is_contiguous()
-    path = np.zeros((R, TS_MAX_D), np.int32)
-    plen = np.zeros(R, np.int32)
-    bonus = np.zeros(R, np.int32)
+    if out is None:
+        path = np.zeros((R, TS_MAX_D), np.int32)
+        plen = np.zeros(R, np.int32)
+        bonus = np.zeros(R, np.int32)
+    else:
+        path, plen, bonus = out
+        assert path.shape == (R, TS_MAX_D) and plen.shape == (R,) and bonus.shape == (R,)
+        assert path.dtype == plen.dtype == bonus.dtype == np.int32
+        assert path.flags.c_contiguous and plen.flags.c_contiguous and bonus.flags.c_contiguous
     if workspace is None:
         n = verify_workspace_size(d, cap, T)
         workspace = torch.empty((max(n, 1),), dtype=torch.uint8, device=target.device)
@@ -356,13 +363,13 @@ def tree_mask(parent, n, cap, pos_offset=None, stream=None, out=None):
     R = parent.shape[0]
     assert tuple(parent.shape) == (R, cap) and parent.dtype == torch.int32 and parent.is_contiguous()
     assert tuple(n.shape) == (R,) and n.dtype == torch.int32
-    W = lib().ts_tree_mask_words(cap)
     if out is None:
+        W = lib().ts_tree_mask_words(cap)
         mask = torch.empty((R, cap, W), dtype=torch.int32, device=parent.device)
         pos = torch.empty((R, cap), dtype=torch.int32, device=parent.device)
     else:
         mask, pos = out
-        assert tuple(mask.shape) == (R, cap, W) and tuple(pos.shape) == (R, cap)
+        assert tuple(mask.shape) == (R, cap, (cap + 31) // 32) and tuple(pos.shape) == (R, cap)
     off = ctypes.c_void_p(pos_offset.data_ptr()) if pos_offset is not None else None
     rc = lib().ts_tree_mask(ctypes.c_void_p(parent.data_ptr()), ctypes.c_void_p(n.data_ptr()), R, cap, off,
                             ctypes.c_void_p(mask.data_ptr()), ctypes.c_void_p(pos.data_ptr()), _stream(stream))
