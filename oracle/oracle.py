@@ -53,7 +53,7 @@ class _Tree(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int), ("evals", ctypes.c_int)] + [
         (name, ctypes.c_void_p) for name in
         ("token", "parent", "depth", "rank", "path", "log_surv", "log_q0", "log_qT", "key",
-         "margin", "eval_gap")] + [("stop_key", ctypes.c_double)]
+         "margin", "eval_gap", "draw_gap")] + [("stop_key", ctypes.c_double)]
 
 
 _P = ctypes.c_void_p
@@ -178,13 +178,14 @@ class Tree:
     key: np.ndarray
     margin: np.ndarray
     eval_gap: np.ndarray
+    draw_gap: np.ndarray
     stop_key: float
     _keep: tuple = ()
 
     def struct(self):
         s = _Tree(self.n, self.evals, *[a.ctypes.data for a in (
             self.token, self.parent, self.depth, self.rank, self.path, self.log_surv, self.log_q0,
-            self.log_qT, self.key, self.margin, self.eval_gap)], self.stop_key)
+            self.log_qT, self.key, self.margin, self.eval_gap, self.draw_gap)], self.stop_key)
         return s
 
 
@@ -195,7 +196,7 @@ def expand_tree(model: Model, request, anchor, theta, N, K, T, seed, a=0.67, b=-
                depth=np.zeros(cap, np.int32), rank=np.zeros(cap, np.int32),
                path=np.zeros(cap, np.uint64), log_surv=np.zeros(cap), log_q0=np.zeros(cap),
                log_qT=np.zeros(cap), key=np.zeros(cap), margin=np.zeros(cap),
-               eval_gap=np.zeros(cap))
+               eval_gap=np.zeros(cap), draw_gap=np.zeros(cap))
     t = Tree(0, 0, stop_key=float("nan"), **arr)
     s = t.struct()
     rc = lib().tso_expand_tree(model.struct, request, anchor, float(theta), N, K, float(a), float(b),
@@ -229,26 +230,26 @@ def verify_greedy(tree: Tree, target: np.ndarray):
     V = target.shape[-1]
     assert target.shape[0] >= tree.n + 1
     path = np.zeros(max(1, tree.n), np.int32)
-    plen = np.zeros(1, np.int32); bonus = np.zeros(1, np.int32); gap = np.zeros(1)
+    plen = np.zeros(1, np.int32); bonus = np.zeros(1, np.int32); gap = np.zeros(tree.n + 1)
     s = _tree_struct(tree)
     rc = lib().tso_verify_greedy(ctypes.byref(s), _ptr(target), V, _ptr(path), _ptr(plen), _ptr(bonus),
                                  _ptr(gap))
     if rc != 0:
         raise ValueError("tso_verify_greedy: invalid arguments")
-    return path[:plen[0]].copy(), int(bonus[0]), float(gap[0])
+    return path[:plen[0]].copy(), int(bonus[0]), gap[:plen[0] + 1].copy()
 
 
 def verify_sample(model: Model, request, tree: Tree, target: np.ndarray, T, seed):
     target = np.ascontiguousarray(target, dtype=np.float32)
     assert target.shape[-1] == model.V and target.shape[0] >= tree.n + 1
     path = np.zeros(max(1, tree.n), np.int32)
-    plen = np.zeros(1, np.int32); bonus = np.zeros(1, np.int32); margin = np.zeros(1)
+    plen = np.zeros(1, np.int32); bonus = np.zeros(1, np.int32); margin = np.zeros(tree.n + 1)
     s = _tree_struct(tree)
     rc = lib().tso_verify_sample(model.struct, request, ctypes.byref(s), _ptr(target), float(T), seed,
                                  _ptr(path), _ptr(plen), _ptr(bonus), _ptr(margin))
     if rc != 0:
         raise ValueError("tso_verify_sample: invalid arguments")
-    return path[:plen[0]].copy(), int(bonus[0]), float(margin[0])
+    return path[:plen[0]].copy(), int(bonus[0]), margin[:plen[0] + 1].copy()
 
 
 def residual_stages(p, qT, x):
@@ -283,7 +284,7 @@ def expand_forest(model: Model, anchors, thetas, N, budget, K, T, seed, a=0.67, 
                    depth=np.zeros(cap, np.int32), rank=np.zeros(cap, np.int32),
                    path=np.zeros(cap, np.uint64), log_surv=np.zeros(cap), log_q0=np.zeros(cap),
                    log_qT=np.zeros(cap), key=np.zeros(cap), margin=np.zeros(cap),
-                   eval_gap=np.zeros(cap))
+                   eval_gap=np.zeros(cap), draw_gap=np.zeros(cap))
         trees.append(Tree(0, 0, stop_key=float("nan"), **arr))
     structs = (_Tree * R)(*[t.struct() for t in trees])
     anc = np.ascontiguousarray(anchors, np.int32)
@@ -296,7 +297,7 @@ def expand_forest(model: Model, anchors, thetas, N, budget, K, T, seed, a=0.67, 
         t.n, t.evals, t.stop_key = s.n, s.evals, s.stop_key
         n1 = t.n + 1
         for name in ("token", "parent", "depth", "rank", "path", "log_surv", "log_q0", "log_qT", "key",
-                     "margin", "eval_gap"):
+                     "margin", "eval_gap", "draw_gap"):
             setattr(t, name, getattr(t, name)[:n1].copy())
     return trees
 

@@ -349,7 +349,10 @@ typedef struct {
   double* log_qT;   /* log qT(token | parent), NaN at T = 0 */
   double* key;      /* key of the slot whose pop created the node */
   double* margin;   /* popped key minus the best key left in the heap (INFINITY if none) */
-  double* eval_gap; /* smallest gap between consecutive sorted scores of the node's eval, NaN if not evaluated */
+  double* eval_gap; /* smallest relative gap between consecutive sorted scores of the node's eval (top-k
+                       logits; Gumbel keys), NaN if not evaluated */
+  double* draw_gap; /* sequential draws: smallest gap of a pick to a cumulative boundary, relative to
+                       the level's total (a mass, not a score); NaN otherwise or if not evaluated */
   double stop_key;  /* key of the slot that met the theta stop, NaN if none */
 } tso_tree;
 
@@ -438,7 +441,7 @@ int tso_expand_tree(const tso_model* m, int request, int anchor, double theta, i
   out->token[0] = anchor; out->parent[0] = -1; out->depth[0] = 0; out->rank[0] = 0;
   out->path[0] = 0; out->log_surv[0] = 0.0; out->log_q0[0] = 0.0; out->log_qT[0] = NAN;
   out->key[0] = 0.0; out->margin[0] = INFINITY;
-  for (int i = 0; i <= N; ++i) out->eval_gap[i] = NAN;
+  for (int i = 0; i <= N; ++i) out->eval_gap[i] = out->draw_gap[i] = NAN;
   out->stop_key = NAN;
   out->evals = 0;
   int n = 0;
@@ -456,9 +459,9 @@ int tso_expand_tree(const tso_model* m, int request, int anchor, double theta, i
              sampler, K, NULL, &e_->lse0, &e_->lseT, e_->pi, e_->pi_z, e_->sigma,            \
              e_->sigma_g, e_->sigma_z);                                                      \
     double g_ = min_rel_gap(e_->pi_z, K + 1);                                                \
-    if (T > 0.0)                                                                             \
-      g_ = fmin(g_, sampler == 1 ? min_of(e_->sigma_g, K) : min_rel_gap(e_->sigma_g, K + 1)); \
+    if (T > 0.0 && sampler != 1) g_ = fmin(g_, min_rel_gap(e_->sigma_g, K + 1));             \
     out->eval_gap[node] = g_;                                                                \
+    out->draw_gap[node] = (T > 0.0 && sampler == 1) ? min_of(e_->sigma_g, K) : NAN;          \
     out->evals++;                                                                            \
   } while (0)
 
@@ -531,12 +534,15 @@ int tso_expand_tree(const tso_model* m, int request, int anchor, double theta, i
 /* root path of node i (the row of node i under the tree attention mask).    */
 /* ------------------------------------------------------------------------- */
 
-/* Greedy verification by exact target-token match (§3.2 item 3; §3.3). */
+/* Greedy verification by exact target-token match (§3.2 item 3; §3.3).
+ * level_gap (optional, room for n + 1 values) receives, for each visited
+ * node in walk order, the relative gap (best - second) / max(1, |best|) of
+ * its target row: the decision taken there is unambiguous in fp32 unless
+ * that gap is tiny. */
 int tso_verify_greedy(const tso_tree* t, const float* target, int V, int32_t* path_nodes,
-                      int32_t* path_len, int32_t* bonus, double* min_gap) {
+                      int32_t* path_len, int32_t* bonus, double* level_gap) {
   if (!t || !target || V < 1) return -1;
   int cur = 0, len = 0;
-  double gap = INFINITY;
   for (;;) {
     const float* row = target + (size_t)cur * V;
     int g = 0;
@@ -546,7 +552,7 @@ int tso_verify_greedy(const tso_tree* t, const float* target, int V, int32_t* pa
     for (int y = 0; y < V; ++y)
       if (y != g && row[y] > second) second = row[y];
     double d = ((double)row[g] - second) / fmax(1.0, fabs((double)row[g]));
-    if (d < gap) gap = d;
+    if (level_gap) level_gap[len] = d;
     int next = -1;
     for (int c = 1; c <= t->n; ++c)
       if (t->parent[c] == cur && t->token[c] == g) { next = c; break; }
@@ -555,7 +561,6 @@ int tso_verify_greedy(const tso_tree* t, const float* target, int V, int32_t* pa
     cur = next;
   }
   *path_len = len;
-  if (min_gap) *min_gap = gap;
   return 0;
 }
 
@@ -598,12 +603,14 @@ int tso_residual_stages(int V, const double* p_in, const double* qT, int m, cons
 /*
  * Sampled verification (§3.3, Proposition 1; Algorithm 1 return line: each
  * visited parent's proposal is rebuilt from the logits and the draw order).
- * min_margin receives the smallest |log u - log ratio| over acceptance tests
- * and the smallest relative gap of the bonus keys.
+ * level_margin (optional, room for n + 1 values) receives, for each visited
+ * node in walk order, the smallest relative margin of the decisions taken
+ * there: |log u - log ratio| / max(1, |log ratio|) over its acceptance tests
+ * and, at the last node, (best - second) / max(1, |best|) of the bonus keys.
  */
 int tso_verify_sample(const tso_model* m, int request, const tso_tree* t, const float* target,
                       double T, uint64_t seed, int32_t* path_nodes, int32_t* path_len,
-                      int32_t* bonus, double* min_margin) {
+                      int32_t* bonus, double* level_margin) {
   if (!m || !t || !target || T <= 0.0) return -1;
   const int V = m->V;
   double* p = (double*)malloc(sizeof(double) * (size_t)V);
@@ -613,8 +620,8 @@ int tso_verify_sample(const tso_model* m, int request, const tso_tree* t, const 
   unsigned char* drawn = (unsigned char*)malloc((size_t)V);
   int* kids = (int*)malloc(sizeof(int) * (size_t)(t->n + 1));
   int cur = 0, len = 0;
-  double margin = INFINITY;
   for (;;) {
+    double margin = INFINITY; /* of the decisions at this node */
     /* target residual starts at p = softmax(target row / T) */
     const float* row = target + (size_t)cur * V;
     double mx = -INFINITY;
@@ -644,7 +651,7 @@ int tso_verify_sample(const tso_model* m, int request, const tso_tree* t, const 
         for (int y = 0; y < V; ++y) q[y] = drawn[y] ? 0.0 : qT[y] / R;
         double u = tso_u_stage(seed, request, t->depth[cur], t->path[cur], TSO_TAG_ACCEPT, j);
         double log_ratio = log(p[x]) - ((z[x] / T - lseT) - log(R));
-        double d = fabs(log(u) - log_ratio);
+        double d = fabs(log(u) - log_ratio) / fmax(1.0, fabs(log_ratio));
         if (d < margin) margin = d;
         if (log(u) < log_ratio) {
           accepted = kids[j - 1];
@@ -662,6 +669,7 @@ int tso_verify_sample(const tso_model* m, int request, const tso_tree* t, const 
       }
     }
     if (accepted >= 0) {
+      if (level_margin) level_margin[len] = margin;
       path_nodes[len++] = accepted;
       cur = accepted;
       continue;
@@ -678,11 +686,11 @@ int tso_verify_sample(const tso_model* m, int request, const tso_tree* t, const 
     }
     double d = (bk - second) / fmax(1.0, fabs(bk));
     if (d < margin) margin = d;
+    if (level_margin) level_margin[len] = margin;
     *bonus = best;
     break;
   }
   *path_len = len;
-  if (min_margin) *min_margin = margin;
   free(p); free(qT); free(q); free(z); free(drawn); free(kids);
   return 0;
 }
@@ -757,7 +765,7 @@ int tso_expand_forest(const tso_model* m, int R, const int32_t* anchor, const do
     out->token[0] = anchor[q]; out->parent[0] = -1; out->depth[0] = 0; out->rank[0] = 0;
     out->path[0] = 0; out->log_surv[0] = 0.0; out->log_q0[0] = 0.0; out->log_qT[0] = NAN;
     out->key[0] = 0.0; out->margin[0] = INFINITY;
-    for (int i = 0; i <= N; ++i) out->eval_gap[i] = NAN;
+    for (int i = 0; i <= N; ++i) out->eval_gap[i] = out->draw_gap[i] = NAN;
     out->stop_key = NAN;
     out->evals = 0;
     out->n = 0;
@@ -777,9 +785,9 @@ int tso_expand_forest(const tso_model* m, int R, const int32_t* anchor, const do
              NULL, &e_->lse0, &e_->lseT, e_->pi, e_->pi_z, e_->sigma, e_->sigma_g,           \
              e_->sigma_z);                                                                   \
     double g_ = min_rel_gap(e_->pi_z, K + 1);                                                \
-    if (T > 0.0)                                                                             \
-      g_ = fmin(g_, sampler == 1 ? min_of(e_->sigma_g, K) : min_rel_gap(e_->sigma_g, K + 1)); \
+    if (T > 0.0 && sampler != 1) g_ = fmin(g_, min_rel_gap(e_->sigma_g, K + 1));             \
     t_->eval_gap[node] = g_;                                                                 \
+    t_->draw_gap[node] = (T > 0.0 && sampler == 1) ? min_of(e_->sigma_g, K) : NAN;           \
     t_->evals++;                                                                             \
   } while (0)
 
