@@ -35,8 +35,10 @@ def close(a, b, tol) -> bool:
 
 @dataclass
 class Tally:
-    compared: int = 0
-    near_ties: int = 0
+    compared: int = 0        # parents, trees or walks looked at
+    near_ties: int = 0       # of those, how many hit a near-tie (compared only up to it)
+    units: int = 0           # tree nodes or walk levels that exist on the oracle's side
+    units_compared: int = 0  # of those, how many were compared
     max_err: float = 0.0
     failures: list = field(default_factory=list)
 
@@ -120,8 +122,9 @@ def compare_parent(gpu: dict, i: int, ev: o.Eval, log_surv_p: float, T: float, K
 
 def tree_compare_limit(ref: o.Tree, theta: float, T: float = 1.0):
     """Number of leading nodes of the oracle tree that no near-tie can change, and the tie count.
-    Evaluation gaps use TIE * max(1, 1/T) (see first_draw_tie)."""
-    gap_thr = TIE * max(1.0, 1.0 / T) if T > 0 else TIE
+    Score gaps of an evaluation (top-k logits, Gumbel keys) use TIE; the picks of sequential
+    draws, whose gaps are relative masses, use TIE * max(1, 1/T) (see first_draw_tie)."""
+    draw_thr = TIE * max(1.0, 1.0 / T) if T > 0 else TIE
     lt = math.log(theta) if theta > 0 else -math.inf
     limit = ref.n + 1
     ties = 0
@@ -130,7 +133,9 @@ def tree_compare_limit(ref: o.Tree, theta: float, T: float = 1.0):
         if ref.margin[c] <= TIE * max(1.0, abs(ref.key[c])):
             tied = True
         p = ref.parent[c]
-        if np.isfinite(ref.eval_gap[p]) and ref.eval_gap[p] <= gap_thr:
+        if np.isfinite(ref.eval_gap[p]) and ref.eval_gap[p] <= TIE:
+            tied = True
+        if np.isfinite(ref.draw_gap[p]) and ref.draw_gap[p] <= draw_thr:
             tied = True
         if math.isfinite(lt) and abs(ref.key[c] - lt) <= TIE * max(1.0, abs(lt)):
             tied = True
@@ -151,6 +156,8 @@ def compare_tree(gpu_tree, q: int, ref: o.Tree, theta: float, dtype: str, tally:
     if ties == 0:
         tally.check(n == ref.n, f"{tag} tree size {n} vs {ref.n}")
     upto = min(limit, n + 1, ref.n + 1)
+    tally.units += ref.n
+    tally.units_compared += max(0, min(limit, ref.n + 1) - 1)
     for name in ("token", "parent", "depth", "rank"):
         g = list(getattr(gpu_tree, name)[q][:upto])
         r = list(getattr(ref, name)[:upto])
@@ -163,3 +170,47 @@ def compare_tree(gpu_tree, q: int, ref: o.Tree, theta: float, dtype: str, tally:
             tally.err(got, want)
             tally.check(close(got, want, tol), f"{tag} {name}[{c}] {got} vs {want}")
     return upto
+
+
+def oracle_tree(tree, q: int) -> o.Tree:
+    """The oracle's view of request q of a HostTree (for the verification walks)."""
+    n1 = int(tree.n[q]) + 1
+    return o.Tree(int(tree.n[q]), 0, tree.token[q, :n1].copy(), tree.parent[q, :n1].copy(),
+                  tree.depth[q, :n1].copy(), tree.rank[q, :n1].copy(), tree.path[q, :n1].copy(),
+                  tree.log_surv[q, :n1].astype(np.float64), tree.log_q0[q, :n1].astype(np.float64),
+                  tree.log_qT[q, :n1].astype(np.float64), tree.key[q, :n1].astype(np.float64),
+                  np.zeros(n1), np.zeros(n1), np.zeros(n1), float("nan"))
+
+
+def compare_walk(path, plen, bonus, ref_path, ref_bonus, margins, tally: Tally, tag=""):
+    """One verification walk (accepted node ids and bonus token) against the oracle's.
+    margins[i] is the oracle's smallest relative margin of the decisions taken at the i-th node
+    of its walk.  The nodes accepted before the first level whose margin is <= TIE must be
+    identical; without a near-tie the whole walk and the bonus must be.  Returns True if the
+    walk was compared whole."""
+    levels = len(margins)
+    tie = next((i for i, m in enumerate(margins) if m <= TIE), levels)
+    tally.compared += 1
+    tally.units += levels
+    tally.units_compared += tie
+    if tie < levels:
+        tally.near_ties += 1
+        upto = min(tie, len(ref_path))
+        tally.check(int(plen) >= upto and list(path[:upto]) == list(ref_path[:upto]),
+                    f"{tag} walk {list(path[:plen])} vs {list(ref_path)} (near-tie at level {tie})")
+        return False
+    tally.check(int(plen) == len(ref_path) and list(path[:plen]) == list(ref_path),
+                f"{tag} walk {list(path[:plen])} vs {list(ref_path)}")
+    tally.check(int(bonus) == int(ref_bonus), f"{tag} bonus {int(bonus)} vs {int(ref_bonus)}")
+    return True
+
+
+# Near-tie accounting of every parity comparison in this session, written out by conftest.py at
+# the end (the parity bar counts and reports near-ties).
+RECORDS: list = []
+
+
+def record(test: str, what: str, tally: Tally):
+    RECORDS.append(dict(test=test, what=what, compared=tally.compared, near_ties=tally.near_ties,
+                        units=tally.units, units_compared=tally.units_compared,
+                        max_rel_err=tally.max_err, failures=len(tally.failures)))

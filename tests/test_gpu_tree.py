@@ -7,7 +7,8 @@ from scipy import special, stats
 
 from oracle import oracle as o
 from paper_2609_22098_amd import synth
-from helpers import TIE, Tally, close, compare_tree, tree_compare_limit, value_tol
+from helpers import (TIE, Tally, close, compare_tree, compare_walk, oracle_tree, record, tree_compare_limit,
+                     value_tol)
 
 pytestmark = pytest.mark.gpu
 
@@ -38,9 +39,44 @@ def _compare_all(dr, tree, anchors, thetas, N, K, T, seed, requests=None, tag=""
         compare_tree(tree, q, ref, float(thetas[q]), dr.dtype, tally, tag=f"{tag} request {q}", T=T)
     sizes = [int(tree.n[q]) for q in refs]
     print(f"{tag}: {tally.compared} trees, sizes {min(sizes)}..{max(sizes)}, near-ties {tally.near_ties}, "
-          f"max rel err {tally.max_err:.2e}")
+          f"{tally.units_compared}/{tally.units} nodes compared, max rel err {tally.max_err:.2e}")
+    record(tag, "ts_build_tree trees", tally)
     assert not tally.failures, tally.failures[:5]
+    # nodes after a tree's first near-tie are not compared: most nodes must be
+    assert tally.units_compared >= 0.75 * tally.units, (tally.units_compared, tally.units)
     return refs
+
+
+def _verify_compare(dd, dr, tree, tgt32, requests, T, seed, tag, min_whole=0.75):
+    """ts_verify on all requests of the tree against the oracle's walk on `requests`; tgt32[q] holds
+    request q's target rows (float32 values of what the GPU read).  Walks are compared up to the
+    first near-tie level; at least min_whole of them must be compared whole."""
+    from paper_2609_22098_amd import binding
+    import torch
+    cap = tree.cap
+    tgt = np.zeros((dr.R, cap, dr.V), np.uint16 if dr.dtype == "bf16" else np.float32)
+    for q, rows in tgt32.items():
+        tgt[q, :len(rows)] = synth.f32_to_bf16_bits(rows) if dr.dtype == "bf16" else rows
+    t = torch.from_numpy(tgt)
+    target = (t.view(torch.bfloat16) if dr.dtype == "bf16" else t).cuda()
+    path, plen, bonus = binding.verify(dd, tree, target, T, seed)
+    om = o.Model(dr.U32, dr.E32, dr.W2_32)
+    tally = Tally()
+    whole = 0
+    for q in requests:
+        ot = oracle_tree(tree, q)
+        rows = tgt32[q][: int(tree.n[q]) + 1]
+        if T == 0:
+            rp, rb, margins = o.verify_greedy(ot, rows)
+        else:
+            rp, rb, margins = o.verify_sample(om, q, ot, rows, T, seed)
+        whole += compare_walk(path[q], plen[q], bonus[q], rp, rb, margins, tally, tag=f"{tag} request {q}")
+    print(f"{tag}: {tally.compared} walks compared ({whole} whole), near-ties {tally.near_ties}, "
+          f"accepted lengths {[int(plen[q]) for q in requests][:32]}")
+    record(tag, "ts_verify walks", tally)
+    assert not tally.failures, tally.failures[:5]
+    assert tally.compared == len(requests) and whole >= min_whole * len(requests), (whole, len(requests))
+    return path, plen, bonus
 
 
 @pytest.mark.parametrize("T", [0.0, 1.0])
@@ -133,11 +169,12 @@ def test_sequential_serving_natural_trees(torch):
 
 @pytest.fixture(scope="module")
 def chain_workload(torch):
-    """The high-load workload's shapes: V=151936, D=16, r=128, bf16, theta swept geometrically from
-    0.01 to 0.5 over the requests (one drafter for both temperatures).  64 of its 256 requests, the
-    same sweep: generating all 256 requests' inputs takes over a minute of host time."""
+    """The high-load workload: 256 requests, V=151936, D=16, r=128, bf16, theta swept geometrically
+    from 0.01 to 0.5 over the requests (one drafter for both temperatures)."""
     w = synth.WORKLOADS[4]
-    dr = synth.make_workload_drafter(4, seed=0, R=64)
+    print("generating the 256-request chain workload", flush=True)
+    dr = synth.make_workload_drafter(4, seed=0)
+    assert dr.R == 256
     anchors, thetas, _ = synth.make_controls(dr.R, dr.V, w["theta"], seed=0)
     from paper_2609_22098_amd import binding
     return w, dr, anchors, thetas, binding.drafter_from_host(dr)
@@ -145,15 +182,16 @@ def chain_workload(torch):
 
 @pytest.mark.parametrize("T", [0.0, 1.0])
 def test_chain_collapse_theta_sweep(torch, chain_workload, T):
-    """All trees of the high-load workload in one call; 12 requests across the theta sweep
-    against the oracle.  With the deployed calibration (a=0.67, b=-0.46) an edge estimate of
-    at least 0.4 needs q0 >= 0.52, so at theta >= 0.4 no node can keep two children: those
-    trees are chains (one node per depth)."""
+    """All 256 trees of the high-load workload in one call; 32 requests across the theta sweep
+    against the oracle, then their verification against target rows U + N(0, 1).  With the
+    deployed calibration (a=0.67, b=-0.46) an edge estimate of at least 0.4 needs q0 >= 0.52, so
+    at theta >= 0.4 no node can keep two children: those trees are chains (one node per depth)."""
     from paper_2609_22098_amd import binding
     w, dr, anchors, thetas, dd = chain_workload
     N, K = w["N"], w["K"]
     tree = binding.build_tree(dd, anchors, thetas, N, K, T, 0)
-    picks = sorted(set(np.linspace(0, dr.R - 1, 12).round().astype(int).tolist()))
+    picks = sorted(set(np.linspace(0, dr.R - 1, 32).round().astype(int).tolist()))
+    assert len(picks) == 32
     _compare_all(dr, tree, anchors, thetas, N, K, T, 0, requests=picks, tag=f"chain T={T}")
     sizes = tree.n.astype(int)
     print(f"chain T={T}: tree sizes {sizes.min()}..{sizes.max()}, mean {sizes.mean():.1f}; "
@@ -167,38 +205,10 @@ def test_chain_collapse_theta_sweep(torch, chain_workload, T):
         assert n <= dr.D
     # the low end of the sweep keeps more nodes than the high end
     assert sizes[: dr.R // 4].mean() > sizes[-dr.R // 4:].mean()
-
-    # verification of the compared requests against target rows U + N(0, 1) (other rows zero)
-    cap = N + 1
-    tgt = np.zeros((dr.R, cap, dr.V), np.uint16)
     tgt32 = {}
     for q in picks:
-        n1 = int(tree.n[q]) + 1
-        st, v = synth.make_target_rows(dr, q, tree.depth[q, :n1], w["target_sigma"], seed=4)
-        tgt[q, :n1] = st
-        tgt32[q] = v
-    target = torch.from_numpy(tgt).view(torch.bfloat16).cuda()
-    path, plen, bonus = binding.verify(dd, tree, target, T, 77)
-    om = o.Model(dr.U32, dr.E32, dr.W2_32)
-    ties = 0
-    for q in picks:
-        n1 = int(tree.n[q]) + 1
-        ot = o.Tree(int(tree.n[q]), 0, tree.token[q, :n1].copy(), tree.parent[q, :n1].copy(),
-                    tree.depth[q, :n1].copy(), tree.rank[q, :n1].copy(), tree.path[q, :n1].copy(),
-                    tree.log_surv[q, :n1].astype(np.float64), tree.log_q0[q, :n1].astype(np.float64),
-                    tree.log_qT[q, :n1].astype(np.float64), tree.key[q, :n1].astype(np.float64),
-                    np.zeros(n1), np.zeros(n1), float("nan"))
-        if T == 0:
-            rp, rb, gap = o.verify_greedy(ot, tgt32[q])
-        else:
-            rp, rb, gap = o.verify_sample(om, q, ot, tgt32[q], T, 77)
-        if gap <= 1e-4:
-            ties += 1
-            continue
-        assert list(path[q, :plen[q]]) == list(rp), (q, path[q, :plen[q]], rp)
-        assert bonus[q] == rb, (q, bonus[q], rb)
-    print(f"chain verify T={T}: {len(picks) - ties} requests compared, near-ties {ties}, "
-          f"accepted lengths {[int(plen[q]) for q in picks]}")
+        _, tgt32[q] = synth.make_target_rows(dr, q, tree.depth[q, :int(tree.n[q]) + 1], w["target_sigma"], seed=4)
+    _verify_compare(dd, dr, tree, tgt32, picks, T, 77, tag=f"chain verify T={T}")
 
 
 # ---------------------------------------------------------------- verification
@@ -213,42 +223,14 @@ def _prefixes(tree, q):
 @pytest.mark.parametrize("T", [0.0, 1.0, 0.7])
 def test_verify_parity_multi_request(torch, T):
     """ts_verify against the oracle walk on 8 requests (greedy and recursive rejection)."""
-    from paper_2609_22098_amd import binding
     dr = synth.make_drafter(3000, 6, 32, R=8, dtype="bf16", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
                             ew_sigma=0.3, seed=5, u_scale=2.0)
     anchors, _, _ = synth.make_controls(8, dr.V, 0.0, seed=5)
     thetas = np.full(8, 0.01, np.float32)
     N, K = 24, 4
     dd, tree = _trees(dr, anchors, thetas, N, K, T, 21)
-    cap = N + 1
-    tgt = np.zeros((8, cap, dr.V), np.uint16)
-    tgt32 = np.zeros((8, cap, dr.V), np.float32)
-    for q in range(8):
-        n1 = int(tree.n[q]) + 1
-        s, v = synth.make_target_rows(dr, q, tree.depth[q, :n1], 1.0, seed=2)
-        tgt[q, :n1], tgt32[q, :n1] = s, v
-    target = torch.from_numpy(tgt).view(torch.bfloat16).cuda()
-    path, plen, bonus = binding.verify(dd, tree, target, T, 33)
-    om = o.Model(dr.U32, dr.E32, dr.W2_32)
-    ties = 0
-    for q in range(8):
-        n1 = int(tree.n[q]) + 1
-        ot = o.Tree(int(tree.n[q]), 0, tree.token[q, :n1].copy(), tree.parent[q, :n1].copy(),
-                    tree.depth[q, :n1].copy(), tree.rank[q, :n1].copy(), tree.path[q, :n1].copy(),
-                    tree.log_surv[q, :n1].astype(np.float64), tree.log_q0[q, :n1].astype(np.float64),
-                    tree.log_qT[q, :n1].astype(np.float64), tree.key[q, :n1].astype(np.float64),
-                    np.zeros(n1), np.zeros(n1), float("nan"))
-        if T == 0:
-            rp, rb, gap = o.verify_greedy(ot, tgt32[q, :n1])
-        else:
-            rp, rb, gap = o.verify_sample(om, q, ot, tgt32[q, :n1], T, 33)
-        if gap <= 1e-4:
-            ties += 1
-            continue
-        assert list(path[q, :plen[q]]) == list(rp), (q, path[q, :plen[q]], rp)
-        assert bonus[q] == rb, (q, bonus[q], rb)
-    print(f"verify T={T}: {8 - ties} requests compared, near-ties {ties}, "
-          f"accepted lengths {list(plen)}")
+    tgt32 = {q: synth.make_target_rows(dr, q, tree.depth[q, :int(tree.n[q]) + 1], 1.0, seed=2)[1] for q in range(8)}
+    _verify_compare(dd, dr, tree, tgt32, list(range(8)), T, 33, tag=f"verify multi T={T}")
 
 
 @pytest.mark.parametrize("T", [0.7, 1.0])
@@ -256,7 +238,6 @@ def test_verify_parity_many_chunks(torch, T):
     """ts_verify against the oracle walk with a 300000-token vocabulary and two requests: each
     level item spans 293 chunks, more than the 256 whose Z partials a stage loads up front, so
     the stages also sum the rest in the same order."""
-    from paper_2609_22098_amd import binding
     R, V = 2, 300000
     dr = synth.make_drafter(V, 3, 32, R=R, dtype="bf16", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
                             ew_sigma=0.3, seed=9, u_scale=2.0)
@@ -264,33 +245,44 @@ def test_verify_parity_many_chunks(torch, T):
     thetas = np.full(R, 0.001, np.float32)
     N, K = 6, 3
     dd, tree = _trees(dr, anchors, thetas, N, K, T, 4)
-    cap = N + 1
-    tgt = np.zeros((R, cap, dr.V), np.uint16)
-    tgt32 = np.zeros((R, cap, dr.V), np.float32)
-    for q in range(R):
-        n1 = int(tree.n[q]) + 1
-        s, v = synth.make_target_rows(dr, q, tree.depth[q, :n1], 1.0, seed=3)
-        tgt[q, :n1], tgt32[q, :n1] = s, v
-    target = torch.from_numpy(tgt).view(torch.bfloat16).cuda()
-    path, plen, bonus = binding.verify(dd, tree, target, T, 41)
-    om = o.Model(dr.U32, dr.E32, dr.W2_32)
-    compared = 0
-    for q in range(R):
-        n1 = int(tree.n[q]) + 1
-        ot = o.Tree(int(tree.n[q]), 0, tree.token[q, :n1].copy(), tree.parent[q, :n1].copy(),
-                    tree.depth[q, :n1].copy(), tree.rank[q, :n1].copy(), tree.path[q, :n1].copy(),
-                    tree.log_surv[q, :n1].astype(np.float64), tree.log_q0[q, :n1].astype(np.float64),
-                    tree.log_qT[q, :n1].astype(np.float64), tree.key[q, :n1].astype(np.float64),
-                    np.zeros(n1), np.zeros(n1), float("nan"))
-        rp, rb, gap = o.verify_sample(om, q, ot, tgt32[q, :n1], T, 41)
-        if gap <= 1e-4:
-            continue
-        compared += 1
-        assert list(path[q, :plen[q]]) == list(rp), (q, path[q, :plen[q]], rp)
-        assert bonus[q] == rb, (q, bonus[q], rb)
-    assert compared > 0
-    print(f"verify V={V} T={T}: {compared} of {R} requests compared, tree sizes {list(tree.n)}, "
-          f"accepted lengths {list(plen)}")
+    tgt32 = {q: synth.make_target_rows(dr, q, tree.depth[q, :int(tree.n[q]) + 1], 1.0, seed=3)[1] for q in range(R)}
+    _verify_compare(dd, dr, tree, tgt32, list(range(R)), T, 41, tag=f"verify V={V} T={T}", min_whole=0.5)
+
+
+def test_verify_serving_sequential(torch):
+    """The benchmark's verification: 64 requests, V=151936, bf16, r=64 (the logit recompute with
+    two 32-deep MFMA steps), T=0.7, trees built with sequential draws under the requests' theta,
+    target rows U + N(0, 1); every request's walk against the oracle."""
+    w = synth.WORKLOADS[3]
+    dr = synth.make_workload_drafter(3, seed=0)
+    anchors, thetas, _ = synth.make_controls(dr.R, dr.V, w["theta"], seed=0)
+    dd, tree = _trees(dr, anchors, thetas, w["N"], w["K"], 0.7, 0, sampler="sequential")
+    with_kids = int(np.sum(tree.n > 0))
+    print(f"serving trees: sizes {int(tree.n.min())}..{int(tree.n.max())}, {with_kids} with children", flush=True)
+    assert with_kids >= 16
+    tgt32 = {q: synth.make_target_rows(dr, q, tree.depth[q, :int(tree.n[q]) + 1], w["target_sigma"], seed=0)[1]
+             for q in range(dr.R)}
+    _verify_compare(dd, dr, tree, tgt32, list(range(dr.R)), 0.7, 0, tag="verify serving T=0.7 sequential")
+
+
+@pytest.mark.parametrize("sampler", ["gumbel", "sequential"])
+def test_verify_single_v151936_r256(torch, sampler):
+    """The single-request sampling workload's verification: V=151936, bf16, r=256 (the logit
+    recompute with eight 32-deep MFMA steps), a 128-node tree at T=1, target rows U + N(0, 1.5^2)
+    for all 129 nodes; eight verification seeds, each walk against the oracle."""
+    from paper_2609_22098_amd import binding
+    w = synth.WORKLOADS[2]
+    dr = synth.make_workload_drafter(2, seed=0)
+    anchors, _, _ = synth.make_controls(1, dr.V, 0.0, seed=0)
+    dd, tree = _trees(dr, anchors, np.zeros(1, np.float32), w["N"], w["K"], 1.0, 0, sampler=sampler)
+    assert int(tree.n[0]) == w["N"]
+    rows = synth.make_target_rows(dr, 0, tree.depth[0], w["target_sigma"], seed=0)[1]
+    tally_lens = []
+    for vseed in range(8):
+        _, plen, _ = _verify_compare(dd, dr, tree, {0: rows}, [0], 1.0, 100 + vseed,
+                                     tag=f"verify v151936 r256 {sampler} seed {100 + vseed}", min_whole=0.0)
+        tally_lens.append(int(plen[0]))
+    print(f"accepted lengths over 8 seeds: {tally_lens}")
 
 
 @pytest.mark.parametrize("sampler", ["gumbel", "sequential"])
