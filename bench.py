@@ -87,6 +87,14 @@ class HipEvents:
         assert rc == 0, f"hipEventElapsedTime failed ({rc})"
         return t.value
 
+    def close(self):
+        """Destroy the events while the runtime is up (nothing is left for exit-time teardown)."""
+        for i in range(len(self.ev)):
+            if self.ev[i]:
+                rc = self.hip.hipEventDestroy(self.ev[i])
+                assert rc == 0, f"hipEventDestroy failed ({rc})"
+                self.ev[i] = None
+
 
 def copy_calibration(gib, args_out=""):
     """A plain device copy of known size, for scaling the FETCH_SIZE / WRITE_SIZE counters."""
@@ -344,6 +352,11 @@ def main():
     # the binding roofline is the one with the longer floor, i.e. the larger fraction
     result["roofline"] = alu if alu["frac"] > hbm["frac"] else hbm
     result["roofline_other"] = hbm if alu["frac"] > hbm["frac"] else alu
+    # release every HIP object this process made before exit: the events, the library's pinned
+    # staging buffer and events (the GPU work is finished)
+    torch.cuda.synchronize()
+    ev.close()
+    binding.release_thread_state()
     if not args.no_cpu:
         log("timing the CPU oracle")
         result["cpu_baseline"] = cpu_baseline(dr, fr, K, T, seed, args.cpu_seconds, sampler)

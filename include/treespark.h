@@ -23,7 +23,7 @@
  *                     bias is B(x, v) = <W1[x], W2[v]> (§3.1); as an r x V
  *                     matrix W this is W2 transposed
  *     All three share one dtype (TS_F32 or TS_BF16) and start at 16-byte
-     aligned addresses (TS_EINVAL otherwise).  Accumulation is fp32.
+ *     aligned addresses (TS_EINVAL otherwise).  Accumulation is fp32.
  *   - The library never frees, retains or writes caller tensors other than
  *     the documented outputs.  It allocates no device memory: scratch comes
  *     from the caller's workspace (sizes from the *_workspace_size calls).
@@ -357,6 +357,20 @@ int32_t ts_calib_fit(const float* x, const int32_t* y, const int32_t* sel, int32
 
 /* Description of the last error on the calling thread ("" if none). */
 const char* ts_last_error(void);
+
+/*
+ * ts_release_thread_state: free what the library keeps for the calling host
+ * thread between calls: a page-locked staging buffer (the small transfers of
+ * ts_build_tree, ts_verify and ts_calib_labels, which kernels also read and
+ * write directly) and the events that pace ts_build_tree's device waves.  It
+ * first waits for the current device (hipDeviceSynchronize).  Call it before
+ * the thread or the process ends, while the HIP runtime is still up: the
+ * library frees nothing from thread-exit or process-exit handlers, since those
+ * may run after the runtime (or a profiler attached to it) has been torn down.
+ * A later call that needs the buffer or the events allocates them again.
+ * Returns TS_OK, or TS_EHIP if a HIP call fails.
+ */
+int32_t ts_release_thread_state(void);
 
 /* Library version string. */
 const char* ts_version(void);

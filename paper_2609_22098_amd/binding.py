@@ -6,6 +6,7 @@ The binding raises if the shared library is missing; there is no fallback.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
 from dataclasses import dataclass
@@ -24,7 +25,7 @@ SAMPLERS = {"gumbel": 0, "sequential": 1}  # ts_sampler
 EXPORTED = ("ts_ladder_lookup", "ts_ladder_default", "ts_tree_mask_words", "ts_tree_mask",
             "ts_expand_workspace_size", "ts_expand", "ts_build_tree_workspace_size", "ts_build_tree",
             "ts_verify_workspace_size", "ts_verify", "ts_calib_labels_workspace_size", "ts_calib_labels",
-            "ts_calib_fit", "ts_last_error", "ts_version")
+            "ts_calib_fit", "ts_last_error", "ts_version", "ts_release_thread_state")
 
 
 class TreeSparkError(RuntimeError):
@@ -105,8 +106,21 @@ def lib():
         L.ts_tree_mask.restype = I32
         L.ts_last_error.restype = ctypes.c_char_p
         L.ts_version.restype = ctypes.c_char_p
+        L.ts_release_thread_state.argtypes = []
+        L.ts_release_thread_state.restype = I32
         _lib = L
+        # atexit runs its handlers last-registered first: this one (registered
+        # after torch's import) frees the library's pinned buffer and events
+        # while torch and the HIP runtime are still up
+        atexit.register(release_thread_state)
     return _lib
+
+
+def release_thread_state():
+    """ts_release_thread_state for the calling thread (a no-op before the library is loaded)."""
+    if _lib is None:
+        return
+    _check(_lib.ts_release_thread_state())
 
 
 def _check(rc):

@@ -40,27 +40,48 @@ int32_t fail(int32_t code, const char* fmt, ...) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Page-locked host staging for the small transfers of the host loops, so that
-// they are true asynchronous DMA copies.  One buffer per host thread, grown on
-// demand and kept until the process ends; every user synchronises its stream
-// before it rewrites or grows the buffer.
-struct HostStage {
-  char* p = nullptr;
-  size_t n = 0;
+// Armed once work is queued on a stream: an error return then waits for that
+// work, so that no kernel or copy is still writing the caller's workspace or
+// the staging buffer when the call returns.  Success paths disarm it.
+struct DrainOnError {
+  hipStream_t s;
+  bool armed = true;
+  ~DrainOnError() {
+    if (armed) (void)hipStreamSynchronize(s);
+  }
 };
+
+// Page-locked host staging for the small transfers of the host loops, so that
+// they are true asynchronous DMA copies, and the events that pace the device
+// waves.  Both belong to the calling host thread, grow on demand and live
+// until ts_release_thread_state() frees them; every user synchronises its
+// stream before it rewrites or grows the buffer.  There is deliberately no
+// destructor: a thread-exit destructor of the main thread would run inside
+// exit(), after the HIP runtime (and any profiler attached to it) may have
+// been torn down.
+struct ThreadState {
+  char* stage = nullptr;
+  size_t stage_bytes = 0;
+  std::vector<hipEvent_t> events;
+};
+ThreadState& thread_state() {
+  thread_local ThreadState st;
+  return st;
+}
+
 int32_t host_stage(size_t bytes, char** out) {
-  thread_local HostStage st;
-  if (st.n < bytes) {
-    if (st.p) TS_HIP(hipHostFree(st.p));
-    st.p = nullptr;
-    st.n = 0;
+  ThreadState& st = thread_state();
+  if (st.stage_bytes < bytes) {
+    if (st.stage) TS_HIP(hipHostFree(st.stage));
+    st.stage = nullptr;
+    st.stage_bytes = 0;
     void* q = nullptr;
     // coherent: kernels read and write parts of it directly
     TS_HIP(hipHostMalloc(&q, bytes, hipHostMallocCoherent));
-    st.p = static_cast<char*>(q);
-    st.n = bytes;
+    st.stage = static_cast<char*>(q);
+    st.stage_bytes = bytes;
   }
-  *out = st.p;
+  *out = st.stage;
   return TS_OK;
 }
 
@@ -472,7 +493,7 @@ WaveTreeOut tree_out_of(const ts_tree* t) {
 }
 
 hipEvent_t* wave_events(int n) {
-  thread_local std::vector<hipEvent_t> ev;
+  std::vector<hipEvent_t>& ev = thread_state().events;
   while ((int)ev.size() < n) {
     hipEvent_t e = nullptr;
     if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
@@ -534,6 +555,7 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   wp.child_log_qT = eo.child_log_qT;
   wp.child_log_surv = eo.child_log_surv;
   wp.slot_key = eo.slot_key;
+  DrainOnError drain{s};
   launch_wave_init(wp, s);
   TS_HIP(hipGetLastError());
 
@@ -600,6 +622,7 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   std::memcpy(out->log_q0, htree + tb.log_q0, rcn * 4);
   std::memcpy(out->log_qT, htree + tb.log_qT, rcn * 4);
   std::memcpy(out->key, htree + tb.key, rcn * 4);
+  drain.armed = false;
   return TS_OK;
 }
 
@@ -682,6 +705,22 @@ VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
   return v;
 }
 
+// Host checks of ts_expand.
+int32_t check_expand_args(const ts_drafter* d, const ts_parent* parents, int P, ts_calib calib, int k, float T,
+                          int sampler, const ts_expand_out* out) {
+  int32_t rc = check_drafter(d);
+  if (rc != TS_OK) return rc;
+  if ((rc = check_k_T(d, k, T)) != TS_OK) return rc;
+  if ((rc = check_sampler(sampler)) != TS_OK) return rc;
+  if (P < 0) return fail(TS_EINVAL, "P=%d is negative", P);
+  if (P == 0) return TS_OK;
+  if (!parents) return fail(TS_EINVAL, "parents is NULL");
+  if (!out || !out->child_token || !out->child_log_q0 || !out->child_log_surv || !out->slot_key)
+    return fail(TS_EINVAL, "a required output pointer is NULL");
+  if (!std::isfinite(calib.a) || !std::isfinite(calib.b)) return fail(TS_EINVAL, "calibration must be finite");
+  return TS_OK;
+}
+
 }  // namespace
 }  // namespace ts
 
@@ -691,7 +730,23 @@ extern "C" {
 
 const char* ts_last_error(void) { return g_last_error.c_str(); }
 
-const char* ts_version(void) { return "treespark-mi355x 0.1 (gfx950)"; }
+const char* ts_version(void) { return "treespark-mi355x 0.2 (gfx950)"; }
+
+int32_t ts_release_thread_state(void) {
+  g_last_error.clear();
+  ThreadState& st = thread_state();
+  if (!st.stage && st.events.empty()) return TS_OK;
+  // every stream that used them has been synchronised by its call, but a
+  // caller's later work may still reference the staging buffer's contents:
+  // wait for the device before freeing anything
+  TS_HIP(hipDeviceSynchronize());
+  for (hipEvent_t e : st.events) TS_HIP(hipEventDestroy(e));
+  st.events.clear();
+  if (st.stage) TS_HIP(hipHostFree(st.stage));
+  st.stage = nullptr;
+  st.stage_bytes = 0;
+  return TS_OK;
+}
 
 size_t ts_expand_workspace_size(const ts_drafter* d, int32_t P, int32_t k, float T) {
   (void)k;
@@ -703,16 +758,8 @@ int32_t ts_expand(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_c
                   int32_t k, float T, uint64_t seed, int32_t sampler, const ts_expand_out* out,
                   void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
-  int32_t rc = check_drafter(d);
-  if (rc != TS_OK) return rc;
-  if ((rc = check_k_T(d, k, T)) != TS_OK) return rc;
-  if ((rc = check_sampler(sampler)) != TS_OK) return rc;
-  if (P < 0) return fail(TS_EINVAL, "P=%d is negative", P);
-  if (P == 0) return TS_OK;
-  if (!parents) return fail(TS_EINVAL, "parents is NULL");
-  if (!out || !out->child_token || !out->child_log_q0 || !out->child_log_surv || !out->slot_key)
-    return fail(TS_EINVAL, "a required output pointer is NULL");
-  if (!std::isfinite(calib.a) || !std::isfinite(calib.b)) return fail(TS_EINVAL, "calibration must be finite");
+  int32_t rc = check_expand_args(d, parents, P, calib, k, T, sampler, out);
+  if (rc != TS_OK || P == 0) return rc;
   const size_t need = make_plan(d, P, T, TS_SAMPLER_GUMBEL, false, true).bytes;
   if (!workspace || workspace_bytes < need)
     return fail(TS_ENOSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
@@ -766,6 +813,7 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
   for (int q = 0; q < R; ++q) log_theta[q] = theta[q] > 0.0f ? logf(theta[q]) : -INFINITY;
   if (device_waves(N, K, budget))
     return build_tree_device(d, anchor, log_theta, N, K, calib, T, seed, sampler, out, device_out, ws, bl, s);
+  DrainOnError drain{s};
   std::vector<std::vector<Slot>> known(R);
   std::vector<ts_parent> frontier;
   std::vector<int32_t> evals(R, 0);
@@ -940,6 +988,7 @@ int32_t ts_build_tree(const ts_drafter* d, const int32_t* anchor, const float* t
     TS_HIP(hipMemcpyAsync(device_out->key, out->key, rcn * 4, h2d, s));
     TS_HIP(hipStreamSynchronize(s));
   }
+  drain.armed = false;
   return TS_OK;
 }
 
@@ -981,6 +1030,7 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
 
+  DrainOnError drain{s};
   // children of every node in creation order (= draw order)
   const KidIndex& kids = kid_index(tree);
   for (int q = 0; q < R; ++q) path_len[q] = 0;
@@ -1018,6 +1068,7 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
       path_len[q] = len;
       base += tree->n[q] + 1;
     }
+    drain.armed = false;
     return TS_OK;
   }
 
@@ -1104,6 +1155,7 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     }
     active.swap(next);
   }
+  drain.armed = false;
   return TS_OK;
 }
 
@@ -1215,6 +1267,7 @@ int32_t ts_calib_labels(const ts_tree* tree, const void* target, int32_t target_
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
+  DrainOnError drain{s};
   TS_HIP(hipMemcpyAsync(ws, hs, cl.upload, hipMemcpyHostToDevice, s));
   int32_t* greedy = reinterpret_cast<int32_t*>(ws + cl.greedy);
   launch_verify_argmax(target, target_dtype == TS_BF16, V, reinterpret_cast<const int*>(ws + cl.rows), nrows,
@@ -1225,6 +1278,7 @@ int32_t ts_calib_labels(const ts_tree* tree, const void* target, int32_t target_
                       cap, greedy, reinterpret_cast<const int32_t*>(ws + cl.off), x, y, sel, s);
   TS_HIP(hipGetLastError());
   TS_HIP(hipStreamSynchronize(s));
+  drain.armed = false;
   return TS_OK;
 }
 

@@ -50,8 +50,10 @@ _SEED_CONTROL = 3_000_017
 
 def f32_to_bf16_bits(x32: np.ndarray) -> np.ndarray:
     """Round float32 values to bfloat16 (nearest even), returned as uint16 bit patterns."""
-    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    # finite values stay below 0xFF800000 after the rounding increment, so
+    # 32-bit arithmetic cannot wrap
+    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32)
+    rounded = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return rounded.astype(np.uint16)
 
 
@@ -97,6 +99,7 @@ def make_drafter(V, D, r, R=1, dtype="bf16", u_sigma=2.5, planted=None, zipf=(6.
     U = np.empty((R, D, V), dtype=np.uint16 if dtype == "bf16" else np.float32)
     U32 = np.empty((R, D, V), dtype=np.float32)
     ranks = np.arange(1, V + 1, dtype=np.float64)
+    boost = zipf[0] * ranks ** (-zipf[1]) if zipf is not None else None
     for q in range(R):
         base = rng.standard_normal((D, V)) * u_sigma
         for d in range(D):
@@ -105,7 +108,7 @@ def make_drafter(V, D, r, R=1, dtype="bf16", u_sigma=2.5, planted=None, zipf=(6.
                 base[d, t] += planted
             elif zipf is not None:
                 perm = rng.permutation(V)
-                base[d, perm] += zipf[0] * ranks ** (-zipf[1])
+                base[d, perm] += boost
         base *= u_scale
         U[q], U32[q] = _store(base, dtype)
     E64 = rng.standard_normal((V, r)) * ew_sigma

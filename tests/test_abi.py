@@ -20,12 +20,17 @@ def _declared():
 
 def test_library_exports_every_declared_symbol():
     declared = _declared()
-    assert len(declared) == 15
+    assert len(declared) == 16
     assert sorted(b.EXPORTED) == declared
     L = b.lib()
     for name in declared:
         assert hasattr(L, name), name
     assert b"gfx950" in L.ts_version()
+
+
+def test_release_without_state_touches_no_device():
+    # nothing allocated on this thread yet: the release returns without a HIP call
+    assert b.lib().ts_release_thread_state() == b.TS_OK
 
 
 def _drafter(R=1, D=4, V=1000, r=16, dtype=b.TS_F32, null=False):
@@ -216,3 +221,4 @@ def test_calib_entry_points_reject_bad_arguments():
     assert L.ts_calib_fit(x, y, sel, -1, 10, 1e-9, out, None) == b.TS_EINVAL
     assert L.ts_calib_fit(x, y, sel, 4, 0, 1e-9, out, None) == b.TS_EINVAL
     assert L.ts_calib_fit(x, y, sel, 4, 10, 0.0, out, None) == b.TS_EINVAL
+
