@@ -154,6 +154,29 @@ int32_t ts_expand(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_c
                   int32_t k, float T, uint64_t seed, int32_t sampler, const ts_expand_out* out,
                   void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of the per-GPU scratch array ts_expand_noalloc works in. */
+#define TS_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/*
+ * ts_expand_noalloc: ts_expand without a workspace argument, for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation.  It calls no allocator.  Its
+ * scratch is a file-scope device array of TS_NOALLOC_SCRATCH_BYTES bytes, one
+ * copy on each GPU the library runs on, held until the process ends.
+ *   - The launch needs what ts_expand's plan for it needs (a function of P, V,
+ *     r, the sampler and the device's compute units; about 24 MB for 2048
+ *     parents at V = 151936 with sequential draws).  A launch that needs more
+ *     returns TS_EUNSUPPORTED before anything is launched.
+ *   - Every call on one GPU shares that GPU's array, which keeps the last
+ *     call's contents (nothing in it needs to start at zero).  Calls that
+ *     overlap in time on one GPU (other streams, other threads) race and give
+ *     undefined results; calls ordered on one stream do not.
+ * Arguments, outputs, checks and errors otherwise as ts_expand.
+ */
+int32_t ts_expand_noalloc(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_calib calib,
+                          int32_t k, float T, uint64_t seed, int32_t sampler, const ts_expand_out* out,
+                          void* stream);
+
 /* A draft tree per request, HOST memory, capacity `cap` = N + 1 rows per
  * request ([R][cap] row-major), node 0 = the root (anchor token, depth 0).
  * Nodes are in creation order, which is the pop order of Algorithm 1. */

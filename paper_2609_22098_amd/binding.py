@@ -25,7 +25,8 @@ SAMPLERS = {"gumbel": 0, "sequential": 1}  # ts_sampler
 EXPORTED = ("ts_ladder_lookup", "ts_ladder_default", "ts_tree_mask_words", "ts_tree_mask",
             "ts_expand_workspace_size", "ts_expand", "ts_build_tree_workspace_size", "ts_build_tree",
             "ts_verify_workspace_size", "ts_verify", "ts_calib_labels_workspace_size", "ts_calib_labels",
-            "ts_calib_fit", "ts_last_error", "ts_version", "ts_release_thread_state")
+            "ts_calib_fit", "ts_last_error", "ts_version", "ts_release_thread_state", "ts_expand_noalloc")
+TS_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 class TreeSparkError(RuntimeError):
@@ -82,6 +83,8 @@ def lib():
         L.ts_expand_workspace_size.restype = SZ
         L.ts_expand.argtypes = [P, P, I32, Calib, I32, F, U64, I32, P, P, SZ, P]
         L.ts_expand.restype = I32
+        L.ts_expand_noalloc.argtypes = [P, P, I32, Calib, I32, F, U64, I32, P, P]
+        L.ts_expand_noalloc.restype = I32
         L.ts_build_tree_workspace_size.argtypes = [P, I32, I32, F]
         L.ts_build_tree_workspace_size.restype = SZ
         L.ts_build_tree.argtypes = [P, P, P, I32, I32, I32, Calib, F, U64, I32, P, P, P, SZ, P]
@@ -242,6 +245,19 @@ def expand(d: DeviceDrafter, parents, P, k, T, seed, calib=(0.67, -0.46), worksp
                          workspace.numel(), _stream(stream))
     _check(rc)
     outputs["_workspace"] = workspace
+    return outputs
+
+
+def expand_noalloc(d: DeviceDrafter, parents, P, k, T, seed, outputs, calib=(0.67, -0.46), stream=None,
+                   sampler="gumbel"):
+    """ts_expand_noalloc: ts_expand in the library's per-GPU scratch array, with no workspace and
+    no allocation in the call.  outputs: a dict of preallocated device tensors, as expand returns
+    (rank_token, rank_log_q0, lse0, lseT, diag and child_log_qT may be absent)."""
+    out = ExpandOut(*[outputs[name].data_ptr() if outputs.get(name) is not None else None
+                      for name, _ in ExpandOut._fields_[:-1]], None)
+    rc = lib().ts_expand_noalloc(d.ref(), ctypes.c_void_p(parents.data_ptr()), P, Calib(*calib), k, float(T),
+                                 ctypes.c_uint64(seed), SAMPLERS[sampler], ctypes.byref(out), _stream(stream))
+    _check(rc)
     return outputs
 
 

@@ -17,6 +17,12 @@
 
 #include "launch.hpp"
 
+// The scratch of ts_expand_noalloc, one copy per GPU.  In host code `scratch`
+// names a host-side stand-in, not device memory: kernels get the device
+// address that hipGetSymbolAddress returns, taken once per device with that
+// device current (noalloc_scratch below).
+static __device__ __align__(256) char scratch[TS_NOALLOC_SCRATCH_BYTES];
+
 namespace ts {
 namespace {
 
@@ -705,7 +711,7 @@ VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
   return v;
 }
 
-// Host checks of ts_expand.
+// Host checks shared by ts_expand and ts_expand_noalloc.
 int32_t check_expand_args(const ts_drafter* d, const ts_parent* parents, int P, ts_calib calib, int k, float T,
                           int sampler, const ts_expand_out* out) {
   int32_t rc = check_drafter(d);
@@ -718,6 +724,23 @@ int32_t check_expand_args(const ts_drafter* d, const ts_parent* parents, int P, 
   if (!out || !out->child_token || !out->child_log_q0 || !out->child_log_surv || !out->slot_key)
     return fail(TS_EINVAL, "a required output pointer is NULL");
   if (!std::isfinite(calib.a) || !std::isfinite(calib.b)) return fail(TS_EINVAL, "calibration must be finite");
+  return TS_OK;
+}
+
+int32_t noalloc_scratch(char** out) {
+  static std::mutex mu;
+  static void* addr[64] = {nullptr};
+  int dev = 0;
+  TS_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return fail(TS_EUNSUPPORTED, "device %d beyond the 64 the library tracks", dev);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    TS_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(TS_EHIP, "hipGetSymbolAddress returned no address for the scratch array");
+    addr[dev] = p;
+  }
+  *out = static_cast<char*>(addr[dev]);
   return TS_OK;
 }
 
@@ -765,6 +788,21 @@ int32_t ts_expand(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_c
     return fail(TS_ENOSPACE, "workspace %zu bytes < %zu needed", workspace_bytes, need);
   return run_expand(d, parents, P, calib, k, T, seed, sampler, out, static_cast<char*>(workspace),
                     static_cast<hipStream_t>(stream));
+}
+
+int32_t ts_expand_noalloc(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_calib calib,
+                          int32_t k, float T, uint64_t seed, int32_t sampler, const ts_expand_out* out,
+                          void* stream) {
+  g_last_error.clear();
+  int32_t rc = check_expand_args(d, parents, P, calib, k, T, sampler, out);
+  if (rc != TS_OK || P == 0) return rc;
+  const size_t need = make_plan(d, P, T, sampler).bytes;
+  if (need > (size_t)TS_NOALLOC_SCRATCH_BYTES)
+    return fail(TS_EUNSUPPORTED, "this launch needs %zu bytes of scratch, more than the %u of ts_expand_noalloc",
+                need, TS_NOALLOC_SCRATCH_BYTES);
+  char* scratch = nullptr;
+  if ((rc = noalloc_scratch(&scratch)) != TS_OK) return rc;
+  return run_expand(d, parents, P, calib, k, T, seed, sampler, out, scratch, static_cast<hipStream_t>(stream));
 }
 
 size_t ts_build_tree_workspace_size(const ts_drafter* d, int32_t N, int32_t K, float T) {

@@ -20,7 +20,7 @@ def _declared():
 
 def test_library_exports_every_declared_symbol():
     declared = _declared()
-    assert len(declared) == 16
+    assert len(declared) == 17
     assert sorted(b.EXPORTED) == declared
     L = b.lib()
     for name in declared:
@@ -222,3 +222,23 @@ def test_calib_entry_points_reject_bad_arguments():
     assert L.ts_calib_fit(x, y, sel, 4, 0, 1e-9, out, None) == b.TS_EINVAL
     assert L.ts_calib_fit(x, y, sel, 4, 10, 0.0, out, None) == b.TS_EINVAL
 
+
+def test_expand_noalloc_host_checks():
+    """ts_expand_noalloc shares ts_expand's argument checks and refuses, before any launch, a
+    launch whose plan needs more than its scratch array."""
+    L = b.lib()
+
+    def call(d, P=4, k=2, T=0.0, sampler=0, out=True):
+        o = b.ExpandOut(FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, None, None, None) if out else None
+        return L.ts_expand_noalloc(ctypes.byref(d), FAKE, P, b.Calib(0.67, -0.46), k, T, 0, sampler,
+                                   ctypes.byref(o) if o else None, None)
+
+    assert call(_drafter(null=True)) == b.TS_EINVAL
+    assert call(_drafter(), out=False) == b.TS_EINVAL
+    assert call(_drafter(), k=0) == b.TS_EINVAL
+    assert call(_drafter(), sampler=5) == b.TS_EINVAL
+    assert call(_drafter(), P=0) == b.TS_OK  # nothing to do, nothing launched
+    # 60000 parents over V = 151936 with sequential draws: the block table alone is ~570 MB
+    big = _drafter(V=151936, r=64, dtype=b.TS_BF16)
+    assert call(big, P=60000, T=0.7, sampler=1) == b.TS_EUNSUPPORTED
+    assert b"scratch" in L.ts_last_error()
