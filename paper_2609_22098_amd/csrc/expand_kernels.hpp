@@ -58,6 +58,8 @@ struct ExpandParams {
   int wpg;        // waves (parent blocks) per workgroup
   int n_pgroups;  // workgroups per chunk
   float cT;       // log2(e) / T  (T > 0)
+  float hr;       // headroom of the streaming pass's lazily raised reference, in logit units:
+                  // 60 / max(log2(e), cT), so that no term of a sum exceeds 2^60
   int need_T;     // T > 0 and T != 1: keep a separate sum for log-sum-exp of z/T
   PhiloxKeys keys;
   float* part_m;   // [P][S] running max of z
@@ -592,10 +594,72 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
 // two buffers used alternately, so no registers hold prefetched data.  The W2
 // tile is laid out in 16-byte pieces in the exact order the A fragments are
 // read (piece (bb*KS + kk)*64 + lane), so every fragment read is one
-// conflict-free ds_read_b128.  Requires V % 8 == 0.
+// conflict-free ds_read_b128.  Requires V % 8 == 0 and chunks of a multiple of
+// 256 tokens.
+//
+// Per (parent, token) the pass spends an FMA, an exp2 and an add on each sum
+// it keeps; everything else is amortised over a lane's 16-token run or over
+// four steps:
+//   - the log-sum-exp sums are taken against a reference per parent that is
+//     raised only when a run maximum passes it by more than the headroom (one
+//     wave-wide vote per run; the raise itself is rare), instead of rescaling
+//     at every run;
+//   - with sequential draws, the q_T sum of each run is taken against the
+//     run's own maximum instead (the draws need every block's mass, however
+//     small next to the parent's largest), the block masses are combined over
+//     four steps at a time with one exchange across the lane groups and
+//     stored a 64-byte line per 16 blocks; the merge takes log-sum-exp of
+//     z / T from the block masses, so no separate sum of z / T is kept.
 __device__ __forceinline__ void lds_dma16(const void* src, u32x4* dst_wave_base) {
   typedef __attribute__((address_space(3))) void* lds_ptr;
   __builtin_amdgcn_global_load_lds(src, (lds_ptr)dst_wave_base, 16, 0, 0);
+}
+
+// A mass held as x * 2^r (x >= 0, r finite): the sum of two, against the
+// larger reference.  Equal references keep the order x1 + x2.
+struct Mass {
+  float x, r;
+};
+__device__ __forceinline__ Mass mass_add(Mass a, Mass b) {
+  const float e = exp2_fast(-__builtin_fabsf(a.r - b.r));
+  const bool ahi = a.r >= b.r;
+  return Mass{ahi ? __builtin_fmaf(b.x, e, a.x) : __builtin_fmaf(a.x, e, b.x), ahi ? a.r : b.r};
+}
+__device__ __forceinline__ Mass swap16_pair(Mass& a, Mass& b) {  // see quad_block_masses
+  const auto x = __builtin_amdgcn_permlane16_swap(__float_as_uint(a.x), __float_as_uint(b.x), false, false);
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a.r), __float_as_uint(b.r), false, false);
+  return mass_add(Mass{__uint_as_float(x[0]), __uint_as_float(r[0])}, Mass{__uint_as_float(x[1]), __uint_as_float(r[1])});
+}
+
+// Block masses of a quad of steps.  m_j is this lane's 16-token share of the
+// quad's block j (step j), against its own run maximum; the four lane groups
+// of a parent (lanes n, n+16, n+32, n+48) hold the four quarters of every
+// block.  Lane group g gets the mass of block g: one swap across row pairs
+// halves the values a lane holds (rows 0 and 2 keep blocks 0 and 2, rows 1
+// and 3 blocks 1 and 3), a swap across the halves of the wave finishes the
+// sums.  Every block is combined in the same order, (q0 + q1) + (q2 + q3)
+// over its quarters, and each partial sum is taken against the larger of
+// its references, so no block underflows however far below the parent's
+// largest logit it lies.
+__device__ __forceinline__ Mass quad_block_masses(Mass m0, Mass m1, Mass m2, Mass m3) {
+  const Mass A = swap16_pair(m0, m1);  // row g: block (g & 1), its row pair
+  const Mass B = swap16_pair(m2, m3);  // row g: block 2 + (g & 1)
+  const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(A.x), __float_as_uint(B.x), false, false);
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(A.r), __float_as_uint(B.r), false, false);
+  return mass_add(Mass{__uint_as_float(x[0]), __uint_as_float(r[0])}, Mass{__uint_as_float(x[1]), __uint_as_float(r[1])});
+}
+
+// 4 x 4 transpose across lane groups: in, lane group g holds h[k] = block
+// 4k + g of a 16-block window; out, it holds h[k] = block 4g + k.
+__device__ __forceinline__ void window_transpose(float (&h)[4]) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(h[0]), __float_as_uint(h[1]), false, false);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(h[2]), __float_as_uint(h[3]), false, false);
+  const auto c = __builtin_amdgcn_permlane32_swap(a[0], b[0], false, false);
+  const auto d = __builtin_amdgcn_permlane32_swap(a[1], b[1], false, false);
+  h[0] = __uint_as_float(c[0]);
+  h[1] = __uint_as_float(d[0]);
+  h[2] = __uint_as_float(c[1]);
+  h[3] = __uint_as_float(d[1]);
 }
 
 template <int KS, int NB, int MODE>
@@ -658,16 +722,35 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
     pc3[nb] = counter_word3(req, dep, 1u);
   }
 
-  float m0[NB], s0[NB], sT[NB];
+  // Per parent (shared by its four lane groups): the reference of the sums,
+  // in logit units, the level that triggers a raise, and the FMA offsets
+  // reference * log2(e) and reference * cT.  It starts below every finite
+  // logit, so the first run with a finite maximum raises it before any term
+  // is summed.
+  float ref[NB], lim[NB], off0[NB], offT[NB], s0[NB], sT[NB];
   RunTop zt[NB], gt[NB];
-  BlkWindow bw[NB];
+  // sequential draws: the q_T sum of the lane's run j of the open quad, as
+  // qx * 2^qr with qr the run maximum times c (c = cT, or log2(e) at T = 1)
+  float qx[NB][4], qr[NB][4];
+  float hw[NB][4];  // sequential draws: the open window's block log-masses, hw[k] = block 4k + g
+  // sequential draws keep no sum of z / T, and at T = 1 no sum at all: the
+  // merge takes those log-sum-exps from the block masses
+  constexpr bool SUM0 = !SEQ || NT;
+  constexpr bool SUMT = NT && !SEQ;
+  const float cX = NT ? p.cT : kLog2e;  // scale of the block masses
   const int bfirst = chunk * (p.Vc >> 6);
   const int blast = (min(chunk * p.Vc + p.Vc, V) - 1) >> 6;
+  // the vocabulary's last chunk may write its last window whole (the row is padded to 16 blocks)
+  const int bstore = blast == p.nblk - 1 ? p.blk_ld - 1 : blast;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    m0[nb] = kNegInf; s0[nb] = 0.0f; sT[nb] = 0.0f;
+    ref[nb] = -1e30f; lim[nb] = -1e30f;
+    off0[nb] = -1e30f * kLog2e; offT[nb] = -1e30f * p.cT;
+    s0[nb] = 0.0f; sT[nb] = 0.0f;
     top_init(zt[nb]);
     top_init(gt[nb]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) { qx[nb][k] = 0.0f; qr[nb][k] = -1e30f; hw[nb][k] = kNegInf; }
   }
 
   auto issue = [&](u32x4* wb, u32x4* ub, int t0) {
@@ -689,79 +772,97 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
       }
   };
 
-  // mask_tag: std::true_type for the vocabulary's last, partial step only; a
-  // separate instantiation keeps the masking out of every other step.
-  auto compute = [&](const u32x4* wb, const u32x4* ub, int t0, int step, auto mask_tag) {
-    constexpr bool kMask = decltype(mask_tag)::value;
-    const int tl = t0 + g * 16;
-    f32x4 acc[4][NB];
+  // The vocabulary's last step when V % 64 != 0: with V % 8 == 0 every 8-token
+  // piece of U lies wholly before V or wholly at or past it; the latter (its
+  // load read a clamped row) become bf16 -inf, so those logits are -inf.
+  auto mask_tail = [&](u32x4* ub, int t0) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      URun<uint16_t> u;
-      const u32x4 a = ub[wv * kU + (nb * 2) * 64 + lane];
-      const u32x4 c = ub[wv * kU + (nb * 2 + 1) * 64 + lane];
-      u.w[0] = a[0]; u.w[1] = a[1]; u.w[2] = a[2]; u.w[3] = a[3];
-      u.w[4] = c[0]; u.w[5] = c[1]; u.w[6] = c[2]; u.w[7] = c[3];
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int bb = 0; bb < 4; ++bb)
-        acc[bb][nb] = f32x4{u.get(bb * 4), u.get(bb * 4 + 1), u.get(bb * 4 + 2), u.get(bb * 4 + 3)};
-      if constexpr (kMask) {  // tokens past the vocabulary: z = -inf
+      for (int h = 0; h < 2; ++h)
+        if (t0 + g * 16 + 8 * h >= V) {
+          const uint32_t ninf2 = 0xFF80FF80u;
+          ub[wv * kU + (nb * 2 + h) * 64 + lane] = u32x4{ninf2, ninf2, ninf2, ninf2};
+        }
+  };
+
+  // Raise the reference of every parent of block nb to the largest of its
+  // lane groups' references and run maxima (all of them agree afterwards);
+  // the sums and the open quad's shares are scaled to it.
+  auto raise = [&](int nb, float bm) {
+    const float nr = fmaxf(cross_row_max(max2_med3(ref[nb], bm)), -1e30f);
+    const float d = ref[nb] - nr;
+    s0[nb] *= exp2_fast(d * kLog2e);
+    if constexpr (SUMT) sT[nb] *= exp2_fast(d * p.cT);
+    ref[nb] = nr;
+    lim[nb] = nr + p.hr;
+    off0[nb] = nr * kLog2e;
+    offT[nb] = nr * p.cT;
+  };
+
+  // z of the parents of block nb for one step: the accumulator starts at U,
+  // then takes the rank-r product on the matrix core.
+  auto logits = [&](const u32x4* wb, const u32x4* ub, int nb, f32x4 (&acc)[4]) {
+    const u32x4 pa = ub[wv * kU + (nb * 2) * 64 + lane];
+    const u32x4 pc = ub[wv * kU + (nb * 2 + 1) * 64 + lane];
+    URun<uint16_t> u;
+    u.w[0] = pa[0]; u.w[1] = pa[1]; u.w[2] = pa[2]; u.w[3] = pa[3];
+    u.w[4] = pc[0]; u.w[5] = pc[1]; u.w[6] = pc[2]; u.w[7] = pc[3];
 #pragma unroll
-        for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (tl + bb * 4 + e >= V) acc[bb][nb][e] = kNegInf;
-      }
-    }
+    for (int bb = 0; bb < 4; ++bb)
+      acc[bb] = f32x4{u.get(bb * 4), u.get(bb * 4 + 1), u.get(bb * 4 + 2), u.get(bb * 4 + 3)};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
-      for (int bb = 0; bb < 4; ++bb) {
-        const FT a = __builtin_bit_cast(FT, wb[(bb * KS + kk) * 64 + lane]);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[bb][nb] = F::mma(a, bfrag[nb][kk], acc[bb][nb]);
-      }
-
-    const int run = step * 4 + g;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      float v[16];
-#pragma unroll
       for (int bb = 0; bb < 4; ++bb)
+        acc[bb] = F::mma(__builtin_bit_cast(FT, wb[(bb * KS + kk) * 64 + lane]), bfrag[nb][kk], acc[bb]);
+  };
+
+  // The run's sums (a0 of z against the parent's reference; ax of z times c
+  // against the run maximum for the block masses, or aT of z / T against the
+  // parent's reference); returns the run maximum.
+  auto run_sums = [&](int nb, const f32x4 (&acc)[4], float (&v)[16], float& a0, float& ax, float& br) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[bb * 4 + e] = acc[bb][nb][e];
-      float bm = max2_med3(v[0], v[1]);
+    for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
-      for (int j = 2; j < 16; ++j) bm = fmaxf(bm, v[j]);
-      // run sums are taken relative to the run's own maximum (a run far below
-      // the running maximum keeps its mass), then folded into the running
-      // sums, which are relative to the running maximum: of the two terms the
-      // one with the lower reference is scaled down (one exponential)
-      const float m0c = fmaxf(m0[nb], -1e30f);
-      const float bref = fmaxf(bm, -1e30f);
-      const bool run_high = bref > m0c;
-      const float gap = -__builtin_fabsf(m0c - bref);
-      const float bl = bref * kLog2e;
-      const float blT = bref * p.cT;
-      float a0, aT = 0.0f;
+      for (int e = 0; e < 4; ++e) v[bb * 4 + e] = acc[bb][e];
+    float bm = max2_med3(v[0], v[1]);
+#pragma unroll
+    for (int i = 2; i < 16; ++i) bm = fmaxf(bm, v[i]);
+    if constexpr (SUM0)
+      if (__builtin_expect(__ballot(bm > lim[nb]) != 0, 0)) raise(nb, bm);
+    a0 = 0.0f; ax = 0.0f; br = 0.0f;
+    if constexpr (SEQ) {
+      // the run's q_T sum against its own maximum (finite: an all -inf run sums to 0)
+      br = max2_med3(bm, -1e30f) * cX;
       if constexpr (NT)
-        sum16_exp2_x2(v, kLog2e, bl, p.cT, blT, a0, aT);
+        sum16_exp2_x2(v, kLog2e, off0[nb], p.cT, br, a0, ax);
       else
-        a0 = sum16_exp2(v, kLog2e, bl);
-      const float f0 = exp2_fast(gap * kLog2e);
-      s0[nb] = run_high ? __builtin_fmaf(s0[nb], f0, a0) : __builtin_fmaf(a0, f0, s0[nb]);
-      if constexpr (NT) {
-        const float fT = exp2_fast(gap * p.cT);
-        sT[nb] = run_high ? __builtin_fmaf(sT[nb], fT, aT) : __builtin_fmaf(aT, fT, sT[nb]);
-      }
-      m0[nb] = fmaxf(m0[nb], bm);
-      top_add(zt[nb], bm, run);
+        ax = sum16_exp2(v, kLog2e, br);
+    } else {
+      if constexpr (SUMT)
+        sum16_exp2_x2(v, kLog2e, off0[nb], p.cT, offT[nb], a0, ax);
+      else
+        a0 = sum16_exp2(v, kLog2e, off0[nb]);
+    }
+    return bm;
+  };
+
+  // One 64-token step; j is the step's place in its quad (known at compile time).
+  auto compute = [&](const u32x4* wb, const u32x4* ub, int t0, int step, auto jtag) {
+    constexpr int j = decltype(jtag)::value;
+    const int tl = t0 + g * 16;
+    const int run = step * 4 + g;
+    auto epilogue = [&](int nb, f32x4 (&acc)[4]) {
+      float v[16], a0, ax, br;
+      const float bm = run_sums(nb, acc, v, a0, ax, br);
+      if constexpr (SUM0) s0[nb] += a0;
+      if constexpr (SUMT) sT[nb] += ax;
       if constexpr (SEQ) {
-        const float lb = NT ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
-        const int bi = t0 >> 6;
-        bw[nb].put(bi, g, lb);
-        if (pidx[nb] < P) bw[nb].flush(p.blk + (size_t)pidx[nb] * p.blk_ld, bi, bfirst, blast, g);
+        qx[nb][j] = ax;
+        qr[nb][j] = br;
       }
+      top_add(zt[nb], bm, run);
       if constexpr (GUMBEL) {
         float gm = kNegInf;
         const uint32_t cbase = (uint32_t)tl >> 2;
@@ -772,12 +873,58 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
           const uint32_t w[4] = {c0, c1, c2, c3};
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int j = i * 4 + q;
-            const float key = gumbel_key2(v[j], p.cT, w[q]);  // -inf past the vocabulary
+            const float key = gumbel_key2(v[i * 4 + q], p.cT, w[q]);  // -inf past the vocabulary
             gm = fmaxf(gm, key);
           }
         }
         top_add(gt[nb], gm, run);
+      }
+    };
+    // block by block: block nb + 1's products run on the matrix core while
+    // block nb's epilogue runs on the vector ALUs
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      f32x4 acc[4];
+      logits(wb, ub, nb, acc);
+      epilogue(nb, acc);
+    }
+  };
+
+  // End of a quad (or of the chunk inside one): the quad's block totals as
+  // base-2 log-masses into the open window; at the window's last quad, or the
+  // chunk's, the window goes to the block table, a 16-byte piece per lane
+  // group (single entries where the window reaches outside the chunk).
+  auto end_quad = [&](int qb) {  // qb: the quad's first block (a multiple of 4)
+    const int k = (qb >> 2) & 3;
+    const int wfirst = qb & ~15;
+    const bool flush = k == 3 || qb + 4 > blast;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const Mass tot = quad_block_masses(Mass{qx[nb][0], qr[nb][0]}, Mass{qx[nb][1], qr[nb][1]},
+                                         Mass{qx[nb][2], qr[nb][2]}, Mass{qx[nb][3], qr[nb][3]});
+      const float lb = tot.x > 0.0f ? tot.r + __builtin_amdgcn_logf(tot.x) : kNegInf;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        hw[nb][i] = k == i ? lb : hw[nb][i];
+        qx[nb][i] = 0.0f;
+        qr[nb][i] = -1e30f;
+      }
+      if (flush) {
+        window_transpose(hw[nb]);
+        if (pidx[nb] < P) {
+          float* dst = p.blk + (size_t)pidx[nb] * p.blk_ld + wfirst + 4 * g;
+          if (wfirst >= bfirst && wfirst + 15 <= bstore) {
+            *reinterpret_cast<f32x4*>(dst) = f32x4{hw[nb][0], hw[nb][1], hw[nb][2], hw[nb][3]};
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int bi = wfirst + 4 * g + i;
+              if (bi >= bfirst && bi <= bstore) dst[i] = hw[nb][i];
+            }
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) hw[nb][i] = kNegInf;
       }
     }
   };
@@ -800,50 +947,51 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
     else if (prio_q == 2) __builtin_amdgcn_s_setprio(1);
     else __builtin_amdgcn_s_setprio(0);
   };
+
+  // One step: wait for its tiles, queue the next step's, compute.  Returns
+  // false after the chunk's last step.  Steps alternate between the two
+  // buffers; a quad is four steps, so its step j uses buffer j & 1.
   int t0 = tbeg, step = 0;
+  auto do_step = [&](auto jtag) -> bool {
+    constexpr int j = decltype(jtag)::value;
+    u32x4* wcur = (j & 1) ? w1 : w0;
+    u32x4* ucur = (j & 1) ? u1 : u0;
+    u32x4* wnext = (j & 1) ? w0 : w1;
+    u32x4* unext = (j & 1) ? u0 : u1;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    lower_priority(step);
+    const bool more = t0 + 64 < tend;
+    if (more) issue(wnext, unext, t0 + 64);
+    if (active) {
+      if (t0 + 64 > V) mask_tail(ucur, t0);
+      compute(wcur, ucur, t0, step, jtag);
+      if (SEQ && (j == 3 || !more)) end_quad((t0 >> 6) & ~3);
+    }
+    if (!more) return false;
+    // the step position is the same in every lane: keep it scalar
+    t0 = __builtin_amdgcn_readfirstlane(t0 + 64);
+    step = __builtin_amdgcn_readfirstlane(step + 1);
+    return true;
+  };
   issue(w0, u0, t0);
   for (;;) {
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    lower_priority(step);
-    const bool more1 = t0 + 64 < tend;
-    if (more1) issue(w1, u1, t0 + 64);
-    if (active) {
-      if (t0 + 64 > V)
-        compute(w0, u0, t0, step, std::true_type{});
-      else
-        compute(w0, u0, t0, step, std::false_type{});
-    }
-    if (!more1) break;
-    t0 += 64; ++step;
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    lower_priority(step);
-    const bool more2 = t0 + 64 < tend;
-    if (more2) issue(w0, u0, t0 + 64);
-    if (active) {
-      if (t0 + 64 > V)
-        compute(w1, u1, t0, step, std::true_type{});
-      else
-        compute(w1, u1, t0, step, std::false_type{});
-    }
-    if (!more2) break;
-    t0 += 64; ++step;
+    if (!do_step(std::integral_constant<int, 0>{})) break;
+    if (!do_step(std::integral_constant<int, 1>{})) break;
+    if (!do_step(std::integral_constant<int, 2>{})) break;
+    if (!do_step(std::integral_constant<int, 3>{})) break;
   }
   if (!active) return;
 
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    float M = m0[nb];
-    M = fmaxf(M, __shfl_xor(M, 16, 64));
-    M = fmaxf(M, __shfl_xor(M, 32, 64));
-    const float Mref = fmaxf(M, -1e30f);
-    float s = s0[nb] * exp2_fast(__builtin_fmaf(m0[nb], kLog2e, -Mref * kLog2e));
+    // the four lane groups of a parent share its reference: their sums add
+    float s = s0[nb];
     s += __shfl_xor(s, 16, 64);
     s += __shfl_xor(s, 32, 64);
     float st = 0.0f;
-    if constexpr (NT) {
-      st = sT[nb] * exp2_fast(__builtin_fmaf(m0[nb], p.cT, -Mref * p.cT));
+    if constexpr (SUMT) {
+      st = sT[nb];
       st += __shfl_xor(st, 16, 64);
       st += __shfl_xor(st, 32, 64);
     }
@@ -855,9 +1003,11 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
     }
     if (g == 0 && pidx[nb] < P) {
       const size_t o = (size_t)pidx[nb] * p.S + chunk;
-      p.part_m[o] = M;
-      p.part_s0[o] = s;
-      if (p.part_sT) p.part_sT[o] = st;
+      if constexpr (SUM0) {
+        p.part_m[o] = ref[nb];
+        p.part_s0[o] = s;
+      }
+      if constexpr (SUMT) p.part_sT[o] = st;
       top_store(p.zs, o, zc);
       if constexpr (GUMBEL) top_store(p.gs, o, gc);
     }

@@ -56,6 +56,7 @@ struct DrawLds {
   alignas(16) float seg_blk[kLdsSegs * 64];  // the parent's block table when V <= 40 * 4096
   int id[TS_MAX_K];              // draw j's token and logit at j - 1
   float z[TS_MAX_K];
+  float lmass;                   // base-2 log of the parent's whole q_T mass (before the draws)
 };
 
 // Workgroup LDS of the merge: four parents of one wave each, or, for
@@ -513,6 +514,19 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
       reduce8(s0, xs);
     }
   }
+  // the parent's whole q_T mass (base-2 log), from the segments before any
+  // draw: the log-sum-exp of z / T is ln 2 times it
+  {
+    float mx = kNegInf;
+#pragma unroll
+    for (int i = 0; i < NSEG; ++i) mx = fmaxf(mx, segL[i]);
+    mx = wave_max_fin(mx);
+    float e = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NSEG; ++i) e += segL[i] == kNegInf ? 0.0f : exp2_fast(segL[i] - mx);
+    e = wave_sum(e);
+    if (lane == 0) L.lmass = mx == kNegInf ? kNegInf : mx + __builtin_amdgcn_logf(e);
+  }
   gl.cnt = 0;
 #pragma unroll 1
   for (int j = 1; j <= p.K; ++j) {
@@ -702,36 +716,43 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   }
   const size_t pbase = (size_t)pidx * S;
 
-  // log-sum-exp over chunks: each lane folds its chunks in index order, then a fixed butterfly.
-  float pm[kRestSlots], ps[kRestSlots], pt[kRestSlots];
+  // log-sum-exp over chunks: each lane folds its chunks in index order, then a
+  // fixed butterfly.  The chunks' sums are against their own references.
+  // With sequential draws the log-sum-exp of z / T (and of z at T = 1) comes
+  // from the block masses instead, once the draws' wave has them.
+  constexpr bool kPartsT = SAMPLE && !SEQ;  // the streaming pass kept sums of z / T
+  const bool parts0 = !SEQ || p.need_T;     // ... and sums of z
+  float lse0 = __builtin_nanf(""), lseT = __builtin_nanf("");
+  if (parts0) {
+    float pm[kRestSlots], ps[kRestSlots], pt[kRestSlots];
 #pragma unroll
-  for (int i = 0; i < kRestSlots; ++i) {
-    const int c = i * 64 + lane;
-    // clamped loads, masked after: all of them in flight together (without
-    // the z/T sums, their loads read the z sums and are masked out)
-    const size_t cc = pbase + min(c, S - 1);
-    const uint32_t in = opaque_mask(c < S);
-    const bool has_T = SAMPLE && p.need_T;
-    pm[i] = keep_or(p.part_m[cc], in, kNegInf);
-    ps[i] = keep_or_zero(p.part_s0[cc], in);
-    pt[i] = keep_or_zero((has_T ? p.part_sT : p.part_s0)[cc], in & opaque_mask(has_T));
+    for (int i = 0; i < kRestSlots; ++i) {
+      const int c = i * 64 + lane;
+      // clamped loads, masked after: all of them in flight together (without
+      // the z/T sums, their loads read the z sums and are masked out)
+      const size_t cc = pbase + min(c, S - 1);
+      const uint32_t in = opaque_mask(c < S);
+      const bool has_T = kPartsT && p.need_T;
+      pm[i] = keep_or(p.part_m[cc], in, kNegInf);
+      ps[i] = keep_or_zero(p.part_s0[cc], in);
+      pt[i] = keep_or_zero((has_T ? p.part_sT : p.part_s0)[cc], in & opaque_mask(has_T));
+    }
+    float M = kNegInf;
+#pragma unroll
+    for (int i = 0; i < kRestSlots; ++i) M = fmaxf(M, pm[i]);
+    M = wave_max(M);
+    const float Mref = fmaxf(M, -1e30f);
+    float s = 0.0f, st = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kRestSlots; ++i) {
+      s += ps[i] * exp2_fast(__builtin_fmaf(pm[i], kLog2e, -Mref * kLog2e));
+      if (kPartsT && p.need_T) st += pt[i] * exp2_fast(__builtin_fmaf(pm[i], p.cT, -Mref * p.cT));
+    }
+    s = wave_sum(s);
+    st = wave_sum(st);
+    lse0 = M + logf(s);
+    if (kPartsT) lseT = p.need_T ? M / p.T + logf(st) : lse0;
   }
-  float M = kNegInf;
-#pragma unroll
-  for (int i = 0; i < kRestSlots; ++i) M = fmaxf(M, pm[i]);
-  M = wave_max(M);
-  const float Mref = fmaxf(M, -1e30f);
-  float s = 0.0f, st = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kRestSlots; ++i) {
-    s += ps[i] * exp2_fast(__builtin_fmaf(pm[i], kLog2e, -Mref * kLog2e));
-    if (SAMPLE && p.need_T) st += pt[i] * exp2_fast(__builtin_fmaf(pm[i], p.cT, -Mref * p.cT));
-  }
-  s = wave_sum(s);
-  st = wave_sum(st);
-  const float lse0 = M + logf(s);
-  float lseT = __builtin_nanf("");
-  if (SAMPLE) lseT = p.need_T ? M / p.T + logf(st) : lse0;
 
   int nitems = 0;
   float thr[2];
@@ -789,6 +810,8 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
       gl.val = 0.0f;
     }
     gl.cnt = K;
+    lseT = sh.d.lmass * kLn2;
+    if (!p.need_T) lse0 = lseT;  // T = 1
   }
 
   // Child scoring: lane j handles slot j + 1 (Algorithm 1; §3.2 pre-draw bound; Eq. 3).

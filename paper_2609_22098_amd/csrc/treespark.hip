@@ -243,7 +243,9 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
   if (!sizing_only && getenv("TS_VC")) vc = atoi(getenv("TS_VC"));
 #endif
   vc = std::max(vc, (d->V + kMaxChunks - 1) / kMaxChunks);
-  vc = ((vc + 63) / 64) * 64;
+  // the LDS kernel sums block masses over quads of steps: chunks of whole quads
+  const int quantum = pl.lds ? 256 : 64;
+  vc = ((vc + quantum - 1) / quantum) * quantum;
   vc = std::min(std::max(vc, 256), 4096);
   pl.Vc = vc;
   pl.S = (d->V + vc - 1) / vc;
@@ -340,6 +342,7 @@ ExpandParams eval_params(const ts_drafter* d, const ts_parent* parents, int P, f
   p.n_pblocks = pl.n_pblocks; p.wpg = pl.wpg; p.n_pgroups = pl.n_pgroups;
   p.cT = T > 0.0f ? kLog2e / T : 0.0f;
   p.need_T = (T > 0.0f && T != 1.0f) ? 1 : 0;
+  p.hr = 60.0f / std::max(kLog2e, p.cT);
   p.keys = philox_keys(seed);
   p.part_m = reinterpret_cast<float*>(ws + pl.off_m);
   p.part_s0 = reinterpret_cast<float*>(ws + pl.off_s0);
