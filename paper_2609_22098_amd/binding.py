@@ -143,6 +143,11 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def torch_empty_bytes(n, device="cuda"):
+    """A device byte buffer of at least one byte (for the workspace arguments)."""
+    return _torch().empty((max(int(n), 1),), dtype=_torch().uint8, device=device)
+
+
 def _dtype_code(t):
     torch = _torch()
     if t.dtype == torch.bfloat16:

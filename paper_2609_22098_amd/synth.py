@@ -4,20 +4,23 @@ This module only draws random inputs: it holds none of the method's
 arithmetic.  Both the HIP path and the CPU oracle consume what it returns, so
 the two sides always see identical values.
 
-Recipe (one numpy PCG64 stream per call, draws in a fixed order):
-  1. U [R][D][V]: N(0, u_sigma^2) in fp64, request-major then depth.
-  2. Per (request, depth), in the same order: either one planted token
-     (uniform over V) that gets +planted, or a fresh random permutation pi of
-     the vocabulary where token pi[k-1] gets +zipf_scale * k^-zipf_exp.
-  3. E [V][r] then W2 [V][r]: N(0, ew_sigma^2) in fp64 (E is shared by all
-     requests, as is W2).
-  4. Values are rounded fp64 -> fp32 (round to nearest even) and, for bf16
+Recipe (numpy PCG64 streams, draws in a fixed order within each stream):
+  1. U [q][D][V] of request q comes from its own stream, keyed (seed, q):
+     N(0, u_sigma^2) in fp64, depth-major; then, per depth in order, either
+     one planted token (uniform over V) that gets +planted, or a fresh random
+     permutation pi of the vocabulary where token pi[k-1] gets
+     +zipf_scale * k^-zipf_exp.  Requests are drawn in parallel threads
+     (independent streams, so the values do not depend on the thread count).
+  2. E [V][r] then W2 [V][r] from the stream keyed (seed, 2^32 - 1):
+     N(0, ew_sigma^2) in fp64 (E is shared by all requests, as is W2).
+  3. Values are rounded fp64 -> fp32 (round to nearest even) and, for bf16
      inputs, fp32 -> bf16 (round to nearest even on the bit pattern).
 Target logits, frontiers and per-request controls come from separate streams
 (seed offsets below) so that adding them never changes the model tensors.
 """
 from __future__ import annotations
 
+import os
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -89,18 +92,23 @@ def _store(x64: np.ndarray, dtype: str):
     return x32, x32
 
 
+_EW_STREAM = 2**32 - 1  # stream key of E and W2 (request streams use keys below 2^20)
+
+
 def make_drafter(V, D, r, R=1, dtype="bf16", u_sigma=2.5, planted=None, zipf=(6.0, 1.1),
                  ew_sigma=0.05, seed=0, u_scale=1.0) -> Drafter:
     """Draw U [R][D][V], E [V][r], W2 [V][r] following the recipe in the module docstring.
 
     u_scale multiplies U after the boosts (a "sharp" variant for deep-tree tests).
     """
-    rng = np.random.Generator(np.random.PCG64(seed))
+    from concurrent.futures import ThreadPoolExecutor
     U = np.empty((R, D, V), dtype=np.uint16 if dtype == "bf16" else np.float32)
     U32 = np.empty((R, D, V), dtype=np.float32)
     ranks = np.arange(1, V + 1, dtype=np.float64)
     boost = zipf[0] * ranks ** (-zipf[1]) if zipf is not None else None
-    for q in range(R):
+
+    def request(q):
+        rng = np.random.Generator(np.random.PCG64([seed, q]))
         base = rng.standard_normal((D, V)) * u_sigma
         for d in range(D):
             if planted is not None:
@@ -111,6 +119,15 @@ def make_drafter(V, D, r, R=1, dtype="bf16", u_sigma=2.5, planted=None, zipf=(6.
                 base[d, perm] += boost
         base *= u_scale
         U[q], U32[q] = _store(base, dtype)
+
+    workers = max(1, min(R, 16, os.cpu_count() or 1))
+    if workers == 1:
+        for q in range(R):
+            request(q)
+    else:
+        with ThreadPoolExecutor(workers) as ex:
+            list(ex.map(request, range(R)))
+    rng = np.random.Generator(np.random.PCG64([seed, _EW_STREAM]))
     E64 = rng.standard_normal((V, r)) * ew_sigma
     W64 = rng.standard_normal((V, r)) * ew_sigma
     E, E32 = _store(E64, dtype)
