@@ -44,11 +44,14 @@ sys.path.insert(0, ROOT)
 
 METRIC = "parent-conditioned node evals/sec at V=151936 + achieved HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
-# VALU issue peak: 256 CUs x 4 SIMDs x 32 fp32 lanes per cycle x 2.4 GHz (the
-# 157.3 TFLOP/s fp32 vector figure counts an FMA as two); transcendentals
-# (v_exp_f32, v_log_f32) issue at a quarter of that rate.
-VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12
-TRANS_WEIGHT = 4
+# VALU issue peak for unpacked fp32 instructions: 256 CUs x 4 SIMDs x 16 lanes
+# per cycle x 2.4 GHz (a wave64 instruction every 4 cycles; the 157.3 TFLOP/s
+# fp32 vector figure needs packed FMAs, 2 per lane, counted as 2 FLOP each).
+# Transcendentals (v_exp_f32, v_log_f32) take two issue slots (the counters of
+# the streaming pass give 4 cycles per plain and 8 per transcendental wave64
+# instruction).
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+TRANS_WEIGHT = 2
 KERNEL_SOURCES = ("paper_2609_22098_amd/csrc/expand_kernels.hpp",
                   "paper_2609_22098_amd/csrc/device_common.hpp")
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "expand_eval_serving_counters.json")
@@ -194,7 +197,9 @@ def write_counters(root, T, sampler):
         mb = _frontier_mean(os.path.join(root, "busy"), "SQ_VALU_MFMA_BUSY_CYCLES")[0]
         cb = _frontier_mean(os.path.join(root, "busy"), "SQ_BUSY_CU_CYCLES")[0]
         rec["SQ_VALU_MFMA_BUSY_CYCLES"], rec["SQ_BUSY_CU_CYCLES"] = mb, cb
-        rec["mfma_busy"] = mb / cb if cb > 0 else None
+        # the MFMA busy cycles are summed over the SIMDs (16 cycles per 16x16x32 bf16
+        # MFMA), the busy cycles over the CUs: four SIMDs per CU
+        rec["mfma_busy"] = mb / (4.0 * cb) if cb > 0 else None
     with open(COUNTERS_FILE, "w") as f:
         json.dump(rec, f, indent=1)
     print(json.dumps(rec))
@@ -420,6 +425,9 @@ def main():
                     help="realisation of the sibling draws at T > 0")
     ap.add_argument("--copy-gib", type=float, default=0.0, help="run only the copy calibration")
     ap.add_argument("--copy-out", default="", help="directory for the copy calibration record")
+    ap.add_argument("--only", default="", choices=("", "serving_T0", "serving_gumbel", "single_v128256_T0",
+                                                      "single_v151936_r256_T1", "chain_256req"),
+                    help="run only this entry of configs and print its record (profiling runs)")
     ap.add_argument("--counters-from", default="",
                     help="directory holding the rocprofv3 --pmc runs (fetch, write, copy_fetch, "
                          "copy_write, valu, busy); writes the counters record and exits")
@@ -440,6 +448,19 @@ def main():
         copy_calibration(args.copy_gib, args.copy_out)
         return
 
+    stream = torch.cuda.current_stream()
+    if args.only in ("single_v128256_T0", "single_v151936_r256_T1", "chain_256req"):
+        if args.only == "single_v128256_T0":
+            rec = single_request_config(binding, synth, 1, 0.0, "sequential", stream)
+        elif args.only == "single_v151936_r256_T1":
+            rec = single_request_config(binding, synth, 2, 1.0, "gumbel", stream)
+        else:
+            rec = chain_config(binding, synth, stream)
+        torch.cuda.synchronize()
+        binding.release_thread_state()
+        print(json.dumps({args.only: rec}), flush=True)
+        return
+
     w = synth.WORKLOADS[3]
     T, K, N, seed = args.T, w["K"], w["N"], 0
     log("generating the 64-request V=151936 workload")
@@ -454,8 +475,14 @@ def main():
     drafters = (dd, dd2)
     parents = binding.parents_to_device(fr["token"], fr["depth"], fr["request"], fr["log_surv"], fr["path"])
     sampler = args.sampler
+    if args.only in ("serving_T0", "serving_gumbel"):
+        Tx, sx = (0.0, sampler) if args.only == "serving_T0" else (T, "gumbel")
+        e, m = time_expand(binding, drafters, parents, P, K, Tx, seed, sx, 100, 10, stream)
+        torch.cuda.synchronize()
+        binding.release_thread_state()
+        print(json.dumps({args.only: expand_record(dr, fr, e, m)}), flush=True)
+        return
     # a serving loop holds its stream and output buffers across rounds
-    stream = torch.cuda.current_stream()
     outs = binding.expand(dd, parents, P, K, T, seed, sampler=sampler, stream=stream)
     ws_e = outs.pop("_workspace")
     ws_b = binding.torch_empty_bytes(binding.build_tree_workspace_size(dd, N, K, T))
@@ -524,9 +551,10 @@ def main():
     es = stats_ms(eval_ms)
     eval_s = es["mean"] / 1e3
     achieved = ab / eval_s / 1e9
-    # algorithmic VALU work per (parent, token) element, in full-rate issue
-    # slots: a running max, and per temperature one FMA (scale and shift), one
-    # exp2 (TRANS_WEIGHT slots) and one add; two temperatures when T != 0, 1
+    # algorithmic VALU work per (parent, token) element, in issue slots of one
+    # unpacked instruction: a running max, and per temperature one FMA (scale
+    # and shift), one exp2 (TRANS_WEIGHT slots) and one add; two temperatures
+    # when T != 0, 1
     n_temps = 2 if (T > 0 and T != 1.0) else 1
     slots_per_elem = 1 + n_temps * (2 + TRANS_WEIGHT)
     alg_ops = slots_per_elem * P * dr.V
