@@ -33,15 +33,9 @@ template <typename TE, int KS>
 static void (*eval_kernel_for(int nb, int mode, bool store_z, bool lds))(ExpandParams) {
   if (store_z) return expand_eval_kernel<TE, KS, 1, kModeGreedy, true>;
   if constexpr (sizeof(TE) == 2) {
-    if (lds) {
-      if (nb == 1) return EvalKernels<TE, KS, 1, true>::get(mode);
-      if (nb == 2) return EvalKernels<TE, KS, 2, true>::get(mode);
-      return EvalKernels<TE, KS, 4, true>::get(mode);
-    }
+    if (lds) return nb == 1 ? EvalKernels<TE, KS, 1, true>::get(mode) : EvalKernels<TE, KS, 2, true>::get(mode);
   }
-  if (nb == 1) return EvalKernels<TE, KS, 1, false>::get(mode);
-  if (nb == 2) return EvalKernels<TE, KS, 2, false>::get(mode);
-  return EvalKernels<TE, KS, 4, false>::get(mode);
+  return nb == 1 ? EvalKernels<TE, KS, 1, false>::get(mode) : EvalKernels<TE, KS, 2, false>::get(mode);
 }
 
 template <typename TE, int KS>

@@ -614,6 +614,14 @@ __device__ __forceinline__ void lds_dma16(const void* src, u32x4* dst_wave_base)
   typedef __attribute__((address_space(3))) void* lds_ptr;
   __builtin_amdgcn_global_load_lds(src, (lds_ptr)dst_wave_base, 16, 0, 0);
 }
+// Buffer resource word 3 of a raw (unswizzled, byte-addressed) buffer on gfx9.
+constexpr int kRawBufferFlags = 0x00020000;
+// 16 bytes per lane from a raw buffer at voff + soff into LDS at
+// dst_wave_base + 16 * lane.  Out-of-range bytes read as zero.
+__device__ __forceinline__ void lds_buf16(__amdgpu_buffer_rsrc_t src, uint32_t voff, int soff, u32x4* dst_wave_base) {
+  typedef __attribute__((address_space(3))) void* lds_ptr;
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_ptr)dst_wave_base, 16, (int)voff, soff, 0, 0);
+}
 
 // A mass held as x * 2^r (x >= 0, r finite): the sum of two, against the
 // larger reference.  Equal references keep the order x1 + x2.
@@ -662,8 +670,12 @@ __device__ __forceinline__ void window_transpose(float (&h)[4]) {
   h[3] = __uint_as_float(d[1]);
 }
 
+// At rank <= 64 with two parent blocks per wave the kernel must fit three
+// waves per SIMD (168 VGPRs): a few registers more halve the waves that hide
+// its latencies.
 template <int KS, int NB, int MODE>
-__global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KS <= 2 && NB == 2 ? 3 : 1)))
+void expand_eval_lds_kernel(const ExpandParams p) {
   typedef Frag<uint16_t> F;
   typedef typename F::type FT;
   constexpr int kW = 4 * KS * 64;  // 16-byte pieces of one W2 tile
@@ -678,7 +690,9 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
   constexpr bool GUMBEL = BASE == kModeGumbel;
   constexpr bool SEQ = BASE == kModeSeq;
   constexpr bool NT = SAMPLE && (MODE & kModeNeedT) != 0;  // T != 1: a separate sum for z/T
-  const int wv = threadIdx.x >> 6;
+  // the wave index is uniform: kept scalar, the LDS destinations of the
+  // direct loads need no per-step readfirstlane
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n = lane & 15;
   const int g = lane >> 4;
 
@@ -697,7 +711,10 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
   const uint16_t* W2 = static_cast<const uint16_t*>(p.W2);
   const int V = p.V, r = p.r;
 
-  const uint16_t* urow[NB];
+  // Byte offsets of this lane's U pieces from the step's first token of row
+  // 0: its parent's row plus its lane group's 16 tokens (U is under 4 GiB).
+  // A step's loads add them to a scalar base.
+  uint32_t uoff[NB];
   FT bfrag[NB][KS];
   uint32_t pc1[NB], pc2[NB], pc3[NB];
   int pidx[NB];
@@ -713,7 +730,7 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
         tok = par.token; dep = par.depth; req = par.request; path = par.path;
       }
     }
-    urow[nb] = U + ((size_t)req * p.D + dep) * (size_t)V;
+    uoff[nb] = ((uint32_t)(req * p.D + dep) * (uint32_t)V + (uint32_t)g * 16u) * 2u;
     const uint16_t* erow = E + (size_t)tok * r;
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) bfrag[nb][kk] = F::load(erow, kk * F::kPerStep, g);
@@ -753,23 +770,30 @@ __global__ __launch_bounds__(256) void expand_eval_lds_kernel(const ExpandParams
     for (int k = 0; k < 4; ++k) { qx[nb][k] = 0.0f; qr[nb][k] = -1e30f; hw[nb][k] = kNegInf; }
   }
 
-  auto issue = [&](u32x4* wb, u32x4* ub, int t0) {
-    // W2: this wave loads pieces (wv*KS + j)*64 + lane of the tile
+  // W2: this wave loads pieces (wv*KS + j)*64 + lane of the tile: row
+  // (n >> 2)*16 + bb*4 + (n & 3) of the step, 16 bytes at k = kk*32 + g*8.
+  // U: tokens t0 + g*16 + 8h + [0, 8) of this lane's parent in block nb.
+  // Both are raw buffer loads: a per-lane byte offset fixed for the whole
+  // chunk plus a scalar offset per step, so a step's loads cost no vector
+  // instruction.  Rows past the vocabulary read as zeros (W2, U's last row)
+  // or as the next row's first tokens (U): the last step masks them.
+  uint32_t woff[KS];
 #pragma unroll
-    for (int j = 0; j < KS; ++j) {
-      const int i = wv * KS + j;
-      const int bb = i / KS, kk = i % KS;
-      const int tok = min(t0 + (n >> 2) * 16 + bb * 4 + (n & 3), V - 1);
-      lds_dma16(W2 + (size_t)tok * r + kk * 32 + g * 8, wb + i * 64);
-    }
-    // U: tokens t0 + g*16 + 8h + [0, 8) of this lane's parent in block nb
+  for (int j = 0; j < KS; ++j) {
+    const int bb = (wv * KS + j) / KS, kk = (wv * KS + j) % KS;
+    woff[j] = (uint32_t)((((n >> 2) * 16 + bb * 4 + (n & 3)) * r + kk * 32 + g * 8) * 2);
+  }
+  const __amdgpu_buffer_rsrc_t wsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(W2), 0, V * r * 2, kRawBufferFlags);
+  const __amdgpu_buffer_rsrc_t usrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(U), 0, (int)((uint32_t)p.R * p.D * V * 2), kRawBufferFlags);
+  auto issue = [&](u32x4* wb, u32x4* ub, int t0) {
+#pragma unroll
+    for (int j = 0; j < KS; ++j) lds_buf16(wsrc, woff[j], t0 * r * 2, wb + (wv * KS + j) * 64);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int tt = min(t0 + g * 16 + 8 * h, V - 8);
-        lds_dma16(urow[nb] + tt, ub + wv * kU + (nb * 2 + h) * 64);
-      }
+      for (int h = 0; h < 2; ++h) lds_buf16(usrc, uoff[nb], t0 * 2 + 16 * h, ub + wv * kU + (nb * 2 + h) * 64);
   };
 
   // The vocabulary's last step when V % 64 != 0: with V % 8 == 0 every 8-token

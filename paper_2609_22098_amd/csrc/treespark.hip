@@ -217,11 +217,11 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
   // two parent blocks per wave pay off only when the parents fill them; a
   // bound on a device-held count (max_chunks) usually overstates them
   pl.NB = (P >= 512 && !max_chunks) ? 2 : 1;
-#ifdef TS_FORCE_NB
-  pl.NB = TS_FORCE_NB;
-#endif
   if (store_z) pl.NB = 1;
-  pl.lds = d->dtype == TS_BF16 && d->V % 8 == 0 && !store_z;
+  // the LDS kernel reads U and W2 as raw buffers: byte offsets under 2^31
+  pl.lds = d->dtype == TS_BF16 && d->V % 8 == 0 && !store_z &&
+           ((uint64_t)d->R * d->D + 1) * d->V * 2 + 64 < (1ull << 31) &&
+           (uint64_t)d->V * d->r * 2 < (1ull << 31);
   pl.n_pblocks = (P + 16 * pl.NB - 1) / (16 * pl.NB);
   pl.wpg = pl.lds ? 4 : std::min(4, std::max(1, pl.n_pblocks));
   pl.n_pgroups = (pl.n_pblocks + pl.wpg - 1) / pl.wpg;
