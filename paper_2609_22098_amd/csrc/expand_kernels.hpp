@@ -15,12 +15,13 @@
 //   - an online log-sum-exp (running max and scaled sums for z and z/T);
 //   - "run" maxima for exact top-k: a run is the 16 tokens one lane sees in
 //     one step; per (parent, chunk) the kernel keeps the kTopRuns best run
-//     maxima with their run indices and the best maximum of the other runs.
+//     keys (the maximum with the run index in its low bits) and the best key
+//     of the other runs.
 // Pass 2 (expand_merge, in merge_kernels.hpp) merges the per-chunk partials
 // in a fixed order and finds the exact top-k: with L = the k-th largest
-// recorded run maximum, every top-k token lies in a recorded run whose
-// maximum is >= L, or in a chunk whose other runs reach L (then the whole
-// chunk is rescanned).  Those runs are recomputed with the same MFMA
+// recorded run key, lowered by the keys' slack, every top-k token lies in a
+// recorded run whose key is >= L, or in a chunk whose other runs reach L
+// (then the whole chunk is rescanned).  Those runs are recomputed with the same MFMA
 // sequence as pass 1 (so the recomputed z are bit-identical, which the
 // kernel checks), and the exact top-k is taken by (value desc, id asc).
 //
@@ -38,10 +39,9 @@ namespace ts {
 
 constexpr int kTopRuns = 4;  // best runs recorded per (parent, chunk)
 
-// Per-(parent, chunk) run summaries: m and r are [P][S][kTopRuns], rest is [P][S].
+// Per-(parent, chunk) run summaries: m is [P][S][kTopRuns] run keys, rest is [P][S].
 struct RunSummaryPtr {
   float* m;
-  int* r;
   float* rest;
 };
 
@@ -189,93 +189,95 @@ struct URun<float> {
   __device__ __forceinline__ float get(int i) const { return f[i]; }
 };
 
-// Summary of a set of runs for one key: the kTopRuns best run maxima with
-// their run indices (sorted: larger value first, ties to the smaller run
-// index; empty entries are -inf), and the largest maximum of every other run.
+// A run's maximum is recorded as a key that carries the run index (step * 4
+// + lane group within the chunk, < 256) in its 8 low bits: the top lists then
+// keep the index without selects.  The value is first clamped to finite
+// values (an infinity with low bits set would be a NaN).  In the order of
+// the float bit patterns a key lies within kRunSlack / 2 units of the
+// clamped maximum, so the merge's threshold tests allow kRunSlack.
+constexpr int kRunSlack = 512;
+__device__ __forceinline__ float run_key(float v, int run) {
+  const float c = __builtin_amdgcn_fmed3f(v, -3.40282347e38f, 3.40282347e38f);
+  return __uint_as_float((__float_as_uint(c) & ~0xFFu) | (uint32_t)run);
+}
+__device__ __forceinline__ int run_of(float key) { return (int)(__float_as_uint(key) & 0xFFu); }
+// v lowered by n units in the order of the float bit patterns (v is -inf or
+// a finite key); a result at or below -FLT_MAX, the lowest key, is -inf.
+__device__ __forceinline__ float key_lowered(float v, int n) {
+  if (v == kNegInf) return kNegInf;
+  const uint32_t b = __float_as_uint(v);
+  const int o = (b & 0x80000000u) ? -(int)(b & 0x7FFFFFFFu) : (int)b;
+  const int lo = o - n;
+  if (lo <= -0x7F7FFFFF) return kNegInf;
+  return lo < 0 ? __uint_as_float(0x80000000u | (uint32_t)(-lo)) : __uint_as_float((uint32_t)lo);
+}
+
+// Summary of a set of runs for one key: the kTopRuns largest run keys
+// (sorted, larger first; keys of different runs never tie; empty entries are
+// -inf) and the largest key of every other run.
 struct RunTop {
   float m[kTopRuns];
-  int r[kTopRuns];
   float rest;
 };
 
+// (value desc, index asc): the order of the exact top-k lists
 __device__ __forceinline__ bool run_before(float v, int r, float w, int s) {
   return v > w || (v == w && r < s);
 }
 
 __device__ __forceinline__ void top_init(RunTop& t) {
 #pragma unroll
-  for (int i = 0; i < kTopRuns; ++i) { t.m[i] = kNegInf; t.r[i] = 0x7FFFFFFF; }
+  for (int i = 0; i < kTopRuns; ++i) t.m[i] = kNegInf;
   t.rest = kNegInf;
 }
 
-// Add one run.  Runs arrive in increasing index order within a lane, so a
-// strict comparison keeps the earlier run ahead on ties.  With the list
-// sorted (m[0] >= .. >= m[3] >= rest), the new i-th entry is the median of
-// m[i-1], m[i] and v, and the new rest that of m[3], rest and v.
-__device__ __forceinline__ void top_add(RunTop& t, float v, int run) {
+// Add one run key.  With the list sorted (m[0] >= .. >= m[3] >= rest), the
+// new i-th entry is the median of m[i-1], m[i] and v, and the new rest that
+// of m[3], rest and v.
+__device__ __forceinline__ void top_add(RunTop& t, float v) {
   static_assert(kTopRuns == 4, "unrolled for four entries");
-  bool c[kTopRuns];
-#pragma unroll
-  for (int i = 0; i < kTopRuns; ++i) c[i] = v > t.m[i];
   t.rest = __builtin_amdgcn_fmed3f(t.m[3], t.rest, v);
 #pragma unroll
-  for (int i = kTopRuns - 1; i >= 1; --i) {
-    t.m[i] = __builtin_amdgcn_fmed3f(t.m[i - 1], t.m[i], v);
-    const int x = c[i] ? run : t.r[i];
-    t.r[i] = c[i - 1] ? t.r[i - 1] : x;
-  }
+  for (int i = kTopRuns - 1; i >= 1; --i) t.m[i] = __builtin_amdgcn_fmed3f(t.m[i - 1], t.m[i], v);
   t.m[0] = max2_med3(t.m[0], v);
-  t.r[0] = c[0] ? run : t.r[0];
-}
-
-__device__ __forceinline__ void cswap(float& a, int& ar, float& b, int& br) {
-  if (run_before(b, br, a, ar)) {
-    const float t = a; a = b; b = t;
-    const int tr = ar; ar = br; br = tr;
-  }
 }
 
 // Merge two summaries of disjoint run sets (symmetric in its arguments):
 // the top kTopRuns of the union by a bitonic split, then a bitonic sort.
 __device__ __forceinline__ void top_combine(RunTop& a, const RunTop& b) {
   float c[kTopRuns];
-  int cr[kTopRuns];
   float rest = fmaxf(a.rest, b.rest);
 #pragma unroll
   for (int k = 0; k < kTopRuns; ++k) {
     const float x = a.m[k], y = b.m[kTopRuns - 1 - k];
-    const int xr = a.r[k], yr = b.r[kTopRuns - 1 - k];
-    const bool ax = run_before(x, xr, y, yr);
-    c[k] = ax ? x : y;
-    cr[k] = ax ? xr : yr;
-    rest = fmaxf(rest, ax ? y : x);
+    c[k] = fmaxf(x, y);
+    rest = fmaxf(rest, fminf(x, y));
   }
-  cswap(c[0], cr[0], c[2], cr[2]);
-  cswap(c[1], cr[1], c[3], cr[3]);
-  cswap(c[0], cr[0], c[1], cr[1]);
-  cswap(c[2], cr[2], c[3], cr[3]);
+  auto cs = [](float& u, float& w) {
+    const float hi = fmaxf(u, w), lo = fminf(u, w);
+    u = hi;
+    w = lo;
+  };
+  cs(c[0], c[2]);
+  cs(c[1], c[3]);
+  cs(c[0], c[1]);
+  cs(c[2], c[3]);
 #pragma unroll
-  for (int k = 0; k < kTopRuns; ++k) { a.m[k] = c[k]; a.r[k] = cr[k]; }
+  for (int k = 0; k < kTopRuns; ++k) a.m[k] = c[k];
   a.rest = rest;
 }
 
 __device__ __forceinline__ RunTop top_shfl_xor(const RunTop& t, int o) {
   RunTop u;
 #pragma unroll
-  for (int k = 0; k < kTopRuns; ++k) {
-    u.m[k] = __shfl_xor(t.m[k], o, 64);
-    u.r[k] = __shfl_xor(t.r[k], o, 64);
-  }
+  for (int k = 0; k < kTopRuns; ++k) u.m[k] = __shfl_xor(t.m[k], o, 64);
   u.rest = __shfl_xor(t.rest, o, 64);
   return u;
 }
 
 __device__ __forceinline__ void top_store(const RunSummaryPtr& d, size_t o, const RunTop& t) {
 #pragma unroll
-  for (int k = 0; k < kTopRuns; ++k) {
-    d.m[o * kTopRuns + k] = t.m[k];
-    d.r[o * kTopRuns + k] = t.r[k];
-  }
+  for (int k = 0; k < kTopRuns; ++k) d.m[o * kTopRuns + k] = t.m[k];
   d.rest[o] = t.rest;
 }
 
@@ -495,7 +497,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
         sT[nb] = run_high ? __builtin_fmaf(sT[nb], fT, aT) : __builtin_fmaf(aT, fT, sT[nb]);
       }
       m0[nb] = fmaxf(m0[nb], bm);
-      top_add(zt[nb], bm, run);
+      top_add(zt[nb], run_key(bm, run));
       if constexpr (SEQ) {
         const float lb = p.need_T ? block_log_mass(aT, blT) : block_log_mass(a0, bl);
         const int bi = t0 >> 6;
@@ -517,7 +519,7 @@ __global__ __launch_bounds__(256) void expand_eval_kernel(const ExpandParams p) 
             gm = fmaxf(gm, key);
           }
         }
-        top_add(gt[nb], gm, run);
+        top_add(gt[nb], run_key(gm, run));
       }
     }
   };
@@ -886,7 +888,7 @@ void expand_eval_lds_kernel(const ExpandParams p) {
         qx[nb][j] = ax;
         qr[nb][j] = br;
       }
-      top_add(zt[nb], bm, run);
+      top_add(zt[nb], run_key(bm, run));
       if constexpr (GUMBEL) {
         float gm = kNegInf;
         const uint32_t cbase = (uint32_t)tl >> 2;
@@ -901,7 +903,7 @@ void expand_eval_lds_kernel(const ExpandParams p) {
             gm = fmaxf(gm, key);
           }
         }
-        top_add(gt[nb], gm, run);
+        top_add(gt[nb], run_key(gm, run));
       }
     };
     // block by block: block nb + 1's products run on the matrix core while

@@ -44,7 +44,7 @@ struct MergeLds {
   float bk[kBatch][16];  // their keys (z, or the Gumbel keys)
   int item_t[kItemCap];  // run start token, or -(chunk+1) for a whole chunk
   int item_k[kItemCap];  // key kind: 0 = z, 1 = Gumbel
-  float item_e[kItemCap];  // expected run maximum (NaN if unknown)
+  float item_e[kItemCap];  // expected run key (NaN if unknown)
   uint32_t whole[kMaxChunks / 32];
 };
 
@@ -249,7 +249,7 @@ __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* uro
     const bool live = b < nrun && tb + e < V;
     float rm = live ? kv : kNegInf;
     rm = row_max(rm);  // the run's 16 keys sit in one row of 16 lanes
-    mism += __popcll(__ballot(live && e == 0 && !__builtin_isnan(ex) && rm != ex));
+    mism += __popcll(__ballot(live && e == 0 && !__builtin_isnan(ex) && run_key(rm, (tb % p.Vc) >> 4) != ex));
     const float th = kd ? thr[1] : thr[0];
     uint64_t mask = __ballot(live && kv >= th);
     while (mask) {
@@ -268,13 +268,14 @@ __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* uro
   wave_sync_lds();
 }
 
-// Threshold and candidate items for one key kind.  The threshold is the
-// K-th largest recorded run maximum (counting equal values with their
-// multiplicity): those are maxima of K distinct runs, hence of K distinct
-// tokens, so the K-th largest key over the vocabulary is at least the
-// threshold.  A token whose key reaches the threshold lies in a run whose
-// maximum reaches it: one of its chunk's recorded runs, or, when the chunk's
-// rest maximum reaches it too, somewhere in the chunk (a whole-chunk item).
+// Threshold and candidate items for one key kind.  Let L be the K-th
+// largest recorded run key: those are keys of K distinct runs, whose maxima
+// lie within kRunSlack / 2 units of their keys, so the K-th largest token
+// key over the vocabulary is at least L lowered by kRunSlack / 2 units, and
+// a run holding such a token has a key of at least L lowered by kRunSlack
+// units (the returned threshold).  Such a run is one of its chunk's recorded
+// runs, or, when the chunk's rest key reaches the threshold too, anywhere in
+// the chunk (a whole-chunk item).
 // NE, NR: recorded-run and chunk-rest slots per lane (NE = 4 NR; S <= 64 NR).
 template <int NE, int NR>
 __device__ __forceinline__ float select_items_n(const MergeParams& p, const RunSummaryPtr& sm,
@@ -284,7 +285,6 @@ __device__ __forceinline__ float select_items_n(const MergeParams& p, const RunS
   const int S = p.S, K = p.K;
   const size_t pb = (size_t)pidx * S;
   float ev[kEntrySlots];
-  int er[kEntrySlots];
   float rv[kRestSlots];
   // Every load reads a clamped index, so all are in flight together.  A slot
   // past the last chunk holds a copy of a real entry: it starts out taken in
@@ -295,7 +295,6 @@ __device__ __forceinline__ float select_items_n(const MergeParams& p, const RunS
     const int e = i * 64 + lane;
     const size_t ec = pb * kTopRuns + min(e, S * kTopRuns - 1);
     ev[i] = sm.m[ec];
-    er[i] = sm.r[ec];
     taken |= (e >> 2) < S ? 0u : 1u << i;
   }
 #pragma unroll
@@ -317,6 +316,7 @@ __device__ __forceinline__ float select_items_n(const MergeParams& p, const RunS
     if (picked >= K) { thr = m; break; }
   }
   if (picked < K) thr = kNegInf;  // fewer than K runs recorded: every token is a candidate
+  thr = key_lowered(thr, kRunSlack);
 
   // whole chunks
 #pragma unroll
@@ -341,7 +341,7 @@ __device__ __forceinline__ float select_items_n(const MergeParams& p, const RunS
     const uint64_t mask = __ballot(cand);
     const int off = base + __popcll(mask & lt);
     if (cand && off < kItemCap) {
-      const int run = er[i];
+      const int run = run_of(ev[i]);
       L.item_t[off] = c * p.Vc + (run >> 2) * 64 + (run & 3) * 16;
       L.item_k[off] = kind;
       L.item_e[off] = ev[i];

@@ -146,7 +146,7 @@ struct Plan {
   bool lds;     // LDS-staged bf16 streaming kernel
   int nblk;     // 64-token blocks of the vocabulary
   int blk_ld;   // row stride of the block table (nblk rounded up to 16)
-  size_t off_m, off_s0, off_sT, off_z[3], off_g[3], off_blk;
+  size_t off_m, off_s0, off_sT, off_z[2], off_g[2], off_blk;
   size_t bytes;
 };
 
@@ -262,14 +262,12 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
   pl.off_m = o; o += a;
   pl.off_s0 = o; o += a;
   pl.off_z[0] = o; o += a4;
-  pl.off_z[1] = o; o += a4;
-  pl.off_z[2] = o; o += a;
+  pl.off_z[1] = o; o += a;
   if (pl.sample || (sizing_only && T > 0.0f && !store_z)) {
     pl.off_sT = o; o += a;
     if (pl.mode == kModeGumbel || sizing_only) {
       pl.off_g[0] = o; o += a4;
-      pl.off_g[1] = o; o += a4;
-      pl.off_g[2] = o; o += a;
+      pl.off_g[1] = o; o += a;
     }
     if (pl.mode == kModeSeq || sizing_only) {
       pl.off_blk = o; o += align256((size_t)std::max(P, 1) * pl.blk_ld * 4);
@@ -279,11 +277,10 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
   return pl;
 }
 
-RunSummaryPtr summary_ptr(char* ws, const size_t (&off)[3]) {
+RunSummaryPtr summary_ptr(char* ws, const size_t (&off)[2]) {
   RunSummaryPtr r;
   r.m = reinterpret_cast<float*>(ws + off[0]);
-  r.r = reinterpret_cast<int*>(ws + off[1]);
-  r.rest = reinterpret_cast<float*>(ws + off[2]);
+  r.rest = reinterpret_cast<float*>(ws + off[1]);
   return r;
 }
 
