@@ -684,8 +684,9 @@ void expand_eval_lds_kernel(const ExpandParams p) {
   constexpr int kU = NB * 2 * 64;  // 16-byte pieces of one wave's U tile
   __shared__ __attribute__((aligned(16))) u32x4 w0[kW];
   __shared__ __attribute__((aligned(16))) u32x4 w1[kW];
-  __shared__ __attribute__((aligned(16))) u32x4 u0[4 * kU];
-  __shared__ __attribute__((aligned(16))) u32x4 u1[4 * kU];
+  // U tiles: each wave's region is its own, so one buffer serves: the wave
+  // reads its step's pieces, then queues the next step's into the same place
+  __shared__ __attribute__((aligned(16))) u32x4 ubuf[4 * kU];
   const int lane = threadIdx.x & 63;
   constexpr int BASE = MODE & 3;
   constexpr bool SAMPLE = BASE != kModeGreedy;  // T > 0: lse of z/T and K draws
@@ -789,13 +790,15 @@ void expand_eval_lds_kernel(const ExpandParams p) {
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(W2), 0, V * r * 2, kRawBufferFlags);
   const __amdgpu_buffer_rsrc_t usrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(U), 0, (int)((uint32_t)p.R * p.D * V * 2), kRawBufferFlags);
-  auto issue = [&](u32x4* wb, u32x4* ub, int t0) {
+  auto issue_w = [&](u32x4* wb, int t0) {
 #pragma unroll
     for (int j = 0; j < KS; ++j) lds_buf16(wsrc, woff[j], t0 * r * 2, wb + (wv * KS + j) * 64);
+  };
+  auto issue_u = [&](int t0) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) lds_buf16(usrc, uoff[nb], t0 * 2 + 16 * h, ub + wv * kU + (nb * 2 + h) * 64);
+      for (int h = 0; h < 2; ++h) lds_buf16(usrc, uoff[nb], t0 * 2 + 16 * h, ubuf + wv * kU + (nb * 2 + h) * 64);
   };
 
   // The vocabulary's last step when V % 64 != 0: with V % 8 == 0 every 8-token
@@ -828,9 +831,9 @@ void expand_eval_lds_kernel(const ExpandParams p) {
 
   // z of the parents of block nb for one step: the accumulator starts at U,
   // then takes the rank-r product on the matrix core.
-  auto logits = [&](const u32x4* wb, const u32x4* ub, int nb, f32x4 (&acc)[4]) {
-    const u32x4 pa = ub[wv * kU + (nb * 2) * 64 + lane];
-    const u32x4 pc = ub[wv * kU + (nb * 2 + 1) * 64 + lane];
+  auto logits = [&](const u32x4* wb, const u32x4 (&pu)[NB][2], int nb, f32x4 (&acc)[4]) {
+    const u32x4 pa = pu[nb][0];
+    const u32x4 pc = pu[nb][1];
     URun<uint16_t> u;
     u.w[0] = pa[0]; u.w[1] = pa[1]; u.w[2] = pa[2]; u.w[3] = pa[3];
     u.w[4] = pc[0]; u.w[5] = pc[1]; u.w[6] = pc[2]; u.w[7] = pc[3];
@@ -875,7 +878,7 @@ void expand_eval_lds_kernel(const ExpandParams p) {
   };
 
   // One 64-token step; j is the step's place in its quad (known at compile time).
-  auto compute = [&](const u32x4* wb, const u32x4* ub, int t0, int step, auto jtag) {
+  auto compute = [&](const u32x4* wb, const u32x4 (&pu)[NB][2], int t0, int step, auto jtag) {
     constexpr int j = decltype(jtag)::value;
     const int tl = t0 + g * 16;
     const int run = step * 4 + g;
@@ -911,7 +914,7 @@ void expand_eval_lds_kernel(const ExpandParams p) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       f32x4 acc[4];
-      logits(wb, ub, nb, acc);
+      logits(wb, pu, nb, acc);
       epilogue(nb, acc);
     }
   };
@@ -981,17 +984,23 @@ void expand_eval_lds_kernel(const ExpandParams p) {
   auto do_step = [&](auto jtag) -> bool {
     constexpr int j = decltype(jtag)::value;
     u32x4* wcur = (j & 1) ? w1 : w0;
-    u32x4* ucur = (j & 1) ? u1 : u0;
     u32x4* wnext = (j & 1) ? w0 : w1;
-    u32x4* unext = (j & 1) ? u0 : u1;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     lower_priority(step);
     const bool more = t0 + 64 < tend;
-    if (more) issue(wnext, unext, t0 + 64);
+    if (more) issue_w(wnext, t0 + 64);
     if (active) {
-      if (t0 + 64 > V) mask_tail(ucur, t0);
-      compute(wcur, ucur, t0, step, jtag);
+      if (t0 + 64 > V) mask_tail(ubuf, t0);
+      u32x4 pu[NB][2];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) pu[nb][h] = ubuf[wv * kU + (nb * 2 + h) * 64 + lane];
+      // the pieces are in registers before the next step's loads overwrite them
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+      if (more) issue_u(t0 + 64);
+      compute(wcur, pu, t0, step, jtag);
       if (SEQ && (j == 3 || !more)) end_quad((t0 >> 6) & ~3);
     }
     if (!more) return false;
@@ -1000,7 +1009,8 @@ void expand_eval_lds_kernel(const ExpandParams p) {
     step = __builtin_amdgcn_readfirstlane(step + 1);
     return true;
   };
-  issue(w0, u0, t0);
+  issue_w(w0, t0);
+  if (active) issue_u(t0);
   for (;;) {
     if (!do_step(std::integral_constant<int, 0>{})) break;
     if (!do_step(std::integral_constant<int, 1>{})) break;
