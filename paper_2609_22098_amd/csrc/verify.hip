@@ -19,7 +19,6 @@ static void verify_level_t(const VerifyPass& vp, int mmax, hipStream_t s) {
   const int J = mmax > 1 ? mmax : 1;
   hipLaunchKernelGGL((verify_pass_a_kernel<TT>), grid, block, 0, s, vp);
   for (int j = 1; j <= J; ++j) hipLaunchKernelGGL((verify_stage_kernel<TT>), grid, block, 0, s, vp, j);
-  hipLaunchKernelGGL((verify_bonus_kernel<TT>), grid, block, 0, s, vp, J);
   hipLaunchKernelGGL((verify_resolve_kernel<TT>), dim3(vp.nitems), dim3(64), 0, s, vp, J);
 }
 

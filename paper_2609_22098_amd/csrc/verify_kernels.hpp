@@ -246,8 +246,10 @@ struct VerifyResult {
 //
 // One level of the walk is a fixed sequence of launches over the items (the
 // requests still walking, each at its current node): pass A, stages
-// 1..max(m_max, 1), the bonus pass and the resolve kernel.  No launch needs the
-// host in between.  The stage-1 launch turns the pass-A partials into the
+// 1..max(m_max, 1) and the resolve kernel.  No launch needs the host in
+// between.  The bonus keys are taken by the sweep that already reads the
+// residual they come from: pass A for a leaf, the last child's stage for a
+// node whose children were all rejected.  The stage-1 launch turns the pass-A partials into the
 // item's constants; each stage launch then advances the item's record (alpha,
 // beta, the decision so far) by one stage from the previous launch's record
 // and Z partials.  Every workgroup of an item computes that step in the same
@@ -509,11 +511,55 @@ __device__ __forceinline__ double block_sum_f64(double v, double* red) {
   return ((red[0] + red[1]) + red[2]) + red[3];
 }
 
-// Pass A: per-chunk maxima and sums of the target and draft rows.
+// Bonus draw (Gumbel-max over a residual r): the key of token y is
+// log2 r(y) - log2(-log2 u_y), u_y from word y & 3 of the Philox call
+// c0 = y >> 2 (tag 3).  Keys are only compared within one item, so r may be
+// any fixed positive multiple of the residual; each chunk keeps its best key
+// (ties: smallest token) and its second-best value.
+struct BonusTop {
+  float best = kNegInf, second = kNegInf;
+  int idx = 0x7FFFFFFF;
+  __device__ __forceinline__ void add(float key, int y) {
+    if (key > best) { second = best; best = key; idx = y; }
+    else if (key > second) second = key;
+  }
+};
+__device__ __forceinline__ void bonus_words(uint32_t (&w)[4], int b, uint32_t pc1, uint32_t pc2, uint32_t c3,
+                                            const PhiloxKeys& keys) {
+  uint32_t w0 = (uint32_t)b >> 2, w1 = pc1, w2 = pc2, w3 = c3;
+  philox10(w0, w1, w2, w3, keys);
+  w[0] = w0; w[1] = w1; w[2] = w2; w[3] = w3;
+}
+__device__ __forceinline__ float gumbel_neg(uint32_t w) {  // -log2(-log2 u)
+  return -__builtin_amdgcn_logf(-__builtin_amdgcn_logf(word_to_uniform(w)));
+}
+// The workgroup's best key, token and second-best value into the item's chunk slot.
+__device__ __forceinline__ void store_bonus(const VerifyPass& vp, int it, int ck, const BonusTop& bt, float* redv,
+                                            int* redi) {
+  float vb = bt.best;
+  int id = bt.idx;
+  block_argmax(vb, id, redv, redi);
+  float s2 = (bt.idx == id) ? bt.second : bt.best;
+  s2 = block_max(s2, redv);
+  if (threadIdx.x == 0) {
+    VBonusPart r;
+    r.best = vb;
+    r.second = s2;
+    r.idx = id;
+    r.pad = 0;
+    vp.bp[(size_t)it * vp.nchunks + ck] = r;
+  }
+}
+
+// Pass A: per-chunk maxima and sums of the target and draft rows.  For an
+// item without children (a leaf: the walk ends with a bonus draw from the
+// target itself) it also takes the bonus keys, with r = 2^(t c - mt).
+
 template <typename TT>
 __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPass vp) {
   __shared__ float red[4];
   __shared__ double redd[4];
+  __shared__ int redi[4];
   __shared__ int loc[TS_MAX_K];
   __shared__ int cnt;
   __shared__ VerifyItem sitem;
@@ -537,6 +583,32 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
   // one sweep: running maxima, and sums relative to them (rescaled when a
   // maximum rises); the draft sum leaves the children out, its maximum does not
   float mt = kNegInf, mz = kNegInf, st = 0.0f, snc = 0.0f;
+  const bool leaf = item.m == 0;  // uniform over the workgroup
+  if (leaf) {
+    const uint32_t pc1 = (uint32_t)item.path, pc2 = (uint32_t)(item.path >> 32);
+    const uint32_t c3 = counter_word3(item.request, item.depth, 3u);
+    BonusTop bt;
+    sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
+      uint32_t w[4];
+      bonus_words(w, b, pc1, pc2, c3, vp.keys);
+      float qt = kNegInf;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (e < nv) qt = fmaxf(qt, tq[e] * vp.c);
+      if (qt > mt) {
+        if (st > 0.0f) st *= exp2_fast(mt - qt);
+        mt = qt;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (e < nv) {
+          st += exp2_fast(tq[e] * vp.c - mt);
+          bt.add(tq[e] * vp.c + gumbel_neg(w[e]), b + e);
+        }
+      }
+    });
+    store_bonus(vp, it, ck, bt, red, redi);
+  } else {
   sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
     float qt = kNegInf, qz = kNegInf;
 #pragma unroll
@@ -562,6 +634,7 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
       }
     }
   });
+  }
   // to the workgroup's maxima
   const float Mt = block_max(mt, red), Mz = block_max(mz, red);
   st = st > 0.0f ? st * exp2_fast(mt - Mt) : 0.0f;
@@ -583,12 +656,16 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_pass_a_kernel(VerifyPas
 // Stage j: advances the item's record by one stage (the stage-1 launch also
 // builds the constants); if child j is rejected, this workgroup adds its
 // chunk's share of Z_j = sum max(alpha_j p - beta'_j qT, 0) over tokens not
-// drawn up to j.  Chunk 0 stores the record for the next launch.
+// drawn up to j.  When j is the item's last child, that same residual (up to
+// the factor 1 / Z_j) is the one the bonus token is drawn from, so the sweep
+// also takes the bonus keys.  Chunk 0 stores the record for the next launch.
 template <typename TT>
 __global__ __launch_bounds__(kVerifyThreads) void verify_stage_kernel(VerifyPass vp, int j) {
   __shared__ VRec shr;
   __shared__ float shL[2];
   __shared__ double redd[4];
+  __shared__ float redv[4];
+  __shared__ int redi[4];
   __shared__ int loc[TS_MAX_K];
   __shared__ int cnt;
   __shared__ VerifyItem sitem;
@@ -666,16 +743,39 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_stage_kernel(VerifyPass
   const float Lt = shL[0], Lz = shL[1];
   const bool vec = vector_rows<TT>(vp);
   float acc = 0.0f;
-  sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
+  if (j == sitem.m) {  // the last child: the sweep also takes the bonus keys
+    const uint32_t pc1 = (uint32_t)sitem.path, pc2 = (uint32_t)(sitem.path >> 32);
+    const uint32_t c3 = counter_word3(sitem.request, sitem.depth, 3u);
+    BonusTop bt;
+    sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
+      uint32_t w[4];
+      bonus_words(w, b, pc1, pc2, c3, vp.keys);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (e < nv && !(nloc && is_listed(b + e, loc, nloc))) {
-        const float p = exp2_fast(tq[e] * vp.c - Lt);
-        const float q = exp2_fast(zq[e] * vp.c - Lz);
-        acc += fmaxf(rec.alpha * p - rec.betap * q, 0.0f);
+      for (int e = 0; e < 4; ++e) {
+        if (e < nv && !(nloc && is_listed(b + e, loc, nloc))) {
+          const float p = exp2_fast(tq[e] * vp.c - Lt);
+          const float q = exp2_fast(zq[e] * vp.c - Lz);
+          const float r = rec.alpha * p - rec.betap * q;
+          if (r > 0.0f) {
+            acc += r;
+            bt.add(__builtin_amdgcn_logf(r) + gumbel_neg(w[e]), b + e);
+          }
+        }
       }
-    }
-  });
+    });
+    store_bonus(vp, it, ck, bt, redv, redi);
+  } else {
+    sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (e < nv && !(nloc && is_listed(b + e, loc, nloc))) {
+          const float p = exp2_fast(tq[e] * vp.c - Lt);
+          const float q = exp2_fast(zq[e] * vp.c - Lz);
+          acc += fmaxf(rec.alpha * p - rec.betap * q, 0.0f);
+        }
+      }
+    });
+  }
   const double z = block_sum_f64((double)acc, redd);
   if (threadIdx.x == 0) vp.zp[((size_t)(j - 1) * vp.nitems + it) * vp.nchunks + ck] = z;
 }
@@ -687,71 +787,6 @@ __device__ __forceinline__ VRec verify_final(const VerifyPass& vp, const VerifyI
   const VRec prev = vp.recs[(size_t)(J - 1) * vp.nitems + it];
   const double Z = stage_z(vp, it, J);
   return verify_advance(prev, Z, VChild{}, item.m, J + 1);
-}
-
-// Bonus: when every child was rejected (or there is none), the chunk's best
-// Gumbel-max key log2 r(y) - log2(-log2 u_y) over the final residual r.
-template <typename TT>
-__global__ __launch_bounds__(kVerifyThreads) void verify_bonus_kernel(VerifyPass vp, int J) {
-  __shared__ VRec sh;
-  __shared__ float redv[4];
-  __shared__ int redi[4];
-  __shared__ int loc[TS_MAX_K];
-  __shared__ int cnt;
-  const int it = blockIdx.x / vp.nchunks, ck = blockIdx.x % vp.nchunks;
-  if (it >= vp.nitems) return;
-  const VerifyItem& item = vp.items[it];
-  VRec v;
-  if (threadIdx.x < 64) v = verify_final(vp, item, it, J);
-  v = share(v, &sh);
-  if (v.status == kAccepted) return;
-  const float Lt = vp.consts[it].Lt, Lz = vp.consts[it].Lz;
-  const int y0 = ck * vp.chunk, y1 = min(vp.V, y0 + vp.chunk);
-  const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
-  const float* zrow = item.m > 0 ? vp.zbuf + (size_t)item.zrow * vp.V : nullptr;
-  const int nloc = item.m > 0 ? chunk_children(item, item.m, y0, y1, loc, &cnt) : 0;
-  const uint32_t pc1 = (uint32_t)item.path, pc2 = (uint32_t)(item.path >> 32);
-  const uint32_t c3 = counter_word3(item.request, item.depth, 3u);
-  float bv = kNegInf, sv = kNegInf;
-  int bi = 0x7FFFFFFF;
-  const bool vec = vector_rows<TT>(vp);
-  sweep_chunk(trow, zrow, y0, y1, vec, [&](int b, const float(&tq)[4], const float(&zq)[4], int nv) {
-    uint32_t w0 = (uint32_t)b >> 2, w1 = pc1, w2 = pc2, w3 = c3;
-    philox10(w0, w1, w2, w3, vp.keys);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int y = b + e;
-      if (e >= nv) break;
-      float l2r;
-      if (!zrow) {
-        l2r = tq[e] * vp.c - Lt;
-      } else {
-        if (nloc && is_listed(y, loc, nloc)) continue;
-        const float p = exp2_fast(tq[e] * vp.c - Lt);
-        const float q = exp2_fast(zq[e] * vp.c - Lz);
-        const float r = v.alpha * p - v.beta * q;
-        if (!(r > 0.0f)) continue;
-        l2r = __builtin_amdgcn_logf(r);
-      }
-      const uint32_t w = e == 0 ? w0 : e == 1 ? w1 : e == 2 ? w2 : w3;
-      const float key = l2r - __builtin_amdgcn_logf(-__builtin_amdgcn_logf(word_to_uniform(w)));
-      if (key > bv) { sv = bv; bv = key; bi = y; }
-      else if (key > sv) sv = key;
-    }
-  });
-  float vb = bv;
-  int id = bi;
-  block_argmax(vb, id, redv, redi);
-  float s2 = (bi == id) ? sv : bv;
-  s2 = block_max(s2, redv);
-  if (threadIdx.x == 0) {
-    VBonusPart r;
-    r.best = vb;
-    r.second = s2;
-    r.idx = id;
-    r.pad = 0;
-    vp.bp[(size_t)it * vp.nchunks + ck] = r;
-  }
 }
 
 // Resolve: one wave per item writes the accepted stage, or the bonus token.
