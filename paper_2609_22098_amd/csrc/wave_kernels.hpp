@@ -82,6 +82,7 @@ __global__ __launch_bounds__(kWaveThreads) void wave_control_kernel(const WavePa
   __shared__ WaveSlot Ns[kWaveMaxNew];
   __shared__ int rank_l[kWaveMaxN];
   __shared__ int rank_n[kWaveMaxNew];
+  __shared__ int order[kWaveMaxNew];  // the new children's indices in pop order
   __shared__ int tmp[kWaveThreads];
   __shared__ int base_sh;
   const int q = blockIdx.x, t = threadIdx.x;
@@ -119,23 +120,53 @@ __global__ __launch_bounds__(kWaveThreads) void wave_control_kernel(const WavePa
   }
   __syncthreads();
 
-  // ranks in the merged pop order (slots are distinct: paths differ)
+  // The new children in pop order: a bitonic sort of their indices over the
+  // next power of two (entries past m sort last).  Slots are distinct (their
+  // paths differ), so the order is total and the sort's result unique.
+  int M = 1;
+  while (M < m) M <<= 1;
+  for (int k = t; k < M; k += kWaveThreads) order[k] = k;
+  __syncthreads();
+  auto before_idx = [&](int a, int b) {  // a ahead of b in pop order, indices past m last
+    if (a >= m) return false;
+    if (b >= m) return true;
+    return wslot_before(Ns[a], Ns[b]);
+  };
+  for (int k = 2; k <= M; k <<= 1) {
+    for (int jj = k >> 1; jj > 0; jj >>= 1) {
+      for (int i = t; i < M / 2; i += kWaveThreads) {
+        const int lo = 2 * i - (i & (jj - 1)), hi = lo + jj;
+        const int a = order[lo], b = order[hi];
+        const bool asc = (lo & k) == 0;
+        if (asc ? before_idx(b, a) : before_idx(a, b)) {
+          order[lo] = b;
+          order[hi] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // ranks in the merged pop order: a new child's place among the new ones
+  // plus the list slots ahead of it, and a list slot's place in the list
+  // plus the new children ahead of it (binary searches in sorted sequences)
   for (int k = t; k < m; k += kWaveThreads) {
-    const WaveSlot a = Ns[k];
+    const int e = order[k];
+    const WaveSlot a = Ns[e];
     int lo = 0, hi = s;
     while (lo < hi) {
       const int mid = (lo + hi) >> 1;
       if (wslot_before(Ls[mid], a)) lo = mid + 1; else hi = mid;
     }
-    int r = lo;
-    for (int j = 0; j < m; ++j) r += wslot_before(Ns[j], a) ? 1 : 0;
-    rank_n[k] = r;
+    rank_n[e] = k + lo;
   }
   for (int i = t; i < s; i += kWaveThreads) {
     const WaveSlot a = Ls[i];
-    int r = i;
-    for (int j = 0; j < m; ++j) r += wslot_before(Ns[j], a) ? 1 : 0;
-    rank_l[i] = r;
+    int lo = 0, hi = m;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (wslot_before(Ns[order[mid]], a)) lo = mid + 1; else hi = mid;
+    }
+    rank_l[i] = i + lo;
   }
   __syncthreads();
   const int total = s + m;
