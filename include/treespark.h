@@ -148,6 +148,11 @@ size_t ts_expand_workspace_size(const ts_drafter* d, int32_t P, int32_t k, float
  * Parent fields are checked on the device: a parent with a token, depth or
  * request out of range gets child_token -1 and NaN values, and nothing out
  * of bounds is read.
+ * U may hold -inf (masked tokens).  With fewer than k finite logits in a
+ * parent's row, the sequential draws after the last finite token are empty
+ * (child_token -1; log q0, log qT, log S and slot key -inf), while the greedy
+ * order and the Gumbel draws continue with -inf tokens by id.  No input
+ * value makes a kernel read outside the arrays it was given.
  * Performance note: parents that share (request, depth) should be adjacent.
  */
 int32_t ts_expand(const ts_drafter* d, const ts_parent* parents, int32_t P, ts_calib calib,

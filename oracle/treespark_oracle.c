@@ -243,6 +243,12 @@ void tso_draw_sequential(const double* z, int V, double T, uint64_t seed, int re
       for (int y = sg * TSO_SEGMENT; y < V && y < (sg + 1) * TSO_SEGMENT; ++y) seg[sg] += mass[y];
     }
     const int sg = pick(seg, nseg, word_to_uniform(w[0]), g);
+    if (sg < 0) {
+      /* no mass left: every token with a finite logit is drawn, so this draw
+       * and the ones after it are empty (q_T^(j) has no support) */
+      for (int i = j; i <= K; ++i) { sigma[i - 1] = -1; gap[i - 1] = INFINITY; }
+      break;
+    }
     const int y0 = sg * TSO_SEGMENT;
     const int nb = ((V - y0 < TSO_SEGMENT ? V - y0 : TSO_SEGMENT) + TSO_BLOCK - 1) / TSO_BLOCK;
     for (int b = 0; b < nb; ++b) {
@@ -302,7 +308,7 @@ int tso_eval(const tso_model* m, int request, int token, int depth, uint64_t pat
     tso_draw_sequential(z, V, T, seed, request, depth, path, K, sg, gap);
     for (int i = 0; i < K; ++i) {
       if (sigma) sigma[i] = sg[i];
-      if (sigma_z) sigma_z[i] = z[sg[i]];
+      if (sigma_z) sigma_z[i] = sg[i] < 0 ? -INFINITY : z[sg[i]];
       if (sigma_g) sigma_g[i] = gap[i];
     }
     if (sigma_g) sigma_g[K] = NAN;

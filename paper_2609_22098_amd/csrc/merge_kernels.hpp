@@ -422,8 +422,10 @@ __device__ __forceinline__ int wave_pick(const float (&m)[NS], float u) {
 // level's largest one, so removing drawn tokens never underflows the rest.
 // The parent's block table lives in LDS when it fits (V <= 40 * 4096), else
 // in its rows of the workspace; a drawn token's block is rewritten in place.
-// Draw j lands in lane j - 1 of gl (token, z).  Every value here is finite
-// or -inf (never NaN), so maxima take the median form.
+// Draw j lands in lane j - 1 of gl (token, z); a draw after every token with
+// a finite logit has been drawn is empty (token -1, z = -inf).  Every value
+// here is finite or -inf for finite or -inf logits, so maxima take the median
+// form; whatever the logits hold, every load stays inside the parent's rows.
 
 template <typename TE, int KS, int NSEG>
 __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, const TE* urow,
@@ -559,7 +561,9 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     // way).  Lane y takes run y / 16 and so holds token t0 + y; its seed is
     // that token's U (-inf past V), the other runs' results on it are unused.
     // Every load is issued before the MFMAs (one round trip).
-    const int t0 = bsel * kBlkTokens;
+    // with no mass left (fewer than j tokens have finite logits) both picks
+    // are -1: the loads then read block 0, no lane is live and the draw is empty
+    const int t0 = max(bsel, 0) * kBlkTokens;
     const int y = t0 + lane;
     typename F::type wf[4][KS];
 #pragma unroll
@@ -586,7 +590,7 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     for (int q = 0; q < 4; ++q)
       zq[q] = max2_med3(__builtin_amdgcn_fmed3f(acc[q][0], acc[q][1], acc[q][2]), acc[q][3]);
     const float zy = g == 0 ? zq[0] : g == 1 ? zq[1] : g == 2 ? zq[2] : zq[3];
-    bool live = y < V && bo >= 0;
+    bool live = y < V && bo >= 0 && sg >= 0;
     for (int k = 0; k < j - 1; ++k) live &= lane_i32(gl.id, k) != y;
     const float xy = live ? zy * p.cT : kNegInf;
     const float mt = wave_max_fin(xy);
@@ -597,7 +601,7 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     const float zsel = lane_f32(zy, to < 0 ? 0 : to);
     if (lane == j - 1) {
       gl.id = to < 0 ? -1 : tsel;
-      gl.aux = zsel;
+      gl.aux = to < 0 ? kNegInf : zsel;
       gl.val = 0.0f;
     }
     // the block and the segment lose the drawn token's mass; both sums are

@@ -181,6 +181,33 @@ def test_sequential_low_temperature(torch, T):
     _expand_and_compare(torch, dr, fr, 8, T, seed=3, tag=f"sequential low T={T}", sampler="sequential")
 
 
+@pytest.mark.parametrize("dtype,r,V", [("f32", 16, 1000), ("bf16", 32, 9000)])
+@pytest.mark.parametrize("T,sampler", [(0.0, "sequential"), (0.7, "sequential"), (0.7, "gumbel")])
+def test_masked_logits_fewer_than_k(torch, dtype, r, V, T, sampler):
+    """Rows of U that are -inf except for 3-5 tokens (masked vocabularies) with k = 8: the
+    sequential sampler's draws past the finite tokens are empty (token -1, -inf values), the
+    greedy and Gumbel orders continue with -inf tokens by id, all as the oracle gives."""
+    dr = synth.make_drafter(V, 3, r, R=2, dtype=dtype, u_sigma=2.0, planted=None, zipf=None,
+                            ew_sigma=0.2, seed=14)
+    rng = np.random.default_rng(15)
+    ninf = np.uint16(0xFF80) if dtype == "bf16" else np.float32(-np.inf)
+    for q in range(dr.R):
+        for d in range(dr.D):
+            keep = rng.choice(V, int(rng.integers(3, 6)), replace=False)
+            row = dr.U[q, d].copy()
+            dr.U[q, d] = ninf
+            dr.U[q, d, keep] = row[keep]
+            dr.U32[q, d] = -np.inf
+            dr.U32[q, d, keep] = (synth.bf16_bits_to_f32(row[keep]) if dtype == "bf16" else row[keep])
+    fr = synth.make_frontier(dr, per_depth=4, seed=3)
+    g = _expand_and_compare(torch, dr, fr, 8, T, seed=2, tag=f"masked {dtype} T={T} {sampler}",
+                            sampler=sampler)
+    if T > 0 and sampler == "sequential":
+        empty = g["child_token"] < 0
+        assert empty.any() and np.all(np.isneginf(g["child_log_q0"][empty]))
+        assert np.all(np.isneginf(g["child_log_surv"][empty])) and np.all(np.isneginf(g["slot_key"][empty]))
+
+
 def test_deterministic_and_invalid_parents(torch):
     """Two calls give bitwise-identical outputs; a parent with an out-of-range field gets
     token -1 and NaN values without disturbing the others."""

@@ -220,6 +220,29 @@ def test_sequential_draws_are_distinct_and_cover_the_vocabulary():
     assert sorted(got.tolist()) == list(range(9))
 
 
+def test_sequential_draws_stop_at_the_support():
+    """q_T has no mass on tokens with -inf logits (§3.3): with m finite logits the first m draws
+    are those m tokens, in the order inverse-CDF sampling over them alone gives, and every later
+    draw is empty (-1), across segment edges."""
+    rng = np.random.default_rng(21)
+    for V, m, K in [(50, 3, 8), (9000, 5, 12), (9000, 1, 4)]:
+        z = np.full(V, -np.inf)
+        keep = np.sort(rng.choice(V, m, replace=False))
+        z[keep] = rng.normal(size=m) * 2.0
+        got, _ = o.draw_sequential(z, 0.7, 4, 1, 2, 0x33, K)
+        assert sorted(got[:m].tolist()) == keep.tolist()
+        assert np.all(got[m:] == -1)
+    # one block: the same words drive inverse-CDF draws over the finite tokens
+    z = np.full(40, -np.inf)
+    keep = np.array([3, 17, 30])
+    z[keep] = [0.5, -1.0, 2.0]
+    got, gap = o.draw_sequential(z, 0.9, 9, 0, 1, 0x7, 6)
+    q = np.zeros(40)
+    q[keep] = special.softmax(z[keep] / 0.9)
+    if gap > 1e-9:
+        assert list(got[:3]) == _inverse_cdf_draws(q, 3, 9, 0, 1, 0x7)
+
+
 def test_sequential_draws_low_temperature_limit():
     """As T -> 0 the residual proposal puts all mass on the best unused token: sigma = pi."""
     rng = np.random.default_rng(8)
