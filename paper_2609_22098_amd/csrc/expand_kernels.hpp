@@ -619,11 +619,31 @@ __device__ __forceinline__ void lds_dma16(const void* src, u32x4* dst_wave_base)
 // Buffer resource word 3 of a raw (unswizzled, byte-addressed) buffer on gfx9.
 constexpr int kRawBufferFlags = 0x00020000;
 // 16 bytes per lane from a raw buffer at voff + soff into LDS at
-// dst_wave_base + 16 * lane.  Out-of-range bytes read as zero.
-__device__ __forceinline__ void lds_buf16(__amdgpu_buffer_rsrc_t src, uint32_t voff, int soff, u32x4* dst_wave_base) {
-  typedef __attribute__((address_space(3))) void* lds_ptr;
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (lds_ptr)dst_wave_base, 16, (int)voff, soff, 0, 0);
+// dst_wave_base + 16 * lane; out-of-range bytes read as zero.  Issued as
+// inline assembly: the kernel orders its LDS tiles with explicit vmcnt waits,
+// and the compiler, which does not see these as writes to LDS, inserts no
+// wait of its own before the LDS reads of other tiles (with the builtin, in a
+// loop it cannot tell which tile a queued load writes, and waits for all of
+// them).  The kernel's waits must cover every read of the tile.  M0 holds the
+// wave's LDS destination (no other instruction of the kernel uses M0); rsrc
+// is the buffer resource as four scalar words.
+__device__ __forceinline__ void lds_buf16_asm(u32x4 rsrc, uint32_t voff, int soff, const u32x4* dst_wave_base) {
+  typedef __attribute__((address_space(3))) const void* lds_ptr;
+  const uint32_t m0 = (uint32_t)(uintptr_t)(lds_ptr)dst_wave_base;
+  asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :: "v"(voff), "s"(rsrc), "s"(soff), "s"(m0) : "memory", "m0");
 }
+// Raw buffer resource of n bytes at base, as four scalar words.
+__device__ __forceinline__ u32x4 raw_rsrc(const void* base, uint32_t n) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  return u32x4{(uint32_t)a, (uint32_t)(a >> 32) & 0xFFFFu, n, (uint32_t)kRawBufferFlags};
+}
+
+// s_waitcnt immediate that waits until at most n vector memory operations of
+// the wave are outstanding (gfx9 encoding: vmcnt in bits 3:0 and 15:14,
+// expcnt in 6:4, lgkmcnt in 11:8; the counters not waited on hold their
+// maxima).  Vector memory operations complete in issue order.
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
 // A mass held as x * 2^r (x >= 0, r finite): the sum of two, against the
 // larger reference.  Equal references keep the order x1 + x2.
@@ -682,11 +702,14 @@ void expand_eval_lds_kernel(const ExpandParams p) {
   typedef typename F::type FT;
   constexpr int kW = 4 * KS * 64;  // 16-byte pieces of one W2 tile
   constexpr int kU = NB * 2 * 64;  // 16-byte pieces of one wave's U tile
+  // W2 tiles (from L2, mostly: every parent group reads them) one step
+  // ahead, in two buffers; U tiles (from HBM: each is read once) two steps
+  // ahead, in two buffers per wave: step t reads U buffer t % 2 into
+  // registers, then queues step t + 2's pieces into it
   __shared__ __attribute__((aligned(16))) u32x4 w0[kW];
   __shared__ __attribute__((aligned(16))) u32x4 w1[kW];
-  // U tiles: each wave's region is its own, so one buffer serves: the wave
-  // reads its step's pieces, then queues the next step's into the same place
-  __shared__ __attribute__((aligned(16))) u32x4 ubuf[4 * kU];
+  __shared__ __attribute__((aligned(16))) u32x4 ub0[4 * kU];
+  __shared__ __attribute__((aligned(16))) u32x4 ub1[4 * kU];
   const int lane = threadIdx.x & 63;
   constexpr int BASE = MODE & 3;
   constexpr bool SAMPLE = BASE != kModeGreedy;  // T > 0: lse of z/T and K draws
@@ -741,6 +764,14 @@ void expand_eval_lds_kernel(const ExpandParams p) {
     pc2[nb] = (uint32_t)(path >> 32);
     pc3[nb] = counter_word3(req, dep, 1u);
   }
+  // the E fragments are in registers before the first tile load is queued:
+  // the compiler does not count the queued loads (inline assembly), so its
+  // own waits for these registers inside the loop would otherwise stall on
+  // them
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) asm volatile("" ::"v"(bfrag[nb][kk]));
 
   // Per parent (shared by its four lane groups): the reference of the sums,
   // in logit units, the level that triggers a raise, and the FMA offsets
@@ -786,32 +817,32 @@ void expand_eval_lds_kernel(const ExpandParams p) {
     const int bb = (wv * KS + j) / KS, kk = (wv * KS + j) % KS;
     woff[j] = (uint32_t)((((n >> 2) * 16 + bb * 4 + (n & 3)) * r + kk * 32 + g * 8) * 2);
   }
-  const __amdgpu_buffer_rsrc_t wsrc =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(W2), 0, V * r * 2, kRawBufferFlags);
-  const __amdgpu_buffer_rsrc_t usrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(U), 0, (int)((uint32_t)p.R * p.D * V * 2), kRawBufferFlags);
+  const u32x4 wsrc = raw_rsrc(W2, (uint32_t)V * r * 2);
+  const u32x4 usrc = raw_rsrc(U, (uint32_t)p.R * p.D * V * 2);
   auto issue_w = [&](u32x4* wb, int t0) {
 #pragma unroll
-    for (int j = 0; j < KS; ++j) lds_buf16(wsrc, woff[j], t0 * r * 2, wb + (wv * KS + j) * 64);
+    for (int j = 0; j < KS; ++j) lds_buf16_asm(wsrc, woff[j], t0 * r * 2, wb + (wv * KS + j) * 64);
   };
-  auto issue_u = [&](int t0) {
+  typedef u32x4 UPieces[NB][2];
+  auto issue_u = [&](u32x4* ub, int t0) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) lds_buf16(usrc, uoff[nb], t0 * 2 + 16 * h, ubuf + wv * kU + (nb * 2 + h) * 64);
+      for (int h = 0; h < 2; ++h) lds_buf16_asm(usrc, uoff[nb], t0 * 2 + 16 * h, ub + wv * kU + (nb * 2 + h) * 64);
   };
 
   // The vocabulary's last step when V % 64 != 0: with V % 8 == 0 every 8-token
-  // piece of U lies wholly before V or wholly at or past it; the latter (its
-  // load read a clamped row) become bf16 -inf, so those logits are -inf.
-  auto mask_tail = [&](u32x4* ub, int t0) {
+  // piece of U lies wholly before V or wholly at or past it; the latter (their
+  // loads read the next row, or zeros past the array) become bf16 -inf, so
+  // those logits are -inf.
+  auto mask_tail = [&](UPieces& pu, int t0) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
         if (t0 + g * 16 + 8 * h >= V) {
           const uint32_t ninf2 = 0xFF80FF80u;
-          ub[wv * kU + (nb * 2 + h) * 64 + lane] = u32x4{ninf2, ninf2, ninf2, ninf2};
+          pu[nb][h] = u32x4{ninf2, ninf2, ninf2, ninf2};
         }
   };
 
@@ -829,9 +860,9 @@ void expand_eval_lds_kernel(const ExpandParams p) {
     offT[nb] = nr * p.cT;
   };
 
-  // z of the parents of block nb for one step: the accumulator starts at U,
-  // then takes the rank-r product on the matrix core.
-  auto logits = [&](const u32x4* wb, const u32x4 (&pu)[NB][2], int nb, f32x4 (&acc)[4]) {
+  // z of the parents of block nb for one step: the accumulator starts at U
+  // (seed), then takes the rank-r product on the matrix core (logits).
+  auto seed = [&](const UPieces& pu, int nb, f32x4 (&acc)[4]) {
     const u32x4 pa = pu[nb][0];
     const u32x4 pc = pu[nb][1];
     URun<uint16_t> u;
@@ -840,11 +871,20 @@ void expand_eval_lds_kernel(const ExpandParams p) {
 #pragma unroll
     for (int bb = 0; bb < 4; ++bb)
       acc[bb] = f32x4{u.get(bb * 4), u.get(bb * 4 + 1), u.get(bb * 4 + 2), u.get(bb * 4 + 3)};
+  };
+  // the step's W2 fragments (shared by the NB blocks), read from LDS at once
+  typedef FT AFrags[4][KS];
+  auto read_a = [&](const u32x4* wb, AFrags& af) {
+#pragma unroll
+    for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) af[bb][kk] = __builtin_bit_cast(FT, wb[(bb * KS + kk) * 64 + lane]);
+  };
+  auto logits = [&](const AFrags& af, int nb, f32x4 (&acc)[4]) {
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
-      for (int bb = 0; bb < 4; ++bb)
-        acc[bb] = F::mma(__builtin_bit_cast(FT, wb[(bb * KS + kk) * 64 + lane]), bfrag[nb][kk], acc[bb]);
+      for (int bb = 0; bb < 4; ++bb) acc[bb] = F::mma(af[bb][kk], bfrag[nb][kk], acc[bb]);
   };
 
   // The run's sums (a0 of z against the parent's reference; ax of z times c
@@ -878,7 +918,7 @@ void expand_eval_lds_kernel(const ExpandParams p) {
   };
 
   // One 64-token step; j is the step's place in its quad (known at compile time).
-  auto compute = [&](const u32x4* wb, const u32x4 (&pu)[NB][2], int t0, int step, auto jtag) {
+  auto compute = [&](const AFrags& af, f32x4 (&accs)[NB][4], int t0, int step, auto jtag) {
     constexpr int j = decltype(jtag)::value;
     const int tl = t0 + g * 16;
     const int run = step * 4 + g;
@@ -913,9 +953,8 @@ void expand_eval_lds_kernel(const ExpandParams p) {
     // block nb's epilogue runs on the vector ALUs
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      f32x4 acc[4];
-      logits(wb, pu, nb, acc);
-      epilogue(nb, acc);
+      logits(af, nb, accs[nb]);
+      epilogue(nb, accs[nb]);
     }
   };
 
@@ -977,30 +1016,47 @@ void expand_eval_lds_kernel(const ExpandParams p) {
     else __builtin_amdgcn_s_setprio(0);
   };
 
-  // One step: wait for its tiles, queue the next step's, compute.  Returns
-  // false after the chunk's last step.  Steps alternate between the two
-  // buffers; a quad is four steps, so its step j uses buffer j & 1.
+  // One step: wait for its tiles, queue the next ones, compute.  Returns
+  // false after the chunk's last step.  Step j of a quad reads the buffers
+  // j & 1.  A U load has two steps' compute to land (one step ahead it
+  // waited out most of its latency under load).
   int t0 = tbeg, step = 0;
   auto do_step = [&](auto jtag) -> bool {
     constexpr int j = decltype(jtag)::value;
     u32x4* wcur = (j & 1) ? w1 : w0;
     u32x4* wnext = (j & 1) ? w0 : w1;
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    lower_priority(step);
+    u32x4* ucur = (j & 1) ? ub1 : ub0;
     const bool more = t0 + 64 < tend;
+    const bool more2 = t0 + 128 < tend;
+    // this step's tiles are in LDS once at most the next step's U pieces
+    // (2 NB per lane, queued last) are outstanding; stores issued since only
+    // make the wait longer
+    if (more && active)
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NB));
+    else
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    // the waits above order the tiles' arrival; a barrier with the usual
+    // workgroup fences would wait for every queued load as well
+    asm volatile("s_barrier" ::: "memory");
+    lower_priority(step);
     if (more) issue_w(wnext, t0 + 64);
     if (active) {
-      if (t0 + 64 > V) mask_tail(ubuf, t0);
-      u32x4 pu[NB][2];
+      UPieces pu;
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int h = 0; h < 2; ++h) pu[nb][h] = ubuf[wv * kU + (nb * 2 + h) * 64 + lane];
-      // the pieces are in registers before the next step's loads overwrite them
+        for (int h = 0; h < 2; ++h) pu[nb][h] = ucur[wv * kU + (nb * 2 + h) * 64 + lane];
+      AFrags af;
+      read_a(wcur, af);
+      // the pieces are in registers before the loads two steps ahead overwrite
+      // them (and no LDS read of the step comes after those loads)
       __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-      if (more) issue_u(t0 + 64);
-      compute(wcur, pu, t0, step, jtag);
+      if (more2) issue_u(ucur, t0 + 128);
+      if (t0 + 64 > V) mask_tail(pu, t0);
+      f32x4 accs[NB][4];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) seed(pu, nb, accs[nb]);
+      compute(af, accs, t0, step, jtag);
       if (SEQ && (j == 3 || !more)) end_quad((t0 >> 6) & ~3);
     }
     if (!more) return false;
@@ -1010,7 +1066,10 @@ void expand_eval_lds_kernel(const ExpandParams p) {
     return true;
   };
   issue_w(w0, t0);
-  if (active) issue_u(t0);
+  if (active) {
+    issue_u(ub0, t0);
+    if (t0 + 64 < tend) issue_u(ub1, t0 + 64);
+  }
   for (;;) {
     if (!do_step(std::integral_constant<int, 0>{})) break;
     if (!do_step(std::integral_constant<int, 1>{})) break;
