@@ -693,10 +693,11 @@ __device__ __forceinline__ void window_transpose(float (&h)[4]) {
 }
 
 // At rank <= 64 with two parent blocks per wave the kernel must fit three
-// waves per SIMD (168 VGPRs): a few registers more halve the waves that hide
-// its latencies.
-template <int KS, int NB, int MODE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KS <= 2 && NB == 2 ? 3 : 1)))
+// waves per SIMD (168 VGPRs), four with eight-wave workgroups (128 VGPRs): a
+// few registers more halve the waves that hide its latencies.  WPG waves per
+// workgroup share each W2 tile (loaded by the first four).
+template <int KS, int NB, int MODE, int WPG>
+__global__ __launch_bounds__(64 * WPG) __attribute__((amdgpu_waves_per_eu(KS <= 2 && NB == 2 ? (WPG == 8 ? 4 : 3) : 1)))
 void expand_eval_lds_kernel(const ExpandParams p) {
   typedef Frag<uint16_t> F;
   typedef typename F::type FT;
@@ -708,8 +709,8 @@ void expand_eval_lds_kernel(const ExpandParams p) {
   // registers, then queues step t + 2's pieces into it
   __shared__ __attribute__((aligned(16))) u32x4 w0[kW];
   __shared__ __attribute__((aligned(16))) u32x4 w1[kW];
-  __shared__ __attribute__((aligned(16))) u32x4 ub0[4 * kU];
-  __shared__ __attribute__((aligned(16))) u32x4 ub1[4 * kU];
+  __shared__ __attribute__((aligned(16))) u32x4 ub0[WPG * kU];
+  __shared__ __attribute__((aligned(16))) u32x4 ub1[WPG * kU];
   const int lane = threadIdx.x & 63;
   constexpr int BASE = MODE & 3;
   constexpr bool SAMPLE = BASE != kModeGreedy;  // T > 0: lse of z/T and K draws
@@ -728,8 +729,8 @@ void expand_eval_lds_kernel(const ExpandParams p) {
   const int pgroup = kx % p.n_pgroups;
   if (chunk >= p.S) return;  // uniform over the workgroup
   const int P = launch_parents(p);
-  if (pgroup * 4 * 16 * NB >= P) return;  // uniform: no parent in this workgroup
-  const int pb = pgroup * 4 + wv;
+  if (pgroup * WPG * 16 * NB >= P) return;  // uniform: no parent in this workgroup
+  const int pb = pgroup * WPG + wv;
   const bool active = pb * 16 * NB < P;  // idle waves still load W2 and join the barriers
 
   const uint16_t* U = static_cast<const uint16_t*>(p.U);
@@ -814,14 +815,16 @@ void expand_eval_lds_kernel(const ExpandParams p) {
   uint32_t woff[KS];
 #pragma unroll
   for (int j = 0; j < KS; ++j) {
-    const int bb = (wv * KS + j) / KS, kk = (wv * KS + j) % KS;
+    const int bb = ((wv & 3) * KS + j) / KS, kk = ((wv & 3) * KS + j) % KS;
     woff[j] = (uint32_t)((((n >> 2) * 16 + bb * 4 + (n & 3)) * r + kk * 32 + g * 8) * 2);
   }
   const u32x4 wsrc = raw_rsrc(W2, (uint32_t)V * r * 2);
   const u32x4 usrc = raw_rsrc(U, (uint32_t)p.R * p.D * V * 2);
   auto issue_w = [&](u32x4* wb, int t0) {
+    if (wv < 4) {
 #pragma unroll
-    for (int j = 0; j < KS; ++j) lds_buf16_asm(wsrc, woff[j], t0 * r * 2, wb + (wv * KS + j) * 64);
+      for (int j = 0; j < KS; ++j) lds_buf16_asm(wsrc, woff[j], t0 * r * 2, wb + (wv * KS + j) * 64);
+    }
   };
   typedef u32x4 UPieces[NB][2];
   auto issue_u = [&](u32x4* ub, int t0) {

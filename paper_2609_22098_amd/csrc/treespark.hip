@@ -223,7 +223,11 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
            ((uint64_t)d->R * d->D + 1) * d->V * 2 + 64 < (1ull << 31) &&
            (uint64_t)d->V * d->r * 2 < (1ull << 31);
   pl.n_pblocks = (P + 16 * pl.NB - 1) / (16 * pl.NB);
+  // waves per workgroup (each workgroup loads every W2 tile of its chunk
+  // once): eight for the greedy LDS kernel with two blocks per wave at rank
+  // <= 64 (that kernel fits four waves per SIMD), else four
   pl.wpg = pl.lds ? 4 : std::min(4, std::max(1, pl.n_pblocks));
+  if (pl.lds && pl.NB == 2 && pl.ks <= 2 && pl.mode == kModeGreedy) pl.wpg = 8;
   pl.n_pgroups = (pl.n_pblocks + pl.wpg - 1) / pl.wpg;
   // Chunks: enough workgroups to fill every CU at the kernel's occupancy in
   // whole rounds (all workgroups of a round finish together), chunks of
@@ -236,7 +240,8 @@ Plan make_plan(const ts_drafter* d, int P, float T, int sampler, bool store_z = 
         eval_blocks_per_cu(d->dtype, pl.ks, pl.NB, eval_mode, store_z, pl.lds, 64 * pl.wpg);
     const int s_min = (d->V + 4095) / 4096;
     const int rounds = std::max(1, (pl.n_pgroups * s_min + concurrent - 1) / concurrent);
-    const int s_want = std::max(1, (rounds * concurrent + pl.n_pgroups - 1) / pl.n_pgroups);
+    // at most rounds * concurrent workgroups: a few more would take a round of their own
+    const int s_want = std::max(1, rounds * concurrent / pl.n_pgroups);
     vc = (d->V + s_want - 1) / s_want;
   }
 #ifdef TS_DEBUG_RUNS
