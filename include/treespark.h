@@ -383,6 +383,36 @@ int32_t ts_calib_labels(const ts_tree* tree, const void* target, int32_t target_
 int32_t ts_calib_fit(const float* x, const int32_t* y, const int32_t* sel, int32_t n, int32_t max_iter,
                      double tol, float* out, void* stream);
 
+/*
+ * ts_verify_set_mode: how ts_verify runs its T > 0 levels on the calling
+ * thread.  TS_VERIFY_AUTO (the default): in one launch per level whenever
+ * every workgroup of the level can be resident at once (the workgroups of an
+ * item wait for one another between the walk's steps), else through the
+ * per-stage launches.  TS_VERIFY_STAGED: always through the per-stage
+ * launches, which never wait on other workgroups; for callers that keep
+ * other kernels running on the device during ts_verify (a level's one launch
+ * assumes its workgroups get the whole device, and otherwise waits up to
+ * about a tenth of a second per step before it runs the level again per
+ * stage).  Both give results within the same rounding of the walk.
+ * Errors: an unknown mode.
+ */
+#define TS_VERIFY_AUTO 0
+#define TS_VERIFY_STAGED 1
+int32_t ts_verify_set_mode(int32_t mode);
+
+/*
+ * ts_verify_level_counts: how the T > 0 levels of ts_verify calls on the
+ * calling thread ran.  *fused: levels run in one launch, each workgroup
+ * holding its chunk of the target and draft rows in registers (when every
+ * workgroup of the level can be resident at once); *fallbacks: of those, the
+ * levels run again through the per-stage launches because a wait between
+ * workgroups ran out; *staged: levels run through the per-stage launches from
+ * the start (pass A, one launch per stage, resolve).  The counts are the
+ * thread's totals since its first call (ts_release_thread_state keeps them).
+ * Errors: NULL pointers.
+ */
+int32_t ts_verify_level_counts(int64_t* fused, int64_t* fallbacks, int64_t* staged);
+
 /* Description of the last error on the calling thread ("" if none). */
 const char* ts_last_error(void);
 

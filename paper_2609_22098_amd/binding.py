@@ -25,7 +25,8 @@ SAMPLERS = {"gumbel": 0, "sequential": 1}  # ts_sampler
 EXPORTED = ("ts_ladder_lookup", "ts_ladder_default", "ts_tree_mask_words", "ts_tree_mask",
             "ts_expand_workspace_size", "ts_expand", "ts_build_tree_workspace_size", "ts_build_tree",
             "ts_verify_workspace_size", "ts_verify", "ts_calib_labels_workspace_size", "ts_calib_labels",
-            "ts_calib_fit", "ts_last_error", "ts_version", "ts_release_thread_state", "ts_expand_noalloc")
+            "ts_calib_fit", "ts_last_error", "ts_version", "ts_release_thread_state", "ts_expand_noalloc",
+            "ts_verify_level_counts", "ts_verify_set_mode")
 TS_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
@@ -111,12 +112,31 @@ def lib():
         L.ts_version.restype = ctypes.c_char_p
         L.ts_release_thread_state.argtypes = []
         L.ts_release_thread_state.restype = I32
+        L.ts_verify_level_counts.argtypes = [P, P, P]
+        L.ts_verify_level_counts.restype = I32
+        L.ts_verify_set_mode.argtypes = [I32]
+        L.ts_verify_set_mode.restype = I32
         _lib = L
         # atexit runs its handlers last-registered first: this one (registered
         # after torch's import) frees the library's pinned buffer and events
         # while torch and the HIP runtime are still up
         atexit.register(release_thread_state)
     return _lib
+
+
+VERIFY_MODES = {"auto": 0, "staged": 1}  # TS_VERIFY_AUTO, TS_VERIFY_STAGED
+
+
+def verify_set_mode(mode):
+    """ts_verify_set_mode for the calling thread: "auto" or "staged"."""
+    _check(lib().ts_verify_set_mode(VERIFY_MODES[mode]))
+
+
+def verify_level_counts():
+    """ts_verify_level_counts for the calling thread: (fused, fallbacks, staged) T > 0 levels."""
+    out = [ctypes.c_int64(0) for _ in range(3)]
+    _check(lib().ts_verify_level_counts(*(ctypes.byref(x) for x in out)))
+    return tuple(int(x.value) for x in out)
 
 
 def release_thread_state():

@@ -41,5 +41,13 @@ void launch_calib_fit(const float* x, const int32_t* y, const int32_t* sel, int 
                       float* out, hipStream_t s);
 // One level of the T > 0 walk: pass A, stages 1..max(mmax, 1), bonus, resolve.
 void launch_verify_level(const VerifyPass& vp, bool bf16, int mmax, hipStream_t s);
+// The same level in one launch with register-resident chunks: quads per
+// thread, resident workgroups per CU (0 if unknown), the launch, and the
+// clearing of its counters.
+struct VFused;
+int verify_fused_quads(bool bf16);
+int verify_fused_blocks_per_cu(bool bf16);
+void launch_verify_fused(const VerifyPass& vp, const VFused& f, bool bf16, hipStream_t s);
+void launch_verify_clear(int* p, int n, hipStream_t s);
 
 }  // namespace ts

@@ -16,6 +16,7 @@
 #include <vector>
 
 #include "launch.hpp"
+#include "verify_fused.hpp"
 
 // The scratch of ts_expand_noalloc, one copy per GPU.  In host code `scratch`
 // names a host-side stand-in, not device memory: kernels get the device
@@ -69,6 +70,10 @@ struct ThreadState {
   char* stage = nullptr;
   size_t stage_bytes = 0;
   std::vector<hipEvent_t> events;
+  // T > 0 verification levels run in one launch, run again through the
+  // per-stage launches after a wait ran out, and run per stage from the start
+  int64_t fused_levels = 0, fused_fallbacks = 0, staged_levels = 0;
+  int32_t verify_mode = TS_VERIFY_AUTO;
 };
 ThreadState& thread_state() {
   thread_local ThreadState st;
@@ -677,7 +682,7 @@ const KidIndex& kid_index(const ts_tree* t) {
 
 struct VerifyLayout {
   size_t off_rows, off_arg, off_gap, off_items, off_z, off_exp;
-  size_t off_pa, off_zp, off_bp, off_cst, off_rec, bytes;
+  size_t off_pa, off_zp, off_bp, off_cst, off_rec, off_sync, bytes;
   int max_chunks;
 };
 
@@ -690,6 +695,42 @@ void verify_chunks(int V, int nitems, int* nchunks, int* chunk) {
   len = ((len + kVChunkQuantum - 1) / kVChunkQuantum) * kVChunkQuantum;
   *chunk = len;
   *nchunks = (V + len - 1) / len;
+}
+
+// Launch shape of a level in one launch (register-resident chunks), or ok =
+// false when the level's chunks would not all be resident at once.  Chunks
+// are at least kVChunkQuantum tokens long (the partial arrays hold that many
+// per item) and at most what a workgroup holds.
+struct FusedPlan {
+  bool ok;
+  int cpi, chunk;
+};
+// Polls of one wait before it gives up (a poll takes about a microsecond).
+constexpr int kFusedSpinLimit = 1 << 16;
+FusedPlan fused_plan(int V, int nitems, bool bf16) {
+  FusedPlan fp{false, 0, 0};
+  const int bpc = verify_fused_blocks_per_cu(bf16);
+  if (nitems < 1 || bpc < 1) return fp;
+  const long long capacity = (long long)bpc * device_cus();
+  const int per_wg = verify_fused_quads(bf16) * kVChunkQuantum;
+  const int cpi_min = (V + per_wg - 1) / per_wg;
+  if (cpi_min > kFusedMaxCpi || (long long)nitems * cpi_min > std::min<long long>(capacity, kFusedMaxGrid)) return fp;
+  const int max_chunks = (V + kVChunkQuantum - 1) / kVChunkQuantum;
+  int cpi = (int)std::min<long long>(std::min<long long>(capacity, kFusedMaxGrid) / nitems,
+                                     std::min(max_chunks, kFusedMaxChunks));
+  cpi = std::max(cpi, cpi_min);
+  int chunk = (V + cpi - 1) / cpi;
+  chunk = (chunk + 3) / 4 * 4;
+  fp.ok = true;
+  fp.chunk = chunk;
+  fp.cpi = (V + chunk - 1) / chunk;
+  return fp;
+}
+
+// Slot words of the one-launch levels: kSlotWords per workgroup, for the
+// most workgroups a launch over R items can have.
+size_t fused_slot_words(int R) {
+  return (size_t)kSlotWords * (size_t)std::min<long long>((long long)R * kFusedMaxCpi, kFusedMaxGrid);
 }
 
 VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
@@ -711,6 +752,7 @@ VerifyLayout verify_layout(const ts_drafter* d, int cap, float T) {
     v.off_bp = o; o += align256(ic * sizeof(VBonusPart));
     v.off_cst = o; o += align256((size_t)d->R * sizeof(VConst));
     v.off_rec = o; o += align256((size_t)d->R * TS_MAX_K * sizeof(VRec));
+    v.off_sync = o; o += align256(fused_slot_words(d->R) * 8 + 4);
   }
   v.bytes = o;
   return v;
@@ -759,6 +801,23 @@ extern "C" {
 const char* ts_last_error(void) { return g_last_error.c_str(); }
 
 const char* ts_version(void) { return "treespark-mi355x 0.2 (gfx950)"; }
+
+int32_t ts_verify_set_mode(int32_t mode) {
+  g_last_error.clear();
+  if (mode != TS_VERIFY_AUTO && mode != TS_VERIFY_STAGED) return fail(TS_EINVAL, "unknown verify mode %d", mode);
+  thread_state().verify_mode = mode;
+  return TS_OK;
+}
+
+int32_t ts_verify_level_counts(int64_t* fused, int64_t* fallbacks, int64_t* staged) {
+  g_last_error.clear();
+  if (!fused || !fallbacks || !staged) return fail(TS_EINVAL, "an output is NULL");
+  const ThreadState& st = thread_state();
+  *fused = st.fused_levels;
+  *fallbacks = st.fused_fallbacks;
+  *staged = st.staged_levels;
+  return TS_OK;
+}
 
 int32_t ts_release_thread_state(void) {
   g_last_error.clear();
@@ -1126,8 +1185,20 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
   char* hs = nullptr;
   const size_t hs_items = align256((size_t)R * sizeof(VerifyItem));
   const size_t hs_par = align256((size_t)R * sizeof(ts_parent));
-  if ((rc = host_stage(hs_items + hs_par + (size_t)R * sizeof(VerifyResult), &hs)) != TS_OK) return rc;
+  const size_t hs_res = align256((size_t)R * sizeof(VerifyResult));
+  if ((rc = host_stage(hs_items + hs_par + hs_res + 256, &hs)) != TS_OK) return rc;
   const VerifyResult* res = reinterpret_cast<const VerifyResult*>(hs + hs_items + hs_par);
+  volatile int32_t* herr = reinterpret_cast<volatile int32_t*>(hs + hs_items + hs_par + hs_res);
+  // the one-launch levels' slots and flag start the call at zero; each
+  // launch tags its slot words with an epoch of its own
+  uint64_t* dslots = reinterpret_cast<uint64_t*>(ws + vl.off_sync);
+  const size_t nslots = fused_slot_words(R);
+  int* derr = reinterpret_cast<int*>(dslots + nslots);
+  const int nclear = (int)(nslots * 2 + 1);
+  const bool bf16 = target_dtype == TS_BF16;
+  uint32_t epoch = 0;
+  launch_verify_clear(reinterpret_cast<int*>(dslots), nclear, s);
+  TS_HIP(hipGetLastError());
   while (!active.empty()) {
     items.clear();
     zpar.clear();
@@ -1181,9 +1252,40 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
     vp.results = const_cast<VerifyResult*>(res);  // pinned: the resolve kernel writes it
     int mmax = 0;
     for (const VerifyItem& it : items) mmax = std::max(mmax, it.m);
-    launch_verify_level(vp, target_dtype == TS_BF16, mmax, s);
-    TS_HIP(hipGetLastError());
-    TS_HIP(hipStreamSynchronize(s));
+    const FusedPlan fp = thread_state().verify_mode == TS_VERIFY_STAGED ? FusedPlan{false, 0, 0}
+                                                                          : fused_plan(V, ni, bf16);
+    if (fp.ok) {
+      ++thread_state().fused_levels;
+      // one launch for the level; a wait that ran out (some workgroup was
+      // not resident) sends the level through the per-stage launches
+      VerifyPass fvp = vp;
+      fvp.nchunks = fp.cpi;
+      fvp.chunk = fp.chunk;
+      VFused f{};
+      f.cpi = fp.cpi;
+      f.chunk = fp.chunk;
+      f.slots = dslots;
+      f.epoch = ++epoch;
+      f.err = derr;
+      f.herr = const_cast<int32_t*>(herr);
+      f.spin_limit = kFusedSpinLimit;
+      *herr = 0;
+      launch_verify_fused(fvp, f, bf16, s);
+      TS_HIP(hipGetLastError());
+      TS_HIP(hipStreamSynchronize(s));
+      if (*herr != 0) {
+        ++thread_state().fused_fallbacks;
+        launch_verify_clear(derr, 1, s);
+        launch_verify_level(vp, bf16, mmax, s);
+        TS_HIP(hipGetLastError());
+        TS_HIP(hipStreamSynchronize(s));
+      }
+    } else {
+      ++thread_state().staged_levels;
+      launch_verify_level(vp, bf16, mmax, s);
+      TS_HIP(hipGetLastError());
+      TS_HIP(hipStreamSynchronize(s));
+    }
     std::vector<int> next;
     for (int i = 0; i < ni; ++i) {
       const int q = items[i].request;

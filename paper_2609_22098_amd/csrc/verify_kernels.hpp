@@ -344,14 +344,17 @@ __device__ __forceinline__ VRec stage_test(float lp, float lq, float lR, float i
   return r;
 }
 
-// Constants of item `it` from the pass-A partials (one whole wave; every lane
-// ends with the same values).
-template <typename TT>
-__device__ VConst verify_consts(const VerifyPass& vp, const VerifyItem& item, int it) {
+// Constants of an item from its nc pass-A partials, pa_at(k) for chunk k (one
+// whole wave): every lane gets the normalisers, lane s < m child s's terms
+// (zero on the other lanes).
+struct VConstLane {
+  float Lt, Lz;
+  float lp, lq, lR, invR, lu;
+};
+template <typename TT, typename PartAt>
+__device__ VConstLane verify_consts_lane(const VerifyPass& vp, const VerifyItem& item, int nc, PartAt&& pa_at) {
   const int lane = threadIdx.x & 63;
-  const int nc = vp.nchunks;
   const int m = item.m;
-  const VPartA* pa = vp.pa + (size_t)it * nc;
   // child `lane`'s target value and draft logit, loaded alongside the partials
   const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
   // loaded on every lane from valid addresses (a lane past m reads token 0
@@ -363,25 +366,24 @@ __device__ VConst verify_consts(const VerifyPass& vp, const VerifyItem& item, in
   const float wzl = keep_or_zero(zrow[ctok] * vp.c, mine);
   float mt = kNegInf, mz = kNegInf;
   for (int k = lane; k < nc; k += 64) {
-    mt = fmaxf(mt, pa[k].mt);
-    mz = fmaxf(mz, pa[k].mz);
+    const VPartA a = pa_at(k);
+    mt = fmaxf(mt, a.mt);
+    mz = fmaxf(mz, a.mz);
   }
   mt = wave_max(mt);
   mz = wave_max(mz);
   double st = 0.0, snc = 0.0;
   for (int k = lane; k < nc; k += 64) {
-    st += pa[k].st * (double)exp2_fast(pa[k].mt - mt);
-    if (m > 0) snc += pa[k].snc * (double)exp2_fast(pa[k].mz - mz);
+    const VPartA a = pa_at(k);
+    st += a.st * (double)exp2_fast(a.mt - mt);
+    if (m > 0) snc += a.snc * (double)exp2_fast(a.mz - mz);
   }
   st = wave_sum_f64(st);
   snc = wave_sum_f64(snc);
-  VConst C;
+  VConstLane C;
   C.Lt = mt + (float)log2(st);
   C.Lz = 0.0f;
-#pragma unroll
-  for (int k = 0; k < TS_MAX_K; ++k) {
-    C.lp[k] = 0.0f; C.lq[k] = 0.0f; C.lR[k] = 0.0f; C.invR[k] = 0.0f; C.lu[k] = 0.0f;
-  }
+  C.lp = 0.0f; C.lq = 0.0f; C.lR = 0.0f; C.invR = 0.0f; C.lu = 0.0f;
   if (m == 0) return C;
   // suffix sums of the proposal mass, suf[s] = non-children + children s..m-1,
   // added in the fixed order s = m-1 .. 0 from the children's terms of every lane
@@ -400,29 +402,45 @@ __device__ VConst verify_consts(const VerifyPass& vp, const VerifyItem& item, in
   const double suf0 = acc;
   C.Lz = mz + (float)log2(suf0);
   // lane s: child s's terms
-  float lp = 0.0f, lq = 0.0f, lR = 0.0f, invR = 0.0f, lu = 0.0f;
   if (mine) {
     const double Rs = my_suf / suf0;
-    lp = tv * vp.c - C.Lt;
-    lq = wzl - C.Lz;
-    lR = (float)log2(Rs);
-    invR = (float)(1.0 / Rs);
+    C.lp = tv * vp.c - C.Lt;
+    C.lq = wzl - C.Lz;
+    C.lR = (float)log2(Rs);
+    C.invR = (float)(1.0 / Rs);
     uint32_t w0 = (uint32_t)(lane + 1), w1 = (uint32_t)item.path, w2 = (uint32_t)(item.path >> 32),
              w3 = counter_word3(item.request, item.depth, 2u);
     philox10(w0, w1, w2, w3, vp.keys);
-    lu = __builtin_amdgcn_logf(word_to_uniform(w0));
+    C.lu = __builtin_amdgcn_logf(word_to_uniform(w0));
   }
+  return C;
+}
+// The same constants gathered on every lane.
+template <typename TT, typename PartAt>
+__device__ VConst verify_consts_from(const VerifyPass& vp, const VerifyItem& item, int nc, PartAt&& pa_at) {
+  const VConstLane L = verify_consts_lane<TT>(vp, item, nc, pa_at);
+  const int m = item.m;
+  VConst C;
+  C.Lt = L.Lt;
+  C.Lz = L.Lz;
 #pragma unroll
   for (int s = 0; s < TS_MAX_K; ++s) {
+    C.lp[s] = 0.0f; C.lq[s] = 0.0f; C.lR[s] = 0.0f; C.invR[s] = 0.0f; C.lu[s] = 0.0f;
     if (s < m) {
-      C.lp[s] = lane_f32(lp, s);
-      C.lq[s] = lane_f32(lq, s);
-      C.lR[s] = lane_f32(lR, s);
-      C.invR[s] = lane_f32(invR, s);
-      C.lu[s] = lane_f32(lu, s);
+      C.lp[s] = lane_f32(L.lp, s);
+      C.lq[s] = lane_f32(L.lq, s);
+      C.lR[s] = lane_f32(L.lR, s);
+      C.invR[s] = lane_f32(L.invR, s);
+      C.lu[s] = lane_f32(L.lu, s);
     }
   }
   return C;
+}
+// Constants of item `it` from the partials of the pass-A launch.
+template <typename TT>
+__device__ VConst verify_consts(const VerifyPass& vp, const VerifyItem& item, int it) {
+  const VPartA* pa = vp.pa + (size_t)it * vp.nchunks;
+  return verify_consts_from<TT>(vp, item, vp.nchunks, [&](int k) { return pa[k]; });
 }
 
 // Record after the launch of stage j >= 2 from the record of stage j - 1.
@@ -789,25 +807,21 @@ __device__ __forceinline__ VRec verify_final(const VerifyPass& vp, const VerifyI
   return verify_advance(prev, Z, VChild{}, item.m, J + 1);
 }
 
-// Resolve: one wave per item writes the accepted stage, or the bonus token.
-template <typename TT>
-__global__ __launch_bounds__(64) void verify_resolve_kernel(VerifyPass vp, int J) {
-  const int it = blockIdx.x;
-  if (it >= vp.nitems) return;
-  const VerifyItem& item = vp.items[it];
-  const VRec v = verify_final(vp, item, it, J);
-  const int lane = threadIdx.x;
+// An item's result from its final record and, when no child was accepted,
+// the nc chunk bests of the bonus keys, bp_at(k) for chunk k (one whole wave).
+template <typename BonusAt>
+__device__ VerifyResult verify_result(const VRec& v, int nc, BonusAt&& bp_at) {
+  const int lane = threadIdx.x & 63;
   VerifyResult r;
   r.accepted = v.status == kAccepted ? v.stage : 0;
   r.bonus = -1;
   r.margin = v.margin;
   r.pad = 0;
   if (v.status != kAccepted) {
-    const VBonusPart* bp = vp.bp + (size_t)it * vp.nchunks;
     float best = kNegInf, second = kNegInf;
     int idx = 0x7FFFFFFF;
-    for (int k = lane; k < vp.nchunks; k += 64) {
-      const VBonusPart b = bp[k];
+    for (int k = lane; k < nc; k += 64) {
+      const VBonusPart b = bp_at(k);
       if (b.best > best || (b.best == best && b.idx < idx)) {
         second = fmaxf(second, best);
         best = b.best;
@@ -830,7 +844,19 @@ __global__ __launch_bounds__(64) void verify_resolve_kernel(VerifyPass vp, int J
     r.bonus = id;
     r.margin = fminf(r.margin, gap);
   }
-  if (lane == 0) {
+  return r;
+}
+
+// Resolve: one wave per item writes the accepted stage, or the bonus token.
+template <typename TT>
+__global__ __launch_bounds__(64) void verify_resolve_kernel(VerifyPass vp, int J) {
+  const int it = blockIdx.x;
+  if (it >= vp.nitems) return;
+  const VerifyItem& item = vp.items[it];
+  const VRec v = verify_final(vp, item, it, J);
+  const VBonusPart* bp = vp.bp + (size_t)it * vp.nchunks;
+  const VerifyResult r = verify_result(v, vp.nchunks, [&](int k) { return bp[k]; });
+  if (threadIdx.x == 0) {
     vp.results[it] = r;  // pinned host memory
     __threadfence_system();
   }

@@ -20,12 +20,22 @@ def _declared():
 
 def test_library_exports_every_declared_symbol():
     declared = _declared()
-    assert len(declared) == 17
+    assert len(declared) == 19
     assert sorted(b.EXPORTED) == declared
     L = b.lib()
     for name in declared:
         assert hasattr(L, name), name
     assert b"gfx950" in L.ts_version()
+
+
+def test_verify_level_counts_start_at_zero_and_check_pointers():
+    L = b.lib()
+    x = ctypes.c_int64(-1)
+    assert L.ts_verify_level_counts(None, ctypes.byref(x), ctypes.byref(x)) == b.TS_EINVAL
+    # no ts_verify call has run on this thread
+    assert b.verify_level_counts() == (0, 0, 0)
+    assert L.ts_verify_set_mode(2) == b.TS_EINVAL and L.ts_verify_set_mode(-1) == b.TS_EINVAL
+    assert L.ts_verify_set_mode(1) == b.TS_OK and L.ts_verify_set_mode(0) == b.TS_OK
 
 
 def test_release_without_state_touches_no_device():

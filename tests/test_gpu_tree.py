@@ -48,10 +48,12 @@ def _compare_all(dr, tree, anchors, thetas, N, K, T, seed, requests=None, tag=""
     return refs
 
 
-def _verify_compare(dd, dr, tree, tgt32, requests, T, seed, tag, min_whole=0.75):
+def _verify_compare(dd, dr, tree, tgt32, requests, T, seed, tag, min_whole=0.75, mode="auto", expect=None):
     """ts_verify on all requests of the tree against the oracle's walk on `requests`; tgt32[q] holds
     request q's target rows (float32 values of what the GPU read).  Walks are compared up to the
-    first near-tie level; at least min_whole of them must be compared whole."""
+    first near-tie level; at least min_whole of them must be compared whole.  mode: the thread's
+    verify mode for the call; expect ("fused" or "staged"): how its T > 0 levels must have run
+    (every level in one launch with no wait running out, or every level per stage)."""
     from paper_2609_22098_amd import binding
     import torch
     cap = tree.cap
@@ -60,7 +62,18 @@ def _verify_compare(dd, dr, tree, tgt32, requests, T, seed, tag, min_whole=0.75)
         tgt[q, :len(rows)] = synth.f32_to_bf16_bits(rows) if dr.dtype == "bf16" else rows
     t = torch.from_numpy(tgt)
     target = (t.view(torch.bfloat16) if dr.dtype == "bf16" else t).cuda()
-    path, plen, bonus = binding.verify(dd, tree, target, T, seed)
+    before = binding.verify_level_counts()
+    binding.verify_set_mode(mode)
+    try:
+        path, plen, bonus = binding.verify(dd, tree, target, T, seed)
+    finally:
+        binding.verify_set_mode("auto")
+    fused, fallbacks, staged = (a - b for a, b in zip(binding.verify_level_counts(), before))
+    print(f"{tag}: T > 0 levels fused {fused} (fallbacks {fallbacks}), staged {staged}")
+    if expect == "fused":
+        assert fused >= 1 and fallbacks == 0 and staged == 0, (fused, fallbacks, staged)
+    elif expect == "staged":
+        assert staged >= 1 and fused == 0, (fused, fallbacks, staged)
     om = o.Model(dr.U32, dr.E32, dr.W2_32)
     tally = Tally()
     whole = 0
@@ -223,24 +236,31 @@ def _prefixes(tree, q):
     return pre
 
 
-@pytest.mark.parametrize("T", [0.0, 1.0, 0.7])
-def test_verify_parity_multi_request(torch, T):
-    """ts_verify against the oracle walk on 8 requests (greedy and recursive rejection)."""
-    dr = synth.make_drafter(3000, 6, 32, R=8, dtype="bf16", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
+@pytest.mark.parametrize("T,mode,dtype,V", [(0.0, "auto", "bf16", 3000), (1.0, "auto", "bf16", 3000),
+                                            (0.7, "auto", "bf16", 3000), (0.7, "staged", "bf16", 3000),
+                                            (0.7, "auto", "f32", 3000), (1.0, "staged", "f32", 3000),
+                                            (0.7, "auto", "bf16", 2999), (0.5, "auto", "f32", 2997)])
+def test_verify_parity_multi_request(torch, T, mode, dtype, V):
+    """ts_verify against the oracle walk on 8 requests (greedy and recursive rejection; at T > 0
+    each level in one launch, and through the per-stage launches), bf16 and float targets, rows
+    of a multiple of 4 tokens (quad loads) and not (token loads)."""
+    dr = synth.make_drafter(V, 6, 32, R=8, dtype=dtype, u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
                             ew_sigma=0.3, seed=5, u_scale=2.0)
     anchors, _, _ = synth.make_controls(8, dr.V, 0.0, seed=5)
     thetas = np.full(8, 0.01, np.float32)
     N, K = 24, 4
     dd, tree = _trees(dr, anchors, thetas, N, K, T, 21)
     tgt32 = {q: synth.make_target_rows(dr, q, tree.depth[q, :int(tree.n[q]) + 1], 1.0, seed=2)[1] for q in range(8)}
-    _verify_compare(dd, dr, tree, tgt32, list(range(8)), T, 33, tag=f"verify multi T={T}")
+    _verify_compare(dd, dr, tree, tgt32, list(range(8)), T, 33, tag=f"verify multi T={T} {mode} {dtype} V={V}", mode=mode,
+                    expect=None if T == 0 else ("fused" if mode == "auto" else "staged"))
 
 
-@pytest.mark.parametrize("T", [0.7, 1.0])
-def test_verify_parity_many_chunks(torch, T):
-    """ts_verify against the oracle walk with a 300000-token vocabulary and two requests: each
-    level item spans 293 chunks, more than the 256 whose Z partials a stage loads up front, so
-    the stages also sum the rest in the same order."""
+@pytest.mark.parametrize("T,mode", [(0.7, "staged"), (1.0, "staged"), (0.7, "auto")])
+def test_verify_parity_many_chunks(torch, T, mode):
+    """ts_verify against the oracle walk with a 300000-token vocabulary and two requests.  Per
+    stage, each level item spans 293 chunks, more than the 256 whose Z partials a stage loads up
+    front, so the stages also sum the rest in the same order; in one launch per level, an item
+    spans 32 chunks of 9376 tokens."""
     R, V = 2, 300000
     dr = synth.make_drafter(V, 3, 32, R=R, dtype="bf16", u_sigma=3.0, planted=None, zipf=(6.0, 1.1),
                             ew_sigma=0.3, seed=9, u_scale=2.0)
@@ -249,13 +269,16 @@ def test_verify_parity_many_chunks(torch, T):
     N, K = 6, 3
     dd, tree = _trees(dr, anchors, thetas, N, K, T, 4)
     tgt32 = {q: synth.make_target_rows(dr, q, tree.depth[q, :int(tree.n[q]) + 1], 1.0, seed=3)[1] for q in range(R)}
-    _verify_compare(dd, dr, tree, tgt32, list(range(R)), T, 41, tag=f"verify V={V} T={T}", min_whole=0.5)
+    _verify_compare(dd, dr, tree, tgt32, list(range(R)), T, 41, tag=f"verify V={V} T={T} {mode}", min_whole=0.5,
+                    mode=mode, expect="fused" if mode == "auto" else "staged")
 
 
-def test_verify_serving_sequential(torch):
+@pytest.mark.parametrize("mode", ["auto", "staged"])
+def test_verify_serving_sequential(torch, mode):
     """The benchmark's verification: 64 requests, V=151936, bf16, r=64 (the logit recompute with
     two 32-deep MFMA steps), T=0.7, trees built with sequential draws under the requests' theta,
-    target rows U + N(0, 1); every request's walk against the oracle."""
+    target rows U + N(0, 1); every request's walk against the oracle, each level in one launch
+    (as the benchmark runs it) and through the per-stage launches."""
     w = synth.WORKLOADS[3]
     dr = synth.make_workload_drafter(3, seed=0)
     anchors, thetas, _ = synth.make_controls(dr.R, dr.V, w["theta"], seed=0)
@@ -265,7 +288,8 @@ def test_verify_serving_sequential(torch):
     assert with_kids >= 16
     tgt32 = {q: synth.make_target_rows(dr, q, tree.depth[q, :int(tree.n[q]) + 1], w["target_sigma"], seed=0)[1]
              for q in range(dr.R)}
-    _verify_compare(dd, dr, tree, tgt32, list(range(dr.R)), 0.7, 0, tag="verify serving T=0.7 sequential")
+    _verify_compare(dd, dr, tree, tgt32, list(range(dr.R)), 0.7, 0, tag=f"verify serving T=0.7 sequential {mode}",
+                    mode=mode, expect="fused" if mode == "auto" else "staged")
 
 
 @pytest.mark.parametrize("sampler", ["gumbel", "sequential"])
