@@ -420,12 +420,12 @@ const char* ts_last_error(void);
  * ts_release_thread_state: free what the library keeps for the calling host
  * thread between calls: a page-locked staging buffer (the small transfers of
  * ts_build_tree, ts_verify and ts_calib_labels, which kernels also read and
- * write directly) and the events that pace ts_build_tree's device waves.  It
- * first waits for the current device (hipDeviceSynchronize).  Call it before
+ * write directly).  It first waits for the current device
+ * (hipDeviceSynchronize).  Call it before
  * the thread or the process ends, while the HIP runtime is still up: the
  * library frees nothing from thread-exit or process-exit handlers, since those
  * may run after the runtime (or a profiler attached to it) has been torn down.
- * A later call that needs the buffer or the events allocates them again.
+ * A later call that needs the buffer allocates it again.
  * Returns TS_OK, or TS_EHIP if a HIP call fails.
  */
 int32_t ts_release_thread_state(void);

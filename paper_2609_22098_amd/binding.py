@@ -118,7 +118,7 @@ def lib():
         L.ts_verify_set_mode.restype = I32
         _lib = L
         # atexit runs its handlers last-registered first: this one (registered
-        # after torch's import) frees the library's pinned buffer and events
+        # after torch's import) frees the library's pinned buffer
         # while torch and the HIP runtime are still up
         atexit.register(release_thread_state)
     return _lib

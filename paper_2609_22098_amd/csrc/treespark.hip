@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <climits>
 #include <cmath>
 #include <cstdarg>
@@ -59,9 +60,9 @@ struct DrainOnError {
 };
 
 // Page-locked host staging for the small transfers of the host loops, so that
-// they are true asynchronous DMA copies, and the events that pace the device
-// waves.  Both belong to the calling host thread, grow on demand and live
-// until ts_release_thread_state() frees them; every user synchronises its
+// they are true asynchronous DMA copies (kernels also read and write parts of
+// it directly).  It belongs to the calling host thread, grows on demand and
+// lives until ts_release_thread_state() frees it; every user synchronises its
 // stream before it rewrites or grows the buffer.  There is deliberately no
 // destructor: a thread-exit destructor of the main thread would run inside
 // exit(), after the HIP runtime (and any profiler attached to it) may have
@@ -69,7 +70,6 @@ struct DrainOnError {
 struct ThreadState {
   char* stage = nullptr;
   size_t stage_bytes = 0;
-  std::vector<hipEvent_t> events;
   // T > 0 verification levels run in one launch, run again through the
   // per-stage launches after a wait ran out, and run per stage from the start
   int64_t fused_levels = 0, fused_fallbacks = 0, staged_levels = 0;
@@ -508,21 +508,12 @@ WaveTreeOut tree_out_of(const ts_tree* t) {
   return o;
 }
 
-hipEvent_t* wave_events(int n) {
-  std::vector<hipEvent_t>& ev = thread_state().events;
-  while ((int)ev.size() < n) {
-    hipEvent_t e = nullptr;
-    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return nullptr;
-    ev.push_back(e);
-  }
-  return ev.data();
-}
-
 // ts_build_tree with the waves on the device (no budget; N, K within the
 // control kernel's limits).  Wave w + 1 is queued before the host learns
 // its size (its kernels read the size the control step wrote), so the GPU
 // never waits for the host between waves; the host reads each wave's size
-// through an event and stops queueing at the first empty wave.
+// from the pinned word the control step writes and stops queueing at the
+// first empty wave.
 int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std::vector<float>& log_theta,
                           int N, int K, ts_calib calib, float T, uint64_t seed, int sampler, ts_tree* out,
                           const ts_tree* device_out, char* ws, const BuildLayout& bl, hipStream_t s) {
@@ -532,8 +523,6 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   const size_t hs_up = align256((size_t)R * 8), hs_cnt = align256((size_t)(D + 2) * 4);
   int32_t rc = host_stage(hs_up + hs_cnt + tb.bytes, &hs);
   if (rc != TS_OK) return rc;
-  hipEvent_t* ev = wave_events(D + 2);
-  if (!ev) return fail(TS_EHIP, "hipEventCreate failed");
   // roots and thresholds stay in the pinned buffer: the init kernel reads them
   std::memcpy(hs, anchor, (size_t)R * 4);
   std::memcpy(hs + (size_t)R * 4, log_theta.data(), (size_t)R * 4);
@@ -577,15 +566,36 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
 
   // queue wave w: expansion of par[w & 1] (at most Pub parents; the device
   // holds the count) and the control step, which also writes the next
-  // wave's size into hcnt; an event marks its end
+  // wave's size into hcnt[w + 1] (pinned, -1 until then).  The host polls
+  // that word: an event recorded between the waves' kernels would hold the
+  // next kernel back by about 6 us on the device.
+  for (int i = 0; i < D + 2; ++i) hcnt[i] = -1;
   auto queue_wave = [&](int w, int Pub) -> int32_t {
     int32_t r = run_expand(d, wp.par[w & 1], Pub, calib, K, T, seed, sampler, &eo, ws + bl.off_exp, s,
                            wp.pcount + w);
     if (r != TS_OK) return r;
     launch_wave_control(wp, w, s);
     TS_HIP(hipGetLastError());
-    TS_HIP(hipEventRecord(ev[w + 1], s));
     return TS_OK;
+  };
+  // the size of wave i from its word.  After 20 ms the wait also asks the
+  // stream (a stream query enqueues a marker, which would hold the next
+  // kernel back like an event): one that has drained or failed without
+  // writing the word ends it
+  auto wave_size = [&](int i, int* out_n) -> int32_t {
+    const auto t0 = std::chrono::steady_clock::now();
+    for (unsigned n = 1;; ++n) {
+      const int v = hcnt[i];
+      if (v >= 0) {
+        *out_n = v;
+        return TS_OK;
+      }
+      if ((n & 4095) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(20)) {
+        const hipError_t q = hipStreamQuery(s);
+        if (q != hipSuccess && q != hipErrorNotReady) return fail(TS_EHIP, "HIP error %d while waiting for wave %d", (int)q, i);
+        if (q == hipSuccess && hcnt[i] < 0) return fail(TS_EINTERNAL, "wave %d ended without its size", i);
+      }
+    }
   };
   const int per_req = std::max(0, N - 1);  // children a request can send to the next wave
   int Pw = R;                              // size of wave w, known
@@ -594,8 +604,8 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
     const long long ub = std::min<long long>((long long)Pw * K, (long long)R * per_req);
     if (w + 1 < D && ub > 0)
       if ((rc = queue_wave(w + 1, (int)ub)) != TS_OK) return rc;
-    TS_HIP(hipEventSynchronize(ev[w + 1]));
-    const int Pn = hcnt[w + 1];
+    int Pn = 0;
+    if ((rc = wave_size(w + 1, &Pn)) != TS_OK) return rc;
     if (Pn <= 0 || w + 1 >= D || ub == 0) break;
     if (Pn > ub) return fail(TS_EINTERNAL, "wave %d has %d parents, more than the bound %lld", w + 1, Pn, ub);
     Pw = Pn;
@@ -822,13 +832,11 @@ int32_t ts_verify_level_counts(int64_t* fused, int64_t* fallbacks, int64_t* stag
 int32_t ts_release_thread_state(void) {
   g_last_error.clear();
   ThreadState& st = thread_state();
-  if (!st.stage && st.events.empty()) return TS_OK;
+  if (!st.stage) return TS_OK;
   // every stream that used them has been synchronised by its call, but a
   // caller's later work may still reference the staging buffer's contents:
   // wait for the device before freeing anything
   TS_HIP(hipDeviceSynchronize());
-  for (hipEvent_t e : st.events) TS_HIP(hipEventDestroy(e));
-  st.events.clear();
   if (st.stage) TS_HIP(hipHostFree(st.stage));
   st.stage = nullptr;
   st.stage_bytes = 0;

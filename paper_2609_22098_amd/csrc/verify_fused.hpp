@@ -174,6 +174,7 @@ template <typename TT, int NQ>
 __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(4))) void verify_fused_kernel(
     VerifyPass vp, VFused f) {
   using Q = typename TQuad<TT>::type;
+  static_assert(4 * NQ <= 64, "a thread's tokens fit the 64-bit child mask");
   __shared__ Q tl[NQ * kVerifyThreads];  // each thread's target quads, [q][thread]
   __shared__ VerifyItem sitem;
   __shared__ VConst sC;
@@ -237,8 +238,12 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       if (b0 + 1024 * q >= y1) break;
+      // one quad's Philox words at a time: tied to the keys taken so far,
+      // the next quad's words are not computed ahead (register pressure)
+      int bq = b0 + 1024 * q;
+      asm volatile("" : "+v"(bq) : "v"(bt.best));
       uint32_t w[4];
-      bonus_words(w, b0 + 1024 * q, pc1, pc2, c3, vp.keys);
+      bonus_words(w, bq, pc1, pc2, c3, vp.keys);
 #pragma unroll
       for (int e = 0; e < 4; ++e) bt.add(tquad_at(tq[q], e) * c + gumbel_neg(w[e]), b0 + 1024 * q + e);
     }
@@ -254,6 +259,12 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
     }
     bonus = true;
   } else {
+    // an item with children holds the level's longest chain of steps: its
+    // waves go first when leaves' bonus keys share the SIMDs
+    __builtin_amdgcn_s_setprio(2);
+    // the children's values, for the constants, on their way during pass A
+    VChildVals cv{0.0f, 0.0f};
+    if (tid < 64) cv = load_child_vals<TT>(vp, sitem);
     // pass A: the chunk's maxima, then its sums relative to them; the draft
     // sum leaves every child out.  The target quads then move to LDS.
     float mt = kNegInf, mz = kNegInf;
@@ -280,11 +291,19 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
 #pragma unroll
         for (int e = 0; e < 4; ++e) snc += exp2_fast(zq[q][e] * c - mzs);
     } else {
+      // bit 4 q + e: the thread's token (q, e) is a child, left out of the sum
+      uint64_t cmask = 0;
+      for (int k = 0; k < nloc; ++k) {
+        const int at = loc[k] - b0;
+        if (at >= 0 && at < 1024 * NQ && (at & 1023) < 4) cmask |= 1ull << (4 * (at >> 10) + (at & 3));
+      }
 #pragma unroll
       for (int q = 0; q < NQ; ++q)
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (!is_listed(b0 + 1024 * q + e, loc, nloc)) snc += exp2_fast(zq[q][e] * c - mzs);
+        for (int e = 0; e < 4; ++e) {
+          const float x = exp2_fast(zq[q][e] * c - mzs);
+          snc += ((cmask >> (4 * q + e)) & 1) ? 0.0f : x;
+        }
     }
     const double dst = block_sum_f64((double)st, redd);
     const double dsnc = block_sum_f64((double)snc, redd);
@@ -307,7 +326,7 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
           a.st = (double)__uint_as_float(w[2]);
           a.snc = (double)__uint_as_float(w[3]);
           return a;
-        });
+        }, cv);
         if (lane < m) {
           sC.lp[lane] = C.lp;
           sC.lq[lane] = C.lq;
@@ -366,8 +385,10 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
           for (int q = 0; q < NQ; ++q) {
             if (b0 + 1024 * q >= y1) break;
             const Q t = tl[q * kVerifyThreads + tid];
+            int bq = b0 + 1024 * q;
+            asm volatile("" : "+v"(bq) : "v"(bt.best));
             uint32_t w[4];
-            bonus_words(w, b0 + 1024 * q, pc1, pc2, c3, vp.keys);
+            bonus_words(w, bq, pc1, pc2, c3, vp.keys);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const float r = a * exp2_fast(tquad_at(t, e) * c - Lt) - bb * zq[q][e];

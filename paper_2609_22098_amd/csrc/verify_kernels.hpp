@@ -299,10 +299,28 @@ __device__ __forceinline__ bool vector_rows(const VerifyPass& vp) {
   return (vp.V & 3) == 0 && (reinterpret_cast<uintptr_t>(vp.target) & (4 * sizeof(TT) - 1)) == 0;
 }
 
+// Wave-wide fp64 sum in the fixed order of wave_sum: DPP moves of both
+// halves (pairs, quads, halves of a row, rows), then the four rows' sums in
+// order.  Every lane gets the same value.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, 0xF, 0xF, true);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, true);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ double lane_f64(double v, int l) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), l);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
 __device__ __forceinline__ double wave_sum_f64(double v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += dpp_f64<0xB1>(v);
+  v += dpp_f64<0x4E>(v);
+  v += dpp_f64<0x141>(v);
+  v += dpp_f64<0x140>(v);
+  return ((lane_f64(v, 0) + lane_f64(v, 16)) + lane_f64(v, 32)) + lane_f64(v, 48);
 }
 
 // Per-item constants of one level, written by the stage-1 launch: the base-2
@@ -351,19 +369,31 @@ struct VConstLane {
   float Lt, Lz;
   float lp, lq, lR, invR, lu;
 };
-template <typename TT, typename PartAt>
-__device__ VConstLane verify_consts_lane(const VerifyPass& vp, const VerifyItem& item, int nc, PartAt&& pa_at) {
+// Child `lane`'s target value and draft logit (times c), zero past the
+// children.  Loaded on every lane from valid addresses (a lane past m reads
+// token 0 of the item's rows, logit row 0 when there is none) and masked after.
+struct VChildVals {
+  float tv, wzl;
+};
+template <typename TT>
+__device__ __forceinline__ VChildVals load_child_vals(const VerifyPass& vp, const VerifyItem& item) {
   const int lane = threadIdx.x & 63;
-  const int m = item.m;
-  // child `lane`'s target value and draft logit, loaded alongside the partials
   const TT* trow = static_cast<const TT*>(vp.target) + ((size_t)item.request * vp.cap + item.node) * vp.V;
-  // loaded on every lane from valid addresses (a lane past m reads token 0
-  // of the item's rows, logit row 0 when there is none) and masked after
-  const uint32_t mine = opaque_mask(lane < m);
+  const uint32_t mine = opaque_mask(lane < item.m);
   const int ctok = item.child_tok[min(lane, TS_MAX_K - 1)] & (int)mine;
   const float* zrow = vp.zbuf + (size_t)max(item.zrow, 0) * vp.V;
-  const float tv = keep_or_zero(target_at(trow, ctok), mine);
-  const float wzl = keep_or_zero(zrow[ctok] * vp.c, mine);
+  VChildVals v;
+  v.tv = keep_or_zero(target_at(trow, ctok), mine);
+  v.wzl = keep_or_zero(zrow[ctok] * vp.c, mine);
+  return v;
+}
+template <typename TT, typename PartAt>
+__device__ VConstLane verify_consts_lane(const VerifyPass& vp, const VerifyItem& item, int nc, PartAt&& pa_at,
+                                         const VChildVals& cv) {
+  const int lane = threadIdx.x & 63;
+  const int m = item.m;
+  const uint32_t mine = opaque_mask(lane < m);
+  const float tv = cv.tv, wzl = cv.wzl;
   float mt = kNegInf, mz = kNegInf;
   for (int k = lane; k < nc; k += 64) {
     const VPartA a = pa_at(k);
@@ -418,7 +448,8 @@ __device__ VConstLane verify_consts_lane(const VerifyPass& vp, const VerifyItem&
 // The same constants gathered on every lane.
 template <typename TT, typename PartAt>
 __device__ VConst verify_consts_from(const VerifyPass& vp, const VerifyItem& item, int nc, PartAt&& pa_at) {
-  const VConstLane L = verify_consts_lane<TT>(vp, item, nc, pa_at);
+  // the children's values are loaded alongside the partials
+  const VConstLane L = verify_consts_lane<TT>(vp, item, nc, pa_at, load_child_vals<TT>(vp, item));
   const int m = item.m;
   VConst C;
   C.Lt = L.Lt;
