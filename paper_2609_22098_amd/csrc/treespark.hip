@@ -1194,9 +1194,11 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
   const size_t hs_items = align256((size_t)R * sizeof(VerifyItem));
   const size_t hs_par = align256((size_t)R * sizeof(ts_parent));
   const size_t hs_res = align256((size_t)R * sizeof(VerifyResult));
-  if ((rc = host_stage(hs_items + hs_par + hs_res + 256, &hs)) != TS_OK) return rc;
+  const size_t hs_next = align256((size_t)R * sizeof(VerifyNext));
+  if ((rc = host_stage(hs_items + hs_par + hs_res + hs_next + 256, &hs)) != TS_OK) return rc;
   const VerifyResult* res = reinterpret_cast<const VerifyResult*>(hs + hs_items + hs_par);
-  volatile int32_t* herr = reinterpret_cast<volatile int32_t*>(hs + hs_items + hs_par + hs_res);
+  VerifyNext* hnext = reinterpret_cast<VerifyNext*>(hs + hs_items + hs_par + hs_res);
+  volatile int32_t* herr = reinterpret_cast<volatile int32_t*>(hs + hs_items + hs_par + hs_res + hs_next);
   // the one-launch levels' slots and flag start the call at zero; each
   // launch tags its slot words with an epoch of its own
   uint64_t* dslots = reinterpret_cast<uint64_t*>(ws + vl.off_sync);
@@ -1277,6 +1279,20 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
       f.err = derr;
       f.herr = const_cast<int32_t*>(herr);
       f.spin_limit = kFusedSpinLimit;
+      f.next_host = hnext;
+      // each item's children: node, path, and whether the walk ends there
+      for (int i = 0; i < ni; ++i) {
+        const VerifyItem& it = items[i];
+        VerifyNext nx{};
+        const int* ch = kids.first(it.request, it.node);
+        for (int j = 0; j < it.m; ++j) {
+          const size_t o = (size_t)it.request * cap + ch[j];
+          nx.child_node[j] = ch[j];
+          nx.child_path[j] = tree->path[o];
+          if (kids.count(it.request, ch[j]) == 0) nx.leaf_mask |= 1u << j;
+        }
+        hnext[i] = nx;
+      }
       *herr = 0;
       launch_verify_fused(fvp, f, bf16, s);
       TS_HIP(hipGetLastError());
@@ -1301,7 +1317,10 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
         const int c = kids.first(q, cur[q])[res[i].accepted - 1];
         path_nodes[(size_t)q * TS_MAX_D + path_len[q]++] = c;
         cur[q] = c;
-        next.push_back(q);
+        if (res[i].leaf_bonus)
+          bonus[q] = res[i].bonus;  // the accepted child has no children: its bonus is drawn
+        else
+          next.push_back(q);
       } else {
         bonus[q] = res[i].bonus;
       }

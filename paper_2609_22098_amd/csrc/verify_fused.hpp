@@ -52,6 +52,7 @@ struct VFused {
   int* err;          // device flag: a wait ran out
   int32_t* herr;     // the flag's pinned host copy
   int spin_limit;    // polls before a wait gives up
+  const VerifyNext* next_host;  // [nitems], pinned host memory
 };
 
 // Quad of target values as loaded: four bf16 in two words, or four floats.
@@ -170,6 +171,40 @@ __device__ __forceinline__ bool poll_slots(const VFused& f, int it, int w0, uint
   }
 }
 
+// Bonus keys of a node without children over the thread's quads of its
+// target row (r = 2^(t c - const): the draw comes from the target itself),
+// reduced over the workgroup; thread 0 stores the chunk's best, second best
+// and token in the bonus slots.
+template <typename Q, int NQ>
+__device__ __forceinline__ void leaf_keys(const Q (&tq)[NQ], int b0, int y1, float c, uint64_t path, uint32_t c3,
+                                          const VerifyPass& vp, const VFused& f, int it, int ck, float* redv,
+                                          int* redi) {
+  const uint32_t pc1 = (uint32_t)path, pc2 = (uint32_t)(path >> 32);
+  BonusTop bt;
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    if (b0 + 1024 * q >= y1) break;
+    // one quad's Philox words at a time: tied to the keys taken so far, the
+    // next quad's words are not computed ahead (register pressure)
+    int bq = b0 + 1024 * q;
+    asm volatile("" : "+v"(bq) : "v"(bt.best));
+    uint32_t w[4];
+    bonus_words(w, bq, pc1, pc2, c3, vp.keys);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) bt.add(tquad_at(tq[q], e) * c + gumbel_neg(w[e]), b0 + 1024 * q + e);
+  }
+  float vb = bt.best;
+  int id = bt.idx;
+  block_argmax(vb, id, redv, redi);
+  float s2 = (bt.idx == id) ? bt.second : bt.best;
+  s2 = block_max(s2, redv);
+  if (threadIdx.x == 0) {
+    put_slot(f, it, ck, kSlotB, __float_as_uint(vb));
+    put_slot(f, it, ck, kSlotB + 1, __float_as_uint(s2));
+    put_slot(f, it, ck, kSlotB + 2, (uint32_t)id);
+  }
+}
+
 template <typename TT, int NQ>
 __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(4))) void verify_fused_kernel(
     VerifyPass vp, VFused f) {
@@ -177,6 +212,7 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
   static_assert(4 * NQ <= 64, "a thread's tokens fit the 64-bit child mask");
   __shared__ Q tl[NQ * kVerifyThreads];  // each thread's target quads, [q][thread]
   __shared__ VerifyItem sitem;
+  __shared__ VerifyNext snext;
   __shared__ VConst sC;
   __shared__ VRec shr;
   __shared__ float redv[4];
@@ -189,8 +225,13 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
   if (it >= vp.nitems) return;  // never: the grid is nitems * cpi
   const int tid = threadIdx.x;
   constexpr int kItemWords = (int)(sizeof(VerifyItem) / 4);
+  constexpr int kNextWords = (int)(sizeof(VerifyNext) / 4);
+  static_assert(kItemWords + kNextWords <= kVerifyThreads, "item and next words");
   if (tid < kItemWords)
     reinterpret_cast<int32_t*>(&sitem)[tid] = reinterpret_cast<const int32_t*>(vp.items_host + it)[tid];
+  else if (tid < kItemWords + kNextWords)
+    reinterpret_cast<int32_t*>(&snext)[tid - kItemWords] =
+        reinterpret_cast<const int32_t*>(f.next_host + it)[tid - kItemWords];
   __syncthreads();
   const int m = sitem.m;
   const int y0 = ck * f.chunk, y1 = min(vp.V, y0 + f.chunk);
@@ -233,30 +274,8 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
   rec.margin = __builtin_huge_valf();
 
   if (m == 0) {
-    // leaf: bonus keys with r = 2^(t c - const)
-    BonusTop bt;
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      if (b0 + 1024 * q >= y1) break;
-      // one quad's Philox words at a time: tied to the keys taken so far,
-      // the next quad's words are not computed ahead (register pressure)
-      int bq = b0 + 1024 * q;
-      asm volatile("" : "+v"(bq) : "v"(bt.best));
-      uint32_t w[4];
-      bonus_words(w, bq, pc1, pc2, c3, vp.keys);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) bt.add(tquad_at(tq[q], e) * c + gumbel_neg(w[e]), b0 + 1024 * q + e);
-    }
-    float vb = bt.best;
-    int id = bt.idx;
-    block_argmax(vb, id, redv, redi);
-    float s2 = (bt.idx == id) ? bt.second : bt.best;
-    s2 = block_max(s2, redv);
-    if (tid == 0) {
-      put_slot(f, it, ck, kSlotB, __float_as_uint(vb));
-      put_slot(f, it, ck, kSlotB + 1, __float_as_uint(s2));
-      put_slot(f, it, ck, kSlotB + 2, (uint32_t)id);
-    }
+    // leaf: bonus keys from the target row
+    leaf_keys(tq, b0, y1, c, sitem.path, c3, vp, f, it, ck, redv, redi);
     bonus = true;
   } else {
     // an item with children holds the level's longest chain of steps: its
@@ -437,13 +456,35 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
       }
     }
   }
+  // an accepted child without children ends the walk there: its bonus comes
+  // from its own target row, drawn here instead of at the next level
+  bool leaf_next = false;
+  if (alive && m > 0 && rec.status == kAccepted && ((snext.leaf_mask >> (rec.stage - 1)) & 1u)) {
+    leaf_next = true;
+    const int cn = snext.child_node[rec.stage - 1];
+    const TT* crow = static_cast<const TT*>(vp.target) + ((size_t)sitem.request * vp.cap + cn) * vp.V;
+    Q cq[NQ];
+    f32x4 unused[NQ];
+    if (vector_rows<TT>(vp)) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) load_quad_vec<TT>(crow, nullptr, b0 + 1024 * q, y1, cq[q], unused[q]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) load_quad_tok<TT>(crow, nullptr, b0 + 1024 * q, y1, cq[q], unused[q]);
+    }
+    leaf_keys(cq, b0, y1, c, snext.child_path[rec.stage - 1], counter_word3(sitem.request, sitem.depth + 1, 3u),
+              vp, f, it, ck, redv, redi);
+    bonus = true;
+  }
   // chunk 0 writes the item's result: the accepted child, or the bonus token
-  // from the chunks' best keys
+  // from the chunks' best keys, or both
   if (ck == 0 && alive && tid < 64) {
     uint32_t w[3] = {0u, 0u, 0u};
     const bool ok = bonus ? poll_slots<3>(f, it, kSlotB, w) : true;
     if (ok) {
-      const VerifyResult r = verify_result(rec, f.cpi, [&](int) {
+      VRec rr = rec;
+      if (leaf_next) rr.status = kExhausted;  // the bonus part of the result
+      VerifyResult r = verify_result(rr, f.cpi, [&](int) {
         VBonusPart b;
         b.best = __uint_as_float(w[0]);
         b.second = __uint_as_float(w[1]);
@@ -451,6 +492,10 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
         b.pad = 0;
         return b;
       });
+      if (leaf_next) {
+        r.accepted = rec.stage;
+        r.leaf_bonus = 1;
+      }
       if (tid == 0) {
         vp.results[it] = r;  // pinned host memory
         __threadfence_system();

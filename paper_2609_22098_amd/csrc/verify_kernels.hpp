@@ -237,8 +237,18 @@ struct VerifyItem {
 
 struct VerifyResult {
   int32_t accepted;  // 1-based sibling index of the accepted child, 0 = none
-  int32_t bonus;     // bonus token when accepted == 0
+  int32_t bonus;     // bonus token when accepted == 0, or at the accepted leaf (leaf_bonus)
   float margin;      // smallest |log u - log ratio| (or bonus key gap)
+  int32_t leaf_bonus;  // 1: the accepted child has no children and bonus is its draw
+};
+
+// The children of a level item as the one-launch level needs them to carry
+// on into an accepted child without children: its node, its path and whether
+// it has children (pinned host memory, one per item).
+struct VerifyNext {
+  int32_t child_node[TS_MAX_K];
+  uint64_t child_path[TS_MAX_K];
+  uint32_t leaf_mask;  // bit s: child s (draw order) has no children
   int32_t pad;
 };
 
@@ -847,7 +857,7 @@ __device__ VerifyResult verify_result(const VRec& v, int nc, BonusAt&& bp_at) {
   r.accepted = v.status == kAccepted ? v.stage : 0;
   r.bonus = -1;
   r.margin = v.margin;
-  r.pad = 0;
+  r.leaf_bonus = 0;
   if (v.status != kAccepted) {
     float best = kNegInf, second = kNegInf;
     int idx = 0x7FFFFFFF;
