@@ -823,17 +823,17 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   const float a = p.calib_a, bb = p.calib_b;
   float zb = 0.0f;
   if constexpr (SAMPLE) {
-    // bound of slot j: the first of the greedy order not drawn before j
+    // bound of slot j: the first of the greedy order not drawn before j.
+    // Lane i < K first finds the first draw s < K - 1 that took greedy entry
+    // i (K if none); slot j's bound is then the first entry with drawn_at >= j.
+    int drawn_at = K;
+#pragma unroll
+    for (int s2 = TS_MAX_K - 2; s2 >= 0; --s2)
+      if (s2 < K - 1 && lane_i32(gl.id, s2) == zl.id) drawn_at = s2;
     int bi = K - 1;
-    for (int i = K - 1; i >= 0; --i) {
-      const int pid = lane_i32(zl.id, i);
-      bool used = false;
-      for (int s2 = 0; s2 < K - 1; ++s2) {
-        const int gid = lane_i32(gl.id, s2);
-        used |= (s2 < lane) && (gid == pid);
-      }
-      if (!used) bi = i;
-    }
+#pragma unroll
+    for (int i = TS_MAX_K - 1; i >= 0; --i)
+      if (i < K && lane_i32(drawn_at, i) >= lane) bi = i;
     zb = __shfl(zl.val, bi, 64);
   }
   if (lane < K) {
