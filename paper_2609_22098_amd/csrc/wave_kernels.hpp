@@ -191,13 +191,15 @@ __global__ __launch_bounds__(kWaveThreads) void wave_control_kernel(const WavePa
     const int base = nc > 0 ? atomicAdd(&wp.pcount[w + 1], nc) : 0;
     base_sh = base;
     wp.span[(w + 1) & 1][q] = WaveSpan{base, nc};
-    // the last workgroup to finish hands the next wave's size to the host
-    __threadfence();
-    if (atomicAdd(&wp.done[w + 1], 1) == wp.R - 1) {
-      __threadfence();
-      wp.host_count[w + 1] = atomicAdd(&wp.pcount[w + 1], 0);
-      __threadfence_system();
-    }
+    // the last workgroup to finish hands the next wave's size to the host.
+    // Only the count goes to the host (the lists and parents reach the next
+    // wave's kernels across the launch boundary): this workgroup's count
+    // atomic has returned before its done increment is issued, so the last
+    // one reads the final count; a system-scope store hands it over.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (atomicAdd(&wp.done[w + 1], 1) == wp.R - 1)
+      __hip_atomic_store(const_cast<int32_t*>(wp.host_count + w + 1), atomicAdd(&wp.pcount[w + 1], 0),
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
   __syncthreads();
   ts_parent* out = wp.par[(w + 1) & 1] + base_sh;
