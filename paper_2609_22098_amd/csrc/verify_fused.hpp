@@ -496,10 +496,8 @@ __global__ __launch_bounds__(kVerifyThreads) __attribute__((amdgpu_waves_per_eu(
         r.accepted = rec.stage;
         r.leaf_bonus = 1;
       }
-      if (tid == 0) {
-        vp.results[it] = r;  // pinned host memory
-        __threadfence_system();
-      }
+      // pinned host memory, read by the host after it synchronises the stream
+      if (tid == 0) vp.results[it] = r;
     }
   }
 }

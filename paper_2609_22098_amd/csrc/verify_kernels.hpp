@@ -897,10 +897,8 @@ __global__ __launch_bounds__(64) void verify_resolve_kernel(VerifyPass vp, int J
   const VRec v = verify_final(vp, item, it, J);
   const VBonusPart* bp = vp.bp + (size_t)it * vp.nchunks;
   const VerifyResult r = verify_result(v, vp.nchunks, [&](int k) { return bp[k]; });
-  if (threadIdx.x == 0) {
-    vp.results[it] = r;  // pinned host memory
-    __threadfence_system();
-  }
+  // pinned host memory, read by the host after it synchronises the stream
+  if (threadIdx.x == 0) vp.results[it] = r;
 }
 
 }  // namespace ts
