@@ -466,7 +466,7 @@ TreeBlock tree_block(int R, int cap) {
 struct BuildLayout {
   size_t off_par, off_out, off_exp;
   // device-resident waves
-  size_t off_par2, off_list, off_lsize, off_evals, off_pcount, off_done, off_span, off_anchor, off_ltheta;
+  size_t off_par2, off_list, off_lsize, off_evals, off_pcount, off_span, off_anchor, off_ltheta;
   size_t bytes;
   int Pmax;
 };
@@ -484,8 +484,7 @@ BuildLayout build_layout(const ts_drafter* d, int N, int K, float T) {
   b.off_list = o; o += align256((size_t)R * std::max(N, 1) * sizeof(WaveSlot));
   b.off_lsize = o; o += align256((size_t)R * 4);
   b.off_evals = o; o += align256((size_t)R * 4);
-  b.off_pcount = o; o += align256((size_t)(d->D + 2) * 4);
-  b.off_done = o; o += align256((size_t)(d->D + 2) * 4);
+  b.off_pcount = o; o += align256((size_t)(d->D + 2) * 8);
   b.off_span = o; o += 2 * align256((size_t)R * sizeof(WaveSpan));
   b.off_anchor = o; o += align256((size_t)R * 4);
   b.off_ltheta = o; o += align256((size_t)R * 4);
@@ -537,12 +536,11 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   wp.log_theta_host = reinterpret_cast<const float*>(hs + (size_t)R * 4);
   wp.anchor_w = reinterpret_cast<int32_t*>(ws + bl.off_anchor);
   wp.log_theta_w = reinterpret_cast<float*>(ws + bl.off_ltheta);
-  wp.done = reinterpret_cast<int*>(ws + bl.off_done);
   wp.host_count = hcnt;
   wp.list = reinterpret_cast<WaveSlot*>(ws + bl.off_list);
   wp.lsize = reinterpret_cast<int*>(ws + bl.off_lsize);
   wp.evals = reinterpret_cast<int*>(ws + bl.off_evals);
-  wp.pcount = reinterpret_cast<int*>(ws + bl.off_pcount);
+  wp.pcount = reinterpret_cast<uint64_t*>(ws + bl.off_pcount);
   wp.par[0] = reinterpret_cast<ts_parent*>(ws + bl.off_par);
   wp.par[1] = reinterpret_cast<ts_parent*>(ws + bl.off_par2);
   wp.span[0] = reinterpret_cast<WaveSpan*>(ws + bl.off_span);
@@ -572,7 +570,7 @@ int32_t build_tree_device(const ts_drafter* d, const int32_t* anchor, const std:
   for (int i = 0; i < D + 2; ++i) hcnt[i] = -1;
   auto queue_wave = [&](int w, int Pub) -> int32_t {
     int32_t r = run_expand(d, wp.par[w & 1], Pub, calib, K, T, seed, sampler, &eo, ws + bl.off_exp, s,
-                           wp.pcount + w);
+                           reinterpret_cast<const int*>(wp.pcount + w));
     if (r != TS_OK) return r;
     launch_wave_control(wp, w, s);
     TS_HIP(hipGetLastError());

@@ -60,10 +60,7 @@ __device__ __forceinline__ int wave_block_excl_scan(int v, int* tmp, int& total)
 __global__ __launch_bounds__(kWaveThreads) void wave_init_kernel(const WaveParams wp) {
   const int q = blockIdx.x * kWaveThreads + threadIdx.x;
   if (q == 0) {
-    for (int i = 0; i < wp.D + 2; ++i) {
-      wp.pcount[i] = i == 0 ? wp.R : 0;
-      wp.done[i] = 0;
-    }
+    for (int i = 0; i < wp.D + 2; ++i) wp.pcount[i] = i == 0 ? (uint64_t)wp.R : 0ull;
   }
   if (q >= wp.R) return;
   const int32_t a = wp.anchor_host[q];
@@ -188,18 +185,19 @@ __global__ __launch_bounds__(kWaveThreads) void wave_control_kernel(const WavePa
   int nc = 0;
   int cpos = wave_block_excl_scan(cc, tmp, nc);
   if (t == 0) {
-    const int base = nc > 0 ? atomicAdd(&wp.pcount[w + 1], nc) : 0;
+    // one atomic reserves this request's rows and counts it as done (the
+    // frontier size in the low half, finished workgroups in the high half)
+    const uint64_t old = atomicAdd(&wp.pcount[w + 1], (1ull << 32) | (uint64_t)nc);
+    const int base = (int)(uint32_t)old;
     base_sh = base;
     wp.span[(w + 1) & 1][q] = WaveSpan{base, nc};
-    // the last workgroup to finish hands the next wave's size to the host.
-    // Only the count goes to the host (the lists and parents reach the next
-    // wave's kernels across the launch boundary): this workgroup's count
-    // atomic has returned before its done increment is issued, so the last
-    // one reads the final count; a system-scope store hands it over.
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (atomicAdd(&wp.done[w + 1], 1) == wp.R - 1)
-      __hip_atomic_store(const_cast<int32_t*>(wp.host_count + w + 1), atomicAdd(&wp.pcount[w + 1], 0),
-                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    // the last workgroup to finish knows the final size and hands it to the
+    // host with a system-scope store.  Only the count goes to the host (the
+    // lists and parents reach the next wave's kernels across the launch
+    // boundary).
+    if ((int)(old >> 32) == wp.R - 1)
+      __hip_atomic_store(const_cast<int32_t*>(wp.host_count + w + 1), base + nc, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_SYSTEM);
   }
   __syncthreads();
   ts_parent* out = wp.par[(w + 1) & 1] + base_sh;

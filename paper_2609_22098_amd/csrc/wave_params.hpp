@@ -32,13 +32,14 @@ struct WaveParams {
   const float* log_theta_host;
   int32_t* anchor_w;
   float* log_theta_w;
-  int* done;                     // [D + 2] control workgroups finished after wave w - 1
-  volatile int32_t* host_count;  // [D + 2] pinned host memory: pcount[w], written by the
-                                 // last control workgroup of wave w - 1
+  volatile int32_t* host_count;  // [D + 2] pinned host memory: the size of wave w, written
+                                 // by the last control workgroup of wave w - 1
   WaveSlot* list;          // [R][N] best known slots with key >= log(theta), pop order
   int* lsize;              // [R] entries of list in use
   int* evals;              // [R] parents evaluated so far
-  int* pcount;             // [D + 2] frontier size of each wave (wave w: pcount[w])
+  // [D + 2] wave w: frontier size in the low 32 bits (the expansion reads
+  // that half as an int), control workgroups of wave w - 1 finished in the high
+  uint64_t* pcount;
   ts_parent* par[2];       // frontier of wave w in par[w & 1]
   WaveSpan* span[2];       // [R] rows of each request in par[w & 1]
   // outputs of the current wave's expansion, [P][K] row-major
