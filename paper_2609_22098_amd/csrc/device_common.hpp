@@ -65,19 +65,24 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
 }
 
 // log p-hat = log sigmoid(a * logit(q0) + b) from lq = log q0 (§3.4 Eq. 3),
-// with log(1 - q0) = log1mexp(lq) in the two-branch form of Maechler (2012).
+// without branches, on the base-2 exponential and logarithm of the vector
+// unit.  logit = lq - log(1 - q0): 1 - q0 is the difference 1 - e^lq except
+// near lq = 0, where that difference cancels and the Taylor series of
+// -expm1(lq) (to the x^7 term; below 1e-8 relative for |lq| <= 0.3) is used.
+// log sigmoid(y) = min(y, 0) - log(1 + e^-|y|).  The result is within 5e-7
+// of the fp64 value relative to max(1, |log p-hat|), as for the libm
+// functions.  lq >= 0 (and NaN) gives logit +inf; lq = -inf gives -inf.
 __device__ __forceinline__ float log_phat(float lq, float a, float b) {
-  float logit;
-  if (!(lq < 0.0f)) {
-    logit = __builtin_huge_valf();
-  } else {
-    const float l1m = (lq > -kLn2) ? logf(-expm1f(lq)) : log1pf(-expf(lq));
-    logit = lq - l1m;
-  }
-  const float x = (a == 0.0f) ? b : a * logit + b;
-  if (x == __builtin_huge_valf()) return 0.0f;
-  if (x == -__builtin_huge_valf()) return -__builtin_huge_valf();
-  return (x >= 0.0f) ? -log1pf(expf(-x)) : x - log1pf(expf(x));
+  const float e = exp2_fast(lq * kLog2e);
+  const float x = lq;
+  const float series =
+      x * __builtin_fmaf(x, __builtin_fmaf(x, __builtin_fmaf(x, __builtin_fmaf(x, __builtin_fmaf(x,
+          __builtin_fmaf(x, 1.0f / 5040.0f, 1.0f / 720.0f), 1.0f / 120.0f), 1.0f / 24.0f), 1.0f / 6.0f), 0.5f), 1.0f);
+  const float one_minus_q0 = lq > -0.3f ? -series : 1.0f - e;
+  const float logit = lq < 0.0f ? lq - __builtin_amdgcn_logf(one_minus_q0) * kLn2 : __builtin_huge_valf();
+  const float y = a == 0.0f ? b : __builtin_fmaf(a, logit, b);
+  const float t = exp2_fast(-__builtin_fabsf(y) * kLog2e);
+  return fminf(y, 0.0f) - __builtin_amdgcn_logf(1.0f + t) * kLn2;
 }
 
 // Cross-lane moves with DPP (data-parallel primitives): the source lane's

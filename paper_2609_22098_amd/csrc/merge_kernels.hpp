@@ -148,7 +148,7 @@ __device__ __forceinline__ void u_seeds4(const float* p, float (&u)[4]) {
 // Runs of kind 1 also get their Gumbel keys.  All lanes then check the keys
 // against the kind's threshold; candidates go into the kind's list.  A run
 // whose expected maximum is known counts a mismatch if the recomputed one differs.
-template <typename TE, int KS, bool SAMPLE>
+template <typename TE, int KS, bool SAMPLE, int PARTS>
 __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* urow,
                                              const typename Frag<TE>::type (&bcol)[KS],
                                              uint32_t pc1, uint32_t pc2, uint32_t pc3,
@@ -170,10 +170,10 @@ __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* uro
     const int tb = b < nrun ? t[b] : 0;
     vec = vec && (tb & 3) == 0 && tb + 16 <= V;
   }
-  // in two halves: all loads of a half first (one round trip), then its MFMAs
-  constexpr int kHalf = kBatch / 2;
+  // in PARTS parts: all loads of a part first (one round trip), then its MFMAs
+  constexpr int kHalf = kBatch / PARTS;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
+  for (int h = 0; h < PARTS; ++h) {
     typename F::type wf[kHalf][KS];
     float u[kHalf][4];
 #pragma unroll
@@ -769,6 +769,10 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
   reglist_init(gl);
   int mism = 0;
   const float nan = __builtin_nanf("");
+  // a batch's loads in one round trip at rank <= 64; in two with sequential
+  // draws (beside the draws, which are the longer chain, the wave keeps to
+  // the registers that leave four waves per SIMD) or at higher ranks
+  constexpr int kRescanParts = (SEQ || KS > 2) ? 2 : 1;
   int it = 0, sub = 0;
 #pragma unroll 1
   while (it < nitems) {
@@ -777,6 +781,27 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
 #pragma unroll
     for (int q = 0; q < kBatch; ++q) { qt[q] = 0; qk[q] = 0; qe[q] = nan; }
     int nr = 0;
+    // the leading single-run items of the batch in one read by all lanes
+    // (lane i reads item it + i); they fill the arrays as the loop below
+    // would, the last one read in slot 0
+    if (sub == 0) {
+      const int cnt = min(kBatch, nitems - it);
+      const int li = it + min(lane, cnt - 1);
+      const int code = L.item_t[li];
+      const int kd = L.item_k[li];
+      const float e = L.item_e[li];
+      const uint64_t whole = __ballot(lane < cnt && code < 0);
+      const int m = whole ? min(cnt, __ffsll((unsigned long long)whole) - 1) : cnt;
+#pragma unroll
+      for (int q = 0; q < kBatch; ++q)
+        if (q < m) {
+          qt[q] = lane_i32(code, m - 1 - q);
+          qk[q] = lane_i32(kd, m - 1 - q);
+          qe[q] = lane_f32(e, m - 1 - q);
+        }
+      nr = m;
+      it += m;
+    }
 #pragma unroll 1
     while (nr < kBatch && it < nitems) {
       const int code = L.item_t[it];
@@ -804,7 +829,8 @@ __global__ __launch_bounds__(256) void expand_merge_kernel(const MergeParams p) 
       ++nr;
     }
     if (nr > 0)
-      rescan_batch<TE, KS, GUMBEL>(p, urow, bcol, pc1, pc2, pc3, qt, qk, qe, nr, thr, L, zl, gl, mism);
+      rescan_batch<TE, KS, GUMBEL, kRescanParts>(p, urow, bcol, pc1, pc2, pc3, qt, qk, qe, nr, thr, L, zl, gl,
+                                                 mism);
   }
   if constexpr (SEQ) {
     __syncthreads();  // the draws of wave 1
