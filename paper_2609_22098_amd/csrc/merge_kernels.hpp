@@ -268,6 +268,84 @@ __device__ __forceinline__ void rescan_batch(const MergeParams& p, const TE* uro
   wave_sync_lds();
 }
 
+// Descending bitonic sort of N values in registers (N a power of two).
+template <int N>
+__device__ __forceinline__ void sort_desc(float (&x)[N]) {
+#pragma unroll
+  for (int k = 2; k <= N; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const int l = i ^ j;
+        if (l > i) {
+          const float hi = fmaxf(x[i], x[l]), lo = fminf(x[i], x[l]);
+          const bool desc = (i & k) == 0;
+          x[i] = desc ? hi : lo;
+          x[l] = desc ? lo : hi;
+        }
+      }
+}
+
+// The LL largest of the lane's list a (descending) and b (descending), in
+// descending order: max(a[k], b[LL-1-k]) is a bitonic sequence holding
+// them, and a half-cleaner cascade sorts it.  The result does not depend on
+// which list is a.
+template <int LL>
+__device__ __forceinline__ void merge_top(float (&a)[LL], const float (&b)[LL]) {
+#pragma unroll
+  for (int k = 0; k < LL; ++k) a[k] = fmaxf(a[k], b[LL - 1 - k]);
+#pragma unroll
+  for (int j = LL >> 1; j > 0; j >>= 1)
+#pragma unroll
+    for (int i = 0; i < LL; ++i) {
+      const int l = i ^ j;
+      if (l > i) {
+        const float hi = fmaxf(a[i], a[l]), lo = fminf(a[i], a[l]);
+        a[i] = hi;
+        a[l] = lo;
+      }
+    }
+}
+
+// The K-th largest (K <= LL) of the wave's entries, NE per lane, equal
+// values counted separately; -inf when fewer than K are finite.  Each lane
+// sorts its entries and keeps LL of them; six exchange steps then merge the
+// lists of partner lanes (lanes i^1, i^2, the mirrored lane in its group of
+// 8 and of 16, i^16, i^32), after which every lane holds the wave's top LL.
+template <int LL, int NE>
+__device__ __forceinline__ float wave_kth_largest(const float (&v)[NE], int K) {
+  float x[NE];
+#pragma unroll
+  for (int i = 0; i < NE; ++i) x[i] = v[i];
+  sort_desc<NE>(x);
+  float a[LL], b[LL];
+#pragma unroll
+  for (int k = 0; k < LL; ++k) a[k] = k < NE ? x[k] : kNegInf;
+#pragma unroll
+  for (int k = 0; k < LL; ++k) b[k] = dpp_f32<0xB1>(a[k]);
+  merge_top<LL>(a, b);
+#pragma unroll
+  for (int k = 0; k < LL; ++k) b[k] = dpp_f32<0x4E>(a[k]);
+  merge_top<LL>(a, b);
+#pragma unroll
+  for (int k = 0; k < LL; ++k) b[k] = dpp_f32<0x141>(a[k]);
+  merge_top<LL>(a, b);
+#pragma unroll
+  for (int k = 0; k < LL; ++k) b[k] = dpp_f32<0x140>(a[k]);
+  merge_top<LL>(a, b);
+#pragma unroll
+  for (int k = 0; k < LL; ++k) b[k] = xor16_f32(a[k]);
+  merge_top<LL>(a, b);
+#pragma unroll
+  for (int k = 0; k < LL; ++k) b[k] = xor32_f32(a[k]);
+  merge_top<LL>(a, b);
+  float r = kNegInf;
+#pragma unroll
+  for (int k = 0; k < LL; ++k) r = k == K - 1 ? a[k] : r;
+  return r;
+}
+
 // Threshold and candidate items for one key kind.  Let L be the K-th
 // largest recorded run key: those are keys of K distinct runs, whose maxima
 // lie within kRunSlack / 2 units of their keys, so the K-th largest token
@@ -289,33 +367,18 @@ __device__ __forceinline__ float select_items_n(const MergeParams& p, const RunS
   // Every load reads a clamped index, so all are in flight together.  A slot
   // past the last chunk holds a copy of a real entry: it starts out taken in
   // the threshold rounds below, and every later use checks the chunk range.
-  uint32_t taken = 0u;
+  float live[kEntrySlots];
 #pragma unroll
   for (int i = 0; i < kEntrySlots; ++i) {
     const int e = i * 64 + lane;
     const size_t ec = pb * kTopRuns + min(e, S * kTopRuns - 1);
     ev[i] = sm.m[ec];
-    taken |= (e >> 2) < S ? 0u : 1u << i;
+    live[i] = (e >> 2) < S ? ev[i] : kNegInf;
   }
 #pragma unroll
   for (int i = 0; i < kRestSlots; ++i) rv[i] = sm.rest[pb + min(i * 64 + lane, S - 1)];
-  float thr = kNegInf;
-  int picked = 0;
-  for (int round = 0; round < K; ++round) {
-    float lm = kNegInf;
-#pragma unroll
-    for (int i = 0; i < kEntrySlots; ++i)
-      if (!(taken & (1u << i))) lm = fmaxf(lm, ev[i]);
-    const float m = wave_max(lm);
-    if (m == kNegInf) break;
-    int c = 0;
-#pragma unroll
-    for (int i = 0; i < kEntrySlots; ++i)
-      if (!(taken & (1u << i)) && ev[i] == m) { taken |= 1u << i; ++c; }
-    picked += wave_sum_int(c);
-    if (picked >= K) { thr = m; break; }
-  }
-  if (picked < K) thr = kNegInf;  // fewer than K runs recorded: every token is a candidate
+  // fewer than K runs recorded: -inf, every token is a candidate
+  float thr = K <= 8 ? wave_kth_largest<8, kEntrySlots>(live, K) : wave_kth_largest<16, kEntrySlots>(live, K);
   thr = key_lowered(thr, kRunSlack);
 
   // whole chunks
