@@ -608,12 +608,17 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     for (int i = 0; i < NSEG; ++i) ms[i] = segL[i] == kNegInf ? 0.0f : exp2_fast(segL[i] - mx);
     const int sg = wave_pick(ms, word_to_uniform(w0));
     // level 2: block within the segment (lane = block offset)
+    // The masses are taken relative to the segment's own log-mass, which no
+    // block of it exceeds (a common scale, so no reduction for a maximum).
     const int b = sg * kBps + lane;
     const bool bin = sg >= 0 && b < nblk;
     const float lb = bin ? (in_lds ? L.seg_blk[b] : gblk[b]) : kNegInf;
-    const float mb = wave_max_fin(lb);
+    float sref = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NSEG; ++i)
+      if (sg >= 0 && (sg >> 6) == i) sref = lane_f32(segL[i], sg & 63);
     float m2[1];
-    m2[0] = lb == kNegInf ? 0.0f : exp2_fast(lb - mb);
+    m2[0] = lb == kNegInf ? 0.0f : exp2_fast(lb - sref);
     const int bo = wave_pick(m2, word_to_uniform(w1));
     const int bsel = sg * kBps + bo;
     // level 3: token within the block; recompute its 64 logits (four runs of
@@ -636,6 +641,11 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
       for (int kk = 0; kk < KS; ++kk) wf[q][kk] = F::load(wrow, kk * F::kPerStep, g);
     }
     const float useed = keep_or(F::to_f32(urow[min(y, V - 1)]), opaque_mask(y < V), kNegInf);
+    // while the block's rows are in flight: the log-mass of the segment's
+    // other blocks, so that its new mass after the draw takes no reduction
+    const float lo = lane == bo ? kNegInf : lb;
+    const float mo = wave_max_fin(lo);
+    const float so = wave_sum(lo == kNegInf ? 0.0f : exp2_fast(lo - mo));
     f32x4 acc[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) acc[q] = f32x4{useed, useed, useed, useed};
@@ -653,12 +663,20 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
     for (int q = 0; q < 4; ++q)
       zq[q] = max2_med3(__builtin_amdgcn_fmed3f(acc[q][0], acc[q][1], acc[q][2]), acc[q][3]);
     const float zy = g == 0 ? zq[0] : g == 1 ? zq[1] : g == 2 ? zq[2] : zq[3];
+    // tokens drawn before are out: lanes of gl not drawn yet hold id
+    // 0x7FFFFFFF (an empty draw -1), which no y matches
     bool live = y < V && bo >= 0 && sg >= 0;
-    for (int k = 0; k < j - 1; ++k) live &= lane_i32(gl.id, k) != y;
+#pragma unroll
+    for (int k = 0; k < 7; ++k) live &= lane_i32(gl.id, k) != y;
+    if (p.K > 8) {
+#pragma unroll
+      for (int k = 7; k < TS_MAX_K - 1; ++k) live &= lane_i32(gl.id, k) != y;
+    }
+    // relative to the block's log-mass, which no live token of it exceeds
     const float xy = live ? zy * p.cT : kNegInf;
-    const float mt = wave_max_fin(xy);
+    const float bref = bo >= 0 ? lane_f32(lb, bo) : 0.0f;
     float m3[1];
-    m3[0] = live ? exp2_fast(xy - mt) : 0.0f;
+    m3[0] = live ? exp2_fast(xy - bref) : 0.0f;
     const int to = wave_pick(m3, word_to_uniform(w2));
     const int tsel = t0 + to;
     const float zsel = lane_f32(zy, to < 0 ? 0 : to);
@@ -685,10 +703,10 @@ __device__ __forceinline__ void seq_draws_n(const MergeParams& p, int pidx, cons
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
-    const float lb2 = lane == bo ? lnew : lb;
-    const float mb2 = wave_max_fin(lb2);
-    const float rest2 = wave_sum(lb2 == kNegInf ? 0.0f : exp2_fast(lb2 - mb2));
-    const float snew = mb2 == kNegInf ? kNegInf : mb2 + __builtin_amdgcn_logf(rest2);
+    // the segment: its other blocks (mo, so) and the block's new mass
+    const float M = max2_med3(mo, lnew);
+    const float tot = (mo == kNegInf ? 0.0f : so * exp2_fast(mo - M)) + (lnew == kNegInf ? 0.0f : exp2_fast(lnew - M));
+    const float snew = M == kNegInf ? kNegInf : M + __builtin_amdgcn_logf(tot);
 #pragma unroll
     for (int i = 0; i < NSEG; ++i)
       if (sg == 64 * i + lane) segL[i] = snew;
