@@ -156,6 +156,25 @@ def _torch():
     return torch
 
 
+# Host output arrays reused from call to call: their checked addresses.  An
+# entry holds its array, so the array's id is not reused (and numpy does not
+# resize it) while it is cached; taking an array's address costs about a
+# microsecond.
+_addr_cache = {}
+
+
+def _int32_out_addr(a, shape):
+    e = _addr_cache.get(id(a))
+    if e is not None and e[0] is a and e[2] == shape:
+        return e[1]
+    assert a.shape == shape and a.dtype == np.int32 and a.flags.c_contiguous
+    if len(_addr_cache) >= 64:
+        _addr_cache.clear()
+    addr = a.ctypes.data
+    _addr_cache[id(a)] = (a, addr, shape)
+    return addr
+
+
 def _stream(stream):
     torch = _torch()
     if stream is None:
@@ -170,9 +189,10 @@ def torch_empty_bytes(n, device="cuda"):
 
 def _dtype_code(t):
     torch = _torch()
-    if t.dtype == torch.bfloat16:
+    dt = t.dtype
+    if dt is torch.bfloat16:
         return TS_BF16
-    if t.dtype == torch.float32:
+    if dt is torch.float32:
         return TS_F32
     raise TypeError(f"unsupported dtype {t.dtype}")
 
@@ -239,6 +259,29 @@ def expand_workspace_size(d: DeviceDrafter, P, k, T):
     return lib().ts_expand_workspace_size(d.ref(), P, k, float(T))
 
 
+_EXPAND_OUT_NAMES = tuple(name for name, _ in ExpandOut._fields_[:-1])
+# Output dicts reused from call to call: their ExpandOut, rebuilt whenever a
+# tensor's address differs from the cached one (the events field is set on
+# every call).  An entry holds its dict, so the dict's id is not reused while
+# it is cached.
+_expand_out_cache = {}
+
+
+def _expand_out(outputs, events):
+    ptrs = tuple(outputs[name].data_ptr() if outputs.get(name) is not None else None
+                 for name in _EXPAND_OUT_NAMES)
+    e = _expand_out_cache.get(id(outputs))
+    if e is not None and e[0] is outputs and e[1] == ptrs:
+        out = e[2]
+        out.events = events
+        return out
+    out = ExpandOut(*ptrs, events)
+    if len(_expand_out_cache) >= 64:
+        _expand_out_cache.clear()
+    _expand_out_cache[id(outputs)] = (outputs, ptrs, out)
+    return out
+
+
 def expand(d: DeviceDrafter, parents, P, k, T, seed, calib=(0.67, -0.46), workspace=None,
            stream=None, outputs=None, events=None, sampler="gumbel"):
     """ts_expand.  parents: device uint8 tensor of P ts_parent records.  Returns a dict of
@@ -262,9 +305,7 @@ def expand(d: DeviceDrafter, parents, P, k, T, seed, calib=(0.67, -0.46), worksp
     if workspace is None:
         n = expand_workspace_size(d, P, k, T)
         workspace = torch.empty((max(n, 1),), dtype=torch.uint8, device=dev)
-    out = ExpandOut(*[outputs[name].data_ptr() if outputs.get(name) is not None else None
-                      for name, _ in ExpandOut._fields_[:-1]],
-                    events)
+    out = _expand_out(outputs, events)
     rc = lib().ts_expand(d.ref(), ctypes.c_void_p(parents.data_ptr()), P, Calib(*calib), k, float(T),
                          ctypes.c_uint64(seed), SAMPLERS[sampler], ctypes.byref(out), ctypes.c_void_p(workspace.data_ptr()),
                          workspace.numel(), _stream(stream))
@@ -394,17 +435,16 @@ def verify(d: DeviceDrafter, tree: HostTree, target, T, seed, workspace=None, st
         bonus = np.zeros(R, np.int32)
     else:
         path, plen, bonus = out
-        assert path.shape == (R, TS_MAX_D) and plen.shape == (R,) and bonus.shape == (R,)
-        assert path.dtype == plen.dtype == bonus.dtype == np.int32
-        assert path.flags.c_contiguous and plen.flags.c_contiguous and bonus.flags.c_contiguous
+    a_path = _int32_out_addr(path, (R, TS_MAX_D))
+    a_plen = _int32_out_addr(plen, (R,))
+    a_bonus = _int32_out_addr(bonus, (R,))
     if workspace is None:
         n = verify_workspace_size(d, cap, T)
         workspace = torch.empty((max(n, 1),), dtype=torch.uint8, device=target.device)
     s = tree.struct()
     rc = lib().ts_verify(d.ref(), ctypes.byref(s), ctypes.c_void_p(target.data_ptr()), _dtype_code(target),
-                         float(T), ctypes.c_uint64(seed), path.ctypes.data, plen.ctypes.data,
-                         bonus.ctypes.data, ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
-                         _stream(stream))
+                         float(T), ctypes.c_uint64(seed), a_path, a_plen, a_bonus,
+                         ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream(stream))
     _check(rc)
     return path, plen, bonus
 
