@@ -1139,11 +1139,11 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
   char* ws = static_cast<char*>(workspace);
 
   DrainOnError drain{s};
-  // children of every node in creation order (= draw order)
-  const KidIndex& kids = kid_index(tree);
   for (int q = 0; q < R; ++q) path_len[q] = 0;
 
   if (T == 0.0f) {
+    // children of every node in creation order
+    const KidIndex& kids = kid_index(tree);
     std::vector<int> rows;
     for (int q = 0; q < R; ++q)
       for (int i = 0; i <= tree->n[q]; ++i) rows.push_back(q * cap + i);
@@ -1194,6 +1194,29 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
   const size_t hs_res = align256((size_t)R * sizeof(VerifyResult));
   const size_t hs_next = align256((size_t)R * sizeof(VerifyNext));
   if ((rc = host_stage(hs_items + hs_par + hs_res + hs_next + 256, &hs)) != TS_OK) return rc;
+  // The first level's logit recompute is queued first: its rows are the roots
+  // of the trees that have children (n > 0), in request order, which the
+  // level loop below assigns the same way; the child index and the level's
+  // items are built while it runs.
+  int first_rows = 0;
+  for (int q = 0; q < R; ++q) {
+    if (tree->n[q] <= 0) continue;
+    const size_t o = (size_t)q * cap;
+    reinterpret_cast<ts_parent*>(hs + hs_items)[first_rows++] =
+        ts_parent{tree->token[o], tree->depth[o], q, 0.0f, tree->path[o]};
+  }
+  auto launch_recompute = [&](int P) -> int32_t {
+    const Plan pl = make_plan(d, P, T, TS_SAMPLER_GUMBEL, true);
+    const ExpandParams ep =
+        eval_params(d, reinterpret_cast<const ts_parent*>(hs + hs_items), P, T, seed, pl, ws + vl.off_exp, zbuf);
+    launch_eval(d, ep, pl, s);
+    TS_HIP(hipGetLastError());
+    return TS_OK;
+  };
+  if (first_rows > 0 && (rc = launch_recompute(first_rows)) != TS_OK) return rc;
+  // children of every node in creation order (= draw order)
+  const KidIndex& kids = kid_index(tree);
+  bool first_level = true;
   const VerifyResult* res = reinterpret_cast<const VerifyResult*>(hs + hs_items + hs_par);
   VerifyNext* hnext = reinterpret_cast<VerifyNext*>(hs + hs_items + hs_par + hs_res);
   volatile int32_t* herr = reinterpret_cast<volatile int32_t*>(hs + hs_items + hs_par + hs_res + hs_next);
@@ -1228,16 +1251,16 @@ int32_t ts_verify(const ts_drafter* d, const ts_tree* tree, const void* target, 
       items.push_back(it);
     }
     const int ni = (int)items.size();
-    if (!zpar.empty()) {
-      const int P = (int)zpar.size();
+    if (first_level) {
+      if ((int)zpar.size() != first_rows)
+        return fail(TS_EINTERNAL, "first verification level has %d recompute rows, %d queued", (int)zpar.size(),
+                    first_rows);
+    } else if (!zpar.empty()) {
       // the recompute reads its parents from the pinned buffer
-      std::memcpy(hs + hs_items, zpar.data(), P * sizeof(ts_parent));
-      const Plan pl = make_plan(d, P, T, TS_SAMPLER_GUMBEL, true);
-      const ExpandParams ep =
-          eval_params(d, reinterpret_cast<const ts_parent*>(hs + hs_items), P, T, seed, pl, ws + vl.off_exp, zbuf);
-      launch_eval(d, ep, pl, s);
-      TS_HIP(hipGetLastError());
+      std::memcpy(hs + hs_items, zpar.data(), zpar.size() * sizeof(ts_parent));
+      if ((rc = launch_recompute((int)zpar.size())) != TS_OK) return rc;
     }
+    first_level = false;
     // pass A reads the items from the pinned buffer and stages them in ditems
     std::memcpy(hs, items.data(), ni * sizeof(VerifyItem));
     VerifyPass vp{};
