@@ -67,6 +67,19 @@ def test_ragged_shapes(torch, dtype, r, V, T):
     _expand_and_compare(torch, dr, fr, min(5, V), T, seed=3, tag=f"ragged {dtype} r={r} V={V} T={T}")
 
 
+@pytest.mark.parametrize("dtype,r,V", [("bf16", 64, 30011), ("f32", 32, 5000)])
+@pytest.mark.parametrize("T", [0.0, 1.3])
+def test_max_siblings(torch, dtype, r, V, T):
+    """K = 16 (the library's maximum) with the greedy order and Gumbel draws: the merge's
+    threshold then takes the 16th largest recorded run key, and the candidate lists hold 16
+    entries; a ragged vocabulary over many chunks and a ragged parent count (45)."""
+    dr = synth.make_drafter(V, 6, r, R=3, dtype=dtype, u_sigma=2.0, planted=None, zipf=(6.0, 1.1),
+                            ew_sigma=0.2, seed=13)
+    fr = synth.make_frontier(dr, per_depth=3, seed=4)
+    fr = {k: v[:45] for k, v in fr.items()}
+    _expand_and_compare(torch, dr, fr, 16, T, seed=9, tag=f"K=16 {dtype} r={r} V={V} T={T}")
+
+
 @pytest.mark.parametrize("T", [0.0, 0.7])
 def test_wide_frontier_blocks(torch, T):
     """A frontier of 700 parents (the 4-block-per-wave layout) with shared rows, bf16 r=64."""
