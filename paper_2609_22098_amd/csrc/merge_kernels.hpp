@@ -95,18 +95,20 @@ __device__ __forceinline__ void reglist_init(RegList& l) {
 // Insert a candidate (uniform across the wave).
 __device__ __forceinline__ void reglist_insert(RegList& l, int K, float v, int id, float a) {
   const int lane = threadIdx.x & 63;
-  const bool ahead = lane < l.cnt && run_before(l.val, l.id, v, id);
+  // entry before the candidate: key desc, token asc (run_before, without
+  // the short-circuit branches)
+  const bool ahead = (lane < l.cnt) & ((l.val > v) | ((l.val == v) & (l.id < id)));
   const int pos = __popcll(__ballot(ahead));
   if (pos >= K) return;
   // the entries from pos on move up one lane (DPP wave_shr:1)
   const float pv = dpp_f32<0x138>(l.val);
   const int pid = dpp_i32<0x138>(l.id);
   const float pa = dpp_f32<0x138>(l.aux);
-  if (lane == pos) {
-    l.val = v; l.id = id; l.aux = a;
-  } else if (lane > pos && lane < K) {
-    l.val = pv; l.id = pid; l.aux = pa;
-  }
+  const bool at = lane == pos;
+  const bool up = (lane > pos) & (lane < K);
+  l.val = at ? v : (up ? pv : l.val);
+  l.id = at ? id : (up ? pid : l.id);
+  l.aux = at ? a : (up ? pa : l.aux);
   l.cnt = min(l.cnt + 1, K);
 }
 
