@@ -483,8 +483,11 @@ __device__ __forceinline__ int wave_pick(const float (&m)[NS], float u) {
 // K draws without replacement from q_T, one after another (§3.3 residual
 // proposal): draw j picks a segment, a block in it and a token in it, each in
 // proportion to its remaining mass, from the words of one Philox call
-// (c0 = j, tag 4).  Masses are handled as base-2 logs relative to each
-// level's largest one, so removing drawn tokens never underflows the rest.
+// (c0 = j, tag 4).  Masses are kept as base-2 logs: the segment pick scales
+// them by the largest segment, the block and token picks by the segment's
+// and the block's own log-mass (no member exceeds it), and a block's mass
+// after a removal is summed relative to the largest token left, so removing
+// drawn tokens never underflows the rest.
 // The parent's block table lives in LDS when it fits (V <= 40 * 4096), else
 // in its rows of the workspace; a drawn token's block is rewritten in place.
 // Draw j lands in lane j - 1 of gl (token, z); a draw after every token with
