@@ -53,7 +53,10 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 TRANS_WEIGHT = 2
 KERNEL_SOURCES = ("paper_2609_22098_amd/csrc/expand_kernels.hpp",
-                  "paper_2609_22098_amd/csrc/device_common.hpp")
+                  "paper_2609_22098_amd/csrc/device_common.hpp",
+                  # its translation unit and the build's per-unit compiler flags
+                  "paper_2609_22098_amd/csrc/expand_eval_bf16_ks2.hip",
+                  "__graft_entry__.py")
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "expand_eval_serving_counters.json")
 EVAL_KERNEL = "expand_eval_lds_kernel"
 EVAL_FRONTIER = "expand_eval_lds_kernel<2, 2,"  # rank 64 (KS = 2), two parent blocks per wave

@@ -1,8 +1,7 @@
-// Expansion kernels for bf16 drafter tensors with KS = 1.
+// Merge kernels for bf16 drafter tensors with KS = 1 (the streaming passes
+// are in expand_eval_bf16_ks1.hip).
 #include "expand_inst.hpp"
 
 namespace ts {
-template void launch_eval_t<uint16_t, 1>(const ExpandParams&, int, int, bool, bool, dim3, dim3, hipStream_t);
 template void launch_merge_t<uint16_t, 1>(const MergeParams&, int, dim3, dim3, hipStream_t);
-template int eval_blocks_per_cu_t<uint16_t, 1>(int, int, bool, bool, int);
 }  // namespace ts
