@@ -479,3 +479,45 @@ def test_host_waves_beyond_device_limits(torch):
     _compare_all(dr, tree, anchors, thetas, 600, 3, 1.0, 4, tag="host waves N=600", sampler="sequential",
                  min_share=0.1)
     assert tree.n[0] == 600
+
+
+def test_serving_step_repeats_bit_identical(torch):
+    """The benchmark's step twice on the same inputs: the 2048-parent expansion (sequential draws,
+    T=0.7), the device-wave trees of the 64 requests and their verification give byte-identical
+    outputs.  The waves place each request's frontier rows with atomics (their order changes
+    from run to run) and a verification level's workgroups meet through memory: a race in either
+    would show as a difference."""
+    from paper_2609_22098_amd import binding
+    w = synth.WORKLOADS[3]
+    dr = synth.make_workload_drafter(3, seed=0)
+    anchors, thetas, _ = synth.make_controls(dr.R, dr.V, w["theta"], seed=0)
+    fr = synth.make_frontier(dr, per_depth=w["frontier_per_depth"], seed=0)
+    P = len(fr["token"])
+    dd = binding.drafter_from_host(dr)
+    parents = binding.parents_to_device(fr["token"], fr["depth"], fr["request"], fr["log_surv"], fr["path"])
+    fields = ("n", "token", "parent", "depth", "rank", "path", "log_surv", "log_q0", "log_qT", "key", "evals")
+    runs, target = [], None
+    for rep in range(2):
+        out = binding.expand(dd, parents, P, w["K"], 0.7, 0, sampler="sequential")
+        tree = binding.build_tree(dd, anchors, thetas, w["N"], w["K"], 0.7, 0, sampler="sequential")
+        if target is None:
+            tgt = np.zeros((dr.R, tree.cap, dr.V), np.uint16)
+            for q in range(dr.R):
+                rows = synth.make_target_rows(dr, q, tree.depth[q, :int(tree.n[q]) + 1], w["target_sigma"],
+                                              seed=0)[0]
+                tgt[q, :len(rows)] = rows
+            target = torch.from_numpy(tgt).view(torch.bfloat16).cuda()
+        path, plen, bonus = binding.verify(dd, tree, target, 0.7, 0)
+        torch.cuda.synchronize()
+        runs.append(({k: v.cpu().numpy() for k, v in out.items() if not k.startswith("_")},
+                     {f: getattr(tree, f).copy() for f in fields}, (path.copy(), plen.copy(), bonus.copy())))
+    (e0, t0, v0), (e1, t1, v1) = runs
+
+    def same(a, b):
+        return a.shape == b.shape and np.array_equal(np.ascontiguousarray(a).view(np.uint8),
+                                                     np.ascontiguousarray(b).view(np.uint8))
+
+    assert all(same(e0[k], e1[k]) for k in e0), [k for k in e0 if not same(e0[k], e1[k])]
+    assert all(same(t0[f], t1[f]) for f in fields), [f for f in fields if not same(t0[f], t1[f])]
+    assert all(same(a, b) for a, b in zip(v0, v1))
+    assert int(np.sum(t0["n"] > 0)) >= 16 and int(v0[1].sum()) > 0
